@@ -1,0 +1,408 @@
+"""Plain fp64 CPU oracle for PaDoc's ancestor-masked tree attention.
+
+TEST INFRASTRUCTURE ONLY.  Only the test suite, the smoke check and the
+benchmark's CPU-baseline leg may import this module.  The product library
+never calls it, and it shares no code with the product (no kernels, headers,
+tables or helpers); the two meet only through the seeded inputs of
+``padoc_synth``.
+
+What it computes, and where the paper defines it
+------------------------------------------------
+* Visibility (Sec. 3.2, "Training Paradigm", ancestor sets): every token of a
+  node V attends to all tokens of V's ancestors and to the non-future tokens
+  of V itself.  Generalised to a segment tree: a query token ``(s, p)`` sees
+  key ``(t, j)`` iff ``t == s and j <= p`` or ``t`` is a proper ancestor of
+  ``s`` and ``j < F(s, t)``, where ``F(s, t)`` is the fork offset of the child
+  of ``t`` on the path to ``s`` (the number of leading tokens of ``t`` visible
+  below that child; App. C, packed sample ``[M | Y_1..Y_N]`` with ``M_{<=f_k}``).
+* Attention (App. E, the Attn equation): ``softmax(Q K^T / sqrt(d) + A_M) V``
+  with ``A_M`` the additive mask.  Masked keys are left out of every sum
+  (select-masking), which is the same value.  The log-sum-exp output is
+  ``LSE = ln sum_visible exp(scale * q . k)`` (natural log, scale included).
+* The paper's "reference implementation" materialises the dense Boolean
+  ancestor mask and runs masked softmax attention on it (App. C, Dense SDPA);
+  this oracle does exactly that, per page, in fp64.
+* Masked parallel decoding (App. E, Algorithm "Masked parallel decoding"):
+  :func:`simulate_masked_parallel_decoding` replays the logical fused mask
+  updates (identity append, row copy on fork, row removal on retire) so the
+  tests can pin the visibility rule and the fork-offset reading to it.
+
+Readings of points the paper leaves open are listed in the repository's design
+notes; the ones this file depends on: fork offsets are half-open counts
+(``[0, f)``); the page prefix is causal in itself; a branch's branch-start
+token is its own position 0; GQA maps query head ``h`` to KV head
+``h // (Hq // Hkv)``; queries of a segment are its last ``q_len`` tokens.
+
+Inputs are numpy arrays or torch tensors (converted exactly to float64; bf16
+values are represented exactly).  Nothing here is tuned for speed beyond
+processing query rows in batches (each row's arithmetic is unchanged).
+"""
+from __future__ import annotations
+
+from typing import Dict, Iterable, List, Optional, Sequence, Tuple
+
+import numpy as np
+
+__all__ = [
+    "page_nodes", "canonical_layout", "ancestors", "visible_counts", "page_of",
+    "dense_mask", "masked_attention", "tree_attention", "tree_attention_paged",
+    "gather_paged", "paged_slots", "simulate_masked_parallel_decoding",
+    "visible_pair_count",
+]
+
+Node = Tuple[int, int, int, int]   # (parent, fork, length, q_len)
+
+
+def _f64(x) -> np.ndarray:
+    try:
+        import torch
+        if isinstance(x, torch.Tensor):
+            return x.detach().to("cpu", torch.float64).numpy()
+    except ImportError:  # pragma: no cover
+        pass
+    return np.asarray(x, dtype=np.float64)
+
+
+def _as_nodes(nodes) -> List[Node]:
+    out = []
+    for n in nodes:
+        if isinstance(n, tuple) and len(n) == 4:
+            out.append(tuple(int(v) for v in n))
+        else:
+            out.append((int(n.parent), int(n.fork), int(n.length), int(n.q_len)))
+    return out
+
+
+# --------------------------------------------------------------------------
+# Tree structure
+# --------------------------------------------------------------------------
+
+def page_nodes(pages) -> List[Node]:
+    """The paper's packed sample per page, ``[prefix | stream | Y_1..Y_N]``
+    (App. C), as segments: the prefix is a root; the layout stream is its
+    child and sees the whole prefix (fork = P); branch ``Y_k`` is a child of
+    the stream with fork ``f_k`` (it sees stream tokens ``[0, f_k)``; its
+    branch-start token is its own position 0, Sec. 3.2 last paragraph).
+    Pages are concatenated."""
+    nodes: List[Node] = []
+    for pg in pages:
+        get = (lambda k: pg[k]) if isinstance(pg, dict) else (lambda k: getattr(pg, k))
+        root = len(nodes)
+        nodes.append((-1, 0, int(get("prefix_len")), int(get("prefix_q"))))
+        stream = len(nodes)
+        nodes.append((root, int(get("prefix_len")), int(get("stream_len")), int(get("stream_q"))))
+        for b in get("branches"):
+            bget = (lambda k: b[k]) if isinstance(b, dict) else (lambda k: getattr(b, k))
+            nodes.append((stream, int(bget("fork")), int(bget("length")), int(bget("q_len"))))
+    return nodes
+
+
+def canonical_layout(nodes, block_size: int = 0) -> Tuple[np.ndarray, np.ndarray]:
+    """Packed order = node order.  ``kv_off[s]``: first K/V row of segment s
+    (packed) or first block-table entry (paged: each segment owns
+    ``ceil(len / block_size)`` consecutive entries).  ``q_off[s]``: first
+    Q/O/LSE row (segments' queries concatenated in node order)."""
+    nodes = _as_nodes(nodes)
+    kv_off = np.zeros(len(nodes), dtype=np.int64)
+    q_off = np.zeros(len(nodes), dtype=np.int64)
+    kv = q = 0
+    for i, (_, _, n, ql) in enumerate(nodes):
+        kv_off[i] = kv
+        q_off[i] = q
+        kv += n if block_size == 0 else -(-n // block_size)
+        q += ql
+    return kv_off, q_off
+
+
+def ancestors(nodes, s: int) -> List[Tuple[int, int]]:
+    """Proper ancestors of segment s, root first, each with ``F(s, t)``: the
+    fork of the child of t that lies on the path to s."""
+    nodes = _as_nodes(nodes)
+    chain = []
+    child = s
+    t = nodes[s][0]
+    while t >= 0:
+        chain.append((t, nodes[child][1]))
+        child = t
+        t = nodes[t][0]
+    return chain[::-1]
+
+
+def visible_counts(nodes, s: int, p: int) -> Dict[int, int]:
+    """Query token p of segment s sees keys ``[0, count)`` of each listed
+    segment (ancestors via their fork offsets, itself causally)."""
+    out = {t: f for t, f in ancestors(nodes, s)}
+    out[s] = p + 1
+    return out
+
+
+def page_of(nodes) -> np.ndarray:
+    nodes = _as_nodes(nodes)
+    root = np.zeros(len(nodes), dtype=np.int64)
+    for i, (par, _, _, _) in enumerate(nodes):
+        root[i] = i if par < 0 else root[par]
+    return root
+
+
+def dense_mask(nodes, root: int) -> Tuple[np.ndarray, np.ndarray, np.ndarray]:
+    """Dense Boolean ancestor mask of one page (App. C, Dense SDPA).
+
+    Returns ``(seg, pos, mask)``: the page's tokens in packed order tagged with
+    their segment and position, and ``mask[a, b]`` = token a may see token b,
+    straight from the rule: same segment and not in the future, or an ancestor
+    segment's token before the fork offset on the path."""
+    nodes = _as_nodes(nodes)
+    roots = page_of(nodes)
+    segs = [i for i in range(len(nodes)) if roots[i] == root]
+    seg = np.concatenate([np.full(nodes[i][2], i, dtype=np.int64) for i in segs]) if segs else np.zeros(0, np.int64)
+    pos = np.concatenate([np.arange(nodes[i][2], dtype=np.int64) for i in segs]) if segs else np.zeros(0, np.int64)
+    n = seg.size
+    mask = np.zeros((n, n), dtype=bool)
+    for a in range(n):
+        s, p = int(seg[a]), int(pos[a])
+        anc = dict(ancestors(nodes, s))
+        for b in range(n):
+            t, j = int(seg[b]), int(pos[b])
+            if t == s:
+                mask[a, b] = j <= p
+            elif t in anc:
+                mask[a, b] = j < anc[t]
+    return seg, pos, mask
+
+
+def _dense_mask_fast(nodes, root: int):
+    """Same mask as :func:`dense_mask`, built segment block by segment block
+    (used for pages too large for the per-element loop; tests check that the
+    two agree)."""
+    nodes = _as_nodes(nodes)
+    roots = page_of(nodes)
+    segs = [i for i in range(len(nodes)) if roots[i] == root]
+    starts, total = {}, 0
+    for i in segs:
+        starts[i] = total
+        total += nodes[i][2]
+    mask = np.zeros((total, total), dtype=bool)
+    for s in segs:
+        ns = nodes[s][2]
+        r0 = starts[s]
+        mask[r0:r0 + ns, r0:r0 + ns] = np.tril(np.ones((ns, ns), dtype=bool))
+        for t, f in ancestors(nodes, s):
+            c0 = starts[t]
+            mask[r0:r0 + ns, c0:c0 + f] = True
+    seg = np.concatenate([np.full(nodes[i][2], i, dtype=np.int64) for i in segs]) if segs else np.zeros(0, np.int64)
+    pos = np.concatenate([np.arange(nodes[i][2], dtype=np.int64) for i in segs]) if segs else np.zeros(0, np.int64)
+    return seg, pos, mask
+
+
+def visible_pair_count(nodes) -> int:
+    """Number of visible (query, key) pairs, queries = last q_len tokens."""
+    nodes = _as_nodes(nodes)
+    total = 0
+    for s, (_, _, n, ql) in enumerate(nodes):
+        anc = sum(f for _, f in ancestors(nodes, s))
+        for p in range(n - ql, n):
+            total += anc + p + 1
+    return total
+
+
+# --------------------------------------------------------------------------
+# Attention by definition
+# --------------------------------------------------------------------------
+
+def masked_attention(q, k, v, mask, scale: float, return_probs: bool = False):
+    """Masked softmax attention of one head, fp64, by definition.
+
+    ``q [nq, d]``, ``k, v [nk, d]``, ``mask [nq, nk]`` (True = visible).
+    Per row: scores ``s_j = scale * q . k_j`` over visible j, ``m = max s``,
+    ``w_j = exp(s_j - m)``, ``l = sum w``, ``o = sum (w_j / l) v_j``,
+    ``lse = m + ln l``.  Masked keys enter no sum."""
+    q, k, v = _f64(q), _f64(k), _f64(v)
+    mask = np.asarray(mask, dtype=bool)
+    if mask.shape[0] and not mask.any(axis=1).all():
+        raise ValueError("a query row sees no key")
+    s = scale * (q @ k.T)
+    m = np.max(np.where(mask, s, -np.inf), axis=1, keepdims=True)
+    w = np.where(mask, np.exp(np.where(mask, s - m, 0.0)), 0.0)
+    l = w.sum(axis=1, keepdims=True)
+    p = w / l
+    o = p @ v
+    lse = (m + np.log(l))[:, 0]
+    if return_probs:
+        return o, lse, p
+    return o, lse
+
+
+def tree_attention(nodes, q, k, v, scale: float, num_heads_q: int, num_heads_kv: int,
+                   kv_off=None, q_off=None, rows: Optional[Iterable[int]] = None,
+                   return_probs: bool = False, row_batch: int = 512):
+    """Packed tree attention by definition.
+
+    ``q [n_q, Hq, d]``; ``k, v [T, Hkv, d]`` with segment s's tokens at rows
+    ``kv_off[s] ..``; segment s's queries (its last ``q_len`` tokens) at Q rows
+    ``q_off[s] ..``.  Offsets default to :func:`canonical_layout`.
+
+    Returns ``(O [n_q, Hq, d], LSE [n_q, Hq])`` in fp64 (rows not requested via
+    ``rows`` are NaN).  With ``return_probs`` also ``P [n_q, Hq, T]``."""
+    nodes = _as_nodes(nodes)
+    if num_heads_q % num_heads_kv:
+        raise ValueError("Hq must be a multiple of Hkv")
+    G = num_heads_q // num_heads_kv
+    k64, v64 = _f64(k), _f64(v)
+    q64 = _f64(q)
+    if kv_off is None or q_off is None:
+        ko, qo = canonical_layout(nodes, 0)
+        kv_off = ko if kv_off is None else kv_off
+        q_off = qo if q_off is None else q_off
+    n_q = q64.shape[0]
+    dv = v64.shape[2]
+    O = np.full((n_q, num_heads_q, dv), np.nan)
+    LSE = np.full((n_q, num_heads_q), np.nan)
+    P = np.zeros((n_q, num_heads_q, k64.shape[0])) if return_probs else None
+    want = None if rows is None else set(int(r) for r in rows)
+    roots = page_of(nodes)
+    for root in sorted(set(int(r) for r in roots)):
+        seg, pos, mask = _dense_mask_fast(nodes, root)
+        kv_rows = np.array([kv_off[s] + p for s, p in zip(seg, pos)], dtype=np.int64)
+        # query tokens of this page: (index into page tokens, Q row)
+        qa, qr = [], []
+        for a, (s, p) in enumerate(zip(seg, pos)):
+            n, ql = nodes[s][2], nodes[s][3]
+            if p >= n - ql:
+                r = int(q_off[s] + p - (n - ql))
+                if want is None or r in want:
+                    qa.append(a)
+                    qr.append(r)
+        if not qa:
+            continue
+        qa = np.array(qa)
+        qr = np.array(qr)
+        for h in range(num_heads_q):
+            g = h // G
+            kh = k64[kv_rows, g, :]
+            vh = v64[kv_rows, g, :]
+            for b0 in range(0, qa.size, row_batch):
+                sel = slice(b0, b0 + row_batch)
+                res = masked_attention(q64[qr[sel], h, :], kh, vh, mask[qa[sel]], scale,
+                                       return_probs=return_probs)
+                O[qr[sel], h, :] = res[0]
+                LSE[qr[sel], h] = res[1]
+                if return_probs:
+                    P[np.ix_(qr[sel], [h], kv_rows)] = res[2][:, None, :]
+    if return_probs:
+        return O, LSE, P
+    return O, LSE
+
+
+# --------------------------------------------------------------------------
+# Paged KV cache
+# --------------------------------------------------------------------------
+
+def paged_slots(nodes, block_table, block_size: int, bt_off=None):
+    """Physical location of every token: ``(block_id, slot)`` arrays in packed
+    token order.  Token t of segment s lives in block
+    ``block_table[bt_off[s] + t // block_size]`` at slot ``t % block_size``."""
+    nodes = _as_nodes(nodes)
+    bt = np.asarray(block_table, dtype=np.int64)
+    if bt_off is None:
+        bt_off, _ = canonical_layout(nodes, block_size)
+    blk, slot = [], []
+    for s, (_, _, n, _) in enumerate(nodes):
+        t = np.arange(n, dtype=np.int64)
+        blk.append(bt[bt_off[s] + t // block_size])
+        slot.append(t % block_size)
+    if not blk:
+        return np.zeros(0, np.int64), np.zeros(0, np.int64)
+    return np.concatenate(blk), np.concatenate(slot)
+
+
+def gather_paged(nodes, pool, block_table, block_size: int, bt_off=None) -> np.ndarray:
+    """Read a paged cache ``pool [num_blocks, Hkv, block_size, d]`` back into
+    packed token order ``[T, Hkv, d]`` (fp64)."""
+    blk, slot = paged_slots(nodes, block_table, block_size, bt_off)
+    try:
+        import torch
+        if isinstance(pool, torch.Tensor):
+            bi = torch.as_tensor(blk, device=pool.device)
+            si = torch.as_tensor(slot, device=pool.device)
+            return pool[bi, :, si, :].to("cpu", torch.float64).numpy()
+    except ImportError:  # pragma: no cover
+        pass
+    return _f64(pool)[blk, :, slot, :]
+
+
+def tree_attention_paged(nodes, q, k_pool, v_pool, block_table, scale: float,
+                         num_heads_q: int, num_heads_kv: int, block_size: int = 16,
+                         bt_off=None, q_off=None, rows=None):
+    """Decode form: K/V in a paged cache.  Gathers every segment back into
+    packed order with :func:`gather_paged`, then applies
+    :func:`tree_attention`."""
+    nodes = _as_nodes(nodes)
+    k = gather_paged(nodes, k_pool, block_table, block_size, bt_off)
+    v = gather_paged(nodes, v_pool, block_table, block_size, bt_off)
+    kv_off, qo = canonical_layout(nodes, 0)
+    return tree_attention(nodes, q, k, v, scale, num_heads_q, num_heads_kv,
+                          kv_off=kv_off, q_off=qo if q_off is None else q_off, rows=rows)
+
+
+# --------------------------------------------------------------------------
+# Algorithm "Masked parallel decoding" (App. E), logical fused form
+# --------------------------------------------------------------------------
+
+def simulate_masked_parallel_decoding(prefix_len: int, decide, max_steps: int = 64):
+    """Replay the logical fused mask of masked parallel decoding.
+
+    ``decide(step, stream_id, is_layout)`` returns the event after a stream's
+    decode at ``step``: ``"continue"``, ``"eos"`` (retire), or for the layout
+    stream also ``"fork"`` (its output closes a region).  Stream 0 is the
+    layout stream; content streams get ids 1, 2, ... in creation order.
+
+    Mask semantics (App. E): after prefilling X the layout row sees X; each
+    step appends one input per live stream with an identity block
+    (``M <- [M I_C]``), then decodes every live stream with its row; on a
+    region close the layout row as it stands (before the boundary output is
+    appended) is copied into a new content stream's row; retired rows are
+    removed.
+
+    Returns ``(tags, queries, forks)``: ``tags[l] = (stream, index)`` for each
+    cache position (stream -1 = prefix), ``queries`` = list of ``(stream,
+    index, row)`` with the Boolean mask row used for the query that the stream
+    appended at that step, and ``forks[c]`` = number of layout-stream tokens
+    cached when content stream c was created."""
+    tags: List[Tuple[int, int]] = [(-1, i) for i in range(prefix_len)]
+    rows: Dict[int, np.ndarray] = {0: np.ones(prefix_len, dtype=bool)}
+    count: Dict[int, int] = {0: 0}
+    forks: Dict[int, int] = {}
+    queries = []
+    next_id = 1
+    for step in range(max_steps):
+        live = sorted(rows)
+        if not live:
+            break
+        # append one input per live stream: M <- [M I_C]
+        L = len(tags)
+        for c in live:
+            tags.append((c, count[c]))
+        for c in live:
+            ext = np.zeros(len(live), dtype=bool)
+            ext[live.index(c)] = True
+            rows[c] = np.concatenate([rows[c], ext])
+        # decode: every live stream's new token is queried with its row
+        for c in live:
+            queries.append((c, count[c], rows[c].copy()))
+            count[c] += 1
+        # events
+        for c in live:
+            ev = decide(step, c, c == 0)
+            if c == 0 and ev == "fork":
+                cid = next_id
+                next_id += 1
+                rows[cid] = rows[0].copy()          # pre-boundary layout row
+                count[cid] = 0
+                forks[cid] = count[0]
+            elif ev == "eos":
+                del rows[c]
+        # rows of all streams cover the whole cache
+        for c in rows:
+            assert rows[c].size == len(tags)
+        del L
+    return tags, queries, forks
