@@ -170,30 +170,6 @@ def dense_mask(nodes, root: int) -> Tuple[np.ndarray, np.ndarray, np.ndarray]:
     return seg, pos, mask
 
 
-def _dense_mask_fast(nodes, root: int):
-    """Same mask as :func:`dense_mask`, built segment block by segment block
-    (used for pages too large for the per-element loop; tests check that the
-    two agree)."""
-    nodes = _as_nodes(nodes)
-    roots = page_of(nodes)
-    segs = [i for i in range(len(nodes)) if roots[i] == root]
-    starts, total = {}, 0
-    for i in segs:
-        starts[i] = total
-        total += nodes[i][2]
-    mask = np.zeros((total, total), dtype=bool)
-    for s in segs:
-        ns = nodes[s][2]
-        r0 = starts[s]
-        mask[r0:r0 + ns, r0:r0 + ns] = np.tril(np.ones((ns, ns), dtype=bool))
-        for t, f in ancestors(nodes, s):
-            c0 = starts[t]
-            mask[r0:r0 + ns, c0:c0 + f] = True
-    seg = np.concatenate([np.full(nodes[i][2], i, dtype=np.int64) for i in segs]) if segs else np.zeros(0, np.int64)
-    pos = np.concatenate([np.arange(nodes[i][2], dtype=np.int64) for i in segs]) if segs else np.zeros(0, np.int64)
-    return seg, pos, mask
-
-
 def visible_pair_count(nodes) -> int:
     """Number of visible (query, key) pairs, queries = last q_len tokens."""
     nodes = _as_nodes(nodes)
@@ -261,28 +237,39 @@ def tree_attention(nodes, q, k, v, scale: float, num_heads_q: int, num_heads_kv:
     want = None if rows is None else set(int(r) for r in rows)
     roots = page_of(nodes)
     for root in sorted(set(int(r) for r in roots)):
-        seg, pos, mask = _dense_mask_fast(nodes, root)
-        kv_rows = np.array([kv_off[s] + p for s, p in zip(seg, pos)], dtype=np.int64)
-        # query tokens of this page: (index into page tokens, Q row)
-        qa, qr = [], []
-        for a, (s, p) in enumerate(zip(seg, pos)):
+        segs = [i for i in range(len(nodes)) if roots[i] == root]
+        starts, total = {}, 0
+        for i in segs:
+            starts[i] = total
+            total += nodes[i][2]
+        kv_rows = np.concatenate([kv_off[i] + np.arange(nodes[i][2], dtype=np.int64) for i in segs]) \
+            if total else np.zeros(0, np.int64)
+        # query tokens of this page, in packed order: (segment, position, Q row)
+        qs, qp, qr = [], [], []
+        for s in segs:
             n, ql = nodes[s][2], nodes[s][3]
-            if p >= n - ql:
+            for p in range(n - ql, n):
                 r = int(q_off[s] + p - (n - ql))
                 if want is None or r in want:
-                    qa.append(a)
+                    qs.append(s)
+                    qp.append(p)
                     qr.append(r)
-        if not qa:
+        if not qr:
             continue
-        qa = np.array(qa)
         qr = np.array(qr)
+        # mask rows of the query tokens, straight from the visibility rule
+        mask = np.zeros((len(qr), total), dtype=bool)
+        for a, (s, p) in enumerate(zip(qs, qp)):
+            mask[a, starts[s]: starts[s] + p + 1] = True
+            for t, f in ancestors(nodes, s):
+                mask[a, starts[t]: starts[t] + f] = True
         for h in range(num_heads_q):
             g = h // G
             kh = k64[kv_rows, g, :]
             vh = v64[kv_rows, g, :]
-            for b0 in range(0, qa.size, row_batch):
+            for b0 in range(0, qr.size, row_batch):
                 sel = slice(b0, b0 + row_batch)
-                res = masked_attention(q64[qr[sel], h, :], kh, vh, mask[qa[sel]], scale,
+                res = masked_attention(q64[qr[sel], h, :], kh, vh, mask[sel], scale,
                                        return_probs=return_probs)
                 O[qr[sel], h, :] = res[0]
                 LSE[qr[sel], h] = res[1]

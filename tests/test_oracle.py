@@ -75,14 +75,24 @@ def test_tiny_page_structure_matches_hand_derivation():
     assert gold["causal_pairs_same_length"] == 448 * 449 // 2
 
 
-def test_fast_mask_equals_elementwise_mask():
+def test_attention_mask_rows_equal_elementwise_mask():
+    """The mask rows tree_attention builds (segment slices) equal the
+    element-by-element rule of dense_mask: one-hot V exposes the support."""
     for seed in range(30):
-        nodes = [tuple(n) for n in ((a.parent, a.fork, a.length, a.q_len) for a in syn.random_tree(seed, n_pages=2))]
-        for root in set(ot.page_of(nodes)):
-            a = ot.dense_mask(nodes, int(root))
-            b = ot._dense_mask_fast(nodes, int(root))
-            for x, y in zip(a, b):
-                np.testing.assert_array_equal(x, y)
+        nodes = [(a.parent, a.fork, a.length, a.length) for a in syn.random_tree(seed, n_pages=2)]
+        T = sum(n[2] for n in nodes)
+        q = _rand((T, 1, 3), seed)
+        k = _rand((T, 1, 3), seed + 1)
+        O, _ = oracle.tree_attention(nodes, q, k, np.eye(T)[:, None, :], 0.5, 1, 1)
+        support = O[:, 0, :] > 0
+        roots = ot.page_of(nodes)
+        kv_off, _ = ot.canonical_layout(nodes, 0)
+        for root in set(int(r) for r in roots):
+            seg, pos, mask = ot.dense_mask(nodes, root)
+            rows = np.array([kv_off[s] + p for s, p in zip(seg, pos)])
+            np.testing.assert_array_equal(support[np.ix_(rows, rows)], mask)
+            others = np.setdiff1d(np.arange(T), rows)
+            assert not support[np.ix_(rows, others)].any()
 
 
 def test_closed_form_visible_counts_for_page_trees():
