@@ -1,0 +1,219 @@
+/*
+ * libpadoc_attn -- ancestor-masked attention over a packed token tree
+ * (PaDoc, "Layout-Grounded Parallel Decoding for Document Parsing").
+ *
+ * The operation (Sec. 3.2 ancestor sets; App. C "Attention Backends"; App. E
+ * masked parallel decoding and its Attn equation):
+ *
+ *   A page is a tree of segments.  The root is the page prefix X (image and
+ *   prompt tokens); the layout stream is its child; content branches Y_k are
+ *   children of the stream.  A query token at position p of segment s attends
+ *   to every key at position j of segment t such that
+ *       t == s and j <= p                      (causal inside its own node), or
+ *       t is a proper ancestor of s and j < F   (F = fork offset of the child
+ *                                                of t on the path to s),
+ *   and computes O = softmax(scale * q K^T) V over exactly those keys and
+ *   LSE = ln(sum over those keys of exp(scale * q.k)).  Pages never see each
+ *   other.  The descriptor allows trees of any depth (parent index < own).
+ *
+ * Two entry points:
+ *   padoc_tree_attn_fwd  -- packed variable-length forward: K/V of all tokens
+ *                           in packed order (the training / branch-creation
+ *                           form, App. C tree-varlen relation
+ *                           Q_M -> K_M, Q_{Y_k} -> [K_{M<=f_k}; K_{Y_k}]).
+ *   padoc_branch_decode  -- one step of masked parallel decoding (App. E,
+ *                           algorithm steps "append" then "decode") over a
+ *                           paged KV cache: every live stream's newest
+ *                           q_len tokens query their ancestors + own history;
+ *                           keys shared by sibling streams are read once.
+ *
+ * Layouts (row-major, head dimension innermost, everything contiguous):
+ *   Q, O     [n_q_rows, Hq, d]        segment s's queries = its LAST q_len
+ *                                     tokens, at rows q_off .. q_off+q_len-1
+ *   K, V     packed: [num_kv_rows, Hkv, d], segment s's token j at row kv_off+j
+ *            paged:  [num_blocks, Hkv, 16, d], segment s's token j in block
+ *                    block_table[kv_off + j/16], slot j%16
+ *   LSE      float32 [n_q_rows, Hq], natural log
+ *   GQA      query head h reads KV head h / (Hq/Hkv)
+ *   dtype    Q, K, V and O share one dtype (bf16 or fp32); accumulation is
+ *            fp32; O is rounded to nearest-even.
+ *
+ * Ownership: the caller owns every buffer.  The library never allocates
+ * device memory: it reports a workspace size and the caller passes a device
+ * buffer of at least that size to each launch.  A plan owns host memory only,
+ * is immutable after creation and may be reused for any number of launches
+ * with the same tree; destroy it only after the stream has passed the last
+ * launch that used it.
+ *
+ * Errors: every call returns a padoc_status and never throws.  All tree and
+ * shape validation happens in padoc_plan_create; launches check pointers and
+ * workspace size first.  On any error nothing is enqueued and
+ * padoc_last_error() (thread-local) describes the cause.  Launches are
+ * asynchronous on the caller's stream; a device fault surfaces at the
+ * caller's next synchronisation.  Two launches that share a workspace must be
+ * ordered (same stream or explicit events).
+ */
+#ifndef PADOC_ATTN_H
+#define PADOC_ATTN_H
+
+#include <stddef.h>
+#include <stdint.h>
+#include <hip/hip_runtime_api.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+  PADOC_OK = 0,
+  PADOC_ERR_ARG = -1,        /* null pointer, bad enum value, negative count    */
+  PADOC_ERR_TREE = -2,       /* parent / fork / len / q_len inconsistent        */
+  PADOC_ERR_SHAPE = -3,      /* heads or head_dim unsupported                   */
+  PADOC_ERR_DTYPE = -4,      /* dtype unsupported                               */
+  PADOC_ERR_BOUNDS = -5,     /* offsets outside the buffers, overlapping query
+                                rows, block id outside the pool                 */
+  PADOC_ERR_WORKSPACE = -6,  /* workspace null or too small                     */
+  PADOC_ERR_HIP = -7,        /* a HIP call failed (message has the HIP error)   */
+  PADOC_ERR_MODE = -8        /* plan built for the other entry point            */
+} padoc_status;
+
+typedef enum { PADOC_F32 = 0, PADOC_BF16 = 1 } padoc_dtype;
+
+/* One tree segment: a page prefix (root), a layout stream or a branch. */
+typedef struct {
+  int32_t parent;   /* -1 for a root (one page); else index < own index        */
+  int32_t fork;     /* leading parent tokens visible, 0..len(parent); roots: 0 */
+  int32_t len;      /* tokens (K/V rows) in this segment, including the query
+                       tokens of a decode step (their K/V is already written)  */
+  int32_t q_len;    /* queries = the last q_len tokens, 0..len                 */
+  int64_t kv_off;   /* packed: first K/V row; paged: first block-table entry   */
+  int64_t q_off;    /* first Q/O/LSE row of this segment's queries             */
+} padoc_segment;
+
+/* A document page as the paper's packed sample [prefix | stream | Y_1..Y_N]
+   (App. C): the stream sees the whole prefix, branch k sees the first
+   branch_fork[k] stream tokens (its branch-start token is its own position
+   0, Sec. 3.2).  Arrays have n_branches entries and are read only during the
+   call. */
+typedef struct {
+  int32_t prefix_len, prefix_q_len;
+  int32_t stream_len, stream_q_len;
+  int32_t n_branches;
+  const int32_t* branch_fork;
+  const int32_t* branch_len;
+  const int32_t* branch_q_len;
+} padoc_page;
+
+typedef struct {
+  int32_t n_seg;
+  const padoc_segment* seg;      /* host memory, read during padoc_plan_create  */
+  int32_t num_heads_q;           /* Hq > 0                                      */
+  int32_t num_heads_kv;          /* Hkv > 0, Hq % Hkv == 0, Hq/Hkv <= 64        */
+  int32_t head_dim;              /* 64 or 128                                   */
+  float softmax_scale;           /* > 0, finite; the paper uses 1/sqrt(d)       */
+  padoc_dtype dtype;
+  int32_t block_size;            /* 0: packed K/V (forward); 16: paged (decode) */
+  int64_t num_kv_rows;           /* packed: rows of K/V; paged: blocks in pool  */
+  int64_t num_q_rows;            /* rows of Q/O/LSE                             */
+  const int32_t* block_table_host; /* paged, optional: host copy of the table,
+                                    used only to check ids are in the pool     */
+  int64_t block_table_len;       /* paged: entries in the block table           */
+  int32_t max_chunk_keys;        /* decode: split keys into chunks of at most
+                                    this many (multiple of 64); 0 = automatic */
+  int32_t target_workgroups;     /* decode: aim for about this many work items
+                                    when choosing chunks; 0 = 512              */
+} padoc_tree_desc;
+
+typedef struct padoc_plan padoc_plan;
+
+/* Schedule export (tests and tools).  Pointers stay valid until the plan is
+   destroyed.  A work item processes, for one KV head, the queries
+   toks[tok_begin .. tok_begin+ntok) (Q row indices; column c of the item is
+   token c/G, head c%G) against the key ranges ranges[rng_begin ..
+   rng_begin+rng_count).  Token i of the item sees keys [0, lim) of a range
+   where lim = n_keys if lim_off < 0, else lims[lim_off + i]; every token sees
+   at least [0, min_lim).  Key j of a range is K/V row kv_start + j (packed) or
+   block_table[kv_start + j/16] slot j%16 (paged); seg and key_begin name the
+   segment and the first key of it the range starts at.  For range r,
+   tile_class[tile_class_off[r] + kt] is 1 (full: every token sees all
+   tile_keys keys, no mask) or 2 (partial: masked) for each key tile kt below
+   ceil(n_keys / tile_keys); tiles past n_keys are never visited.  Work items
+   of different KV heads share token and range records.  Decode
+   plans write one partial result per (item, column) at slot out_base + column
+   and combine, for Q row r and KV head g, the slots comb_slot[comb_ptr[r*Hkv+g]
+   .. comb_ptr[r*Hkv+g+1]) (+ head within group) in that order. */
+typedef struct {
+  int32_t tok_begin, ntok, rng_begin, rng_count, kvh, out_base, cost, reserved;
+} padoc_work_view;
+
+typedef struct {
+  int64_t kv_start;
+  int32_t n_keys, min_lim, lim_off, seg, key_begin, reserved;
+} padoc_range_view;
+
+typedef struct {
+  int32_t kind;                  /* 0 = forward (final O), 1 = decode (partials) */
+  int32_t tile_cols, tile_keys;  /* columns per work item, keys per key tile     */
+  int32_t n_work;  const padoc_work_view* work;
+  int32_t n_range; const padoc_range_view* ranges;
+  int32_t n_lim;   const int32_t* lims;
+  int32_t n_tok;   const int32_t* toks;
+  int64_t n_tile_class; const int8_t* tile_class; const int64_t* tile_class_off;
+  int64_t n_comb_ptr; const int32_t* comb_ptr;
+  int64_t n_comb;     const int32_t* comb_slot;
+  int64_t n_slots;
+  size_t workspace_bytes;
+} padoc_schedule_view;
+
+/* Lay out a list of pages as segments in packed order (A1 of the hot path):
+   per page [prefix, stream, branch 1..N]; kv_off/q_off are filled as running
+   sums (packed rows when block_size == 0, block-table entries of
+   ceil(len/block_size) when block_size > 0).  Writes at most `capacity`
+   segments; *n_out receives the number needed (also when it exceeds
+   capacity, which returns PADOC_ERR_ARG). */
+padoc_status padoc_tree_from_pages(const padoc_page* pages, int32_t n_pages, int32_t block_size,
+                                   padoc_segment* out, int32_t capacity, int32_t* n_out);
+
+/* Fill kv_off / q_off of n segments in place with the canonical packed
+   layout (node order, running sums as above).  parent/fork/len/q_len are
+   read, not checked (padoc_plan_create checks them). */
+padoc_status padoc_tree_layout(padoc_segment* seg, int32_t n, int32_t block_size);
+
+/* Validate the tree and build the schedule (host only; no HIP call). */
+padoc_status padoc_plan_create(const padoc_tree_desc* desc, padoc_plan** out);
+padoc_status padoc_plan_workspace_bytes(const padoc_plan* plan, size_t* bytes);
+padoc_status padoc_plan_export(const padoc_plan* plan, padoc_schedule_view* out);
+void padoc_plan_destroy(padoc_plan* plan);
+
+/* Packed forward.  Needs a plan with block_size == 0.  q/k/v/o are device
+   pointers in the plan's dtype, lse a device float pointer; workspace a
+   device buffer of at least padoc_plan_workspace_bytes; stream may be NULL
+   (the null stream). */
+padoc_status padoc_tree_attn_fwd(const padoc_plan* plan, const void* q, const void* k,
+                                 const void* v, void* o, float* lse, void* workspace,
+                                 size_t workspace_bytes, hipStream_t stream);
+
+/* Decode step over a paged cache.  Needs a plan with block_size == 16.
+   block_table is the device copy of the table the plan was built for
+   (block_table_len int32 entries, every id < num_kv_rows). */
+padoc_status padoc_branch_decode(const padoc_plan* plan, const void* q, const void* k_cache,
+                                 const void* v_cache, const int32_t* block_table, void* o,
+                                 float* lse, void* workspace, size_t workspace_bytes,
+                                 hipStream_t stream);
+
+/* Thread-local description of the last error on this thread ("" if none). */
+const char* padoc_last_error(void);
+
+/* Profiling hook (thread-local): when both events are non-null, the next
+   launches on this thread record `before` just before and `after` just after
+   their dominant kernel (the tile kernel), on the launch stream.  Pass nulls
+   to stop. */
+padoc_status padoc_set_kernel_events(hipEvent_t before, hipEvent_t after);
+
+/* Library version string. */
+const char* padoc_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* PADOC_ATTN_H */

@@ -1,0 +1,233 @@
+"""PaDoc tree attention on MI355X: thin Python binding of ``libpadoc_attn``.
+
+Every step of the computation runs in the HIP library; this module only
+marshals arguments.  PyTorch provides device memory and the current stream.
+
+    segs = segments_from_pages(pages, block_size=0)        # tree -> segments
+    plan = TreePlan(segs, Hq, Hkv, d, "bf16", block_size=0,
+                    num_kv_rows=T, num_q_rows=n_q)
+    o, lse = tree_attn_fwd(q, k, v, plan)                    # packed forward
+    o, lse = branch_decode(q, k_cache, v_cache, bt, plan)    # paged decode step
+"""
+from __future__ import annotations
+
+import ctypes as C
+import math
+from typing import Optional, Sequence
+
+import numpy as np
+
+from . import _lib
+from ._lib import PadocError, SEGMENT_DTYPE, WORK_DTYPE, RANGE_DTYPE
+
+__all__ = ["TreePlan", "segments_from_pages", "segments_layout", "tree_attn_fwd", "branch_decode",
+           "PadocError", "SEGMENT_DTYPE", "version", "set_kernel_events", "make_workspace"]
+
+_DTYPES = {"f32": _lib.F32, "fp32": _lib.F32, "float32": _lib.F32, "bf16": _lib.BF16, "bfloat16": _lib.BF16}
+
+
+def version() -> str:
+    return _lib.lib().padoc_version().decode()
+
+
+def _page_struct(pg, keep):
+    get = (lambda k: pg[k]) if isinstance(pg, dict) else (lambda k: getattr(pg, k))
+    br = list(get("branches"))
+    bget = lambda b, k: b[k] if isinstance(b, dict) else getattr(b, k)
+    f = np.ascontiguousarray([bget(b, "fork") for b in br], dtype=np.int32)
+    ln = np.ascontiguousarray([bget(b, "length") for b in br], dtype=np.int32)
+    ql = np.ascontiguousarray([bget(b, "q_len") for b in br], dtype=np.int32)
+    keep.extend([f, ln, ql])
+    P = C.POINTER(C.c_int32)
+    return _lib.Page(int(get("prefix_len")), int(get("prefix_q")), int(get("stream_len")), int(get("stream_q")),
+                     len(br), f.ctypes.data_as(P), ln.ctypes.data_as(P), ql.ctypes.data_as(P))
+
+
+def segments_from_pages(pages: Sequence, block_size: int = 0) -> np.ndarray:
+    """Pages ``[prefix | stream | Y_1..Y_N]`` -> segment records in packed
+    order (``padoc_tree_from_pages``)."""
+    L = _lib.lib()
+    keep: list = []
+    arr = (_lib.Page * max(1, len(pages)))(*[_page_struct(p, keep) for p in pages])
+    n = C.c_int32(0)
+    L.padoc_tree_from_pages(arr, len(pages), block_size, None, 0, C.byref(n))
+    out = np.zeros(n.value, dtype=SEGMENT_DTYPE)
+    _lib.check(L.padoc_tree_from_pages(arr, len(pages), block_size, out.ctypes.data_as(C.c_void_p),
+                                       n.value, C.byref(n)))
+    return out
+
+
+def segments_layout(nodes, block_size: int = 0) -> np.ndarray:
+    """Generic nodes ``(parent, fork, len, q_len)`` -> segment records with the
+    canonical packed offsets (``padoc_tree_layout``)."""
+    out = np.zeros(len(nodes), dtype=SEGMENT_DTYPE)
+    for i, n in enumerate(nodes):
+        if isinstance(n, tuple):
+            out[i] = (n[0], n[1], n[2], n[3], 0, 0)
+        else:
+            out[i] = (n.parent, n.fork, n.length, n.q_len, 0, 0)
+    _lib.check(_lib.lib().padoc_tree_layout(out.ctypes.data_as(C.c_void_p), len(out), block_size))
+    return out
+
+
+class TreePlan:
+    """A validated tree and its schedule (``padoc_plan``)."""
+
+    def __init__(self, segments: np.ndarray, num_heads_q: int, num_heads_kv: int, head_dim: int,
+                 dtype: str = "bf16", block_size: int = 0, num_kv_rows: int = 0, num_q_rows: Optional[int] = None,
+                 softmax_scale: Optional[float] = None, block_table_host: Optional[np.ndarray] = None,
+                 block_table_len: Optional[int] = None, max_chunk_keys: int = 0, target_workgroups: int = 0):
+        segs = np.ascontiguousarray(segments, dtype=SEGMENT_DTYPE)
+        self.segments = segs
+        self.num_heads_q, self.num_heads_kv, self.head_dim = num_heads_q, num_heads_kv, head_dim
+        self.dtype = dtype
+        self.block_size = block_size
+        if num_q_rows is None:
+            num_q_rows = int((segs["q_off"] + segs["q_len"]).max()) if len(segs) else 0
+        self.num_q_rows = num_q_rows
+        self.softmax_scale = 1.0 / math.sqrt(head_dim) if softmax_scale is None else softmax_scale
+        bt = None
+        if block_table_host is not None:
+            bt = np.ascontiguousarray(block_table_host, dtype=np.int32)
+            if block_table_len is None:
+                block_table_len = bt.size
+        if block_table_len is None:
+            block_table_len = 0
+        self.block_table_len = block_table_len
+        desc = _lib.TreeDesc(len(segs), segs.ctypes.data if len(segs) else None, num_heads_q, num_heads_kv,
+                             head_dim, float(self.softmax_scale), _DTYPES[dtype], block_size, int(num_kv_rows),
+                             int(num_q_rows), bt.ctypes.data if bt is not None else None, int(block_table_len),
+                             int(max_chunk_keys), int(target_workgroups))
+        h = C.c_void_p()
+        L = _lib.lib()
+        _lib.check(L.padoc_plan_create(C.byref(desc), C.byref(h)))
+        self._h = h
+        sz = C.c_size_t(0)
+        _lib.check(L.padoc_plan_workspace_bytes(h, C.byref(sz)))
+        self.workspace_bytes = sz.value
+        self._ws = None
+
+    @property
+    def handle(self):
+        if self._h is None:
+            raise ValueError("plan is closed")
+        return self._h
+
+    def close(self):
+        if getattr(self, "_h", None) is not None:
+            _lib.lib().padoc_plan_destroy(self._h)
+            self._h = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+    def export(self) -> dict:
+        """Schedule as numpy arrays (copies)."""
+        v = _lib.ScheduleView()
+        _lib.check(_lib.lib().padoc_plan_export(self.handle, C.byref(v)))
+
+        def arr(ptr, n, dt):
+            if n == 0 or not ptr:
+                return np.zeros(0, dtype=dt)
+            buf = (C.c_char * (n * np.dtype(dt).itemsize)).from_address(ptr)
+            return np.frombuffer(buf, dtype=dt).copy()
+
+        return {
+            "kind": v.kind, "tile_cols": v.tile_cols, "tile_keys": v.tile_keys,
+            "work": arr(v.work, v.n_work, WORK_DTYPE), "ranges": arr(v.ranges, v.n_range, RANGE_DTYPE),
+            "lims": arr(v.lims, v.n_lim, np.int32), "toks": arr(v.toks, v.n_tok, np.int32),
+            "tile_class": arr(v.tile_class, v.n_tile_class, np.int8),
+            "tile_class_off": arr(v.tile_class_off, v.n_range, np.int64),
+            "comb_ptr": arr(v.comb_ptr, v.n_comb_ptr, np.int32), "comb_slot": arr(v.comb_slot, v.n_comb, np.int32),
+            "n_slots": v.n_slots, "workspace_bytes": v.workspace_bytes,
+        }
+
+    def workspace(self, device):
+        """A cached device workspace of the plan's size (256-byte aligned)."""
+        import torch
+        if self._ws is None or self._ws[0] != torch.device(device):
+            raw = torch.empty(self.workspace_bytes + 256, dtype=torch.uint8, device=device)
+            off = (-raw.data_ptr()) % 256
+            self._ws = (torch.device(device), raw, raw[off: off + self.workspace_bytes])
+        return self._ws[2]
+
+
+def make_workspace(plan: TreePlan, device):
+    return plan.workspace(device)
+
+
+def _ptr(t):
+    return C.c_void_p(t.data_ptr())
+
+
+def _check_tensor(name, t, dtype, device):
+    import torch
+    if not isinstance(t, torch.Tensor):
+        raise TypeError(f"{name} must be a torch tensor")
+    if t.device != device:
+        raise ValueError(f"{name} is on {t.device}, expected {device}")
+    if t.dtype != dtype:
+        raise TypeError(f"{name} has dtype {t.dtype}, expected {dtype}")
+    if not t.is_contiguous():
+        raise ValueError(f"{name} must be contiguous")
+
+
+def _torch_dtype(plan):
+    import torch
+    return torch.bfloat16 if _DTYPES[plan.dtype] == _lib.BF16 else torch.float32
+
+
+def _outputs(plan, q, out, lse):
+    import torch
+    if out is None:
+        out = torch.empty(plan.num_q_rows, plan.num_heads_q, plan.head_dim, dtype=q.dtype, device=q.device)
+    if lse is None:
+        lse = torch.empty(plan.num_q_rows, plan.num_heads_q, dtype=torch.float32, device=q.device)
+    return out, lse
+
+
+def tree_attn_fwd(q, k, v, plan: TreePlan, out=None, lse=None, workspace=None, stream=None):
+    """Packed forward (``padoc_tree_attn_fwd``).  q ``[n_q, Hq, d]``; k, v
+    ``[T, Hkv, d]``; returns ``(O [n_q, Hq, d], LSE [n_q, Hq] float32)``."""
+    import torch
+    dt = _torch_dtype(plan)
+    dev = q.device
+    for name, t in (("q", q), ("k", k), ("v", v)):
+        _check_tensor(name, t, dt, dev)
+    out, lse = _outputs(plan, q, out, lse)
+    ws = plan.workspace(dev) if workspace is None else workspace
+    s = torch.cuda.current_stream(dev) if stream is None else stream
+    _lib.check(_lib.lib().padoc_tree_attn_fwd(plan.handle, _ptr(q), _ptr(k), _ptr(v), _ptr(out), _ptr(lse),
+                                              _ptr(ws), ws.numel(), C.c_void_p(s.cuda_stream)))
+    return out, lse
+
+
+def branch_decode(q, k_cache, v_cache, block_table, plan: TreePlan, out=None, lse=None, workspace=None,
+                  stream=None):
+    """Decode step over a paged cache (``padoc_branch_decode``).  q ``[n_q,
+    Hq, d]``; caches ``[blocks, Hkv, 16, d]``; block_table int32 on the
+    device; returns ``(O, LSE)``."""
+    import torch
+    dt = _torch_dtype(plan)
+    dev = q.device
+    for name, t in (("q", q), ("k_cache", k_cache), ("v_cache", v_cache)):
+        _check_tensor(name, t, dt, dev)
+    _check_tensor("block_table", block_table, torch.int32, dev)
+    out, lse = _outputs(plan, q, out, lse)
+    ws = plan.workspace(dev) if workspace is None else workspace
+    s = torch.cuda.current_stream(dev) if stream is None else stream
+    _lib.check(_lib.lib().padoc_branch_decode(plan.handle, _ptr(q), _ptr(k_cache), _ptr(v_cache), _ptr(block_table),
+                                              _ptr(out), _ptr(lse), _ptr(ws), ws.numel(),
+                                              C.c_void_p(s.cuda_stream)))
+    return out, lse
+
+
+def set_kernel_events(before=None, after=None):
+    """Record torch CUDA events around the tile kernel of later launches on
+    this thread (``padoc_set_kernel_events``); call with no arguments to stop."""
+    b = C.c_void_p(before.cuda_event) if before is not None else None
+    a = C.c_void_p(after.cuda_event) if after is not None else None
+    _lib.check(_lib.lib().padoc_set_kernel_events(b, a))

@@ -1,0 +1,132 @@
+// C entry points that launch work: argument checks, schedule upload into the
+// caller's workspace, and the kernel launches on the caller's stream.
+#include <hip/hip_runtime.h>
+
+#include "host/plan.hpp"
+
+namespace padoc {
+hipError_t launch_tile_mfma_bf16(const TileParams& p, int n_work, int D, bool paged, bool partial, hipStream_t s);
+hipError_t launch_tile_valu_f32(const TileParams& p, int n_work, int D, bool paged, bool partial, hipStream_t s);
+hipError_t launch_lse_combine(const CombineParams& p, int D, bool bf16, hipStream_t s);
+
+namespace {
+thread_local hipEvent_t t_ev_before = nullptr;
+thread_local hipEvent_t t_ev_after = nullptr;
+
+padoc_status hip_fail(const char* what, hipError_t e) {
+  return set_error(PADOC_ERR_HIP, "%s failed: %s (%d)", what, hipGetErrorString(e), (int)e);
+}
+
+template <class T>
+const T* at(void* ws, size_t off) {
+  return reinterpret_cast<const T*>(static_cast<char*>(ws) + off);
+}
+
+padoc_status check_common(const padoc_plan* P, const void* q, const void* k, const void* v, const void* o,
+                          const float* lse, void* ws, size_t ws_bytes) {
+  if (!P) return set_error(PADOC_ERR_ARG, "plan is null");
+  if (!P->work.empty()) {
+    if (!q || !k || !v || !o || !lse) return set_error(PADOC_ERR_ARG, "a tensor pointer is null");
+    if (((uintptr_t)q | (uintptr_t)k | (uintptr_t)v | (uintptr_t)o) & 15)
+      return set_error(PADOC_ERR_ARG, "q, k, v and o must be 16-byte aligned");
+    if (((uintptr_t)lse) & 3) return set_error(PADOC_ERR_ARG, "lse must be 4-byte aligned");
+  }
+  if (!ws) return set_error(PADOC_ERR_WORKSPACE, "workspace is null");
+  if (((uintptr_t)ws) & 255) return set_error(PADOC_ERR_WORKSPACE, "workspace must be 256-byte aligned");
+  if (ws_bytes < P->ws_bytes)
+    return set_error(PADOC_ERR_WORKSPACE, "workspace of %zu bytes is smaller than the %zu the plan needs", ws_bytes,
+                     P->ws_bytes);
+  return PADOC_OK;
+}
+
+padoc_status run(const padoc_plan* P, const void* q, const void* k, const void* v, const int32_t* bt, void* o,
+                 float* lse, void* ws, hipStream_t stream) {
+  if (P->work.empty()) return PADOC_OK;
+  hipError_t e = hipMemcpyAsync(ws, P->blob.data(), P->blob.size(), hipMemcpyHostToDevice, stream);
+  if (e != hipSuccess) return hip_fail("hipMemcpyAsync(schedule)", e);
+  TileParams tp{};
+  tp.q = q;
+  tp.k = k;
+  tp.v = v;
+  tp.o = o;
+  tp.lse = lse;
+  tp.block_table = bt;
+  tp.work = at<WorkRec>(ws, P->off_work);
+  tp.ranges = at<RangeRec>(ws, P->off_ranges);
+  tp.lims = at<int32_t>(ws, P->off_lims);
+  tp.toks = at<int32_t>(ws, P->off_toks);
+  tp.part_o = reinterpret_cast<float*>(static_cast<char*>(ws) + P->off_part_o);
+  tp.part_ml = reinterpret_cast<float*>(static_cast<char*>(ws) + P->off_part_ml);
+  tp.Hq = P->Hq;
+  tp.Hkv = P->Hkv;
+  tp.G = P->G;
+  tp.scale_log2 = P->scale * 1.4426950408889634f;
+  const bool paged = P->block_size != 0;
+  const bool partial = P->kind == 1;
+  const int n_work = (int)P->work.size();
+  if (t_ev_before && t_ev_after) {
+    e = hipEventRecord(t_ev_before, stream);
+    if (e != hipSuccess) return hip_fail("hipEventRecord", e);
+  }
+  e = P->dtype == PADOC_BF16 ? launch_tile_mfma_bf16(tp, n_work, P->D, paged, partial, stream)
+                             : launch_tile_valu_f32(tp, n_work, P->D, paged, partial, stream);
+  if (e != hipSuccess) return hip_fail("tile kernel launch", e);
+  if (t_ev_before && t_ev_after) {
+    e = hipEventRecord(t_ev_after, stream);
+    if (e != hipSuccess) return hip_fail("hipEventRecord", e);
+  }
+  if (partial) {
+    CombineParams cp{};
+    cp.comb_ptr = at<int32_t>(ws, P->off_comb_ptr);
+    cp.comb_slot = at<int32_t>(ws, P->off_comb_slot);
+    cp.part_o = tp.part_o;
+    cp.part_ml = tp.part_ml;
+    cp.o = o;
+    cp.lse = lse;
+    cp.n_q = P->num_q_rows;
+    cp.Hq = P->Hq;
+    cp.Hkv = P->Hkv;
+    cp.G = P->G;
+    e = launch_lse_combine(cp, P->D, P->dtype == PADOC_BF16, stream);
+    if (e != hipSuccess) return hip_fail("combine kernel launch", e);
+  }
+  return PADOC_OK;
+}
+}  // namespace
+}  // namespace padoc
+
+using namespace padoc;
+
+extern "C" padoc_status padoc_tree_attn_fwd(const padoc_plan* plan, const void* q, const void* k, const void* v,
+                                            void* o, float* lse, void* workspace, size_t workspace_bytes,
+                                            hipStream_t stream) {
+  clear_error();
+  padoc_status st = check_common(plan, q, k, v, o, lse, workspace, workspace_bytes);
+  if (st != PADOC_OK) return st;
+  if (plan->kind != 0)
+    return set_error(PADOC_ERR_MODE, "plan was built for paged K/V (block_size 16); use padoc_branch_decode");
+  return run(plan, q, k, v, nullptr, o, lse, workspace, stream);
+}
+
+extern "C" padoc_status padoc_branch_decode(const padoc_plan* plan, const void* q, const void* k_cache,
+                                            const void* v_cache, const int32_t* block_table, void* o, float* lse,
+                                            void* workspace, size_t workspace_bytes, hipStream_t stream) {
+  clear_error();
+  padoc_status st = check_common(plan, q, k_cache, v_cache, o, lse, workspace, workspace_bytes);
+  if (st != PADOC_OK) return st;
+  if (plan->kind != 1)
+    return set_error(PADOC_ERR_MODE, "plan was built for packed K/V (block_size 0); use padoc_tree_attn_fwd");
+  if (!plan->work.empty() && !block_table) return set_error(PADOC_ERR_ARG, "block_table is null");
+  return run(plan, q, k_cache, v_cache, block_table, o, lse, workspace, stream);
+}
+
+extern "C" padoc_status padoc_set_kernel_events(hipEvent_t before, hipEvent_t after) {
+  clear_error();
+  if ((before == nullptr) != (after == nullptr))
+    return set_error(PADOC_ERR_ARG, "pass both events or neither");
+  t_ev_before = before;
+  t_ev_after = after;
+  return PADOC_OK;
+}
+
+extern "C" const char* padoc_version(void) { return "padoc_attn 0.1.0 (gfx950)"; }

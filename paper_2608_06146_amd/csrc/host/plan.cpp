@@ -1,0 +1,576 @@
+// Host planner: tree validation, ancestor closure and the tile / split-KV
+// schedules of the two entry points.  No HIP calls.
+//
+// Visibility (Sec. 3.2 ancestor sets; App. C tree-varlen relation): query
+// token p of segment s sees keys [0, F(s,t)) of every proper ancestor t
+// (F = fork offset of the child of t on the path to s) and keys [0, p] of s.
+// Every key range a work item visits is therefore a prefix [0, lim) of one
+// segment, with lim depending only on the query token; the schedule records,
+// per range, the largest and smallest lim over the item's tokens and (when
+// they differ) the per-token limits.  Key tiles below the smallest limit need
+// no mask; keys at or past the largest are never visited, and segments no
+// token of the item sees are never listed, so non-ancestor tiles are skipped
+// by construction (the block-skipping idea of App. C, "Flex Attention").
+#include "plan.hpp"
+
+#include <algorithm>
+#include <cmath>
+#include <cstdarg>
+#include <cstdio>
+#include <cstring>
+#include <limits>
+#include <map>
+#include <memory>
+#include <new>
+#include <utility>
+
+namespace padoc {
+
+namespace {
+thread_local std::string t_err;
+}
+
+padoc_status set_error(padoc_status st, const char* fmt, ...) {
+  char buf[768];
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(buf, sizeof(buf), fmt, ap);
+  va_end(ap);
+  t_err = buf;
+  return st;
+}
+
+void clear_error() { t_err.clear(); }
+const char* last_error() { return t_err.c_str(); }
+
+namespace {
+
+constexpr int64_t kI32Max = std::numeric_limits<int32_t>::max();
+
+int64_t ceil_div(int64_t a, int64_t b) { return (a + b - 1) / b; }
+int64_t round_up(int64_t a, int64_t b) { return ceil_div(a, b) * b; }
+size_t align256(size_t x) { return (x + 255) & ~size_t(255); }
+
+// A set of query tokens processed together (one work item per KV head and
+// key chunk).
+struct Task {
+  std::vector<int32_t> seg, pos;
+};
+
+// A visible segment of a task with each token's limit.
+struct VisRange {
+  int32_t t;
+  std::vector<int32_t> lim;
+  int32_t n_keys;  // max lim
+};
+
+// A key chunk [kb, kb+len) of one VisRange.
+struct Piece {
+  const VisRange* r;
+  int32_t kb, len;
+};
+
+class Builder {
+ public:
+  Builder(padoc_plan& p, const std::vector<std::vector<std::pair<int32_t, int32_t>>>& anc)
+      : P(p), anc_(anc) {}
+
+  // Segments visible to any token of `task` for which include(t) holds.
+  template <class Pred>
+  std::vector<VisRange> visible(const Task& task, Pred include) const {
+    const int32_t nt = (int32_t)task.seg.size();
+    std::map<int32_t, std::vector<int32_t>> per;
+    auto put = [&](int32_t t, int32_t i, int32_t lim) {
+      auto it = per.find(t);
+      if (it == per.end()) it = per.emplace(t, std::vector<int32_t>(nt, 0)).first;
+      it->second[i] = lim;
+    };
+    for (int32_t i = 0; i < nt; ++i) {
+      const int32_t s = task.seg[i], p = task.pos[i];
+      for (const auto& a : anc_[s])
+        if (a.second > 0 && include(a.first)) put(a.first, i, a.second);
+      if (include(s)) put(s, i, p + 1);
+    }
+    std::vector<VisRange> out;
+    for (auto& kv : per) {
+      VisRange r;
+      r.t = kv.first;
+      r.lim = std::move(kv.second);
+      r.n_keys = *std::max_element(r.lim.begin(), r.lim.end());
+      if (r.n_keys > 0) out.push_back(std::move(r));
+    }
+    return out;
+  }
+
+  int32_t add_tokens(const Task& task) {
+    const int32_t begin = (int32_t)P.toks.size();
+    for (size_t i = 0; i < task.seg.size(); ++i) {
+      const padoc_segment& s = P.seg[task.seg[i]];
+      const int32_t p = task.pos[i];
+      P.toks.push_back((int32_t)(s.q_off + (p - (s.len - s.q_len))));
+    }
+    return begin;
+  }
+
+  // Emit the range records of `pieces`; returns {rng_begin, rng_count, cost}
+  // and marks in `sees` the tokens that see at least one key.
+  void emit_ranges(const std::vector<Piece>& pieces, int32_t ntok, int32_t& rng_begin,
+                   int32_t& rng_count, int32_t& cost, std::vector<char>& sees) {
+    rng_begin = (int32_t)P.ranges.size();
+    rng_count = 0;
+    cost = 1;
+    sees.assign(ntok, 0);
+    std::vector<int32_t> l(ntok);
+    for (const Piece& pc : pieces) {
+      int32_t mx = 0, mn = std::numeric_limits<int32_t>::max();
+      for (int32_t i = 0; i < ntok; ++i) {
+        int32_t v = pc.r->lim[i] - pc.kb;
+        v = v < 0 ? 0 : (v > pc.len ? pc.len : v);
+        l[i] = v;
+        mx = std::max(mx, v);
+        mn = std::min(mn, v);
+        if (v > 0) sees[i] = 1;
+      }
+      if (mx == 0) continue;
+      const padoc_segment& t = P.seg[pc.r->t];
+      padoc::RangeRec rr{};
+      rr.kv_start = P.block_size ? t.kv_off + pc.kb / P.block_size : t.kv_off + pc.kb;
+      rr.n_keys = mx;
+      rr.min_lim = mn;
+      rr.seg = pc.r->t;
+      rr.key_begin = pc.kb;
+      if (mn == mx) {
+        rr.lim_off = -1;
+      } else {
+        rr.lim_off = (int32_t)P.lims.size();
+        P.lims.insert(P.lims.end(), l.begin(), l.end());
+      }
+      P.tile_class_off.push_back((int64_t)P.tile_class.size());
+      const int32_t nkt = (int32_t)ceil_div(mx, P.tile_keys);
+      for (int32_t kt = 0; kt < nkt; ++kt)
+        P.tile_class.push_back((int64_t)(kt + 1) * P.tile_keys <= mn ? 1 : 2);
+      P.ranges.push_back(rr);
+      ++rng_count;
+      cost += nkt;
+    }
+  }
+
+  padoc_plan& P;
+
+ private:
+  const std::vector<std::vector<std::pair<int32_t, int32_t>>>& anc_;
+};
+
+padoc_status validate(const padoc_tree_desc* d) {
+  if (d->n_seg < 0) return set_error(PADOC_ERR_ARG, "n_seg = %d is negative", d->n_seg);
+  if (d->n_seg > 0 && !d->seg) return set_error(PADOC_ERR_ARG, "seg is null with n_seg = %d", d->n_seg);
+  if (d->dtype != PADOC_F32 && d->dtype != PADOC_BF16)
+    return set_error(PADOC_ERR_DTYPE, "dtype %d is not PADOC_F32 or PADOC_BF16", (int)d->dtype);
+  if (d->num_heads_q <= 0 || d->num_heads_kv <= 0)
+    return set_error(PADOC_ERR_SHAPE, "head counts must be positive (Hq=%d, Hkv=%d)", d->num_heads_q,
+                     d->num_heads_kv);
+  if (d->num_heads_q % d->num_heads_kv != 0)
+    return set_error(PADOC_ERR_SHAPE, "Hq=%d is not a multiple of Hkv=%d", d->num_heads_q, d->num_heads_kv);
+  if (d->num_heads_q / d->num_heads_kv > 64)
+    return set_error(PADOC_ERR_SHAPE, "Hq/Hkv=%d exceeds 64", d->num_heads_q / d->num_heads_kv);
+  if (d->head_dim != 64 && d->head_dim != 128)
+    return set_error(PADOC_ERR_SHAPE, "head_dim=%d is not 64 or 128", d->head_dim);
+  if (!std::isfinite(d->softmax_scale) || !(d->softmax_scale > 0.f))
+    return set_error(PADOC_ERR_ARG, "softmax_scale must be positive and finite");
+  if (d->block_size != 0 && d->block_size != kBlock)
+    return set_error(PADOC_ERR_ARG, "block_size=%d is not 0 (packed) or 16 (paged)", d->block_size);
+  if (d->num_kv_rows < 0 || d->num_q_rows < 0 || d->block_table_len < 0)
+    return set_error(PADOC_ERR_ARG, "negative buffer size");
+  if (d->num_q_rows > kI32Max) return set_error(PADOC_ERR_BOUNDS, "num_q_rows exceeds 2^31-1");
+  if (d->max_chunk_keys < 0 || d->max_chunk_keys % kTileKeys != 0)
+    return set_error(PADOC_ERR_ARG, "max_chunk_keys=%d must be a non-negative multiple of %d",
+                     d->max_chunk_keys, kTileKeys);
+  if (d->target_workgroups < 0) return set_error(PADOC_ERR_ARG, "target_workgroups is negative");
+  const int32_t n = d->n_seg;
+  for (int32_t i = 0; i < n; ++i) {
+    const padoc_segment& s = d->seg[i];
+    if (s.parent < -1 || s.parent >= i)
+      return set_error(PADOC_ERR_TREE, "segment %d: parent %d is not -1 or an earlier segment", i, s.parent);
+    if (s.len < 0) return set_error(PADOC_ERR_TREE, "segment %d: len %d is negative", i, s.len);
+    if (s.q_len < 0 || s.q_len > s.len)
+      return set_error(PADOC_ERR_TREE, "segment %d: q_len %d outside [0, len=%d]", i, s.q_len, s.len);
+    if (s.parent < 0) {
+      if (s.fork != 0) return set_error(PADOC_ERR_TREE, "segment %d: a root must have fork 0 (got %d)", i, s.fork);
+    } else if (s.fork < 0 || s.fork > d->seg[s.parent].len) {
+      return set_error(PADOC_ERR_TREE, "segment %d: fork %d outside [0, len(parent %d)=%d]", i, s.fork,
+                       s.parent, d->seg[s.parent].len);
+    }
+    if (s.kv_off < 0) return set_error(PADOC_ERR_BOUNDS, "segment %d: kv_off %lld is negative", i, (long long)s.kv_off);
+    if (d->block_size == 0) {
+      if (s.kv_off + s.len > d->num_kv_rows)
+        return set_error(PADOC_ERR_BOUNDS, "segment %d: K/V rows [%lld, %lld) exceed num_kv_rows=%lld", i,
+                         (long long)s.kv_off, (long long)(s.kv_off + s.len), (long long)d->num_kv_rows);
+    } else {
+      const int64_t nb = ceil_div(s.len, d->block_size);
+      if (s.kv_off + nb > d->block_table_len)
+        return set_error(PADOC_ERR_BOUNDS, "segment %d: block-table entries [%lld, %lld) exceed block_table_len=%lld",
+                         i, (long long)s.kv_off, (long long)(s.kv_off + nb), (long long)d->block_table_len);
+      if (d->block_table_host) {
+        for (int64_t b = s.kv_off; b < s.kv_off + nb; ++b) {
+          const int32_t id = d->block_table_host[b];
+          if (id < 0 || id >= d->num_kv_rows)
+            return set_error(PADOC_ERR_BOUNDS, "segment %d: block_table[%lld]=%d outside the pool of %lld blocks",
+                             i, (long long)b, id, (long long)d->num_kv_rows);
+        }
+      }
+    }
+    if (s.q_off < 0 || s.q_off + s.q_len > d->num_q_rows)
+      return set_error(PADOC_ERR_BOUNDS, "segment %d: query rows [%lld, %lld) exceed num_q_rows=%lld", i,
+                       (long long)s.q_off, (long long)(s.q_off + s.q_len), (long long)d->num_q_rows);
+  }
+  // Query rows of different segments must not overlap (outputs would race).
+  std::vector<std::pair<int64_t, int32_t>> qr;
+  for (int32_t i = 0; i < n; ++i)
+    if (d->seg[i].q_len > 0) qr.push_back({d->seg[i].q_off, i});
+  std::sort(qr.begin(), qr.end());
+  for (size_t j = 1; j < qr.size(); ++j) {
+    const padoc_segment& a = d->seg[qr[j - 1].second];
+    if (a.q_off + a.q_len > qr[j].first)
+      return set_error(PADOC_ERR_BOUNDS, "query rows of segments %d and %d overlap", qr[j - 1].second, qr[j].second);
+  }
+  return PADOC_OK;
+}
+
+void build_forward(padoc_plan& P, Builder& B) {
+  // Tokens are packed into tasks of tile_tokens; consecutive siblings share
+  // tasks (their ancestor ranges coincide), a root starts its own.
+  const int32_t n = (int32_t)P.seg.size();
+  std::vector<Task> tasks;
+  Task cur;
+  int64_t group = std::numeric_limits<int64_t>::min();
+  auto flush = [&] {
+    if (!cur.seg.empty()) {
+      tasks.push_back(std::move(cur));
+      cur = Task();
+    }
+  };
+  for (int32_t s = 0; s < n; ++s) {
+    const padoc_segment& sg = P.seg[s];
+    if (sg.q_len == 0) continue;
+    const int64_t g = sg.parent >= 0 ? (int64_t)sg.parent : -(int64_t)s - 1;
+    if (g != group) {
+      flush();
+      group = g;
+    }
+    for (int32_t p = sg.len - sg.q_len; p < sg.len; ++p) {
+      cur.seg.push_back(s);
+      cur.pos.push_back(p);
+      if ((int32_t)cur.seg.size() == P.tile_tokens) flush();
+    }
+  }
+  flush();
+  std::vector<char> sees;
+  for (const Task& task : tasks) {
+    auto vis = B.visible(task, [](int32_t) { return true; });
+    std::vector<Piece> pieces;
+    for (const auto& r : vis) pieces.push_back({&r, 0, r.n_keys});
+    const int32_t ntok = (int32_t)task.seg.size();
+    const int32_t tok_begin = B.add_tokens(task);
+    int32_t rb, rc, cost;
+    B.emit_ranges(pieces, ntok, rb, rc, cost, sees);
+    for (int32_t g = 0; g < P.Hkv; ++g) {
+      padoc::WorkRec w{};
+      w.tok_begin = tok_begin;
+      w.ntok = ntok;
+      w.rng_begin = rb;
+      w.rng_count = rc;
+      w.kvh = g;
+      w.out_base = 0;
+      w.cost = cost;
+      P.work.push_back(w);
+    }
+  }
+}
+
+void build_decode(padoc_plan& P, Builder& B, const std::vector<std::vector<std::pair<int32_t, int32_t>>>& anc,
+                  const padoc_tree_desc* d) {
+  const int32_t n = (int32_t)P.seg.size();
+  const int32_t NT = P.tile_tokens;
+  // A segment is shared when a query token of another segment sees any of it.
+  std::vector<int64_t> viewers(n, 0);
+  for (int32_t s = 0; s < n; ++s)
+    if (P.seg[s].q_len > 0)
+      for (const auto& a : anc[s])
+        if (a.second > 0) viewers[a.first] += P.seg[s].q_len;
+  auto shared = [&](int32_t t) { return viewers[t] > 0; };
+  auto priv = [&](int32_t t) { return viewers[t] == 0; };
+
+  // Shared tasks: per page, every query token that sees a shared segment.
+  std::vector<int32_t> root(n);
+  for (int32_t s = 0; s < n; ++s) root[s] = P.seg[s].parent < 0 ? s : root[P.seg[s].parent];
+  std::vector<Task> shared_tasks, private_tasks;
+  {
+    std::map<int32_t, Task> per_page;  // root -> tokens in node order
+    std::vector<int32_t> order;
+    for (int32_t s = 0; s < n; ++s) {
+      const padoc_segment& sg = P.seg[s];
+      if (sg.q_len == 0) continue;
+      bool any_anc = false;
+      for (const auto& a : anc[s]) any_anc |= a.second > 0;
+      if (!any_anc && !shared(s)) continue;
+      Task& t = per_page[root[s]];
+      for (int32_t p = sg.len - sg.q_len; p < sg.len; ++p) {
+        t.seg.push_back(s);
+        t.pos.push_back(p);
+      }
+    }
+    for (auto& kv : per_page) {
+      const Task& all = kv.second;
+      for (size_t b = 0; b < all.seg.size(); b += NT) {
+        Task t;
+        const size_t e = std::min(all.seg.size(), b + (size_t)NT);
+        t.seg.assign(all.seg.begin() + b, all.seg.begin() + e);
+        t.pos.assign(all.pos.begin() + b, all.pos.begin() + e);
+        shared_tasks.push_back(std::move(t));
+      }
+    }
+    for (int32_t s = 0; s < n; ++s) {
+      const padoc_segment& sg = P.seg[s];
+      if (sg.q_len == 0 || shared(s)) continue;
+      for (int32_t b = sg.len - sg.q_len; b < sg.len; b += NT) {
+        Task t;
+        for (int32_t p = b; p < std::min(sg.len, b + NT); ++p) {
+          t.seg.push_back(s);
+          t.pos.push_back(p);
+        }
+        private_tasks.push_back(std::move(t));
+      }
+    }
+  }
+  std::vector<std::vector<VisRange>> svis, pvis;
+  int64_t total = 0;
+  for (const Task& t : shared_tasks) {
+    svis.push_back(B.visible(t, shared));
+    for (const auto& r : svis.back()) total += round_up(r.n_keys, P.tile_keys) * P.Hkv;
+  }
+  for (const Task& t : private_tasks) {
+    pvis.push_back(B.visible(t, priv));
+    for (const auto& r : pvis.back()) total += round_up(r.n_keys, P.tile_keys) * P.Hkv;
+  }
+  int64_t CH = d->max_chunk_keys;
+  if (CH == 0) {
+    const int64_t target = d->target_workgroups > 0 ? d->target_workgroups : 512;
+    CH = round_up(std::max<int64_t>(1, ceil_div(total, target)), P.tile_keys);
+    CH = std::min<int64_t>(std::max<int64_t>(CH, 256), 16384);
+  }
+
+  // Per (query row, KV head): partial slots in creation order.
+  std::vector<std::vector<int32_t>> comb((size_t)P.num_q_rows * P.Hkv);
+  std::vector<char> sees;
+  auto make_items = [&](const Task& task, const std::vector<VisRange>& vis) {
+    const int32_t ntok = (int32_t)task.seg.size();
+    if (vis.empty()) return;
+    const int32_t tok_begin = B.add_tokens(task);
+    std::vector<std::vector<Piece>> items(1);
+    int64_t room = CH;
+    for (const auto& r : vis) {
+      int32_t kb = 0;
+      while (kb < r.n_keys) {
+        if (room <= 0) {
+          items.emplace_back();
+          room = CH;
+        }
+        const int32_t take = (int32_t)std::min<int64_t>(r.n_keys - kb, room);
+        items.back().push_back({&r, kb, take});
+        kb += take;
+        room -= round_up(take, P.tile_keys);
+      }
+    }
+    for (const auto& pieces : items) {
+      if (pieces.empty()) continue;
+      int32_t rb, rc, cost;
+      B.emit_ranges(pieces, ntok, rb, rc, cost, sees);
+      if (rc == 0) continue;
+      for (int32_t g = 0; g < P.Hkv; ++g) {
+        padoc::WorkRec w{};
+        w.tok_begin = tok_begin;
+        w.ntok = ntok;
+        w.rng_begin = rb;
+        w.rng_count = rc;
+        w.kvh = g;
+        w.out_base = (int32_t)P.n_slots;
+        w.cost = cost;
+        for (int32_t i = 0; i < ntok; ++i)
+          if (sees[i]) comb[(size_t)P.toks[tok_begin + i] * P.Hkv + g].push_back(w.out_base + i * P.G);
+        P.n_slots += (int64_t)ntok * P.G;
+        P.work.push_back(w);
+      }
+    }
+  };
+  for (size_t i = 0; i < shared_tasks.size(); ++i) make_items(shared_tasks[i], svis[i]);
+  for (size_t i = 0; i < private_tasks.size(); ++i) make_items(private_tasks[i], pvis[i]);
+
+  P.comb_ptr.assign(comb.size() + 1, 0);
+  for (size_t r = 0; r < comb.size(); ++r) P.comb_ptr[r + 1] = P.comb_ptr[r] + (int32_t)comb[r].size();
+  P.comb_slot.reserve(P.comb_ptr.back());
+  for (const auto& c : comb) P.comb_slot.insert(P.comb_slot.end(), c.begin(), c.end());
+}
+
+template <class T>
+void put(std::vector<unsigned char>& blob, size_t off, const std::vector<T>& v) {
+  if (!v.empty()) std::memcpy(blob.data() + off, v.data(), v.size() * sizeof(T));
+}
+
+void serialise(padoc_plan& P) {
+  P.off_work = 0;
+  P.off_ranges = align256(P.off_work + P.work.size() * sizeof(padoc::WorkRec));
+  P.off_lims = align256(P.off_ranges + P.ranges.size() * sizeof(padoc::RangeRec));
+  P.off_toks = align256(P.off_lims + P.lims.size() * 4);
+  P.off_comb_ptr = align256(P.off_toks + P.toks.size() * 4);
+  P.off_comb_slot = align256(P.off_comb_ptr + P.comb_ptr.size() * 4);
+  const size_t blob_bytes = P.off_comb_slot + P.comb_slot.size() * 4;
+  P.off_part_o = align256(blob_bytes);
+  P.off_part_ml = align256(P.off_part_o + (size_t)P.n_slots * P.D * 4);
+  P.ws_bytes = std::max<size_t>(256, align256(P.off_part_ml + (size_t)P.n_slots * 8));
+  P.blob.assign(blob_bytes, 0);
+  put(P.blob, P.off_work, P.work);
+  put(P.blob, P.off_ranges, P.ranges);
+  put(P.blob, P.off_lims, P.lims);
+  put(P.blob, P.off_toks, P.toks);
+  put(P.blob, P.off_comb_ptr, P.comb_ptr);
+  put(P.blob, P.off_comb_slot, P.comb_slot);
+}
+
+}  // namespace
+}  // namespace padoc
+
+using namespace padoc;
+
+extern "C" padoc_status padoc_tree_layout(padoc_segment* seg, int32_t n, int32_t block_size) {
+  clear_error();
+  if (n < 0 || (n > 0 && !seg)) return set_error(PADOC_ERR_ARG, "bad segment array (n=%d)", n);
+  if (block_size < 0) return set_error(PADOC_ERR_ARG, "block_size %d is negative", block_size);
+  int64_t kv = 0, q = 0;
+  for (int32_t i = 0; i < n; ++i) {
+    seg[i].kv_off = kv;
+    seg[i].q_off = q;
+    kv += block_size == 0 ? seg[i].len : ceil_div(seg[i].len, block_size);
+    q += seg[i].q_len;
+  }
+  return PADOC_OK;
+}
+
+extern "C" padoc_status padoc_tree_from_pages(const padoc_page* pages, int32_t n_pages, int32_t block_size,
+                                              padoc_segment* out, int32_t capacity, int32_t* n_out) {
+  clear_error();
+  if (!n_out) return set_error(PADOC_ERR_ARG, "n_out is null");
+  *n_out = 0;
+  if (n_pages < 0 || (n_pages > 0 && !pages)) return set_error(PADOC_ERR_ARG, "bad page array (n_pages=%d)", n_pages);
+  if (block_size < 0) return set_error(PADOC_ERR_ARG, "block_size %d is negative", block_size);
+  int64_t need = 0;
+  for (int32_t i = 0; i < n_pages; ++i) {
+    const padoc_page& p = pages[i];
+    if (p.n_branches < 0) return set_error(PADOC_ERR_ARG, "page %d: n_branches %d is negative", i, p.n_branches);
+    if (p.n_branches > 0 && (!p.branch_fork || !p.branch_len || !p.branch_q_len))
+      return set_error(PADOC_ERR_ARG, "page %d: branch arrays are null", i);
+    need += 2 + (int64_t)p.n_branches;
+  }
+  if (need > kI32Max) return set_error(PADOC_ERR_ARG, "too many segments (%lld)", (long long)need);
+  *n_out = (int32_t)need;
+  if (need > capacity || (need > 0 && !out))
+    return set_error(PADOC_ERR_ARG, "capacity %d < %lld segments needed", capacity, (long long)need);
+  int32_t k = 0;
+  for (int32_t i = 0; i < n_pages; ++i) {
+    const padoc_page& p = pages[i];
+    const int32_t root = k;
+    out[k++] = padoc_segment{-1, 0, p.prefix_len, p.prefix_q_len, 0, 0};
+    const int32_t stream = k;
+    out[k++] = padoc_segment{root, p.prefix_len, p.stream_len, p.stream_q_len, 0, 0};
+    for (int32_t b = 0; b < p.n_branches; ++b)
+      out[k++] = padoc_segment{stream, p.branch_fork[b], p.branch_len[b], p.branch_q_len[b], 0, 0};
+  }
+  return padoc_tree_layout(out, k, block_size);
+}
+
+extern "C" padoc_status padoc_plan_create(const padoc_tree_desc* d, padoc_plan** out) {
+  clear_error();
+  if (!out) return set_error(PADOC_ERR_ARG, "out is null");
+  *out = nullptr;
+  if (!d) return set_error(PADOC_ERR_ARG, "desc is null");
+  padoc_status st = validate(d);
+  if (st != PADOC_OK) return st;
+  try {
+    std::unique_ptr<padoc_plan> P(new padoc_plan());
+    P->kind = d->block_size == 0 ? 0 : 1;
+    P->Hq = d->num_heads_q;
+    P->Hkv = d->num_heads_kv;
+    P->G = d->num_heads_q / d->num_heads_kv;
+    P->D = d->head_dim;
+    P->scale = d->softmax_scale;
+    P->dtype = d->dtype;
+    P->block_size = d->block_size;
+    P->num_kv_rows = d->num_kv_rows;
+    P->num_q_rows = d->num_q_rows;
+    P->block_table_len = d->block_table_len;
+    P->seg.assign(d->seg, d->seg + d->n_seg);
+    P->tile_tokens = std::max(1, P->tile_cols / P->G);
+    std::vector<std::vector<std::pair<int32_t, int32_t>>> anc(d->n_seg);
+    for (int32_t s = 0; s < d->n_seg; ++s) {
+      const int32_t par = P->seg[s].parent;
+      if (par >= 0) {
+        anc[s] = anc[par];
+        anc[s].push_back({par, P->seg[s].fork});
+      }
+    }
+    Builder B(*P, anc);
+    if (P->kind == 0)
+      build_forward(*P, B);
+    else
+      build_decode(*P, B, anc, d);
+    if (P->n_slots > kI32Max) return set_error(PADOC_ERR_ARG, "schedule too large (%lld partial slots)", (long long)P->n_slots);
+    if ((int64_t)P->lims.size() > kI32Max || (int64_t)P->ranges.size() > kI32Max)
+      return set_error(PADOC_ERR_ARG, "schedule too large");
+    // Costliest items first: the hardware dispatcher then assigns work
+    // greedily to the first free compute unit (longest-processing-time order).
+    std::stable_sort(P->work.begin(), P->work.end(),
+                     [](const padoc::WorkRec& a, const padoc::WorkRec& b) { return a.cost > b.cost; });
+    serialise(*P);
+    *out = P.release();
+  } catch (const std::bad_alloc&) {
+    return set_error(PADOC_ERR_ARG, "out of host memory while planning");
+  }
+  return PADOC_OK;
+}
+
+extern "C" padoc_status padoc_plan_workspace_bytes(const padoc_plan* plan, size_t* bytes) {
+  clear_error();
+  if (!plan || !bytes) return set_error(PADOC_ERR_ARG, "null argument");
+  *bytes = plan->ws_bytes;
+  return PADOC_OK;
+}
+
+extern "C" padoc_status padoc_plan_export(const padoc_plan* P, padoc_schedule_view* v) {
+  clear_error();
+  if (!P || !v) return set_error(PADOC_ERR_ARG, "null argument");
+  std::memset(v, 0, sizeof(*v));
+  v->kind = P->kind;
+  v->tile_cols = P->tile_cols;
+  v->tile_keys = P->tile_keys;
+  v->n_work = (int32_t)P->work.size();
+  v->work = P->work.data();
+  v->n_range = (int32_t)P->ranges.size();
+  v->ranges = P->ranges.data();
+  v->n_lim = (int32_t)P->lims.size();
+  v->lims = P->lims.data();
+  v->n_tok = (int32_t)P->toks.size();
+  v->toks = P->toks.data();
+  v->n_tile_class = (int64_t)P->tile_class.size();
+  v->tile_class = P->tile_class.data();
+  v->tile_class_off = P->tile_class_off.data();
+  v->n_comb_ptr = (int64_t)P->comb_ptr.size();
+  v->comb_ptr = P->comb_ptr.data();
+  v->n_comb = (int64_t)P->comb_slot.size();
+  v->comb_slot = P->comb_slot.data();
+  v->n_slots = P->n_slots;
+  v->workspace_bytes = P->ws_bytes;
+  return PADOC_OK;
+}
+
+extern "C" void padoc_plan_destroy(padoc_plan* plan) { delete plan; }
+
+extern "C" const char* padoc_last_error(void) { return padoc::last_error(); }

@@ -1,0 +1,50 @@
+// Host-side plan: validated tree + serialised schedule.  Pure C++17, no HIP
+// calls, so it builds and runs on machines without a GPU.
+#pragma once
+
+#include <stddef.h>
+#include <stdint.h>
+
+#include <string>
+#include <vector>
+
+#include "../schedule.hpp"
+
+struct padoc_plan {
+  int32_t kind = 0;  // 0 forward (final O/LSE), 1 decode (partials + combine)
+  int32_t Hq = 0, Hkv = 0, G = 0, D = 0;
+  float scale = 0.f;
+  padoc_dtype dtype = PADOC_BF16;
+  int32_t block_size = 0;
+  int64_t num_kv_rows = 0, num_q_rows = 0, block_table_len = 0;
+  std::vector<padoc_segment> seg;
+
+  int32_t tile_cols = padoc::kTileCols;
+  int32_t tile_keys = padoc::kTileKeys;
+  int32_t tile_tokens = 0;  // tokens per work item = tile_cols / G
+
+  std::vector<padoc::WorkRec> work;
+  std::vector<padoc::RangeRec> ranges;
+  std::vector<int32_t> lims;
+  std::vector<int32_t> toks;
+  std::vector<int8_t> tile_class;
+  std::vector<int64_t> tile_class_off;  // per range: first entry in tile_class
+  std::vector<int32_t> comb_ptr;
+  std::vector<int32_t> comb_slot;
+  int64_t n_slots = 0;
+
+  // Serialised schedule (uploaded into the workspace before every launch).
+  std::vector<unsigned char> blob;
+  size_t off_work = 0, off_ranges = 0, off_lims = 0, off_toks = 0;
+  size_t off_comb_ptr = 0, off_comb_slot = 0, off_part_o = 0, off_part_ml = 0;
+  size_t ws_bytes = 0;
+};
+
+namespace padoc {
+
+// Thread-local error state shared by every C entry point.
+padoc_status set_error(padoc_status st, const char* fmt, ...);
+void clear_error();
+const char* last_error();
+
+}  // namespace padoc

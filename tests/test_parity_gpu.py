@@ -1,0 +1,210 @@
+"""GPU parity of the HIP path (through the C ABI) against the fp64 oracle.
+
+Every case draws seeded inputs with padoc_synth, runs the library and the
+oracle on the same values and compares element by element (sampled rows at
+the full benchmark sizes) with the tolerances of the hot path.
+"""
+import math
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from oracle import dense as od
+import padoc_synth as syn
+import paper_2608_06146_amd as pa
+from _cases import compare, decode_case, forward_case
+
+pytestmark = pytest.mark.gpu
+
+
+# ---------------------------------------------------------------- forward
+
+@pytest.mark.parametrize("prescale", [False, True])
+def test_tiny_fp32_forward(prescale):
+    """1 page, P=256, S=64, 4 branches of 32 at forks 8/24/40/56, fp32."""
+    wl = syn.make_workload("tiny_fp32_forward")
+    forward_case(wl.pages, 4, 1, 64, "f32", 0, prescale=prescale)
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+@pytest.mark.parametrize("heads", [(4, 1), (16, 2), (28, 4)])
+@pytest.mark.parametrize("d", [64, 128])
+def test_forward_random_trees(dtype, heads, d):
+    """Random trees of depth <= 5, segments up to 90 tokens (several key
+    tiles, ragged tails), forks anywhere in [0, len(parent)]."""
+    Hq, Hkv = heads
+    for seed in range(3):
+        nodes = syn.random_tree(100 * seed + d + Hq, n_pages=2, max_depth=5, max_len=90,
+                                q_mode="all" if seed != 2 else "some", max_nodes=14)
+        forward_case(nodes, Hq, Hkv, d, dtype, seed)
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_forward_page_trees(dtype):
+    """Paper-shaped pages, scaled down: prefix, stream, many short siblings."""
+    rng = np.random.default_rng(5)
+    pages = []
+    for _ in range(3):
+        P, S = int(rng.integers(60, 400)), int(rng.integers(8, 120))
+        N = int(rng.integers(1, 20))
+        f = np.sort(rng.integers(0, S + 1, N))
+        L = rng.integers(1, 70, N)
+        pages.append(syn.Page(P, P, S, S, tuple(syn.Branch(int(a), int(b), int(b)) for a, b in zip(f, L))))
+    forward_case(pages, 16, 2, 128, dtype, 1)
+
+
+def test_forward_edge_cases_bf16():
+    # single tokens everywhere, forks 0 and full, q_len 0 segments, G=1
+    nodes = [(-1, 0, 1, 1), (0, 0, 1, 1), (0, 1, 3, 0), (2, 3, 2, 2), (2, 0, 1, 1), (-1, 0, 200, 7),
+             (5, 200, 1, 1), (5, 0, 65, 65), (7, 64, 64, 64), (7, 65, 1, 0)]
+    for heads in [(1, 1), (8, 1), (12, 3)]:
+        forward_case(nodes, heads[0], heads[1], 128, "bf16", 3)
+        forward_case(nodes, heads[0], heads[1], 64, "f32", 3)
+
+
+def test_forward_long_single_segment():
+    """One long causal sequence (ragged length, many tiles) equals plain
+    causal attention; checked against the oracle."""
+    forward_case([(-1, 0, 1000, 1000)], 16, 2, 128, "bf16", 4)
+
+
+def test_forward_sentinel_gaps():
+    """Segments laid out with NaN rows between them: a read of any K/V row
+    outside the visible ranges would poison the output."""
+    nodes = [(-1, 0, 70, 70), (0, 33, 50, 50), (1, 20, 40, 40), (1, 50, 9, 9), (-1, 0, 65, 65)]
+    kv_off, q_off, pos = [], [], 5
+    for n in nodes:
+        kv_off.append(pos)
+        pos += n[2] + 7
+    q_off = list(np.cumsum([0] + [n[3] for n in nodes[:-1]]))
+    T = pos
+    for dtype in ("bf16", "f32"):
+        o, lse, plan, (q, k, v) = forward_case(nodes, 8, 2, 128, dtype, 5, kv_off=np.array(kv_off),
+                                                q_off=np.array(q_off), kv_rows=T, check=False)
+        mask = torch.ones(T, dtype=torch.bool, device=k.device)
+        for a, n in zip(kv_off, nodes):
+            mask[a: a + n[2]] = False
+        k[mask] = float("nan")
+        v[mask] = float("nan")
+        o, lse = pa.tree_attn_fwd(q, k, v, plan)
+        torch.cuda.synchronize()
+        O_ref, L_ref = oracle.tree_attention(nodes, q, k, v, 1 / math.sqrt(128), 8, 2,
+                                             kv_off=np.array(kv_off), q_off=np.array(q_off))
+        compare("sentinel", o, lse, O_ref, L_ref, dtype)
+
+
+def test_forward_empty_tree_is_noop():
+    plan = pa.TreePlan(np.zeros(0, dtype=pa.SEGMENT_DTYPE), 4, 1, 64, "bf16", 0, num_kv_rows=0, num_q_rows=0)
+    q = torch.zeros(0, 4, 64, dtype=torch.bfloat16, device="cuda")
+    k = torch.zeros(0, 1, 64, dtype=torch.bfloat16, device="cuda")
+    o, lse = pa.tree_attn_fwd(q, k, k, plan)
+    torch.cuda.synchronize()
+    assert o.numel() == 0
+
+
+def test_forward_determinism():
+    wl = syn.make_workload("tiny_fp32_forward")
+    pages = [syn.Page(300, 300, 70, 70, tuple(syn.Branch(f, 40, 40) for f in (5, 30, 70)))]
+    o1, l1, plan, (q, k, v) = forward_case(pages, 16, 2, 128, "bf16", 6, check=False)
+    o2, l2 = pa.tree_attn_fwd(q, k, v, plan)
+    torch.cuda.synchronize()
+    assert torch.equal(o1, o2) and torch.equal(l1, l2)
+
+
+@pytest.mark.slow
+def test_packed_forward_8pages_full_size_sampled():
+    """The 8-page packed forward at full size (about 43k tokens), in the
+    launch configuration the benchmark times; sampled rows vs the oracle."""
+    wl = syn.make_workload("packed_forward_8pages")
+    nq = syn.count_queries(wl.pages)
+    rng = np.random.default_rng(0)
+    nodes = od.page_nodes(wl.pages)
+    _, q_off = od.canonical_layout(nodes, 0)
+    rows = set(rng.choice(nq, 150, replace=False).tolist())
+    for s, n in enumerate(nodes):          # first and last query of every 7th segment
+        if s % 7 == 0:
+            rows.update([int(q_off[s]), int(q_off[s] + n[3] - 1)])
+    forward_case(wl.pages, 16, 2, 128, "bf16", 0, rows=sorted(rows))
+
+
+# ---------------------------------------------------------------- decode
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+@pytest.mark.parametrize("heads", [(4, 1), (16, 2), (28, 4)])
+@pytest.mark.parametrize("d", [64, 128])
+def test_decode_random_trees(dtype, heads, d):
+    Hq, Hkv = heads
+    for seed in range(3):
+        nodes = syn.random_tree(200 * seed + d + Hq, n_pages=2, max_depth=5, max_len=150, q_mode="tail",
+                                max_nodes=14)
+        if sum(n.q_len for n in nodes) == 0:
+            continue
+        decode_case(nodes, Hq, Hkv, d, dtype, seed, max_chunk_keys=64 * (seed + 1))
+
+
+@pytest.mark.parametrize("chunk", [0, 64, 192])
+def test_single_page_decode_full(chunk):
+    """The single-page decode workload (P=2048, S=256, 16 branches), all 17
+    queries, with automatic and forced small key chunks."""
+    wl = syn.make_workload("single_page_decode")
+    decode_case(wl.pages, 16, 2, 128, "bf16", 0, max_chunk_keys=chunk)
+
+
+def test_decode_mixed_q_len_pages():
+    """Scaled-down mixed step: decoding branches plus new forks whose 8
+    tokens are all queries, G = 7."""
+    rng = np.random.default_rng(9)
+    S = 100
+    f = np.sort(rng.integers(1, S, 20))
+    br = [syn.Branch(int(f[i]), int(rng.integers(5, 300)), 1) for i in range(14)]
+    br += [syn.Branch(int(f[i]), 8, 8) for i in range(14, 20)]
+    pages = [syn.Page(700, 0, S, 1, tuple(br)), syn.Page(90, 0, 10, 1, (syn.Branch(3, 17, 1),))]
+    decode_case(pages, 28, 4, 128, "bf16", 2)
+    decode_case(pages, 28, 4, 64, "f32", 2)
+
+
+def test_decode_determinism():
+    wl = syn.make_workload("single_page_decode")
+    o1, l1, plan, (q, kc, vc, bt, ids) = decode_case(wl.pages, 16, 2, 128, "bf16", 0, check=False)
+    for _ in range(2):
+        o2, l2 = pa.branch_decode(q, kc, vc, bt, plan)
+        torch.cuda.synchronize()
+        assert torch.equal(o1, o2) and torch.equal(l1, l2)
+
+
+def test_decode_equals_packed_forward_rows():
+    """P8: a decode step's rows equal the packed forward's rows for the same
+    tokens (same values, K/V moved from packed rows into paged blocks)."""
+    pages = [syn.Page(300, 0, 40, 1, tuple(syn.Branch(f, L, 1) for f, L in ((3, 20), (17, 64), (39, 100))))]
+    pages_fwd = [syn.Page(300, 0, 40, 1, tuple(syn.Branch(f, L, 1) for f, L in ((3, 20), (17, 64), (39, 100))))]
+    o_f, l_f, _, (q, k, v) = forward_case(pages_fwd, 16, 2, 128, "bf16", 7, check=False)
+    nodes = od.page_nodes(pages)
+    kc, vc, ids = __import__("_cases").fill_pool(nodes, k, v, 200, 7)
+    segs = pa.segments_from_pages(pages, 16)
+    plan = pa.TreePlan(segs, 16, 2, 128, "bf16", 16, num_kv_rows=200, num_q_rows=q.shape[0], block_table_host=ids)
+    o_d, l_d = pa.branch_decode(q, kc, vc, torch.as_tensor(ids, device="cuda"), plan)
+    torch.cuda.synchronize()
+    d = (o_d.float() - o_f.float()).abs()
+    assert d.max().item() <= 1.5e-2 and d.mean().item() <= 2e-3
+    assert (l_d - l_f).abs().max().item() <= 1.5e-2
+
+
+@pytest.mark.slow
+def test_concurrent_decode_64pages_full_size():
+    """64 pages x 24 branches at full size (about 1.02M cached tokens), all
+    1600 queries, in the benchmark's launch configuration."""
+    wl = syn.make_workload("concurrent_decode_64pages")
+    decode_case(wl.pages, 16, 2, 128, "bf16", 0, pool_extra=5000)
+
+
+@pytest.mark.slow
+def test_dense_page_mixed_step_full_size_sampled():
+    """1 page, P=8192, S=1024, 128 branches (96 decoding + 32 new 8-token
+    forks), 353 queries, Hq=28, Hkv=4; sampled rows vs the oracle."""
+    wl = syn.make_workload("dense_page_mixed_step")
+    rng = np.random.default_rng(1)
+    nq = syn.count_queries(wl.pages)
+    rows = sorted(set(rng.choice(nq, 60, replace=False).tolist()) | {0, nq - 1})
+    decode_case(wl.pages, 28, 4, 128, "bf16", 0, pool_extra=3000, rows=rows)
