@@ -1,0 +1,335 @@
+#!/usr/bin/env python3
+"""Benchmark of PaDoc tree attention on one MI355X.
+
+    python bench.py [--steps K] [--warmup W] [--gpus 1]
+
+A step is one decode step of masked parallel decoding over the paged cache of
+the concurrent-decode workload (64 pages x [prefix 3072, layout stream 256,
+24 branches with lengths U[1,1024]]; 1600 live streams, Hq=16, Hkv=2, d=128,
+bf16, 16-token blocks shuffled across a pool that fills most of HBM): the
+decode plan is uploaded, the split-KV tile kernel runs and the partials are
+combined.  Inputs (Q, the paged K/V cache, the block table) are resident in
+HBM before timing starts.  The headline value is branch tokens (queries) per
+second of one attention-layer call.  The same run also times the packed
+forward of the 8-page training/branch-creation workload (TFLOP/s), and the
+CPU oracle on a bounded sample of the decode workload.
+
+One JSON line is printed (rank 0, one GPU).  Kernel durations for the
+roofline come from HIP events the library records around its tile kernel on
+the launch stream.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import math
+import os
+import statistics
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+METRIC = "branch-decode tokens/s + HBM GB/s; packed tree-attn TFLOP/s (% roofline)"
+HBM_PEAK_GBS = 8000.0
+BF16_PEAK_TFLOPS = 2516.6
+
+
+def log(msg: str) -> None:
+    print(f"[bench] {msg}", file=sys.stderr, flush=True)
+
+
+def parse_args(argv=None):
+    ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=50)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--seed", type=int, default=0)
+    ap.add_argument("--workload", default="concurrent_decode_64pages")
+    ap.add_argument("--forward-workload", default="packed_forward_8pages",
+                    help="packed-forward workload timed alongside ('none' to skip)")
+    ap.add_argument("--pool-gib", type=float, default=0.0,
+                    help="bytes of each of the K and V pools in GiB (0: 45%% of HBM each, backing off on failure)")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-pages", type=int, default=64, help="pages of the decode workload the oracle times")
+    return ap.parse_args(argv)
+
+
+# ---------------------------------------------------------------- helpers
+
+def visible_pairs_of(segs):
+    """Visible (query, key) pairs of a segment tree: ancestors' fork prefixes
+    plus the causal own part, for each of the last q_len tokens."""
+    import numpy as np
+    n = len(segs)
+    anc = np.zeros(n, dtype=np.int64)
+    for i in range(n):
+        p = int(segs["parent"][i])
+        if p >= 0:
+            anc[i] = anc[p] + int(segs["fork"][i])
+    L = segs["len"].astype(np.int64)
+    Q = segs["q_len"].astype(np.int64)
+    # sum over p in [L-Q, L) of (anc + p + 1)
+    own = Q * L - Q * (Q - 1) // 2
+    return int((Q * anc + own).sum())
+
+
+def timed_steps(fn, steps, warmup, torch, pa):
+    """Run `fn` warmup + steps times; returns (ms_per_step, [kernel ms])."""
+    for _ in range(warmup):
+        fn()
+    torch.cuda.synchronize()
+    evs = []
+    for _ in range(steps):
+        b = torch.cuda.Event(enable_timing=True)
+        a = torch.cuda.Event(enable_timing=True)
+        b.record()  # creates the underlying events
+        a.record()
+        evs.append((b, a))
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for b, a in evs:
+        pa.set_kernel_events(b, a)
+        fn()
+    torch.cuda.synchronize()
+    t1 = time.perf_counter()
+    pa.set_kernel_events()
+    kms = [b.elapsed_time(a) for b, a in evs]
+    return (t1 - t0) * 1e3 / steps, kms
+
+
+def alloc_pools(torch, n_blocks_needed, Hkv, d, pool_gib, dev):
+    """K and V pools sized to most of HBM (each pool gets half), backing off
+    8 GiB at a time until both allocations succeed."""
+    block_bytes = Hkv * 16 * d * 2
+    total = torch.cuda.get_device_properties(dev).total_memory
+    want = int(pool_gib * (1 << 30)) if pool_gib > 0 else int(0.45 * total)
+    while want > 0:
+        n = max(n_blocks_needed, want // block_bytes)
+        try:
+            kc = torch.empty((n, Hkv, 16, d), dtype=torch.bfloat16, device=dev)
+            vc = torch.empty((n, Hkv, 16, d), dtype=torch.bfloat16, device=dev)
+            return kc, vc, n
+        except RuntimeError:
+            torch.cuda.empty_cache()
+            if want <= 8 << 30:
+                break
+            want -= 8 << 30
+    n = n_blocks_needed
+    return (torch.empty((n, Hkv, 16, d), dtype=torch.bfloat16, device=dev),
+            torch.empty((n, Hkv, 16, d), dtype=torch.bfloat16, device=dev), n)
+
+
+# ---------------------------------------------------------------- decode leg
+
+def run_decode(args, torch, np, syn, pa, dev):
+    wl = syn.make_workload(args.workload, args.seed)
+    assert wl.kind == "decode"
+    Hq, Hkv, d = wl.num_heads_q, wl.num_heads_kv, wl.head_dim
+    T = syn.count_tokens(wl.pages)
+    nq = syn.count_queries(wl.pages)
+    nb = syn.count_blocks(wl.pages)
+    segs_paged = pa.segments_from_pages(wl.pages, 16)
+    segs_packed = pa.segments_from_pages(wl.pages, 0)
+
+    kc, vc, n_pool = alloc_pools(torch, nb, Hkv, d, args.pool_gib, dev)
+    pool_gib = 2 * n_pool * Hkv * 16 * d * 2 / (1 << 30)
+    log(f"decode workload {wl.name}: {len(wl.pages)} pages, {T} cached tokens, {nq} queries, "
+        f"{nb} blocks in a {pool_gib:.1f} GiB K+V pool")
+    ids = syn.draw_block_ids(nb, n_pool, args.seed)
+
+    # plan creation (host) is timed on its own
+    pts = []
+    for _ in range(5):
+        t0 = time.perf_counter()
+        plan = pa.TreePlan(segs_paged, Hq, Hkv, d, "bf16", 16, num_kv_rows=n_pool, num_q_rows=nq,
+                           block_table_len=nb)
+        pts.append((time.perf_counter() - t0) * 1e3)
+    plan_ms = statistics.median(pts)
+
+    # fill the used blocks: token t of segment s -> block ids[bt_off + t//16], slot t%16
+    k = syn.draw_normal((T, Hkv, d), args.seed, 2, "bf16", device=dev)
+    v = syn.draw_normal((T, Hkv, d), args.seed, 3, "bf16", device=dev)
+    q = syn.draw_normal((nq, Hq, d), args.seed, 1, "bf16", device=dev)
+    blk = np.empty(T, dtype=np.int64)
+    slot = np.empty(T, dtype=np.int64)
+    for s in range(len(segs_paged)):
+        L = int(segs_paged["len"][s])
+        r0 = int(segs_packed["kv_off"][s])
+        t = np.arange(L)
+        blk[r0:r0 + L] = ids[int(segs_paged["kv_off"][s]) + t // 16]
+        slot[r0:r0 + L] = t % 16
+    bi = torch.as_tensor(blk, device=dev)
+    si = torch.as_tensor(slot, device=dev)
+    kc[bi, :, si, :] = k
+    vc[bi, :, si, :] = v
+    del k, v, bi, si
+    bt = torch.as_tensor(ids, device=dev)
+    o = torch.empty(nq, Hq, d, dtype=torch.bfloat16, device=dev)
+    lse = torch.empty(nq, Hq, dtype=torch.float32, device=dev)
+    ws = plan.workspace(dev)
+    torch.cuda.synchronize()
+
+    def step():
+        pa.branch_decode(q, kc, vc, bt, plan, out=o, lse=lse, workspace=ws)
+
+    ms, kms = timed_steps(step, args.steps, args.warmup, torch, pa)
+    k_ms = statistics.mean(kms)
+
+    # algorithmic bytes: every cached K/V token read once, Q read, O/LSE written,
+    # block-table ids of the referenced blocks read
+    kv_bytes = T * Hkv * d * 2 * 2
+    q_bytes = nq * Hq * d * 2
+    o_bytes = nq * Hq * d * 2 + nq * Hq * 4
+    bt_bytes = nb * 4
+    kernel_bytes = kv_bytes + q_bytes + bt_bytes
+    step_bytes = kernel_bytes + o_bytes
+    naive = 0
+    anc = {}
+    for s in range(len(segs_paged)):
+        p = int(segs_paged["parent"][s])
+        anc[s] = (anc[p] + int(segs_paged["fork"][s])) if p >= 0 else 0
+        if int(segs_paged["q_len"][s]) > 0:
+            naive += anc[s] + int(segs_paged["len"][s])
+    flops = 4 * d * Hq * visible_pairs_of(segs_paged)
+    ex = plan.export()
+    res = {
+        "workload": wl.name, "ms_per_step": ms, "kernel_ms": k_ms,
+        "kernel_ms_p10": float(np.percentile(kms, 10)), "kernel_ms_p90": float(np.percentile(kms, 90)),
+        "tokens_per_s": nq / (ms * 1e-3), "step_gbps": step_bytes / (ms * 1e-3) / 1e9,
+        "kernel_gbps": kernel_bytes / (k_ms * 1e-3) / 1e9, "kernel_bytes": kernel_bytes,
+        "kv_bytes": kv_bytes, "naive_per_stream_kv_bytes": naive * Hkv * d * 2 * 2,
+        "sharing_factor": naive / T, "flops": flops, "kernel_tflops": flops / (k_ms * 1e-3) / 1e12,
+        "plan_ms": plan_ms, "tokens_per_s_with_plan": nq / ((ms + plan_ms) * 1e-3),
+        "work_items": int(len(ex["work"])), "partial_slots": int(ex["n_slots"]), "pool_gib": pool_gib,
+        "pages": len(wl.pages), "queries": nq, "cached_tokens": T, "Hq": Hq, "Hkv": Hkv, "d": d,
+    }
+    del kc, vc
+    torch.cuda.empty_cache()
+    return res, wl
+
+
+# ---------------------------------------------------------------- forward leg
+
+def run_forward(args, torch, np, syn, pa, dev):
+    wl = syn.make_workload(args.forward_workload, args.seed)
+    assert wl.kind == "forward"
+    Hq, Hkv, d = wl.num_heads_q, wl.num_heads_kv, wl.head_dim
+    T = syn.count_tokens(wl.pages)
+    nq = syn.count_queries(wl.pages)
+    segs = pa.segments_from_pages(wl.pages, 0)
+    t0 = time.perf_counter()
+    plan = pa.TreePlan(segs, Hq, Hkv, d, wl.dtype, 0, num_kv_rows=T, num_q_rows=nq)
+    plan_ms = (time.perf_counter() - t0) * 1e3
+    q = syn.draw_normal((nq, Hq, d), args.seed, 1, wl.dtype, device=dev)
+    k = syn.draw_normal((T, Hkv, d), args.seed, 2, wl.dtype, device=dev)
+    v = syn.draw_normal((T, Hkv, d), args.seed, 3, wl.dtype, device=dev)
+    o = torch.empty_like(q)
+    lse = torch.empty(nq, Hq, dtype=torch.float32, device=dev)
+    ws = plan.workspace(dev)
+    log(f"forward workload {wl.name}: {len(wl.pages)} pages, {T} tokens")
+
+    def step():
+        pa.tree_attn_fwd(q, k, v, plan, out=o, lse=lse, workspace=ws)
+
+    ms, kms = timed_steps(step, max(10, args.steps), args.warmup, torch, pa)
+    k_ms = statistics.mean(kms)
+    pairs = visible_pairs_of(segs)
+    flops = 4 * d * Hq * pairs
+    return {
+        "workload": wl.name, "tokens": T, "visible_pairs": pairs, "flops": flops,
+        "ms_per_step": ms, "kernel_ms": k_ms, "tflops": flops / (ms * 1e-3) / 1e12,
+        "kernel_tflops": flops / (k_ms * 1e-3) / 1e12, "plan_ms": plan_ms,
+        "roofline": {"bound": "mfma", "achieved": flops / (k_ms * 1e-3) / 1e12, "peak": BF16_PEAK_TFLOPS,
+                     "unit": "TFLOP/s", "frac": flops / (k_ms * 1e-3) / 1e12 / BF16_PEAK_TFLOPS, "traffic": None},
+    }
+
+
+# ---------------------------------------------------------------- CPU oracle leg
+
+def run_cpu_baseline(args, wl, np, syn):
+    """The oracle as it stands on a bounded sample: the first `cpu_pages`
+    pages of the decode workload (pages are independent trees)."""
+    import oracle
+    from oracle import dense as od
+    pages = wl.pages[: args.cpu_pages]
+    nodes = od.page_nodes(pages)
+    T = syn.count_tokens(pages)
+    nq = syn.count_queries(pages)
+    k = syn.draw_normal((T, wl.num_heads_kv, wl.head_dim), args.seed, 2, "bf16")
+    v = syn.draw_normal((T, wl.num_heads_kv, wl.head_dim), args.seed, 3, "bf16")
+    q = syn.draw_normal((nq, wl.num_heads_q, wl.head_dim), args.seed, 1, "bf16")
+    t0 = time.perf_counter()
+    oracle.tree_attention(nodes, q, k, v, 1.0 / math.sqrt(wl.head_dim), wl.num_heads_q, wl.num_heads_kv)
+    dt = time.perf_counter() - t0
+    try:
+        import threadpoolctl
+        info = threadpoolctl.threadpool_info()
+        cores = max([i.get("num_threads", 1) for i in info if i.get("user_api") == "blas"] or [1])
+    except Exception:
+        cores = len(os.sched_getaffinity(0))
+    return {"value": nq / dt, "unit": "tokens/s", "cores": int(cores), "kind": "oracle",
+            "sample": f"{len(pages)} of {len(wl.pages)} pages ({nq} queries, {T} cached tokens), fp64 dense "
+                      f"ancestor mask per page, {dt:.1f} s wall"}
+
+
+def main(argv=None) -> int:
+    args = parse_args(argv)
+    world = int(os.environ.get("WORLD_SIZE", "1"))
+    if args.gpus != 1 or world != 1:
+        print(f"bench.py runs on exactly one GPU (asked for --gpus {args.gpus}, WORLD_SIZE={world}); pages are "
+              "independent trees, so several GPUs would shard by page with no exchange -- not built here.",
+              file=sys.stderr)
+        return 2
+    import numpy as np
+    import torch
+
+    import padoc_synth as syn
+    import paper_2608_06146_amd as pa
+
+    if not torch.cuda.is_available():
+        print("bench.py needs a GPU", file=sys.stderr)
+        return 2
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    pa.version()  # loads the library (fails loudly if it was not built)
+
+    dec, wl = run_decode(args, torch, np, syn, pa, dev)
+    fwd = None
+    if args.forward_workload != "none":
+        fwd = run_forward(args, torch, np, syn, pa, dev)
+    cpu = None if args.no_cpu_baseline else run_cpu_baseline(args, wl, np, syn)
+
+    line = {
+        "metric": METRIC,
+        "value": dec["tokens_per_s"],
+        "unit": "tokens/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": dec["ms_per_step"],
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic",
+        "config": {"workload": dec["workload"], "pages": dec["pages"], "branches_per_page": 24,
+                   "queries": dec["queries"], "cached_tokens": dec["cached_tokens"], "Hq": dec["Hq"],
+                   "Hkv": dec["Hkv"], "d": dec["d"], "block": 16, "pool_gib": round(dec["pool_gib"], 1)},
+        "hbm_gbps": dec["step_gbps"],
+        "roofline": {"bound": "hbm", "achieved": dec["kernel_gbps"], "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                     "frac": dec["kernel_gbps"] / HBM_PEAK_GBS, "traffic": None,
+                     "kernel": "tile_mfma_bf16_kernel<128,paged,partial>", "kernel_ms": dec["kernel_ms"],
+                     "bytes_per_launch": dec["kernel_bytes"]},
+        "cpu_baseline": cpu,
+        "decode": dec,
+        "forward": fwd,
+    }
+    print(json.dumps(line), flush=True)
+    return 0
+
+
+if __name__ == "__main__":
+    sys.exit(main())

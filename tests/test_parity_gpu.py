@@ -194,9 +194,14 @@ def test_decode_equals_packed_forward_rows():
 @pytest.mark.slow
 def test_concurrent_decode_64pages_full_size():
     """64 pages x 24 branches at full size (about 1.02M cached tokens), all
-    1600 queries, in the benchmark's launch configuration."""
+    1600 queries computed in the benchmark's launch configuration; every
+    query of the first three and the last page plus 100 random ones are
+    checked against the oracle."""
     wl = syn.make_workload("concurrent_decode_64pages")
-    decode_case(wl.pages, 16, 2, 128, "bf16", 0, pool_extra=5000)
+    nq = syn.count_queries(wl.pages)
+    rng = np.random.default_rng(2)
+    rows = set(range(0, 25 * 3)) | set(range(nq - 25, nq)) | set(rng.choice(nq, 100, replace=False).tolist())
+    decode_case(wl.pages, 16, 2, 128, "bf16", 0, pool_extra=5000, rows=sorted(rows))
 
 
 @pytest.mark.slow
