@@ -110,7 +110,7 @@ def alloc_pools(torch, n_blocks_needed, Hkv, d, pool_gib, dev):
         n = max(n_blocks_needed, want // block_bytes)
         try:
             kc = torch.empty((n, Hkv, 16, d), dtype=torch.bfloat16, device=dev)
-            vc = torch.empty((n, Hkv, 16, d), dtype=torch.bfloat16, device=dev)
+            vc = torch.empty((n, Hkv, d, 16), dtype=torch.bfloat16, device=dev)  # d-major V blocks
             return kc, vc, n
         except RuntimeError:
             torch.cuda.empty_cache()
@@ -119,7 +119,7 @@ def alloc_pools(torch, n_blocks_needed, Hkv, d, pool_gib, dev):
             want -= 8 << 30
     n = n_blocks_needed
     return (torch.empty((n, Hkv, 16, d), dtype=torch.bfloat16, device=dev),
-            torch.empty((n, Hkv, 16, d), dtype=torch.bfloat16, device=dev), n)
+            torch.empty((n, Hkv, d, 16), dtype=torch.bfloat16, device=dev), n)
 
 
 # ---------------------------------------------------------------- decode leg
@@ -164,7 +164,7 @@ def run_decode(args, torch, np, syn, pa, dev):
     bi = torch.as_tensor(blk, device=dev)
     si = torch.as_tensor(slot, device=dev)
     kc[bi, :, si, :] = k
-    vc[bi, :, si, :] = v
+    vc[bi, :, :, si] = v
     del k, v, bi, si
     bt = torch.as_tensor(ids, device=dev)
     o = torch.empty(nq, Hq, d, dtype=torch.bfloat16, device=dev)
@@ -321,7 +321,7 @@ def main(argv=None) -> int:
         "hbm_gbps": dec["step_gbps"],
         "roofline": {"bound": "hbm", "achieved": dec["kernel_gbps"], "peak": HBM_PEAK_GBS, "unit": "GB/s",
                      "frac": dec["kernel_gbps"] / HBM_PEAK_GBS, "traffic": None,
-                     "kernel": "tile_mfma_bf16_kernel<128,paged,partial>", "kernel_ms": dec["kernel_ms"],
+                     "kernel": "decode_stream_kernel<128>", "kernel_ms": dec["kernel_ms"],
                      "bytes_per_launch": dec["kernel_bytes"]},
         "cpu_baseline": cpu,
         "decode": dec,

@@ -31,8 +31,11 @@
  *   Q, O     [n_q_rows, Hq, d]        segment s's queries = its LAST q_len
  *                                     tokens, at rows q_off .. q_off+q_len-1
  *   K, V     packed: [num_kv_rows, Hkv, d], segment s's token j at row kv_off+j
- *            paged:  [num_blocks, Hkv, 16, d], segment s's token j in block
- *                    block_table[kv_off + j/16], slot j%16
+ *   K cache  paged:  [num_blocks, Hkv, 16, d]  (16 token rows per block)
+ *   V cache  paged:  [num_blocks, Hkv, d, 16]  (d-major: the 16 tokens of a
+ *                    block are contiguous for each d)
+ *            segment s's token j lives in block block_table[kv_off + j/16],
+ *            slot j%16, of both caches
  *   LSE      float32 [n_q_rows, Hq], natural log
  *   GQA      query head h reads KV head h / (Hq/Hkv)
  *   dtype    Q, K, V and O share one dtype (bf16 or fp32); accumulation is
@@ -138,12 +141,15 @@ typedef struct padoc_plan padoc_plan;
    tile_class[tile_class_off[r] + kt] is 1 (full: every token sees all
    tile_keys keys, no mask) or 2 (partial: masked) for each key tile kt below
    ceil(n_keys / tile_keys); tiles past n_keys are never visited.  Work items
-   of different KV heads share token and range records.  Decode
+   of different KV heads share token and range records.  Forward plans: work
+   item i is one workgroup.  Decode plans: work item i is wavefront i%4 of
+   workgroup i/4 (items with ntok == 0 are idle waves).  Decode
    plans write one partial result per (item, column) at slot out_base + column
    and combine, for Q row r and KV head g, the slots comb_slot[comb_ptr[r*Hkv+g]
    .. comb_ptr[r*Hkv+g+1]) (+ head within group) in that order. */
 typedef struct {
-  int32_t tok_begin, ntok, rng_begin, rng_count, kvh, out_base, cost, reserved;
+  int32_t tok_begin, ntok, rng_begin, rng_count, kvh, out_base, cost;
+  int32_t nblk;  /* decode: 32-column blocks the wave computes (1 or 2); forward: 0 */
 } padoc_work_view;
 
 typedef struct {

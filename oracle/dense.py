@@ -302,30 +302,34 @@ def paged_slots(nodes, block_table, block_size: int, bt_off=None):
     return np.concatenate(blk), np.concatenate(slot)
 
 
-def gather_paged(nodes, pool, block_table, block_size: int, bt_off=None) -> np.ndarray:
-    """Read a paged cache ``pool [num_blocks, Hkv, block_size, d]`` back into
-    packed token order ``[T, Hkv, d]`` (fp64)."""
+def gather_paged(nodes, pool, block_table, block_size: int, bt_off=None, d_major: bool = False) -> np.ndarray:
+    """Read a paged cache back into packed token order ``[T, Hkv, d]``
+    (fp64).  Row-major blocks: ``pool [num_blocks, Hkv, block_size, d]``;
+    d-major blocks (``d_major``): ``pool [num_blocks, Hkv, d, block_size]``."""
     blk, slot = paged_slots(nodes, block_table, block_size, bt_off)
     try:
         import torch
         if isinstance(pool, torch.Tensor):
             bi = torch.as_tensor(blk, device=pool.device)
             si = torch.as_tensor(slot, device=pool.device)
-            return pool[bi, :, si, :].to("cpu", torch.float64).numpy()
+            got = pool[bi, :, :, si] if d_major else pool[bi, :, si, :]
+            return got.to("cpu", torch.float64).numpy()
     except ImportError:  # pragma: no cover
         pass
-    return _f64(pool)[blk, :, slot, :]
+    p = _f64(pool)
+    return p[blk, :, :, slot] if d_major else p[blk, :, slot, :]
 
 
 def tree_attention_paged(nodes, q, k_pool, v_pool, block_table, scale: float,
                          num_heads_q: int, num_heads_kv: int, block_size: int = 16,
                          bt_off=None, q_off=None, rows=None):
-    """Decode form: K/V in a paged cache.  Gathers every segment back into
-    packed order with :func:`gather_paged`, then applies
-    :func:`tree_attention`."""
+    """Decode form: K/V in a paged cache, the library's cache format: K blocks
+    row-major ``[num_blocks, Hkv, 16, d]``, V blocks d-major
+    ``[num_blocks, Hkv, d, 16]``.  Gathers every segment back into packed
+    order with :func:`gather_paged`, then applies :func:`tree_attention`."""
     nodes = _as_nodes(nodes)
     k = gather_paged(nodes, k_pool, block_table, block_size, bt_off)
-    v = gather_paged(nodes, v_pool, block_table, block_size, bt_off)
+    v = gather_paged(nodes, v_pool, block_table, block_size, bt_off, d_major=True)
     kv_off, qo = canonical_layout(nodes, 0)
     return tree_attention(nodes, q, k, v, scale, num_heads_q, num_heads_kv,
                           kv_off=kv_off, q_off=qo if q_off is None else q_off, rows=rows)

@@ -22,7 +22,7 @@ F32, BF16 = 0, 1
 SEGMENT_DTYPE = np.dtype([("parent", "<i4"), ("fork", "<i4"), ("len", "<i4"), ("q_len", "<i4"),
                           ("kv_off", "<i8"), ("q_off", "<i8")])
 WORK_DTYPE = np.dtype([("tok_begin", "<i4"), ("ntok", "<i4"), ("rng_begin", "<i4"), ("rng_count", "<i4"),
-                       ("kvh", "<i4"), ("out_base", "<i4"), ("cost", "<i4"), ("reserved", "<i4")])
+                       ("kvh", "<i4"), ("out_base", "<i4"), ("cost", "<i4"), ("nblk", "<i4")])
 RANGE_DTYPE = np.dtype([("kv_start", "<i8"), ("n_keys", "<i4"), ("min_lim", "<i4"), ("lim_off", "<i4"),
                         ("seg", "<i4"), ("key_begin", "<i4"), ("reserved", "<i4")])
 

@@ -5,8 +5,9 @@
 #include "host/plan.hpp"
 
 namespace padoc {
-hipError_t launch_tile_mfma_bf16(const TileParams& p, int n_work, int D, bool paged, bool partial, hipStream_t s);
-hipError_t launch_tile_valu_f32(const TileParams& p, int n_work, int D, bool paged, bool partial, hipStream_t s);
+hipError_t launch_tile_mfma_bf16(const TileParams& p, int n_work, int D, hipStream_t s);
+hipError_t launch_decode_stream_bf16(const TileParams& p, int n_items, int D, hipStream_t s);
+hipError_t launch_tile_valu_f32(const TileParams& p, int n_work, int D, bool paged, hipStream_t s);
 hipError_t launch_lse_combine(const CombineParams& p, int D, bool bf16, hipStream_t s);
 
 namespace {
@@ -62,14 +63,16 @@ padoc_status run(const padoc_plan* P, const void* q, const void* k, const void* 
   tp.G = P->G;
   tp.scale_log2 = P->scale * 1.4426950408889634f;
   const bool paged = P->block_size != 0;
-  const bool partial = P->kind == 1;
+  const bool partial = P->kind == 1;  // decode plans: wave items, split-KV partials
   const int n_work = (int)P->work.size();
   if (t_ev_before && t_ev_after) {
     e = hipEventRecord(t_ev_before, stream);
     if (e != hipSuccess) return hip_fail("hipEventRecord", e);
   }
-  e = P->dtype == PADOC_BF16 ? launch_tile_mfma_bf16(tp, n_work, P->D, paged, partial, stream)
-                             : launch_tile_valu_f32(tp, n_work, P->D, paged, partial, stream);
+  if (P->dtype == PADOC_BF16)
+    e = paged ? launch_decode_stream_bf16(tp, n_work, P->D, stream) : launch_tile_mfma_bf16(tp, n_work, P->D, stream);
+  else
+    e = launch_tile_valu_f32(tp, n_work, P->D, paged, stream);
   if (e != hipSuccess) return hip_fail("tile kernel launch", e);
   if (t_ev_before && t_ev_after) {
     e = hipEventRecord(t_ev_after, stream);

@@ -22,6 +22,7 @@
 #include <map>
 #include <memory>
 #include <new>
+#include <tuple>
 #include <utility>
 
 namespace padoc {
@@ -287,11 +288,21 @@ void build_forward(padoc_plan& P, Builder& B) {
   }
 }
 
+// Decode: wave items.  A wave item is one wavefront's work: the columns
+// (query token x head) of at most 64/G tokens -- or 32/G, computed with one
+// 32-column block, when a private stream's queries fit -- for one KV head
+// against one key chunk.  Four wave items form a workgroup.  The wave items
+// of one page's shared tokens (up to four per group) process the same key
+// chunks in the same workgroup, so the shared prefix and stream keys are
+// fetched from HBM once per chunk and served to the sibling waves by the
+// compute unit's cache.  Private segments (seen only by their own queries)
+// get their own wave items, packed four per workgroup by similar cost.
 void build_decode(padoc_plan& P, Builder& B, const std::vector<std::vector<std::pair<int32_t, int32_t>>>& anc,
                   const padoc_tree_desc* d) {
   const int32_t n = (int32_t)P.seg.size();
-  const int32_t NT = P.tile_tokens;
-  // A segment is shared when a query token of another segment sees any of it.
+  const int32_t G = P.G;
+  const int32_t NT64 = std::max(1, 64 / G);
+  const int32_t NT32 = 32 / G;
   std::vector<int64_t> viewers(n, 0);
   for (int32_t s = 0; s < n; ++s)
     if (P.seg[s].q_len > 0)
@@ -299,14 +310,14 @@ void build_decode(padoc_plan& P, Builder& B, const std::vector<std::vector<std::
         if (a.second > 0) viewers[a.first] += P.seg[s].q_len;
   auto shared = [&](int32_t t) { return viewers[t] > 0; };
   auto priv = [&](int32_t t) { return viewers[t] == 0; };
-
-  // Shared tasks: per page, every query token that sees a shared segment.
   std::vector<int32_t> root(n);
   for (int32_t s = 0; s < n; ++s) root[s] = P.seg[s].parent < 0 ? s : root[P.seg[s].parent];
-  std::vector<Task> shared_tasks, private_tasks;
+
+  // Shared groups: per page, the tokens that see a shared segment, cut into
+  // wave tasks of NT64 tokens, four wave tasks per group.
+  std::vector<std::vector<Task>> groups;
   {
-    std::map<int32_t, Task> per_page;  // root -> tokens in node order
-    std::vector<int32_t> order;
+    std::map<int32_t, Task> per_page;
     for (int32_t s = 0; s < n; ++s) {
       const padoc_segment& sg = P.seg[s];
       if (sg.q_len == 0) continue;
@@ -321,89 +332,163 @@ void build_decode(padoc_plan& P, Builder& B, const std::vector<std::vector<std::
     }
     for (auto& kv : per_page) {
       const Task& all = kv.second;
-      for (size_t b = 0; b < all.seg.size(); b += NT) {
+      std::vector<Task> waves;
+      for (size_t b = 0; b < all.seg.size(); b += NT64) {
         Task t;
-        const size_t e = std::min(all.seg.size(), b + (size_t)NT);
+        const size_t e = std::min(all.seg.size(), b + (size_t)NT64);
         t.seg.assign(all.seg.begin() + b, all.seg.begin() + e);
         t.pos.assign(all.pos.begin() + b, all.pos.begin() + e);
-        shared_tasks.push_back(std::move(t));
-      }
-    }
-    for (int32_t s = 0; s < n; ++s) {
-      const padoc_segment& sg = P.seg[s];
-      if (sg.q_len == 0 || shared(s)) continue;
-      for (int32_t b = sg.len - sg.q_len; b < sg.len; b += NT) {
-        Task t;
-        for (int32_t p = b; p < std::min(sg.len, b + NT); ++p) {
-          t.seg.push_back(s);
-          t.pos.push_back(p);
+        waves.push_back(std::move(t));
+        if (waves.size() == 4) {
+          groups.push_back(std::move(waves));
+          waves.clear();
         }
-        private_tasks.push_back(std::move(t));
       }
+      if (!waves.empty()) groups.push_back(std::move(waves));
     }
   }
-  std::vector<std::vector<VisRange>> svis, pvis;
-  int64_t total = 0;
-  for (const Task& t : shared_tasks) {
-    svis.push_back(B.visible(t, shared));
-    for (const auto& r : svis.back()) total += round_up(r.n_keys, P.tile_keys) * P.Hkv;
+  // Private wave tasks.
+  std::vector<Task> ptasks;
+  std::vector<int32_t> pnb;
+  for (int32_t s = 0; s < n; ++s) {
+    const padoc_segment& sg = P.seg[s];
+    if (sg.q_len == 0 || shared(s)) continue;
+    const bool narrow = NT32 > 0 && sg.q_len <= NT32;
+    const int32_t per = narrow ? NT32 : NT64;
+    for (int32_t b = sg.len - sg.q_len; b < sg.len; b += per) {
+      Task t;
+      for (int32_t p = b; p < std::min(sg.len, b + per); ++p) {
+        t.seg.push_back(s);
+        t.pos.push_back(p);
+      }
+      ptasks.push_back(std::move(t));
+      pnb.push_back(narrow ? 1 : 2);
+    }
   }
-  for (const Task& t : private_tasks) {
+
+  // Visible ranges: per group the union over its tokens (chunk boundaries
+  // are cut on the union so sibling waves stay in step), per wave task its
+  // own limits.
+  std::vector<std::vector<VisRange>> gunion(groups.size());
+  std::vector<std::vector<std::vector<VisRange>>> gvis(groups.size());
+  int64_t total = 0;
+  for (size_t g = 0; g < groups.size(); ++g) {
+    Task all;
+    for (const Task& t : groups[g]) {
+      all.seg.insert(all.seg.end(), t.seg.begin(), t.seg.end());
+      all.pos.insert(all.pos.end(), t.pos.begin(), t.pos.end());
+      gvis[g].push_back(B.visible(t, shared));
+    }
+    gunion[g] = B.visible(all, shared);
+    for (const auto& r : gunion[g]) total += round_up(r.n_keys, P.tile_keys) * P.Hkv;
+  }
+  std::vector<std::vector<VisRange>> pvis;
+  for (const Task& t : ptasks) {
     pvis.push_back(B.visible(t, priv));
-    for (const auto& r : pvis.back()) total += round_up(r.n_keys, P.tile_keys) * P.Hkv;
+    for (const auto& r : pvis.back()) total += round_up(r.n_keys, P.tile_keys) * P.Hkv / 4;
   }
   int64_t CH = d->max_chunk_keys;
   if (CH == 0) {
-    const int64_t target = d->target_workgroups > 0 ? d->target_workgroups : 512;
-    CH = round_up(std::max<int64_t>(1, ceil_div(total, target)), P.tile_keys);
-    CH = std::min<int64_t>(std::max<int64_t>(CH, 256), 16384);
+    const int64_t target = d->target_workgroups > 0 ? d->target_workgroups : 1024;
+    CH = round_up(std::max<int64_t>(1, ceil_div(total, target)), 64);
+    CH = std::min<int64_t>(std::max<int64_t>(CH, 256), 8192);
   }
-
-  // Per (query row, KV head): partial slots in creation order.
-  std::vector<std::vector<int32_t>> comb((size_t)P.num_q_rows * P.Hkv);
-  std::vector<char> sees;
-  auto make_items = [&](const Task& task, const std::vector<VisRange>& vis) {
-    const int32_t ntok = (int32_t)task.seg.size();
-    if (vis.empty()) return;
-    const int32_t tok_begin = B.add_tokens(task);
-    std::vector<std::vector<Piece>> items(1);
+  auto cut = [&](const std::vector<VisRange>& vis) {
+    // [(t, kb, len)] pieces of at most CH keys in total per chunk
+    std::vector<std::vector<std::tuple<int32_t, int32_t, int32_t>>> chunks(1);
     int64_t room = CH;
     for (const auto& r : vis) {
       int32_t kb = 0;
       while (kb < r.n_keys) {
         if (room <= 0) {
-          items.emplace_back();
+          chunks.emplace_back();
           room = CH;
         }
         const int32_t take = (int32_t)std::min<int64_t>(r.n_keys - kb, room);
-        items.back().push_back({&r, kb, take});
+        chunks.back().emplace_back(r.t, kb, take);
         kb += take;
-        room -= round_up(take, P.tile_keys);
+        room -= round_up(take, 64);
       }
     }
-    for (const auto& pieces : items) {
-      if (pieces.empty()) continue;
-      int32_t rb, rc, cost;
-      B.emit_ranges(pieces, ntok, rb, rc, cost, sees);
-      if (rc == 0) continue;
-      for (int32_t g = 0; g < P.Hkv; ++g) {
-        padoc::WorkRec w{};
-        w.tok_begin = tok_begin;
-        w.ntok = ntok;
-        w.rng_begin = rb;
-        w.rng_count = rc;
-        w.kvh = g;
-        w.out_base = (int32_t)P.n_slots;
-        w.cost = cost;
-        for (int32_t i = 0; i < ntok; ++i)
-          if (sees[i]) comb[(size_t)P.toks[tok_begin + i] * P.Hkv + g].push_back(w.out_base + i * P.G);
-        P.n_slots += (int64_t)ntok * P.G;
-        P.work.push_back(w);
-      }
-    }
+    if (chunks.back().empty()) chunks.pop_back();
+    return chunks;
   };
-  for (size_t i = 0; i < shared_tasks.size(); ++i) make_items(shared_tasks[i], svis[i]);
-  for (size_t i = 0; i < private_tasks.size(); ++i) make_items(private_tasks[i], pvis[i]);
+
+  std::vector<std::vector<int32_t>> comb((size_t)P.num_q_rows * P.Hkv);
+  std::vector<char> sees;
+  struct WG {
+    std::vector<padoc::WorkRec> items;
+    int32_t cost;
+  };
+  std::vector<WG> wgs;
+  std::vector<padoc::WorkRec> pitems;
+  // One wave item: returns false if the wave sees nothing in this chunk.
+  auto make_item = [&](const Task& task, int32_t tok_begin, const std::vector<VisRange>& vis,
+                       const std::vector<std::tuple<int32_t, int32_t, int32_t>>& chunk, int32_t kvh, int32_t nb,
+                       padoc::WorkRec& w) {
+    std::vector<Piece> pieces;
+    for (const auto& c : chunk)
+      for (const auto& r : vis)
+        if (r.t == std::get<0>(c)) pieces.push_back({&r, std::get<1>(c), std::get<2>(c)});
+    const int32_t ntok = (int32_t)task.seg.size();
+    int32_t rb, rc, cost;
+    B.emit_ranges(pieces, ntok, rb, rc, cost, sees);
+    if (rc == 0) return false;
+    w = padoc::WorkRec{};
+    w.tok_begin = tok_begin;
+    w.ntok = ntok;
+    w.rng_begin = rb;
+    w.rng_count = rc;
+    w.kvh = kvh;
+    w.out_base = (int32_t)P.n_slots;
+    w.cost = cost;
+    w.nblk = nb;
+    for (int32_t i = 0; i < ntok; ++i)
+      if (sees[i]) comb[(size_t)P.toks[tok_begin + i] * P.Hkv + kvh].push_back(w.out_base + i * G);
+    P.n_slots += (int64_t)ntok * G;
+    return true;
+  };
+  for (size_t g = 0; g < groups.size(); ++g) {
+    std::vector<int32_t> tb;
+    for (const Task& t : groups[g]) tb.push_back(B.add_tokens(t));
+    for (const auto& chunk : cut(gunion[g])) {
+      for (int32_t kvh = 0; kvh < P.Hkv; ++kvh) {
+        WG wg{{}, 0};
+        for (size_t wv = 0; wv < groups[g].size(); ++wv) {
+          padoc::WorkRec w;
+          if (make_item(groups[g][wv], tb[wv], gvis[g][wv], chunk, kvh, 2, w)) {
+            wg.cost = std::max(wg.cost, w.cost);
+            wg.items.push_back(w);
+          }
+        }
+        if (!wg.items.empty()) wgs.push_back(std::move(wg));
+      }
+    }
+  }
+  for (size_t i = 0; i < ptasks.size(); ++i) {
+    const int32_t tb = B.add_tokens(ptasks[i]);
+    for (const auto& chunk : cut(pvis[i]))
+      for (int32_t kvh = 0; kvh < P.Hkv; ++kvh) {
+        padoc::WorkRec w;
+        if (make_item(ptasks[i], tb, pvis[i], chunk, kvh, pnb[i], w)) pitems.push_back(w);
+      }
+  }
+  std::stable_sort(pitems.begin(), pitems.end(),
+                   [](const padoc::WorkRec& a, const padoc::WorkRec& b) { return a.cost > b.cost; });
+  for (size_t i = 0; i < pitems.size(); i += 4) {
+    WG wg{{}, 0};
+    for (size_t j = i; j < std::min(pitems.size(), i + 4); ++j) {
+      wg.cost = std::max(wg.cost, pitems[j].cost);
+      wg.items.push_back(pitems[j]);
+    }
+    wgs.push_back(std::move(wg));
+  }
+  // Costliest workgroups first (longest-processing-time order).
+  std::stable_sort(wgs.begin(), wgs.end(), [](const WG& a, const WG& b) { return a.cost > b.cost; });
+  for (const WG& wg : wgs) {
+    for (const auto& w : wg.items) P.work.push_back(w);
+    for (size_t j = wg.items.size(); j < 4; ++j) P.work.push_back(padoc::WorkRec{});  // idle wave
+  }
 
   P.comb_ptr.assign(comb.size() + 1, 0);
   for (size_t r = 0; r < comb.size(); ++r) P.comb_ptr[r + 1] = P.comb_ptr[r] + (int32_t)comb[r].size();
@@ -508,6 +593,10 @@ extern "C" padoc_status padoc_plan_create(const padoc_tree_desc* d, padoc_plan**
     P->num_q_rows = d->num_q_rows;
     P->block_table_len = d->block_table_len;
     P->seg.assign(d->seg, d->seg + d->n_seg);
+    if (P->kind == 1) {  // decode: wave items of at most 64 columns, 32-key steps
+      P->tile_cols = 64;
+      P->tile_keys = 32;
+    }
     P->tile_tokens = std::max(1, P->tile_cols / P->G);
     std::vector<std::vector<std::pair<int32_t, int32_t>>> anc(d->n_seg);
     for (int32_t s = 0; s < d->n_seg; ++s) {
@@ -526,9 +615,11 @@ extern "C" padoc_status padoc_plan_create(const padoc_tree_desc* d, padoc_plan**
     if ((int64_t)P->lims.size() > kI32Max || (int64_t)P->ranges.size() > kI32Max)
       return set_error(PADOC_ERR_ARG, "schedule too large");
     // Costliest items first: the hardware dispatcher then assigns work
-    // greedily to the first free compute unit (longest-processing-time order).
-    std::stable_sort(P->work.begin(), P->work.end(),
-                     [](const padoc::WorkRec& a, const padoc::WorkRec& b) { return a.cost > b.cost; });
+    // greedily to the first free compute unit (longest-processing-time
+    // order).  Decode items are already ordered by workgroup.
+    if (P->kind == 0)
+      std::stable_sort(P->work.begin(), P->work.end(),
+                       [](const padoc::WorkRec& a, const padoc::WorkRec& b) { return a.cost > b.cost; });
     serialise(*P);
     *out = P.release();
   } catch (const std::bad_alloc&) {

@@ -1,4 +1,4 @@
-// bf16 tree-attention tile kernel for gfx950 (CDNA4) matrix cores.
+// bf16 packed-forward tile kernel for gfx950 (CDNA4) matrix cores.
 //
 // One workgroup (4 waves) processes one work item: up to 256 columns
 // (query token x head of one KV-head group; GQA heads of a token share every
@@ -316,25 +316,12 @@ __global__ __launch_bounds__(256, 1) void tile_mfma_bf16_kernel(TileParams p) {
   }
 }
 
-hipError_t launch_tile_mfma_bf16(const TileParams& p, int n_work, int D, bool paged, bool partial,
-                                 hipStream_t stream) {
+hipError_t launch_tile_mfma_bf16(const TileParams& p, int n_work, int D, hipStream_t stream) {
   const dim3 grid(n_work), block(256);
-#define PADOC_LAUNCH(DD, PG, PT) \
-  hipLaunchKernelGGL((tile_mfma_bf16_kernel<DD, PG, PT>), grid, block, 0, stream, p)
-  if (D == 64) {
-    if (paged) {
-      if (partial) PADOC_LAUNCH(64, true, true); else PADOC_LAUNCH(64, true, false);
-    } else {
-      if (partial) PADOC_LAUNCH(64, false, true); else PADOC_LAUNCH(64, false, false);
-    }
-  } else {
-    if (paged) {
-      if (partial) PADOC_LAUNCH(128, true, true); else PADOC_LAUNCH(128, true, false);
-    } else {
-      if (partial) PADOC_LAUNCH(128, false, true); else PADOC_LAUNCH(128, false, false);
-    }
-  }
-#undef PADOC_LAUNCH
+  if (D == 64)
+    hipLaunchKernelGGL((tile_mfma_bf16_kernel<64, false, false>), grid, block, 0, stream, p);
+  else
+    hipLaunchKernelGGL((tile_mfma_bf16_kernel<128, false, false>), grid, block, 0, stream, p);
   return hipGetLastError();
 }
 

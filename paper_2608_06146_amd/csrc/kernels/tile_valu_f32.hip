@@ -1,7 +1,10 @@
 // fp32 tile kernel: one thread per (query token, head) column of a work item,
 // keys visited one by one with an exact online softmax in fp32 on the vector
-// ALUs.  This is the fp32 path of both entry points (the MFMA path is bf16);
-// it reads the same schedule as the bf16 kernel.
+// ALUs.  This is the fp32 path of both entry points (the MFMA paths are
+// bf16); it reads the same schedules as the bf16 kernels: packed forward
+// items of up to 256 columns (one per workgroup), decode wave items of up to
+// 64 columns (four per workgroup, one per wavefront) over the paged cache
+// (K blocks [16][d], V blocks d-major [d][16]).
 //
 // Per column and visible key j (App. E Attn equation, with the scale applied
 // in log2 units): s = scale*log2(e) * q.k_j; m' = max(m, s);
@@ -10,10 +13,11 @@
 
 namespace padoc {
 
-template <int D, bool PAGED, bool PARTIAL>
+template <int D, bool PAGED>
 __global__ __launch_bounds__(256) void tile_valu_f32_kernel(TileParams p) {
-  const WorkRec w = p.work[blockIdx.x];
-  const int c = threadIdx.x;
+  constexpr bool PARTIAL = PAGED;  // decode plans write split-KV partials
+  const WorkRec w = PAGED ? p.work[blockIdx.x * 4 + (threadIdx.x >> 6)] : p.work[blockIdx.x];
+  const int c = PAGED ? (threadIdx.x & 63) : threadIdx.x;
   const int t = c / p.G;
   const int h = c - t * p.G;
   if (t >= w.ntok) return;  // no barriers below
@@ -41,7 +45,6 @@ __global__ __launch_bounds__(256) void tile_valu_f32_kernel(TileParams p) {
     for (int j = 0; j < lim; ++j) {
       const int64_t off = key_offset<D, PAGED>(R, j, w.kvh, p.Hkv, p.block_table);
       const float4* kp = reinterpret_cast<const float4*>(K + off);
-      const float4* vp = reinterpret_cast<const float4*>(V + off);
       float s = 0.f;
 #pragma unroll
       for (int i = 0; i < D / 4; ++i) {
@@ -52,6 +55,16 @@ __global__ __launch_bounds__(256) void tile_valu_f32_kernel(TileParams p) {
         s = fmaf(q[4 * i + 3], x.w, s);
       }
       s *= p.scale_log2;
+      // V row j: packed [T, Hkv, D]; paged d-major blocks [Hkv][D][16]
+      int64_t voff, vstride;
+      if constexpr (PAGED) {
+        const int64_t blk = p.block_table[R.kv_start + (j >> 4)];
+        voff = (blk * p.Hkv + w.kvh) * (int64_t)D * kBlock + (j & 15);
+        vstride = kBlock;
+      } else {
+        voff = off;
+        vstride = 1;
+      }
       if (s > m) {
         const float a = fast_exp2(m - s);
         l *= a;
@@ -62,13 +75,7 @@ __global__ __launch_bounds__(256) void tile_valu_f32_kernel(TileParams p) {
       const float e = fast_exp2(s - m);
       l += e;
 #pragma unroll
-      for (int i = 0; i < D / 4; ++i) {
-        const float4 x = vp[i];
-        acc[4 * i] = fmaf(e, x.x, acc[4 * i]);
-        acc[4 * i + 1] = fmaf(e, x.y, acc[4 * i + 1]);
-        acc[4 * i + 2] = fmaf(e, x.z, acc[4 * i + 2]);
-        acc[4 * i + 3] = fmaf(e, x.w, acc[4 * i + 3]);
-      }
+      for (int dd = 0; dd < D; ++dd) acc[dd] = fmaf(e, V[voff + dd * vstride], acc[dd]);
     }
   }
   if constexpr (PARTIAL) {
@@ -88,25 +95,15 @@ __global__ __launch_bounds__(256) void tile_valu_f32_kernel(TileParams p) {
   }
 }
 
-hipError_t launch_tile_valu_f32(const TileParams& p, int n_work, int D, bool paged, bool partial,
-                                hipStream_t stream) {
-  const dim3 grid(n_work), block(256);
-#define PADOC_LAUNCH(DD, PG, PT) \
-  hipLaunchKernelGGL((tile_valu_f32_kernel<DD, PG, PT>), grid, block, 0, stream, p)
+hipError_t launch_tile_valu_f32(const TileParams& p, int n_work, int D, bool paged, hipStream_t stream) {
+  const dim3 grid(paged ? (n_work + 3) / 4 : n_work), block(256);
   if (D == 64) {
-    if (paged) {
-      if (partial) PADOC_LAUNCH(64, true, true); else PADOC_LAUNCH(64, true, false);
-    } else {
-      if (partial) PADOC_LAUNCH(64, false, true); else PADOC_LAUNCH(64, false, false);
-    }
+    if (paged) hipLaunchKernelGGL((tile_valu_f32_kernel<64, true>), grid, block, 0, stream, p);
+    else hipLaunchKernelGGL((tile_valu_f32_kernel<64, false>), grid, block, 0, stream, p);
   } else {
-    if (paged) {
-      if (partial) PADOC_LAUNCH(128, true, true); else PADOC_LAUNCH(128, true, false);
-    } else {
-      if (partial) PADOC_LAUNCH(128, false, true); else PADOC_LAUNCH(128, false, false);
-    }
+    if (paged) hipLaunchKernelGGL((tile_valu_f32_kernel<128, true>), grid, block, 0, stream, p);
+    else hipLaunchKernelGGL((tile_valu_f32_kernel<128, false>), grid, block, 0, stream, p);
   }
-#undef PADOC_LAUNCH
   return hipGetLastError();
 }
 

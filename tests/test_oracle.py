@@ -388,10 +388,10 @@ def test_P8_paged_equals_packed():
         pool_n = nb + 7
         ids = syn.draw_block_ids(nb, pool_n, seed)
         pool_k = np.full((pool_n, Hkv, 16, d), np.nan)
-        pool_v = np.full((pool_n, Hkv, 16, d), np.nan)
+        pool_v = np.full((pool_n, Hkv, d, 16), np.nan)      # V blocks are d-major
         blk, slot = ot.paged_slots(nodes, ids, 16)
         pool_k[blk, :, slot, :] = k
-        pool_v[blk, :, slot, :] = v
+        pool_v[blk, :, :, slot] = v
         O_d, L_d = oracle.tree_attention_paged(nodes, q, pool_k, pool_v, ids, 0.3, 4, Hkv, 16)
         np.testing.assert_allclose(O_d, O_p, atol=1e-12)
         np.testing.assert_allclose(L_d, L_p, atol=1e-12)
