@@ -111,7 +111,8 @@ typedef struct {
   int32_t n_seg;
   const padoc_segment* seg;      /* host memory, read during padoc_plan_create  */
   int32_t num_heads_q;           /* Hq > 0                                      */
-  int32_t num_heads_kv;          /* Hkv > 0, Hq % Hkv == 0, Hq/Hkv <= 64        */
+  int32_t num_heads_kv;          /* Hkv > 0, Hq % Hkv == 0, Hq/Hkv <= 64
+                                    (<= 32 for paged decode plans)             */
   int32_t head_dim;              /* 64 or 128                                   */
   float softmax_scale;           /* > 0, finite; the paper uses 1/sqrt(d)       */
   padoc_dtype dtype;
@@ -142,14 +143,14 @@ typedef struct padoc_plan padoc_plan;
    tile_keys keys, no mask) or 2 (partial: masked) for each key tile kt below
    ceil(n_keys / tile_keys); tiles past n_keys are never visited.  Work items
    of different KV heads share token and range records.  Forward plans: work
-   item i is one workgroup.  Decode plans: work item i is wavefront i%4 of
-   workgroup i/4 (items with ntok == 0 are idle waves).  Decode
+   item i is one workgroup.  Decode plans: work item i is wavefront i%8 of
+   workgroup i/8 (items with ntok == 0 are idle waves).  Decode
    plans write one partial result per (item, column) at slot out_base + column
    and combine, for Q row r and KV head g, the slots comb_slot[comb_ptr[r*Hkv+g]
    .. comb_ptr[r*Hkv+g+1]) (+ head within group) in that order. */
 typedef struct {
   int32_t tok_begin, ntok, rng_begin, rng_count, kvh, out_base, cost;
-  int32_t nblk;  /* decode: 32-column blocks the wave computes (1 or 2); forward: 0 */
+  int32_t nblk;  /* decode: 32-column blocks the wave computes (1); forward: 0 */
 } padoc_work_view;
 
 typedef struct {

@@ -174,6 +174,9 @@ padoc_status validate(const padoc_tree_desc* d) {
     return set_error(PADOC_ERR_SHAPE, "Hq=%d is not a multiple of Hkv=%d", d->num_heads_q, d->num_heads_kv);
   if (d->num_heads_q / d->num_heads_kv > 64)
     return set_error(PADOC_ERR_SHAPE, "Hq/Hkv=%d exceeds 64", d->num_heads_q / d->num_heads_kv);
+  if (d->block_size != 0 && d->num_heads_q / d->num_heads_kv > 32)
+    return set_error(PADOC_ERR_SHAPE, "decode (paged) plans need Hq/Hkv <= 32 (got %d)",
+                     d->num_heads_q / d->num_heads_kv);
   if (d->head_dim != 64 && d->head_dim != 128)
     return set_error(PADOC_ERR_SHAPE, "head_dim=%d is not 64 or 128", d->head_dim);
   if (!std::isfinite(d->softmax_scale) || !(d->softmax_scale > 0.f))
@@ -289,20 +292,19 @@ void build_forward(padoc_plan& P, Builder& B) {
 }
 
 // Decode: wave items.  A wave item is one wavefront's work: the columns
-// (query token x head) of at most 64/G tokens -- or 32/G, computed with one
-// 32-column block, when a private stream's queries fit -- for one KV head
-// against one key chunk.  Four wave items form a workgroup.  The wave items
-// of one page's shared tokens (up to four per group) process the same key
+// (query token x head) of at most 32/G tokens for one KV head against one key
+// chunk.  kDecodeWaves wave items form a workgroup.  The wave items of one
+// page's shared tokens (up to kDecodeWaves per group) process the same key
 // chunks in the same workgroup, so the shared prefix and stream keys are
 // fetched from HBM once per chunk and served to the sibling waves by the
 // compute unit's cache.  Private segments (seen only by their own queries)
-// get their own wave items, packed four per workgroup by similar cost.
+// get their own wave items, packed kDecodeWaves per workgroup by similar cost.
 void build_decode(padoc_plan& P, Builder& B, const std::vector<std::vector<std::pair<int32_t, int32_t>>>& anc,
                   const padoc_tree_desc* d) {
   const int32_t n = (int32_t)P.seg.size();
   const int32_t G = P.G;
-  const int32_t NT64 = std::max(1, 64 / G);
-  const int32_t NT32 = 32 / G;
+  const int32_t NT = P.tile_tokens;  // 32 / G tokens per wave item
+  const int32_t NW = kDecodeWaves;
   std::vector<int64_t> viewers(n, 0);
   for (int32_t s = 0; s < n; ++s)
     if (P.seg[s].q_len > 0)
@@ -314,7 +316,7 @@ void build_decode(padoc_plan& P, Builder& B, const std::vector<std::vector<std::
   for (int32_t s = 0; s < n; ++s) root[s] = P.seg[s].parent < 0 ? s : root[P.seg[s].parent];
 
   // Shared groups: per page, the tokens that see a shared segment, cut into
-  // wave tasks of NT64 tokens, four wave tasks per group.
+  // wave tasks of NT tokens, NW wave tasks per group.
   std::vector<std::vector<Task>> groups;
   {
     std::map<int32_t, Task> per_page;
@@ -333,13 +335,13 @@ void build_decode(padoc_plan& P, Builder& B, const std::vector<std::vector<std::
     for (auto& kv : per_page) {
       const Task& all = kv.second;
       std::vector<Task> waves;
-      for (size_t b = 0; b < all.seg.size(); b += NT64) {
+      for (size_t b = 0; b < all.seg.size(); b += NT) {
         Task t;
-        const size_t e = std::min(all.seg.size(), b + (size_t)NT64);
+        const size_t e = std::min(all.seg.size(), b + (size_t)NT);
         t.seg.assign(all.seg.begin() + b, all.seg.begin() + e);
         t.pos.assign(all.pos.begin() + b, all.pos.begin() + e);
         waves.push_back(std::move(t));
-        if (waves.size() == 4) {
+        if ((int32_t)waves.size() == NW) {
           groups.push_back(std::move(waves));
           waves.clear();
         }
@@ -349,20 +351,16 @@ void build_decode(padoc_plan& P, Builder& B, const std::vector<std::vector<std::
   }
   // Private wave tasks.
   std::vector<Task> ptasks;
-  std::vector<int32_t> pnb;
   for (int32_t s = 0; s < n; ++s) {
     const padoc_segment& sg = P.seg[s];
     if (sg.q_len == 0 || shared(s)) continue;
-    const bool narrow = NT32 > 0 && sg.q_len <= NT32;
-    const int32_t per = narrow ? NT32 : NT64;
-    for (int32_t b = sg.len - sg.q_len; b < sg.len; b += per) {
+    for (int32_t b = sg.len - sg.q_len; b < sg.len; b += NT) {
       Task t;
-      for (int32_t p = b; p < std::min(sg.len, b + per); ++p) {
+      for (int32_t p = b; p < std::min(sg.len, b + NT); ++p) {
         t.seg.push_back(s);
         t.pos.push_back(p);
       }
       ptasks.push_back(std::move(t));
-      pnb.push_back(narrow ? 1 : 2);
     }
   }
 
@@ -385,11 +383,11 @@ void build_decode(padoc_plan& P, Builder& B, const std::vector<std::vector<std::
   std::vector<std::vector<VisRange>> pvis;
   for (const Task& t : ptasks) {
     pvis.push_back(B.visible(t, priv));
-    for (const auto& r : pvis.back()) total += round_up(r.n_keys, P.tile_keys) * P.Hkv / 4;
+    for (const auto& r : pvis.back()) total += round_up(r.n_keys, P.tile_keys) * P.Hkv / NW;
   }
   int64_t CH = d->max_chunk_keys;
   if (CH == 0) {
-    const int64_t target = d->target_workgroups > 0 ? d->target_workgroups : 1024;
+    const int64_t target = d->target_workgroups > 0 ? d->target_workgroups : 512;
     CH = round_up(std::max<int64_t>(1, ceil_div(total, target)), 64);
     CH = std::min<int64_t>(std::max<int64_t>(CH, 256), 8192);
   }
@@ -424,7 +422,7 @@ void build_decode(padoc_plan& P, Builder& B, const std::vector<std::vector<std::
   std::vector<padoc::WorkRec> pitems;
   // One wave item: returns false if the wave sees nothing in this chunk.
   auto make_item = [&](const Task& task, int32_t tok_begin, const std::vector<VisRange>& vis,
-                       const std::vector<std::tuple<int32_t, int32_t, int32_t>>& chunk, int32_t kvh, int32_t nb,
+                       const std::vector<std::tuple<int32_t, int32_t, int32_t>>& chunk, int32_t kvh,
                        padoc::WorkRec& w) {
     std::vector<Piece> pieces;
     for (const auto& c : chunk)
@@ -442,7 +440,7 @@ void build_decode(padoc_plan& P, Builder& B, const std::vector<std::vector<std::
     w.kvh = kvh;
     w.out_base = (int32_t)P.n_slots;
     w.cost = cost;
-    w.nblk = nb;
+    w.nblk = 1;
     for (int32_t i = 0; i < ntok; ++i)
       if (sees[i]) comb[(size_t)P.toks[tok_begin + i] * P.Hkv + kvh].push_back(w.out_base + i * G);
     P.n_slots += (int64_t)ntok * G;
@@ -456,7 +454,7 @@ void build_decode(padoc_plan& P, Builder& B, const std::vector<std::vector<std::
         WG wg{{}, 0};
         for (size_t wv = 0; wv < groups[g].size(); ++wv) {
           padoc::WorkRec w;
-          if (make_item(groups[g][wv], tb[wv], gvis[g][wv], chunk, kvh, 2, w)) {
+          if (make_item(groups[g][wv], tb[wv], gvis[g][wv], chunk, kvh, w)) {
             wg.cost = std::max(wg.cost, w.cost);
             wg.items.push_back(w);
           }
@@ -470,14 +468,14 @@ void build_decode(padoc_plan& P, Builder& B, const std::vector<std::vector<std::
     for (const auto& chunk : cut(pvis[i]))
       for (int32_t kvh = 0; kvh < P.Hkv; ++kvh) {
         padoc::WorkRec w;
-        if (make_item(ptasks[i], tb, pvis[i], chunk, kvh, pnb[i], w)) pitems.push_back(w);
+        if (make_item(ptasks[i], tb, pvis[i], chunk, kvh, w)) pitems.push_back(w);
       }
   }
   std::stable_sort(pitems.begin(), pitems.end(),
                    [](const padoc::WorkRec& a, const padoc::WorkRec& b) { return a.cost > b.cost; });
-  for (size_t i = 0; i < pitems.size(); i += 4) {
+  for (size_t i = 0; i < pitems.size(); i += NW) {
     WG wg{{}, 0};
-    for (size_t j = i; j < std::min(pitems.size(), i + 4); ++j) {
+    for (size_t j = i; j < std::min(pitems.size(), i + (size_t)NW); ++j) {
       wg.cost = std::max(wg.cost, pitems[j].cost);
       wg.items.push_back(pitems[j]);
     }
@@ -487,7 +485,7 @@ void build_decode(padoc_plan& P, Builder& B, const std::vector<std::vector<std::
   std::stable_sort(wgs.begin(), wgs.end(), [](const WG& a, const WG& b) { return a.cost > b.cost; });
   for (const WG& wg : wgs) {
     for (const auto& w : wg.items) P.work.push_back(w);
-    for (size_t j = wg.items.size(); j < 4; ++j) P.work.push_back(padoc::WorkRec{});  // idle wave
+    for (size_t j = wg.items.size(); j < (size_t)NW; ++j) P.work.push_back(padoc::WorkRec{});  // idle wave
   }
 
   P.comb_ptr.assign(comb.size() + 1, 0);
@@ -593,8 +591,8 @@ extern "C" padoc_status padoc_plan_create(const padoc_tree_desc* d, padoc_plan**
     P->num_q_rows = d->num_q_rows;
     P->block_table_len = d->block_table_len;
     P->seg.assign(d->seg, d->seg + d->n_seg);
-    if (P->kind == 1) {  // decode: wave items of at most 64 columns, 32-key steps
-      P->tile_cols = 64;
+    if (P->kind == 1) {  // decode: wave items of at most 32 columns, 32-key steps
+      P->tile_cols = 32;
       P->tile_keys = 32;
     }
     P->tile_tokens = std::max(1, P->tile_cols / P->G);

@@ -1,6 +1,6 @@
 // Split-KV decode kernel over the paged cache, one wave item per wavefront.
 //
-// A wave item is up to 64 columns (query token x head of one KV-head group)
+// A wave item is up to 32 columns (query token x head of one KV-head group)
 // against one key chunk (App. E: one decode step of the live streams; Attn
 // equation with the ancestor mask).  Each wavefront streams its keys straight
 // from HBM into matrix-core operand registers, 32 keys per step, and keeps
@@ -15,6 +15,8 @@
 //                     d-major V block ([d][16 slots]) delivers as one 16-byte
 //                     load per lane -- no LDS, no transposes, no barriers.
 //
+// The B operand (Q fragments) is kept in a per-wave LDS slice rather than in
+// registers, so two 8-wave workgroups' worth of waves fit per SIMD pair.
 // Waves of one workgroup that belong to the same page's shared group stream
 // identical addresses in step, so the prefix and layout-stream keys are read
 // from HBM once and served to the sibling waves from the compute unit's
@@ -36,9 +38,9 @@ __device__ __forceinline__ int perm_key(int m) { return (m & ~12) | ((m & 4) << 
 
 __device__ __forceinline__ bf16x8_t as_bf16x8(const uint4& u) { return *reinterpret_cast<const bf16x8_t*>(&u); }
 
-// Zero the bf16 elements at positions >= keep (0..8) of an 8-element chunk.
+// Zero the bf16 elements at positions >= keep of an 8-element chunk (keep
+// may be <= 0 or >= 8).
 __device__ __forceinline__ uint4 keep_first(uint4 u, int keep) {
-  if (keep >= 8) return u;
   uint32_t w[4] = {u.x, u.y, u.z, u.w};
 #pragma unroll
   for (int i = 0; i < 4; ++i) {
@@ -49,16 +51,12 @@ __device__ __forceinline__ uint4 keep_first(uint4 u, int keep) {
   return make_uint4(w[0], w[1], w[2], w[3]);
 }
 
-template <int D>
-struct StepRegs {
-  uint4 k[D / 16];        // K operand: this lane's key row, d = kk*16 + hf*8 .. +7
-  uint4 v[D / 32][2];     // V^T operand: d = db*32 + l32, keys 16j + 8hf .. +7
-};
-
 template <int D, int NB>
-__device__ __forceinline__ void stream_item(const TileParams& p, const WorkRec& w, const int lane) {
+__device__ __forceinline__ void stream_item(const TileParams& p, const WorkRec& w, const int lane,
+                                            uint16_t* __restrict__ qs) {
   constexpr int NKK = D / 16;
   constexpr int NDB = D / 32;
+  constexpr int CPR = D / 8;  // 16-byte chunks per Q row
   const int l32 = lane & 31, hf = lane >> 5;
   const int G = p.G;
   const int kvh = w.kvh;
@@ -79,51 +77,56 @@ __device__ __forceinline__ void stream_item(const TileParams& p, const WorkRec& 
     qrow[nb] = valid[nb] ? p.toks[w.tok_begin + t] : 0;
     hq[nb] = kvh * G + (c - t * G);
   }
-  bf16x8_t bq[NB][NKK];
+  // Q tile of this wave in LDS: row = column l32 (32 rows), 16-byte chunk c
+  // of row r stored at chunk c ^ (r % CPR) so the fragment reads below hit
+  // distinct banks.  Lane (l32, hf) writes half hf of its row.
   const uint16_t* Q = static_cast<const uint16_t*>(p.q);
+  {
+    const uint16_t* qp = Q + ((int64_t)qrow[0] * p.Hq + hq[0]) * D;
 #pragma unroll
-  for (int nb = 0; nb < NB; ++nb) {
-    const uint16_t* qp = Q + ((int64_t)qrow[nb] * p.Hq + hq[nb]) * D + hf * 8;
-#pragma unroll
-    for (int kk = 0; kk < NKK; ++kk) {
-      const uint4 z = valid[nb] ? *reinterpret_cast<const uint4*>(qp + kk * 16) : make_uint4(0, 0, 0, 0);
-      bq[nb][kk] = as_bf16x8(z);
+    for (int i = 0; i < CPR / 2; ++i) {
+      const int c = hf * (CPR / 2) + i;
+      const uint4 z = valid[0] ? *reinterpret_cast<const uint4*>(qp + c * 8) : make_uint4(0, 0, 0, 0);
+      *reinterpret_cast<uint4*>(qs + l32 * D + ((c ^ (l32 % CPR)) * 8)) = z;
     }
   }
+  auto qfrag = [&](int kk) -> bf16x8_t {
+    const int c = 2 * kk + hf;  // d = kk*16 + hf*8 .. +7
+    return as_bf16x8(*reinterpret_cast<const uint4*>(qs + l32 * D + ((c ^ (l32 % CPR)) * 8)));
+  };
 
   const int kperm = perm_key(l32);  // key of this lane's K row within a step
 
-  auto load_step = [&](const RangeRec& R, int kb, StepRegs<D>& s) {
+  // Loads of one 32-key step, branch-free: addresses are clamped to a valid
+  // block of the range and lanes past its end are zeroed after the load.
+  // K and V each have one register set; the next step's K is loaded right
+  // after the score MFMAs consumed the current K, the next V right after the
+  // PV MFMAs consumed the current V, so each load has about one step of
+  // compute to arrive.
+  uint4 kreg[NKK];
+  uint4 vreg[NDB][2];
+  int64_t vb0 = 0, vb1 = 0;  // blocks of the step whose V is loaded next
+  auto load_k = [&](const RangeRec& R, int kb) {
     const int nk = R.n_keys;
     const int64_t base = R.kv_start + (kb >> 4);
-    const int64_t b0 = bt[base];
-    const int64_t b1 = (kb + 16 < nk) ? (int64_t)bt[base + 1] : b0;
-    // K rows
-    const int j = kb + kperm;
-    if (j < nk) {
-      const int64_t blk = (kperm & 16) ? b1 : b0;
-      const uint16_t* kp = Kc + ((blk * Hkv + kvh) * kBlock + (kperm & 15)) * D + hf * 8;
+    vb0 = bt[base];
+    vb1 = bt[base + ((kb + 16 < nk) ? 1 : 0)];
+    const bool ok = kb + kperm < nk;
+    const uint16_t* kp = Kc + (((kperm & 16) ? vb1 : vb0) * Hkv + kvh) * (kBlock * D) + (kperm & 15) * D + hf * 8;
 #pragma unroll
-      for (int kk = 0; kk < NKK; ++kk) s.k[kk] = *reinterpret_cast<const uint4*>(kp + kk * 16);
-    } else {
-#pragma unroll
-      for (int kk = 0; kk < NKK; ++kk) s.k[kk] = make_uint4(0, 0, 0, 0);
+    for (int kk = 0; kk < NKK; ++kk) {
+      const uint4 x = *reinterpret_cast<const uint4*>(kp + kk * 16);
+      kreg[kk] = ok ? x : make_uint4(0, 0, 0, 0);
     }
-    // V^T rows (d-major blocks)
+  };
+  auto load_v = [&](int nk, int kb) {
 #pragma unroll
     for (int jj = 0; jj < 2; ++jj) {
-      const int first = kb + 16 * jj + 8 * hf;  // first key of this lane's 8
-      const int keep = nk - first;
-      const int64_t blk = jj ? b1 : b0;
-      if (keep > 0) {
-        const uint16_t* vp = Vc + ((blk * Hkv + kvh) * D + l32) * kBlock + 8 * hf;
+      const int keep = nk - (kb + 16 * jj + 8 * hf);
+      const uint16_t* vp = Vc + ((jj ? vb1 : vb0) * Hkv + kvh) * (kBlock * D) + l32 * kBlock + 8 * hf;
 #pragma unroll
-        for (int db = 0; db < NDB; ++db)
-          s.v[db][jj] = keep_first(*reinterpret_cast<const uint4*>(vp + (int64_t)db * 32 * kBlock), keep);
-      } else {
-#pragma unroll
-        for (int db = 0; db < NDB; ++db) s.v[db][jj] = make_uint4(0, 0, 0, 0);
-      }
+      for (int db = 0; db < NDB; ++db)
+        vreg[db][jj] = keep_first(*reinterpret_cast<const uint4*>(vp + db * 32 * kBlock), keep);
     }
   };
 
@@ -148,9 +151,9 @@ __device__ __forceinline__ void stream_item(const TileParams& p, const WorkRec& 
       lim[nb] = R.lim_off < 0 ? R.n_keys : (valid[nb] ? p.lims[R.lim_off + tok[nb]] : 0);
   };
   load_lims();
-  StepRegs<D> cur, nxt;
-  load_step(R, 0, cur);
   const float sl2 = p.scale_log2;
+  load_k(R, 0);
+  load_v(R.n_keys, 0);
 
   while (true) {
     int nri = ri, nst = st + 1;
@@ -164,8 +167,6 @@ __device__ __forceinline__ void stream_item(const TileParams& p, const WorkRec& 
       else
         has_next = false;
     }
-    if (has_next) load_step(NR, nst * 32, nxt);
-
     const int kb = st * 32;
     f32x16_t S[NB];
 #pragma unroll
@@ -174,10 +175,11 @@ __device__ __forceinline__ void stream_item(const TileParams& p, const WorkRec& 
       for (int i = 0; i < 16; ++i) S[nb][i] = 0.f;
 #pragma unroll
     for (int kk = 0; kk < NKK; ++kk) {
-      const bf16x8_t a = as_bf16x8(cur.k[kk]);
-#pragma unroll
-      for (int nb = 0; nb < NB; ++nb) S[nb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, bq[nb][kk], S[nb], 0, 0, 0);
+      const bf16x8_t a = as_bf16x8(kreg[kk]);
+      S[0] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, qfrag(kk), S[0], 0, 0, 0);
     }
+    if (has_next) load_k(NR, nst * 32);  // also selects the next step's blocks for load_v
+
     if (kb + 32 > R.min_lim) {
 #pragma unroll
       for (int nb = 0; nb < NB; ++nb)
@@ -220,21 +222,20 @@ __device__ __forceinline__ void stream_item(const TileParams& p, const WorkRec& 
       }
 #pragma unroll
       for (int db = 0; db < NDB; ++db) {
-        const bf16x8_t a = as_bf16x8(cur.v[db][jj]);
+        const bf16x8_t a = as_bf16x8(vreg[db][jj]);
 #pragma unroll
         for (int nb = 0; nb < NB; ++nb)
           acc[db][nb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, pb[nb], acc[db][nb], 0, 0, 0);
       }
     }
-
     if (!has_next) break;
+    load_v(NR.n_keys, nst * 32);
     if (nri != ri) {
       R = NR;
       ri = nri;
       load_lims();
     }
     st = nst;
-    cur = nxt;
   }
 
 #pragma unroll
@@ -259,21 +260,19 @@ __device__ __forceinline__ void stream_item(const TileParams& p, const WorkRec& 
 }
 
 template <int D>
-__global__ __launch_bounds__(256, 1) void decode_stream_kernel(TileParams p) {
+__global__ __launch_bounds__(64 * kDecodeWaves) void decode_stream_kernel(TileParams p) {
+  __shared__ __attribute__((aligned(16))) uint16_t qs[kDecodeWaves][32 * D];
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int lane = threadIdx.x & 63;
-  const WorkRec w = p.work[blockIdx.x * 4 + wave];
+  const WorkRec w = p.work[blockIdx.x * kDecodeWaves + wave];
   if (w.ntok <= 0 || w.rng_count <= 0) return;  // idle wave; no barriers in this kernel
-  if (w.nblk == 1)
-    stream_item<D, 1>(p, w, lane);
-  else
-    stream_item<D, 2>(p, w, lane);
+  stream_item<D, 1>(p, w, lane, qs[wave]);
 }
 
 }  // namespace
 
 hipError_t launch_decode_stream_bf16(const TileParams& p, int n_items, int D, hipStream_t stream) {
-  const dim3 grid((n_items + 3) / 4), block(256);
+  const dim3 grid((n_items + kDecodeWaves - 1) / kDecodeWaves), block(64 * kDecodeWaves);
   if (D == 64)
     hipLaunchKernelGGL((decode_stream_kernel<64>), grid, block, 0, stream, p);
   else

@@ -3,7 +3,7 @@
 // ALUs.  This is the fp32 path of both entry points (the MFMA paths are
 // bf16); it reads the same schedules as the bf16 kernels: packed forward
 // items of up to 256 columns (one per workgroup), decode wave items of up to
-// 64 columns (four per workgroup, one per wavefront) over the paged cache
+// 32 columns (eight per workgroup, one per wavefront) over the paged cache
 // (K blocks [16][d], V blocks d-major [d][16]).
 //
 // Per column and visible key j (App. E Attn equation, with the scale applied
@@ -14,9 +14,10 @@
 namespace padoc {
 
 template <int D, bool PAGED>
-__global__ __launch_bounds__(256) void tile_valu_f32_kernel(TileParams p) {
+__global__ __launch_bounds__(512) void tile_valu_f32_kernel(TileParams p) {
   constexpr bool PARTIAL = PAGED;  // decode plans write split-KV partials
-  const WorkRec w = PAGED ? p.work[blockIdx.x * 4 + (threadIdx.x >> 6)] : p.work[blockIdx.x];
+  if (!PAGED && threadIdx.x >= kTileCols) return;
+  const WorkRec w = PAGED ? p.work[blockIdx.x * kDecodeWaves + (threadIdx.x >> 6)] : p.work[blockIdx.x];
   const int c = PAGED ? (threadIdx.x & 63) : threadIdx.x;
   const int t = c / p.G;
   const int h = c - t * p.G;
@@ -96,7 +97,8 @@ __global__ __launch_bounds__(256) void tile_valu_f32_kernel(TileParams p) {
 }
 
 hipError_t launch_tile_valu_f32(const TileParams& p, int n_work, int D, bool paged, hipStream_t stream) {
-  const dim3 grid(paged ? (n_work + 3) / 4 : n_work), block(256);
+  const dim3 grid(paged ? (n_work + kDecodeWaves - 1) / kDecodeWaves : n_work),
+      block(paged ? 64 * kDecodeWaves : kTileCols);
   if (D == 64) {
     if (paged) hipLaunchKernelGGL((tile_valu_f32_kernel<64, true>), grid, block, 0, stream, p);
     else hipLaunchKernelGGL((tile_valu_f32_kernel<64, false>), grid, block, 0, stream, p);

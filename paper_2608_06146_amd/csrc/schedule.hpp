@@ -20,6 +20,7 @@ static_assert(sizeof(RangeRec) == 32, "range record is 32 bytes");
 constexpr int kTileKeys = 64;
 constexpr int kTileCols = 256;
 constexpr int kBlock = 16;  // paged KV block (tokens)
+constexpr int kDecodeWaves = 8;  // wavefronts (wave items) per decode workgroup
 
 // Everything a tile kernel needs.  Pointers are device pointers.
 struct TileParams {
