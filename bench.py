@@ -54,6 +54,10 @@ def parse_args(argv=None):
                     help="bytes of each of the K and V pools in GiB (0: 45%% of HBM each, backing off on failure)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-pages", type=int, default=64, help="pages of the decode workload the oracle times")
+    ap.add_argument("--decode-chunk", type=int, default=0,
+                    help="decode plan: max keys per work item (0 = planner's choice)")
+    ap.add_argument("--decode-target-wg", type=int, default=0,
+                    help="decode plan: workgroups the planner aims for when it chooses chunks (0 = default)")
     ap.add_argument("--calibrate-copy", action="store_true",
                     help="only run a plain 1 GiB device-to-device copy three times (reference for HBM counters)")
     return ap.parse_args(argv)
@@ -147,7 +151,8 @@ def run_decode(args, torch, np, syn, pa, dev):
     for _ in range(5):
         t0 = time.perf_counter()
         plan = pa.TreePlan(segs_paged, Hq, Hkv, d, "bf16", 16, num_kv_rows=n_pool, num_q_rows=nq,
-                           block_table_len=nb)
+                           block_table_len=nb, max_chunk_keys=args.decode_chunk,
+                           target_workgroups=args.decode_target_wg)
         pts.append((time.perf_counter() - t0) * 1e3)
     plan_ms = statistics.median(pts)
 

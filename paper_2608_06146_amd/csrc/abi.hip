@@ -2,6 +2,8 @@
 // caller's workspace, and the kernel launches on the caller's stream.
 #include <hip/hip_runtime.h>
 
+#include <cstring>
+
 #include "host/plan.hpp"
 
 namespace padoc {
@@ -40,10 +42,24 @@ padoc_status check_common(const padoc_plan* P, const void* q, const void* k, con
   return PADOC_OK;
 }
 
+// The plan's schedule in pinned host memory (made once per plan).
+const void* pinned_blob(const padoc_plan* P) {
+  std::call_once(P->pin_once, [P] {
+    void* h = nullptr;
+    hipError_t e = hipHostMalloc(&h, P->blob.size(), hipHostMallocDefault);
+    if (e == hipSuccess) {
+      std::memcpy(h, P->blob.data(), P->blob.size());
+      P->pinned = h;
+    }
+    P->pin_status = (int)e;
+  });
+  return P->pinned ? P->pinned : P->blob.data();
+}
+
 padoc_status run(const padoc_plan* P, const void* q, const void* k, const void* v, const int32_t* bt, void* o,
                  float* lse, void* ws, hipStream_t stream) {
   if (P->work.empty()) return PADOC_OK;
-  hipError_t e = hipMemcpyAsync(ws, P->blob.data(), P->blob.size(), hipMemcpyHostToDevice, stream);
+  hipError_t e = hipMemcpyAsync(ws, pinned_blob(P), P->blob.size(), hipMemcpyHostToDevice, stream);
   if (e != hipSuccess) return hip_fail("hipMemcpyAsync(schedule)", e);
   TileParams tp{};
   tp.q = q;
@@ -121,6 +137,12 @@ extern "C" padoc_status padoc_branch_decode(const padoc_plan* plan, const void* 
     return set_error(PADOC_ERR_MODE, "plan was built for packed K/V (block_size 0); use padoc_tree_attn_fwd");
   if (!plan->work.empty() && !block_table) return set_error(PADOC_ERR_ARG, "block_table is null");
   return run(plan, q, k_cache, v_cache, block_table, o, lse, workspace, stream);
+}
+
+extern "C" void padoc_plan_destroy(padoc_plan* plan) {
+  if (!plan) return;
+  if (plan->pinned) (void)hipHostFree(plan->pinned);
+  delete plan;
 }
 
 extern "C" padoc_status padoc_set_kernel_events(hipEvent_t before, hipEvent_t after) {

@@ -660,6 +660,4 @@ extern "C" padoc_status padoc_plan_export(const padoc_plan* P, padoc_schedule_vi
   return PADOC_OK;
 }
 
-extern "C" void padoc_plan_destroy(padoc_plan* plan) { delete plan; }
-
 extern "C" const char* padoc_last_error(void) { return padoc::last_error(); }

@@ -5,6 +5,7 @@
 #include <stddef.h>
 #include <stdint.h>
 
+#include <mutex>
 #include <string>
 #include <vector>
 
@@ -38,6 +39,12 @@ struct padoc_plan {
   size_t off_work = 0, off_ranges = 0, off_lims = 0, off_toks = 0;
   size_t off_comb_ptr = 0, off_comb_slot = 0, off_part_o = 0, off_part_ml = 0;
   size_t ws_bytes = 0;
+
+  // Pinned host copy of `blob`, made on the first launch so the schedule
+  // upload is a true asynchronous DMA (freed by padoc_plan_destroy).
+  mutable std::once_flag pin_once;
+  mutable void* pinned = nullptr;
+  mutable int pin_status = 0;  // hipError_t of the pinned allocation
 };
 
 namespace padoc {

@@ -7,7 +7,7 @@
 
 #include <stdint.h>
 
-#include "../../include/padoc_attn.h"
+#include "padoc_attn.h"  // include/ is on the include path
 
 namespace padoc {
 
