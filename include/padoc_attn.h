@@ -112,7 +112,7 @@ typedef struct {
   const padoc_segment* seg;      /* host memory, read during padoc_plan_create  */
   int32_t num_heads_q;           /* Hq > 0                                      */
   int32_t num_heads_kv;          /* Hkv > 0, Hq % Hkv == 0, Hq/Hkv <= 64
-                                    (<= 32 for paged decode plans)             */
+                                                                               */
   int32_t head_dim;              /* 64 or 128                                   */
   float softmax_scale;           /* > 0, finite; the paper uses 1/sqrt(d)       */
   padoc_dtype dtype;
@@ -132,8 +132,9 @@ typedef struct padoc_plan padoc_plan;
 
 /* Schedule export (tests and tools).  Pointers stay valid until the plan is
    destroyed.  A work item processes, for one KV head, the queries
-   toks[tok_begin .. tok_begin+ntok) (Q row indices; column c of the item is
-   token c/G, head c%G) against the key ranges ranges[rng_begin ..
+   toks[tok_begin .. tok_begin+ntok) (Q row indices; column c of the task is
+   token c/G, head c%G; the item computes columns col0 .. col0+ncol-1) against
+   the key ranges ranges[rng_begin ..
    rng_begin+rng_count).  Token i of the item sees keys [0, lim) of a range
    where lim = n_keys if lim_off < 0, else lims[lim_off + i]; every token sees
    at least [0, min_lim).  Key j of a range is K/V row kv_start + j (packed) or
@@ -142,15 +143,26 @@ typedef struct padoc_plan padoc_plan;
    tile_class[tile_class_off[r] + kt] is 1 (full: every token sees all
    tile_keys keys, no mask) or 2 (partial: masked) for each key tile kt below
    ceil(n_keys / tile_keys); tiles past n_keys are never visited.  Work items
-   of different KV heads share token and range records.  Forward plans: work
-   item i is one workgroup.  Decode plans: work item i is wavefront i%8 of
-   workgroup i/8 (items with ntok == 0 are idle waves).  Decode
+   of different KV heads share token and range records.  Forward plans: one
+   workgroup per item.  Decode plans: the first n_work_shared items (shared
+   prefix / stream keys, up to 256 columns) run one per workgroup on the
+   matrix-core tile kernel, the remaining items (a private branch's keys, 16
+   columns) one per wavefront on the streaming kernel; every item writes the
+   split partial of column c to slot out_base + c, except items with fin = 1,
+   which merge their rows' shared partials (their own slot is the last entry
+   of each row's list) and write O and LSE; the combine kernel merges the
+   rows listed in comb_rows.  Decode
    plans write one partial result per (item, column) at slot out_base + column
    and combine, for Q row r and KV head g, the slots comb_slot[comb_ptr[r*Hkv+g]
    .. comb_ptr[r*Hkv+g+1]) (+ head within group) in that order. */
 typedef struct {
   int32_t tok_begin, ntok, rng_begin, rng_count, kvh, out_base, cost;
-  int32_t nblk;  /* decode: 32-column blocks the wave computes (1); forward: 0 */
+  int32_t col0;  /* first column of the task this item computes              */
+  int32_t ncol;  /* columns this item computes: col0 .. col0+ncol-1, clipped
+                    to the task's ntok*G columns                             */
+  int32_t fin;   /* decode: 1 = this private item also merges its rows' other
+                    partials (all from shared items) and writes O and LSE    */
+  int32_t reserved[2];
 } padoc_work_view;
 
 typedef struct {
@@ -162,12 +174,15 @@ typedef struct {
   int32_t kind;                  /* 0 = forward (final O), 1 = decode (partials) */
   int32_t tile_cols, tile_keys;  /* columns per work item, keys per key tile     */
   int32_t n_work;  const padoc_work_view* work;
+  int32_t n_work_shared;
   int32_t n_range; const padoc_range_view* ranges;
   int32_t n_lim;   const int32_t* lims;
   int32_t n_tok;   const int32_t* toks;
   int64_t n_tile_class; const int8_t* tile_class; const int64_t* tile_class_off;
   int64_t n_comb_ptr; const int32_t* comb_ptr;
   int64_t n_comb;     const int32_t* comb_slot;
+  int64_t n_comb_rows; const int32_t* comb_rows; /* (row*Hkv + kv head) merged
+                                                    by the combine kernel     */
   int64_t n_slots;
   size_t workspace_bytes;
 } padoc_schedule_view;
@@ -211,10 +226,11 @@ padoc_status padoc_branch_decode(const padoc_plan* plan, const void* q, const vo
 /* Thread-local description of the last error on this thread ("" if none). */
 const char* padoc_last_error(void);
 
-/* Profiling hook (thread-local): when both events are non-null, the next
-   launches on this thread record `before` just before and `after` just after
-   their dominant kernel (the tile kernel), on the launch stream.  Pass nulls
-   to stop. */
+/* Profiling hook (thread-local): when both events are non-null, later calls
+   on this thread record `before` just before their first kernel and `after`
+   just after their last (every kernel of the call: attention kernels and,
+   for decode plans, the combine), on the launch stream.  The events are owned
+   by the caller and must outlive the calls.  Pass nulls to stop. */
 padoc_status padoc_set_kernel_events(hipEvent_t before, hipEvent_t after);
 
 /* Library version string. */

@@ -136,12 +136,13 @@ class TreePlan:
             return np.frombuffer(buf, dtype=dt).copy()
 
         return {
-            "kind": v.kind, "tile_cols": v.tile_cols, "tile_keys": v.tile_keys,
+            "kind": v.kind, "tile_cols": v.tile_cols, "tile_keys": v.tile_keys, "n_work_shared": v.n_work_shared,
             "work": arr(v.work, v.n_work, WORK_DTYPE), "ranges": arr(v.ranges, v.n_range, RANGE_DTYPE),
             "lims": arr(v.lims, v.n_lim, np.int32), "toks": arr(v.toks, v.n_tok, np.int32),
             "tile_class": arr(v.tile_class, v.n_tile_class, np.int8),
             "tile_class_off": arr(v.tile_class_off, v.n_range, np.int64),
             "comb_ptr": arr(v.comb_ptr, v.n_comb_ptr, np.int32), "comb_slot": arr(v.comb_slot, v.n_comb, np.int32),
+            "comb_rows": arr(v.comb_rows, v.n_comb_rows, np.int32),
             "n_slots": v.n_slots, "workspace_bytes": v.workspace_bytes,
         }
 
@@ -226,8 +227,8 @@ def branch_decode(q, k_cache, v_cache, block_table, plan: TreePlan, out=None, ls
 
 
 def set_kernel_events(before=None, after=None):
-    """Record torch CUDA events around the tile kernel of later launches on
-    this thread (``padoc_set_kernel_events``); call with no arguments to stop."""
+    """Record torch CUDA events around all kernels of later calls on this
+    thread (``padoc_set_kernel_events``); call with no arguments to stop."""
     b = C.c_void_p(before.cuda_event) if before is not None else None
     a = C.c_void_p(after.cuda_event) if after is not None else None
     _lib.check(_lib.lib().padoc_set_kernel_events(b, a))

@@ -23,7 +23,8 @@ F32, BF16 = 0, 1
 SEGMENT_DTYPE = np.dtype([("parent", "<i4"), ("fork", "<i4"), ("len", "<i4"), ("q_len", "<i4"),
                           ("kv_off", "<i8"), ("q_off", "<i8")])
 WORK_DTYPE = np.dtype([("tok_begin", "<i4"), ("ntok", "<i4"), ("rng_begin", "<i4"), ("rng_count", "<i4"),
-                       ("kvh", "<i4"), ("out_base", "<i4"), ("cost", "<i4"), ("nblk", "<i4")])
+                       ("kvh", "<i4"), ("out_base", "<i4"), ("cost", "<i4"), ("col0", "<i4"),
+                       ("ncol", "<i4"), ("fin", "<i4"), ("reserved", "<i4", (2,))])
 RANGE_DTYPE = np.dtype([("kv_start", "<i8"), ("n_keys", "<i4"), ("min_lim", "<i4"), ("lim_off", "<i4"),
                         ("seg", "<i4"), ("key_begin", "<i4"), ("reserved", "<i4")])
 
@@ -50,13 +51,14 @@ class TreeDesc(C.Structure):
 
 class ScheduleView(C.Structure):
     _fields_ = [("kind", C.c_int32), ("tile_cols", C.c_int32), ("tile_keys", C.c_int32),
-                ("n_work", C.c_int32), ("work", C.c_void_p),
+                ("n_work", C.c_int32), ("work", C.c_void_p), ("n_work_shared", C.c_int32),
                 ("n_range", C.c_int32), ("ranges", C.c_void_p),
                 ("n_lim", C.c_int32), ("lims", C.c_void_p),
                 ("n_tok", C.c_int32), ("toks", C.c_void_p),
                 ("n_tile_class", C.c_int64), ("tile_class", C.c_void_p), ("tile_class_off", C.c_void_p),
                 ("n_comb_ptr", C.c_int64), ("comb_ptr", C.c_void_p),
                 ("n_comb", C.c_int64), ("comb_slot", C.c_void_p),
+                ("n_comb_rows", C.c_int64), ("comb_rows", C.c_void_p),
                 ("n_slots", C.c_int64), ("workspace_bytes", C.c_size_t)]
 
 

@@ -26,7 +26,7 @@ SOURCES = [
     "csrc/host/plan.cpp",
     "csrc/abi.hip",
     "csrc/kernels/tile_mfma_bf16.hip",
-    "csrc/kernels/decode_stream.hip",
+    "csrc/kernels/decode_private.hip",
     "csrc/kernels/tile_valu_f32.hip",
     "csrc/kernels/lse_combine.hip",
 ]

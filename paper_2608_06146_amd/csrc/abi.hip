@@ -7,8 +7,8 @@
 #include "host/plan.hpp"
 
 namespace padoc {
-hipError_t launch_tile_mfma_bf16(const TileParams& p, int n_work, int D, hipStream_t s);
-hipError_t launch_decode_stream_bf16(const TileParams& p, int n_items, int D, hipStream_t s);
+hipError_t launch_tile_mfma_bf16(const TileParams& p, int n_work, int D, bool paged, hipStream_t s);
+hipError_t launch_decode_private_bf16(const TileParams& p, int n_items, int D, hipStream_t s);
 hipError_t launch_tile_valu_f32(const TileParams& p, int n_work, int D, bool paged, hipStream_t s);
 hipError_t launch_lse_combine(const CombineParams& p, int D, bool bf16, hipStream_t s);
 
@@ -74,6 +74,8 @@ padoc_status run(const padoc_plan* P, const void* q, const void* k, const void* 
   tp.toks = at<int32_t>(ws, P->off_toks);
   tp.part_o = reinterpret_cast<float*>(static_cast<char*>(ws) + P->off_part_o);
   tp.part_ml = reinterpret_cast<float*>(static_cast<char*>(ws) + P->off_part_ml);
+  tp.comb_ptr = at<int32_t>(ws, P->off_comb_ptr);
+  tp.comb_slot = at<int32_t>(ws, P->off_comb_slot);
   tp.Hq = P->Hq;
   tp.Hkv = P->Hkv;
   tp.G = P->G;
@@ -85,19 +87,28 @@ padoc_status run(const padoc_plan* P, const void* q, const void* k, const void* 
     e = hipEventRecord(t_ev_before, stream);
     if (e != hipSuccess) return hip_fail("hipEventRecord", e);
   }
-  if (P->dtype == PADOC_BF16)
-    e = paged ? launch_decode_stream_bf16(tp, n_work, P->D, stream) : launch_tile_mfma_bf16(tp, n_work, P->D, stream);
-  else
+  if (P->dtype == PADOC_BF16) {
+    if (!paged) {
+      e = launch_tile_mfma_bf16(tp, n_work, P->D, false, stream);
+    } else {
+      // Shared keys (all sibling columns per tile) on the tile kernel, then
+      // private keys on the streaming kernel, whose epilogue also merges the
+      // shared partials of its rows (they are complete: same stream, earlier).
+      TileParams tq = tp;
+      tq.work = tp.work + P->n_work_shared;
+      e = launch_tile_mfma_bf16(tp, P->n_work_shared, P->D, true, stream);
+      if (e == hipSuccess) e = launch_decode_private_bf16(tq, n_work - P->n_work_shared, P->D, stream);
+    }
+  } else {
     e = launch_tile_valu_f32(tp, n_work, P->D, paged, stream);
-  if (e != hipSuccess) return hip_fail("tile kernel launch", e);
-  if (t_ev_before && t_ev_after) {
-    e = hipEventRecord(t_ev_after, stream);
-    if (e != hipSuccess) return hip_fail("hipEventRecord", e);
   }
+  if (e != hipSuccess) return hip_fail("tile kernel launch", e);
   if (partial) {
     CombineParams cp{};
     cp.comb_ptr = at<int32_t>(ws, P->off_comb_ptr);
     cp.comb_slot = at<int32_t>(ws, P->off_comb_slot);
+    cp.comb_rows = at<int32_t>(ws, P->off_comb_rows);
+    cp.n_rows = (int64_t)P->comb_rows.size();
     cp.part_o = tp.part_o;
     cp.part_ml = tp.part_ml;
     cp.o = o;
@@ -108,6 +119,10 @@ padoc_status run(const padoc_plan* P, const void* q, const void* k, const void* 
     cp.G = P->G;
     e = launch_lse_combine(cp, P->D, P->dtype == PADOC_BF16, stream);
     if (e != hipSuccess) return hip_fail("combine kernel launch", e);
+  }
+  if (t_ev_before && t_ev_after) {
+    e = hipEventRecord(t_ev_after, stream);
+    if (e != hipSuccess) return hip_fail("hipEventRecord", e);
   }
   return PADOC_OK;
 }

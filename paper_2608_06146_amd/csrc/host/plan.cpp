@@ -174,9 +174,6 @@ padoc_status validate(const padoc_tree_desc* d) {
     return set_error(PADOC_ERR_SHAPE, "Hq=%d is not a multiple of Hkv=%d", d->num_heads_q, d->num_heads_kv);
   if (d->num_heads_q / d->num_heads_kv > 64)
     return set_error(PADOC_ERR_SHAPE, "Hq/Hkv=%d exceeds 64", d->num_heads_q / d->num_heads_kv);
-  if (d->block_size != 0 && d->num_heads_q / d->num_heads_kv > 32)
-    return set_error(PADOC_ERR_SHAPE, "decode (paged) plans need Hq/Hkv <= 32 (got %d)",
-                     d->num_heads_q / d->num_heads_kv);
   if (d->head_dim != 64 && d->head_dim != 128)
     return set_error(PADOC_ERR_SHAPE, "head_dim=%d is not 64 or 128", d->head_dim);
   if (!std::isfinite(d->softmax_scale) || !(d->softmax_scale > 0.f))
@@ -286,25 +283,27 @@ void build_forward(padoc_plan& P, Builder& B) {
       w.kvh = g;
       w.out_base = 0;
       w.cost = cost;
+      w.col0 = 0;
+      w.ncol = ntok * P.G;
       P.work.push_back(w);
     }
   }
 }
 
-// Decode: wave items.  A wave item is one wavefront's work: the columns
-// (query token x head) of at most 32/G tokens for one KV head against one key
-// chunk.  kDecodeWaves wave items form a workgroup.  The wave items of one
-// page's shared tokens (up to kDecodeWaves per group) process the same key
-// chunks in the same workgroup, so the shared prefix and stream keys are
-// fetched from HBM once per chunk and served to the sibling waves by the
-// compute unit's cache.  Private segments (seen only by their own queries)
-// get their own wave items, packed kDecodeWaves per workgroup by similar cost.
+// Decode.  A segment is shared when a query token of another segment sees
+// any of it (page prefix, layout stream), private otherwise (a branch seen
+// only by its own queries).  Shared keys are processed by the matrix-core
+// tile kernel: per page, the tokens that see shared segments are cut into
+// items of at most 256 columns, so siblings share every K/V tile (loaded from
+// HBM once per item and key chunk).  Private keys are streamed by wavefront
+// items of 16 columns.  Both kinds write split partials; the combine map lists
+// them per (query row, KV head) in creation order.
 void build_decode(padoc_plan& P, Builder& B, const std::vector<std::vector<std::pair<int32_t, int32_t>>>& anc,
                   const padoc_tree_desc* d) {
   const int32_t n = (int32_t)P.seg.size();
   const int32_t G = P.G;
-  const int32_t NT = P.tile_tokens;  // 32 / G tokens per wave item
-  const int32_t NW = kDecodeWaves;
+  const int32_t NTs = std::max(1, kTileCols / G);
+  const int32_t NTp = std::max(1, kPrivateCols / G);
   std::vector<int64_t> viewers(n, 0);
   for (int32_t s = 0; s < n; ++s)
     if (P.seg[s].q_len > 0)
@@ -315,9 +314,7 @@ void build_decode(padoc_plan& P, Builder& B, const std::vector<std::vector<std::
   std::vector<int32_t> root(n);
   for (int32_t s = 0; s < n; ++s) root[s] = P.seg[s].parent < 0 ? s : root[P.seg[s].parent];
 
-  // Shared groups: per page, the tokens that see a shared segment, cut into
-  // wave tasks of NT tokens, NW wave tasks per group.
-  std::vector<std::vector<Task>> groups;
+  std::vector<Task> stasks, ptasks;
   {
     std::map<int32_t, Task> per_page;
     for (int32_t s = 0; s < n; ++s) {
@@ -334,66 +331,49 @@ void build_decode(padoc_plan& P, Builder& B, const std::vector<std::vector<std::
     }
     for (auto& kv : per_page) {
       const Task& all = kv.second;
-      std::vector<Task> waves;
-      for (size_t b = 0; b < all.seg.size(); b += NT) {
+      for (size_t b = 0; b < all.seg.size(); b += NTs) {
         Task t;
-        const size_t e = std::min(all.seg.size(), b + (size_t)NT);
+        const size_t e = std::min(all.seg.size(), b + (size_t)NTs);
         t.seg.assign(all.seg.begin() + b, all.seg.begin() + e);
         t.pos.assign(all.pos.begin() + b, all.pos.begin() + e);
-        waves.push_back(std::move(t));
-        if ((int32_t)waves.size() == NW) {
-          groups.push_back(std::move(waves));
-          waves.clear();
+        stasks.push_back(std::move(t));
+      }
+    }
+    for (int32_t s = 0; s < n; ++s) {
+      const padoc_segment& sg = P.seg[s];
+      if (sg.q_len == 0 || shared(s)) continue;
+      for (int32_t b = sg.len - sg.q_len; b < sg.len; b += NTp) {
+        Task t;
+        for (int32_t p = b; p < std::min(sg.len, b + NTp); ++p) {
+          t.seg.push_back(s);
+          t.pos.push_back(p);
         }
+        ptasks.push_back(std::move(t));
       }
-      if (!waves.empty()) groups.push_back(std::move(waves));
     }
   }
-  // Private wave tasks.
-  std::vector<Task> ptasks;
-  for (int32_t s = 0; s < n; ++s) {
-    const padoc_segment& sg = P.seg[s];
-    if (sg.q_len == 0 || shared(s)) continue;
-    for (int32_t b = sg.len - sg.q_len; b < sg.len; b += NT) {
-      Task t;
-      for (int32_t p = b; p < std::min(sg.len, b + NT); ++p) {
-        t.seg.push_back(s);
-        t.pos.push_back(p);
-      }
-      ptasks.push_back(std::move(t));
-    }
-  }
-
-  // Visible ranges: per group the union over its tokens (chunk boundaries
-  // are cut on the union so sibling waves stay in step), per wave task its
-  // own limits.
-  std::vector<std::vector<VisRange>> gunion(groups.size());
-  std::vector<std::vector<std::vector<VisRange>>> gvis(groups.size());
+  // Work estimate in key-steps of one wavefront (a shared item keeps four
+  // wavefronts busy) for the chunk size.
+  std::vector<std::vector<VisRange>> svis, pvis;
   int64_t total = 0;
-  for (size_t g = 0; g < groups.size(); ++g) {
-    Task all;
-    for (const Task& t : groups[g]) {
-      all.seg.insert(all.seg.end(), t.seg.begin(), t.seg.end());
-      all.pos.insert(all.pos.end(), t.pos.begin(), t.pos.end());
-      gvis[g].push_back(B.visible(t, shared));
-    }
-    gunion[g] = B.visible(all, shared);
-    for (const auto& r : gunion[g]) total += round_up(r.n_keys, P.tile_keys) * P.Hkv;
+  for (const Task& t : stasks) {
+    svis.push_back(B.visible(t, shared));
+    for (const auto& r : svis.back()) total += 4 * round_up(r.n_keys, 64) * P.Hkv;
   }
-  std::vector<std::vector<VisRange>> pvis;
   for (const Task& t : ptasks) {
     pvis.push_back(B.visible(t, priv));
-    for (const auto& r : pvis.back()) total += round_up(r.n_keys, P.tile_keys) * P.Hkv / NW;
+    const int64_t splits = ceil_div((int64_t)t.seg.size() * G, kPrivateCols);
+    for (const auto& r : pvis.back()) total += round_up(r.n_keys, 32) * P.Hkv * splits;
   }
   int64_t CH = d->max_chunk_keys;
   if (CH == 0) {
-    const int64_t target = d->target_workgroups > 0 ? d->target_workgroups : 512;
+    // about target_workgroups x 4 wavefronts' worth of equal pieces
+    const int64_t target = 4 * (d->target_workgroups > 0 ? d->target_workgroups : 1024);
     CH = round_up(std::max<int64_t>(1, ceil_div(total, target)), 64);
-    CH = std::min<int64_t>(std::max<int64_t>(CH, 256), 8192);
+    CH = std::min<int64_t>(std::max<int64_t>(CH, 512), 8192);
   }
   auto cut = [&](const std::vector<VisRange>& vis) {
-    // [(t, kb, len)] pieces of at most CH keys in total per chunk
-    std::vector<std::vector<std::tuple<int32_t, int32_t, int32_t>>> chunks(1);
+    std::vector<std::vector<Piece>> chunks(1);
     int64_t room = CH;
     for (const auto& r : vis) {
       int32_t kb = 0;
@@ -403,7 +383,7 @@ void build_decode(padoc_plan& P, Builder& B, const std::vector<std::vector<std::
           room = CH;
         }
         const int32_t take = (int32_t)std::min<int64_t>(r.n_keys - kb, room);
-        chunks.back().emplace_back(r.t, kb, take);
+        chunks.back().push_back({&r, kb, take});
         kb += take;
         room -= round_up(take, 64);
       }
@@ -414,84 +394,67 @@ void build_decode(padoc_plan& P, Builder& B, const std::vector<std::vector<std::
 
   std::vector<std::vector<int32_t>> comb((size_t)P.num_q_rows * P.Hkv);
   std::vector<char> sees;
-  struct WG {
-    std::vector<padoc::WorkRec> items;
-    int32_t cost;
-  };
-  std::vector<WG> wgs;
-  std::vector<padoc::WorkRec> pitems;
-  // One wave item: returns false if the wave sees nothing in this chunk.
-  auto make_item = [&](const Task& task, int32_t tok_begin, const std::vector<VisRange>& vis,
-                       const std::vector<std::tuple<int32_t, int32_t, int32_t>>& chunk, int32_t kvh,
-                       padoc::WorkRec& w) {
-    std::vector<Piece> pieces;
-    for (const auto& c : chunk)
-      for (const auto& r : vis)
-        if (r.t == std::get<0>(c)) pieces.push_back({&r, std::get<1>(c), std::get<2>(c)});
+  std::vector<padoc::WorkRec> sitems, pitems;
+  auto emit = [&](const Task& task, int32_t tok_begin, const std::vector<Piece>& pieces, int32_t width,
+                  std::vector<padoc::WorkRec>& out) {
     const int32_t ntok = (int32_t)task.seg.size();
     int32_t rb, rc, cost;
     B.emit_ranges(pieces, ntok, rb, rc, cost, sees);
-    if (rc == 0) return false;
-    w = padoc::WorkRec{};
-    w.tok_begin = tok_begin;
-    w.ntok = ntok;
-    w.rng_begin = rb;
-    w.rng_count = rc;
-    w.kvh = kvh;
-    w.out_base = (int32_t)P.n_slots;
-    w.cost = cost;
-    w.nblk = 1;
-    for (int32_t i = 0; i < ntok; ++i)
-      if (sees[i]) comb[(size_t)P.toks[tok_begin + i] * P.Hkv + kvh].push_back(w.out_base + i * G);
-    P.n_slots += (int64_t)ntok * G;
-    return true;
-  };
-  for (size_t g = 0; g < groups.size(); ++g) {
-    std::vector<int32_t> tb;
-    for (const Task& t : groups[g]) tb.push_back(B.add_tokens(t));
-    for (const auto& chunk : cut(gunion[g])) {
-      for (int32_t kvh = 0; kvh < P.Hkv; ++kvh) {
-        WG wg{{}, 0};
-        for (size_t wv = 0; wv < groups[g].size(); ++wv) {
-          padoc::WorkRec w;
-          if (make_item(groups[g][wv], tb[wv], gvis[g][wv], chunk, kvh, w)) {
-            wg.cost = std::max(wg.cost, w.cost);
-            wg.items.push_back(w);
-          }
-        }
-        if (!wg.items.empty()) wgs.push_back(std::move(wg));
+    if (rc == 0) return;
+    for (int32_t kvh = 0; kvh < P.Hkv; ++kvh) {
+      const int32_t base = (int32_t)P.n_slots;
+      for (int32_t i = 0; i < ntok; ++i)
+        if (sees[i]) comb[(size_t)P.toks[tok_begin + i] * P.Hkv + kvh].push_back(base + i * G);
+      P.n_slots += (int64_t)ntok * G;
+      for (int32_t c0 = 0; c0 < ntok * G; c0 += width) {
+        padoc::WorkRec w{};
+        w.tok_begin = tok_begin;
+        w.ntok = ntok;
+        w.rng_begin = rb;
+        w.rng_count = rc;
+        w.kvh = kvh;
+        w.out_base = base;
+        w.cost = cost;
+        w.col0 = c0;
+        w.ncol = std::min(width, ntok * G - c0);
+        out.push_back(w);
       }
     }
+  };
+  for (size_t i = 0; i < stasks.size(); ++i) {
+    const int32_t tb = B.add_tokens(stasks[i]);
+    for (const auto& chunk : cut(svis[i])) emit(stasks[i], tb, chunk, kTileCols, sitems);
   }
+  // A private task cut into a single chunk finishes its rows in the
+  // streaming kernel (bf16): every other partial of those rows comes from a
+  // shared item, which runs earlier on the same stream.
+  std::vector<char> finished((size_t)P.num_q_rows * P.Hkv, 0);
   for (size_t i = 0; i < ptasks.size(); ++i) {
     const int32_t tb = B.add_tokens(ptasks[i]);
-    for (const auto& chunk : cut(pvis[i]))
-      for (int32_t kvh = 0; kvh < P.Hkv; ++kvh) {
-        padoc::WorkRec w;
-        if (make_item(ptasks[i], tb, pvis[i], chunk, kvh, w)) pitems.push_back(w);
+    const auto chunks = cut(pvis[i]);
+    const size_t first = pitems.size();
+    for (const auto& chunk : chunks) emit(ptasks[i], tb, chunk, kPrivateCols, pitems);
+    if (P.dtype == PADOC_BF16 && chunks.size() == 1) {
+      for (size_t j = first; j < pitems.size(); ++j) {
+        pitems[j].fin = 1;
+        for (int32_t t = 0; t < pitems[j].ntok; ++t)
+          finished[(size_t)P.toks[tb + t] * P.Hkv + pitems[j].kvh] = 1;
       }
-  }
-  std::stable_sort(pitems.begin(), pitems.end(),
-                   [](const padoc::WorkRec& a, const padoc::WorkRec& b) { return a.cost > b.cost; });
-  for (size_t i = 0; i < pitems.size(); i += NW) {
-    WG wg{{}, 0};
-    for (size_t j = i; j < std::min(pitems.size(), i + (size_t)NW); ++j) {
-      wg.cost = std::max(wg.cost, pitems[j].cost);
-      wg.items.push_back(pitems[j]);
     }
-    wgs.push_back(std::move(wg));
   }
-  // Costliest workgroups first (longest-processing-time order).
-  std::stable_sort(wgs.begin(), wgs.end(), [](const WG& a, const WG& b) { return a.cost > b.cost; });
-  for (const WG& wg : wgs) {
-    for (const auto& w : wg.items) P.work.push_back(w);
-    for (size_t j = wg.items.size(); j < (size_t)NW; ++j) P.work.push_back(padoc::WorkRec{});  // idle wave
-  }
+  auto by_cost = [](const padoc::WorkRec& a, const padoc::WorkRec& b) { return a.cost > b.cost; };
+  std::stable_sort(sitems.begin(), sitems.end(), by_cost);
+  std::stable_sort(pitems.begin(), pitems.end(), by_cost);
+  P.work = sitems;
+  P.work.insert(P.work.end(), pitems.begin(), pitems.end());
+  P.n_work_shared = (int32_t)sitems.size();
 
   P.comb_ptr.assign(comb.size() + 1, 0);
   for (size_t r = 0; r < comb.size(); ++r) P.comb_ptr[r + 1] = P.comb_ptr[r] + (int32_t)comb[r].size();
   P.comb_slot.reserve(P.comb_ptr.back());
   for (const auto& c : comb) P.comb_slot.insert(P.comb_slot.end(), c.begin(), c.end());
+  for (size_t r = 0; r < comb.size(); ++r)
+    if (!comb[r].empty() && !finished[r]) P.comb_rows.push_back((int32_t)r);
 }
 
 template <class T>
@@ -506,7 +469,8 @@ void serialise(padoc_plan& P) {
   P.off_toks = align256(P.off_lims + P.lims.size() * 4);
   P.off_comb_ptr = align256(P.off_toks + P.toks.size() * 4);
   P.off_comb_slot = align256(P.off_comb_ptr + P.comb_ptr.size() * 4);
-  const size_t blob_bytes = P.off_comb_slot + P.comb_slot.size() * 4;
+  P.off_comb_rows = align256(P.off_comb_slot + P.comb_slot.size() * 4);
+  const size_t blob_bytes = P.off_comb_rows + P.comb_rows.size() * 4;
   P.off_part_o = align256(blob_bytes);
   P.off_part_ml = align256(P.off_part_o + (size_t)P.n_slots * P.D * 4);
   P.ws_bytes = std::max<size_t>(256, align256(P.off_part_ml + (size_t)P.n_slots * 8));
@@ -517,6 +481,7 @@ void serialise(padoc_plan& P) {
   put(P.blob, P.off_toks, P.toks);
   put(P.blob, P.off_comb_ptr, P.comb_ptr);
   put(P.blob, P.off_comb_slot, P.comb_slot);
+  put(P.blob, P.off_comb_rows, P.comb_rows);
 }
 
 }  // namespace
@@ -591,10 +556,7 @@ extern "C" padoc_status padoc_plan_create(const padoc_tree_desc* d, padoc_plan**
     P->num_q_rows = d->num_q_rows;
     P->block_table_len = d->block_table_len;
     P->seg.assign(d->seg, d->seg + d->n_seg);
-    if (P->kind == 1) {  // decode: wave items of at most 32 columns, 32-key steps
-      P->tile_cols = 32;
-      P->tile_keys = 32;
-    }
+    if (P->kind == 1) P->tile_keys = 32;  // decode ranges are classified per 32-key step
     P->tile_tokens = std::max(1, P->tile_cols / P->G);
     std::vector<std::vector<std::pair<int32_t, int32_t>>> anc(d->n_seg);
     for (int32_t s = 0; s < d->n_seg; ++s) {
@@ -642,6 +604,7 @@ extern "C" padoc_status padoc_plan_export(const padoc_plan* P, padoc_schedule_vi
   v->tile_keys = P->tile_keys;
   v->n_work = (int32_t)P->work.size();
   v->work = P->work.data();
+  v->n_work_shared = P->n_work_shared;
   v->n_range = (int32_t)P->ranges.size();
   v->ranges = P->ranges.data();
   v->n_lim = (int32_t)P->lims.size();
@@ -655,6 +618,8 @@ extern "C" padoc_status padoc_plan_export(const padoc_plan* P, padoc_schedule_vi
   v->comb_ptr = P->comb_ptr.data();
   v->n_comb = (int64_t)P->comb_slot.size();
   v->comb_slot = P->comb_slot.data();
+  v->n_comb_rows = (int64_t)P->comb_rows.size();
+  v->comb_rows = P->comb_rows.data();
   v->n_slots = P->n_slots;
   v->workspace_bytes = P->ws_bytes;
   return PADOC_OK;

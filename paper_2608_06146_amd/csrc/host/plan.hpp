@@ -25,6 +25,7 @@ struct padoc_plan {
   int32_t tile_tokens = 0;  // tokens per work item = tile_cols / G
 
   std::vector<padoc::WorkRec> work;
+  int32_t n_work_shared = 0;  // decode: work[0 .. n_work_shared) run on the tile kernel
   std::vector<padoc::RangeRec> ranges;
   std::vector<int32_t> lims;
   std::vector<int32_t> toks;
@@ -32,12 +33,13 @@ struct padoc_plan {
   std::vector<int64_t> tile_class_off;  // per range: first entry in tile_class
   std::vector<int32_t> comb_ptr;
   std::vector<int32_t> comb_slot;
+  std::vector<int32_t> comb_rows;  // (row*Hkv + kvh) pairs the combine kernel merges
   int64_t n_slots = 0;
 
   // Serialised schedule (uploaded into the workspace before every launch).
   std::vector<unsigned char> blob;
   size_t off_work = 0, off_ranges = 0, off_lims = 0, off_toks = 0;
-  size_t off_comb_ptr = 0, off_comb_slot = 0, off_part_o = 0, off_part_ml = 0;
+  size_t off_comb_ptr = 0, off_comb_slot = 0, off_comb_rows = 0, off_part_o = 0, off_part_ml = 0;
   size_t ws_bytes = 0;
 
   // Pinned host copy of `blob`, made on the first launch so the schedule

@@ -1,0 +1,257 @@
+// Decode kernel for private keys (a branch's own history, seen only by its
+// own queries): one wavefront per work item of up to 16 columns (query token
+// x head), streaming the item's paged keys from HBM straight into
+// matrix-core operand registers, 32 keys per step (App. E: one decode step
+// of the live streams; Attn equation with the ancestor mask).
+//
+// Per step, with v_mfma_f32_16x16x32_bf16 (lane l: row/column l%16, group
+// g = l/16 holding eight consecutive K-dimension elements):
+//   S^T = K Q^T     two 16-key M blocks; row m of block mb holds key
+//                   8*(m/4) + 4*mb + m%4, so each lane's eight scores are the
+//                   keys 8g .. 8g+7 of the step
+//   online softmax  one column per lane group (4 lanes x 8 scores)
+//   O^T += V^T P^T  P^T is the lane's 8 scores; V^T comes from d-major V
+//                   blocks ([d][16 tokens]) as one 16-byte load per lane.
+// Two register sets hold the K and V of two future steps: a set is refilled
+// right after its last use, so every load has two steps of compute to land.
+// Keys past a range's end are never used: K lanes are zeroed, V elements past
+// the end are zeroed before they reach a product.  Outputs are split
+// partials (unnormalised O, running max in log2 units, sum) for the combine,
+// or -- for an item that is its rows' only private piece -- O and LSE
+// directly, after merging the rows' shared-key partials in the plan's order.
+#include <type_traits>
+
+#include "device_common.hpp"
+
+namespace padoc {
+
+namespace {
+
+typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
+typedef float f32x4_t __attribute__((ext_vector_type(4)));
+
+__device__ __forceinline__ bf16x8_t as_bf16x8(const uint4& u) { return *reinterpret_cast<const bf16x8_t*>(&u); }
+
+// Key (within a 32-key step) held by row m of 16-key M block mb.
+__device__ __forceinline__ int step_key(int mb, int m) { return 8 * (m >> 2) + 4 * mb + (m & 3); }
+
+template <int D>
+__global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(2, 2))) void decode_private_kernel(TileParams p) {
+  constexpr int NDS = D / 32;  // K-slices (32 d each) of the score product
+  constexpr int NDM = D / 16;  // 16-row blocks of O^T
+  const WorkRec w = p.work[blockIdx.x];
+  const int lane = threadIdx.x;
+  const int n = lane & 15, g = lane >> 4;
+  const int G = p.G;
+  const int kvh = w.kvh;
+  const int64_t Hkv = p.Hkv;
+  const int col = w.col0 + n;
+  const int t = col / G;
+  const bool valid = n < w.ncol && t < w.ntok;
+  const int32_t qrow = valid ? p.toks[w.tok_begin + t] : 0;
+  const int32_t hq = kvh * G + (col - t * G);
+  const uint16_t* Kc = static_cast<const uint16_t*>(p.k);
+  const uint16_t* Vc = static_cast<const uint16_t*>(p.v);
+  const int32_t* bt = p.block_table;
+
+  // Q fragments (B operand): column n, d = ds*32 + 8g .. +7.
+  bf16x8_t bq[NDS];
+  {
+    const uint16_t* qp = static_cast<const uint16_t*>(p.q) + ((int64_t)qrow * p.Hq + hq) * D + 8 * g;
+#pragma unroll
+    for (int ds = 0; ds < NDS; ++ds)
+      bq[ds] = as_bf16x8(valid ? *reinterpret_cast<const uint4*>(qp + ds * 32) : make_uint4(0, 0, 0, 0));
+  }
+
+  // Step cursors over the item's ranges: C = step being computed, L = next
+  // step to load (two ahead of C once the pipeline is full).
+  struct Cursor {
+    int ri, st;
+    RangeRec R;
+    bool ok;
+  };
+  auto advance = [&](Cursor& c) {
+    if (++c.st * 32 >= c.R.n_keys) {
+      c.st = 0;
+      if (++c.ri < w.rng_count)
+        c.R = p.ranges[w.rng_begin + c.ri];
+      else
+        c.ok = false;
+    }
+  };
+  Cursor C{0, 0, p.ranges[w.rng_begin], true};
+  Cursor L = C;
+
+  uint4 kf[2][2][NDS];  // [set][M block][K-slice]
+  uint4 vf[2][NDM];     // [set][16-row d block]
+  int64_t blk[2][2];    // [set][block of the step's first/second 16 keys]
+
+  auto load_k = [&](const Cursor& c, int X) {
+    const int nk = c.R.n_keys, kb = c.st * 32;
+    const int64_t base = c.R.kv_start + (kb >> 4);
+    blk[X][0] = bt[base];
+    blk[X][1] = bt[base + ((kb + 16 < nk) ? 1 : 0)];
+#pragma unroll
+    for (int mb = 0; mb < 2; ++mb) {
+      const int key = step_key(mb, n);
+      const bool ok = kb + key < nk;
+      const uint16_t* kp = Kc + ((blk[X][key >> 4] * Hkv + kvh) * kBlock + (key & 15)) * D + 8 * g;
+#pragma unroll
+      for (int ds = 0; ds < NDS; ++ds) {
+        const uint4 x = *reinterpret_cast<const uint4*>(kp + ds * 32);
+        kf[X][mb][ds] = ok ? x : make_uint4(0, 0, 0, 0);
+      }
+    }
+  };
+  auto load_v = [&](const Cursor& c, int X) {
+    const int keep = c.R.n_keys - (c.st * 32 + 8 * g);  // keys 8g .. 8g+7 of the step
+    const uint16_t* vp = Vc + ((blk[X][g >> 1] * Hkv + kvh) * D + n) * kBlock + 8 * (g & 1);
+#pragma unroll
+    for (int dm = 0; dm < NDM; ++dm)
+      vf[X][dm] = keep_first(*reinterpret_cast<const uint4*>(vp + dm * 16 * kBlock), keep);
+  };
+
+  float m_run = -INFINITY, l_part = 0.f;
+  f32x4_t acc[NDM];
+#pragma unroll
+  for (int dm = 0; dm < NDM; ++dm) acc[dm] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+  int lim = 0;
+  auto load_lim = [&]() { lim = C.R.lim_off < 0 ? C.R.n_keys : (valid ? p.lims[C.R.lim_off + t] : 0); };
+  load_lim();
+  const float sl2 = p.scale_log2;
+
+  // Prologue: steps 0 and 1 into sets 0 and 1.
+  load_k(L, 0);
+  load_v(L, 0);
+  advance(L);
+  if (L.ok) {
+    load_k(L, 1);
+    load_v(L, 1);
+    advance(L);
+  }
+
+  auto step = [&](auto xc) -> bool {
+    constexpr int X = decltype(xc)::value;
+    const int kb = C.st * 32;
+    f32x4_t S[2];
+#pragma unroll
+    for (int mb = 0; mb < 2; ++mb) {
+      S[mb] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int ds = 0; ds < NDS; ++ds)
+        S[mb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf16x8(kf[X][mb][ds]), bq[ds], S[mb], 0, 0, 0);
+    }
+    const bool more = L.ok;
+    if (more) load_k(L, X);  // set X's K is consumed
+    if (kb + 32 > C.R.min_lim) {
+#pragma unroll
+      for (int mb = 0; mb < 2; ++mb)
+#pragma unroll
+        for (int i = 0; i < 4; ++i)
+          if (kb + 8 * g + 4 * mb + i >= lim) S[mb][i] = -INFINITY;
+    }
+    float mx = fmaxf(fmaxf(fmaxf(S[0][0], S[0][1]), fmaxf(S[0][2], S[0][3])),
+                     fmaxf(fmaxf(S[1][0], S[1][1]), fmaxf(S[1][2], S[1][3])));
+    mx = fmaxf(mx, __shfl_xor(mx, 16));
+    mx = fmaxf(mx, __shfl_xor(mx, 32));
+    const float m_new = fmaxf(m_run, mx * sl2);
+    const float m_sub = m_new == -INFINITY ? 0.f : m_new;
+    const float alpha = fast_exp2(m_run - m_sub);
+    m_run = m_new;
+    float e[8];
+    float ls = 0.f;
+#pragma unroll
+    for (int mb = 0; mb < 2; ++mb)
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        e[4 * mb + i] = fast_exp2(fmaf(S[mb][i], sl2, -m_sub));
+        ls += e[4 * mb + i];
+      }
+    l_part = fmaf(l_part, alpha, ls);
+    bf16x8_t pb;
+#pragma unroll
+    for (int s = 0; s < 8; ++s) pb[s] = (__bf16)e[s];
+#pragma unroll
+    for (int dm = 0; dm < NDM; ++dm) {
+      acc[dm] *= alpha;
+      acc[dm] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf16x8(vf[X][dm]), pb, acc[dm], 0, 0, 0);
+    }
+    if (more) {
+      load_v(L, X);  // set X's V is consumed
+      advance(L);
+    }
+    const int ri_before = C.ri;
+    advance(C);
+    if (!C.ok) return false;
+    if (C.ri != ri_before) load_lim();
+    return true;
+  };
+  while (step(std::integral_constant<int, 0>{}) && step(std::integral_constant<int, 1>{})) {
+  }
+
+  float lt = l_part + __shfl_xor(l_part, 16);
+  lt += __shfl_xor(lt, 32);
+  if (!valid) return;
+  if (w.fin) {
+    // Merge the row's other partials (shared items, complete: they ran
+    // earlier on this stream; this item's own slot is the list's last entry)
+    // with this one and write O and LSE (same arithmetic as the combine).
+    const int h = col - t * G;
+    const int64_t rk = (int64_t)qrow * Hkv + kvh;
+    const int32_t e0 = p.comb_ptr[rk], e1 = p.comb_ptr[rk + 1] - 1;
+    float M = m_run;
+    for (int32_t e = e0; e < e1; ++e) M = fmaxf(M, p.part_ml[2 * (int64_t)(p.comb_slot[e] + h)]);
+    const float so = fast_exp2(m_run - M);
+    float Ls = lt * so;
+#pragma unroll
+    for (int dm = 0; dm < NDM; ++dm) acc[dm] *= so;
+    for (int32_t e = e0; e < e1; ++e) {
+      const int64_t slot = p.comb_slot[e] + h;
+      const float sc = fast_exp2(p.part_ml[2 * slot] - M);
+      Ls = fmaf(p.part_ml[2 * slot + 1], sc, Ls);
+      const float* src = p.part_o + slot * D + 4 * g;
+#pragma unroll
+      for (int dm = 0; dm < NDM; ++dm) {
+        const float4 x = *reinterpret_cast<const float4*>(src + dm * 16);
+        acc[dm][0] = fmaf(x.x, sc, acc[dm][0]);
+        acc[dm][1] = fmaf(x.y, sc, acc[dm][1]);
+        acc[dm][2] = fmaf(x.z, sc, acc[dm][2]);
+        acc[dm][3] = fmaf(x.w, sc, acc[dm][3]);
+      }
+    }
+    const float inv = 1.f / Ls;
+    uint16_t* op = static_cast<uint16_t*>(p.o) + ((int64_t)qrow * p.Hq + hq) * D + 4 * g;
+#pragma unroll
+    for (int dm = 0; dm < NDM; ++dm) {
+      uint2 pk;
+      pk.x = (uint32_t)f32_to_bf16_bits(acc[dm][0] * inv) | ((uint32_t)f32_to_bf16_bits(acc[dm][1] * inv) << 16);
+      pk.y = (uint32_t)f32_to_bf16_bits(acc[dm][2] * inv) | ((uint32_t)f32_to_bf16_bits(acc[dm][3] * inv) << 16);
+      *reinterpret_cast<uint2*>(op + dm * 16) = pk;
+    }
+    if (g == 0) p.lse[(int64_t)qrow * p.Hq + hq] = (M + __log2f(Ls)) * kLn2;
+    return;
+  }
+  const int64_t slot = (int64_t)w.out_base + col;
+  float* op = p.part_o + slot * D + 4 * g;
+#pragma unroll
+  for (int dm = 0; dm < NDM; ++dm)
+    *reinterpret_cast<float4*>(op + dm * 16) = make_float4(acc[dm][0], acc[dm][1], acc[dm][2], acc[dm][3]);
+  if (g == 0) {
+    p.part_ml[2 * slot] = m_run;
+    p.part_ml[2 * slot + 1] = lt;
+  }
+}
+
+}  // namespace
+
+hipError_t launch_decode_private_bf16(const TileParams& p, int n_items, int D, hipStream_t stream) {
+  if (n_items <= 0) return hipSuccess;
+  const dim3 grid(n_items), block(64);
+  if (D == 64)
+    hipLaunchKernelGGL((decode_private_kernel<64>), grid, block, 0, stream, p);
+  else
+    hipLaunchKernelGGL((decode_private_kernel<128>), grid, block, 0, stream, p);
+  return hipGetLastError();
+}
+
+}  // namespace padoc

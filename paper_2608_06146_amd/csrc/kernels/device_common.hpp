@@ -35,4 +35,17 @@ __device__ __forceinline__ uint16_t f32_to_bf16_bits(float f) {
 
 __device__ __forceinline__ float bf16_bits_to_f32(uint16_t b) { return __uint_as_float((uint32_t)b << 16); }
 
+// Zero the bf16 elements at positions >= keep of an 8-element (16-byte)
+// chunk; keep may be <= 0 (all zero) or >= 8 (unchanged).
+__device__ __forceinline__ uint4 keep_first(uint4 u, int keep) {
+  uint32_t w[4] = {u.x, u.y, u.z, u.w};
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const int lo = 2 * i;
+    const uint32_t m = (lo + 1 < keep) ? 0xffffffffu : (lo < keep ? 0x0000ffffu : 0u);
+    w[i] &= m;
+  }
+  return make_uint4(w[0], w[1], w[2], w[3]);
+}
+
 }  // namespace padoc

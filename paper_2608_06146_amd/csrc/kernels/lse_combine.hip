@@ -6,7 +6,9 @@
 //   M = max m_i;  L = sum l_i 2^(m_i - M);  O = sum o_i 2^(m_i - M) / L;
 //   LSE = (M + log2 L) ln 2.
 // Partials are read in the planner's fixed order, so results are bitwise
-// reproducible.  32 threads per (query row, head), 8 rows per block.
+// reproducible.  32 threads per (query row, head), 8 per block, over the
+// (row, KV head) pairs the plan lists (rows a decode kernel already finished
+// are not listed).
 #include "device_common.hpp"
 
 namespace padoc {
@@ -16,13 +18,14 @@ __global__ __launch_bounds__(256) void lse_combine_kernel(CombineParams p) {
   constexpr int PER = D / 32;
   const int64_t pair = (int64_t)blockIdx.x * 8 + (threadIdx.x >> 5);
   const int sub = threadIdx.x & 31;
-  if (pair >= p.n_q * p.Hq) return;
-  const int64_t row = pair / p.Hq;
-  const int hq = (int)(pair - row * p.Hq);
-  const int g = hq / p.G;
-  const int h = hq - g * p.G;
-  const int32_t e0 = p.comb_ptr[row * p.Hkv + g];
-  const int32_t e1 = p.comb_ptr[row * p.Hkv + g + 1];
+  if (pair >= p.n_rows * p.G) return;
+  const int64_t rk = p.comb_rows[pair / p.G];
+  const int h = (int)(pair % p.G);
+  const int64_t row = rk / p.Hkv;
+  const int g = (int)(rk - row * p.Hkv);
+  const int hq = g * p.G + h;
+  const int32_t e0 = p.comb_ptr[rk];
+  const int32_t e1 = p.comb_ptr[rk + 1];
   if (e0 == e1) return;
   float M = -INFINITY;
   for (int32_t e = e0; e < e1; ++e) M = fmaxf(M, p.part_ml[2 * (int64_t)(p.comb_slot[e] + h)]);
@@ -69,7 +72,7 @@ __global__ __launch_bounds__(256) void lse_combine_kernel(CombineParams p) {
 }
 
 hipError_t launch_lse_combine(const CombineParams& p, int D, bool bf16, hipStream_t stream) {
-  const int64_t pairs = p.n_q * p.Hq;
+  const int64_t pairs = p.n_rows * p.G;
   if (pairs == 0) return hipSuccess;
   const dim3 grid((unsigned)((pairs + 7) / 8)), block(256);
   if (D == 64) {

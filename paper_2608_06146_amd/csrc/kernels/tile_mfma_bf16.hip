@@ -1,30 +1,47 @@
-// bf16 packed-forward tile kernel for gfx950 (CDNA4) matrix cores.
+// bf16 tile kernel for gfx950 (CDNA4) matrix cores: the packed forward, and
+// the shared-segment part of a decode step (paged K/V, split partials).
 //
-// One workgroup (4 waves) processes one work item: up to 256 columns
-// (query token x head of one KV-head group; GQA heads of a token share every
-// K/V tile) against the item's key ranges, 64 keys per step.  Per step the
-// workgroup stages the K tile row-major and the V tile transposed in LDS,
-// then every wave, for its 64 columns:
-//   S^T = K Q^T            v_mfma_f32_32x32x16_bf16, keys on M, columns on N
-//   online softmax         per column = per lane (the 32x32 accumulator
-//                          layout gives a lane one column and 16 key rows;
-//                          the other 16 rows are in lane^32)
-//   O^T += V^T P^T         P^T comes straight from the S^T registers
-// (App. E Attn equation; App. C tree-varlen relation).  Only tiles of
-// ancestor prefixes and the own causal range are ever visited: the planner
-// lists no other segment.  Tiles wholly below every column's limit skip the
-// mask; keys past a range's end are zero-filled in LDS so no stale or
-// sentinel memory enters a product.
+// One workgroup of 8 wavefronts processes one work item: up to 256 columns
+// (query token x head of one KV-head group -- the G heads of a token share
+// every K/V tile) against the item's key ranges, 64 keys per tile.  The
+// workgroup stages each K tile row-major and each V tile transposed in LDS
+// (double-buffered, one barrier per tile) while every wavefront computes, for
+// its 32 columns:
+//   S^T = K Q^T         v_mfma_f32_32x32x16_bf16, keys on M, columns on N
+//   online softmax      per column = per lane (the 32x32 accumulator layout
+//                       gives a lane one column and 16 key rows; the other 16
+//                       rows are in lane^32)
+//   O^T += V^T P^T      P^T comes straight from the S^T registers
+// (App. E Attn equation; App. C tree-varlen relation).  Only tiles of ancestor
+// prefixes and the own causal range are visited: the planner lists no other
+// segment.  Tiles wholly below every column's limit skip the mask; keys past
+// a range's end are zeroed in LDS so no stale or sentinel memory enters a
+// product.
 //
-// Accumulation is fp32; scores are scaled into log2 units so the
-// exponentials are single v_exp_f32; O is rounded to bf16 (RNE) at the end.
+// Accumulation is fp32 and scores are in log2 units, so each probability is
+// one v_exp_f32.  The reference maximum of a column is raised only when a
+// tile's maximum exceeds it by more than 2^8 (probabilities stay <= 256); the
+// accumulator is rescaled only then.  Any reference gives the same O and LSE.
+// O is rounded to bf16 (RNE) at the end.
+//
+// Paged K/V: K blocks [16 tokens][d] are read like packed rows through the
+// block table; V blocks are d-major ([d][16 tokens]), so a 16-byte load holds
+// 8 consecutive keys of one d row and lands in the transposed LDS tile as two
+// 8-byte stores.  A tile's block ids are wave-uniform scalars fetched one tile
+// ahead of its K/V loads.
 #include "device_common.hpp"
 
 namespace padoc {
 
+namespace {
+
 typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
 typedef float f32x8_t __attribute__((ext_vector_type(8)));
 typedef float f32x16_t __attribute__((ext_vector_type(16)));
+
+constexpr int kWaves = 8;
+constexpr int kThreads = 64 * kWaves;
+constexpr float kRescaleSlack = 8.0f;  // log2 units: probabilities <= 2^8
 
 // Position of key r (0..63) inside a transposed V row.  Within each group of
 // 16 keys, lane half 0 of the 32x32 P^T fragment holds keys
@@ -35,293 +52,336 @@ __device__ __forceinline__ int vt_pos(int r) {
   return (r & ~15) + ((q >> 2) & 1) * 8 + (q >> 3) * 4 + (q & 3);
 }
 
-template <int D, bool PAGED, bool PARTIAL>
-__global__ __launch_bounds__(256, 1) void tile_mfma_bf16_kernel(TileParams p) {
-  constexpr int KT = kTileKeys;     // 64 keys per step
-  constexpr int KS = D + 8;         // K row stride in LDS (elements); +8 spreads banks
-  constexpr int VS = KT + 8;        // V^T row stride in LDS
-  constexpr int NKK = D / 16;       // K-slices of the score product
-  constexpr int NDB = D / 32;       // 32-row blocks of O^T
-  constexpr int CPR = D / 8;        // 16-byte chunks per key row
-  constexpr int KPT = KT * CPR / 256;        // K chunks per thread
-  constexpr int VPT = KT * CPR / 512;        // V key-pair chunks per thread
+__device__ __forceinline__ int64_t uniform64(int64_t x) {
+  return (int64_t)(((uint64_t)(uint32_t)__builtin_amdgcn_readfirstlane((int)(x >> 32)) << 32) |
+                   (uint32_t)__builtin_amdgcn_readfirstlane((int)x));
+}
 
-  __shared__ __attribute__((aligned(16))) uint16_t Ks[KT * KS];
-  __shared__ __attribute__((aligned(16))) uint16_t Vt[D * VS];
+__device__ __forceinline__ RangeRec uniform_range(RangeRec r) {
+  r.kv_start = uniform64(r.kv_start);
+  r.n_keys = __builtin_amdgcn_readfirstlane(r.n_keys);
+  r.min_lim = __builtin_amdgcn_readfirstlane(r.min_lim);
+  r.lim_off = __builtin_amdgcn_readfirstlane(r.lim_off);
+  return r;
+}
+
+template <int D, bool PAGED, bool PARTIAL>
+__global__ __launch_bounds__(kThreads) void tile_mfma_bf16_kernel(TileParams p) {
+  constexpr int KT = kTileKeys;  // 64 keys per tile
+  constexpr int KS = D + 8;      // K row stride in LDS (elements); +8 spreads banks
+  constexpr int VS = KT + 8;     // V^T row stride in LDS
+  constexpr int NKK = D / 16;    // K-slices of the score product
+  constexpr int NDB = D / 32;    // 32-row blocks of O^T
+  constexpr int CPR = D / 8;     // 16-byte chunks per key row
+  constexpr int KPT = KT * CPR / kThreads;           // K chunks per thread (2 or 1)
+  constexpr int VPT = PAGED ? 8 * D / kThreads : 1;  // V loads per thread (paged chunks / packed pairs)
+  constexpr int NB = KT / kBlock;                    // blocks per tile (paged)
+
+  __shared__ __attribute__((aligned(16))) uint16_t Ks[2][KT * KS];
+  __shared__ __attribute__((aligned(16))) uint16_t Vt[2][D * VS];
 
   const WorkRec w = p.work[blockIdx.x];
   if (w.rng_count <= 0) return;
   const int tid = threadIdx.x;
   const int wave = tid >> 6, lane = tid & 63, l32 = lane & 31, hf = lane >> 5;
   const int G = p.G;
+  const int kvh = w.kvh;
+  const int64_t Hkv = p.Hkv;
 
-  int tok[2];
-  bool valid[2];
-  int32_t qrow[2], hq[2];
-#pragma unroll
-  for (int nb = 0; nb < 2; ++nb) {
-    const int c = wave * 64 + nb * 32 + l32;
-    const int t = c / G;
-    tok[nb] = t;
-    valid[nb] = t < w.ntok;
-    qrow[nb] = valid[nb] ? p.toks[w.tok_begin + t] : 0;
-    hq[nb] = w.kvh * G + (c - t * G);
-  }
+  // This lane's column.
+  const int col = wave * 32 + l32;
+  const int tok = col / G;
+  const bool valid = tok < w.ntok;
+  const int32_t qrow = valid ? p.toks[w.tok_begin + tok] : 0;
+  const int32_t hq = kvh * G + (col - tok * G);
 
-  // Q fragments (B operand of S^T = K Q^T): lane (column l32, half hf) holds
-  // d = kk*16 + hf*8 .. +7.
-  const uint16_t* Q = static_cast<const uint16_t*>(p.q);
-  bf16x8_t bq[2][NKK];
-#pragma unroll
-  for (int nb = 0; nb < 2; ++nb) {
-    const uint16_t* qp = Q + ((int64_t)qrow[nb] * p.Hq + hq[nb]) * D + hf * 8;
+  // Q fragments (B operand of S^T = K Q^T): d = kk*16 + hf*8 .. +7.
+  bf16x8_t bq[NKK];
+  {
+    const uint16_t* qp = static_cast<const uint16_t*>(p.q) + ((int64_t)qrow * p.Hq + hq) * D + hf * 8;
 #pragma unroll
     for (int kk = 0; kk < NKK; ++kk) {
-      if (valid[nb]) {
-        bq[nb][kk] = *reinterpret_cast<const bf16x8_t*>(qp + kk * 16);
-      } else {
-        const uint4 z = make_uint4(0, 0, 0, 0);
-        bq[nb][kk] = *reinterpret_cast<const bf16x8_t*>(&z);
-      }
+      const uint4 z = valid ? *reinterpret_cast<const uint4*>(qp + kk * 16) : make_uint4(0, 0, 0, 0);
+      bq[kk] = *reinterpret_cast<const bf16x8_t*>(&z);
     }
   }
 
   const uint16_t* Kg = static_cast<const uint16_t*>(p.k);
   const uint16_t* Vg = static_cast<const uint16_t*>(p.v);
+
+  // Per-thread load geometry (independent of the tile).
+  int k_key[KPT], k_dc[KPT];
+#pragma unroll
+  for (int i = 0; i < KPT; ++i) {
+    const int u = tid + kThreads * i;
+    k_key[i] = u / CPR;
+    k_dc[i] = u % CPR;
+  }
+  // packed V: key pair (2pr, 2pr+1) and 16-byte chunk dc (threads >= 32*CPR idle)
+  const int v_pr = tid % (KT / 2), v_dc = tid / (KT / 2);
+  const bool v_on = PAGED || v_dc < CPR;
+
   uint4 kr[KPT], vr[2 * VPT];
 
-  auto load_tile = [&](const RangeRec& R, int kt) {
+  auto fetch_ids = [&](const RangeRec& R, int kt, int64_t (&ids)[NB]) {
     const int kbase = kt * KT;
 #pragma unroll
-    for (int i = 0; i < KPT; ++i) {
-      const int c = tid + 256 * i;
-      const int key = c / CPR, dc = c % CPR;
-      const int j = kbase + key;
-      if (j < R.n_keys)
-        kr[i] = *reinterpret_cast<const uint4*>(Kg + key_offset<D, PAGED>(R, j, w.kvh, p.Hkv, p.block_table) + dc * 8);
-      else
-        kr[i] = make_uint4(0, 0, 0, 0);
-    }
+    for (int bi = 0; bi < NB; ++bi)
+      ids[bi] = p.block_table[R.kv_start + (kbase >> 4) + ((kbase + bi * kBlock < R.n_keys) ? bi : 0)];
+  };
+  // Global -> registers, branch-free: rows past the range end are read from
+  // a clamped valid row and zeroed.
+  auto load_tile = [&](const RangeRec& R, int kt, const int64_t (&ids)[NB]) {
+    const int kbase = kt * KT;
+    const int last = R.n_keys - 1 - kbase;  // >= 0
 #pragma unroll
-    for (int i = 0; i < VPT; ++i) {
-      const int u = tid + 256 * i;
-      const int pr = u % (KT / 2), dc = u / (KT / 2);
-      const int j0 = kbase + 2 * pr;
-      if (j0 < R.n_keys)
-        vr[2 * i] = *reinterpret_cast<const uint4*>(Vg + key_offset<D, PAGED>(R, j0, w.kvh, p.Hkv, p.block_table) + dc * 8);
+    for (int i = 0; i < KPT; ++i) {
+      const int key = k_key[i];
+      const int kc = key <= last ? key : last;
+      int64_t off;
+      if constexpr (PAGED)
+        off = ((ids[kc >> 4] * Hkv + kvh) * kBlock + (kc & 15)) * (int64_t)D;
       else
-        vr[2 * i] = make_uint4(0, 0, 0, 0);
-      if (j0 + 1 < R.n_keys)
-        vr[2 * i + 1] =
-            *reinterpret_cast<const uint4*>(Vg + key_offset<D, PAGED>(R, j0 + 1, w.kvh, p.Hkv, p.block_table) + dc * 8);
-      else
-        vr[2 * i + 1] = make_uint4(0, 0, 0, 0);
+        off = ((R.kv_start + kbase + kc) * Hkv + kvh) * (int64_t)D;
+      const uint4 x = *reinterpret_cast<const uint4*>(Kg + off + k_dc[i] * 8);
+      kr[i] = key <= last ? x : make_uint4(0, 0, 0, 0);
+    }
+    if constexpr (PAGED) {
+#pragma unroll
+      for (int i = 0; i < VPT; ++i) {
+        const int u = tid + kThreads * i;
+        const int bi = u / (2 * D), rem = u % (2 * D);
+        const int d = rem >> 1, h = rem & 1;
+        const int keep = R.n_keys - (kbase + bi * kBlock + h * 8);
+        const int64_t blk = ids[keep > 0 ? bi : 0];
+        vr[i] = keep_first(*reinterpret_cast<const uint4*>(Vg + ((blk * Hkv + kvh) * D + d) * kBlock + h * 8), keep);
+      }
+    } else {
+      if (v_on) {
+        const int k0 = 2 * v_pr, k1 = k0 + 1;
+        const int c0 = k0 <= last ? k0 : last, c1 = k1 <= last ? k1 : last;
+        const uint4 x0 = *reinterpret_cast<const uint4*>(Vg + ((R.kv_start + kbase + c0) * Hkv + kvh) * D + v_dc * 8);
+        const uint4 x1 = *reinterpret_cast<const uint4*>(Vg + ((R.kv_start + kbase + c1) * Hkv + kvh) * D + v_dc * 8);
+        vr[0] = k0 <= last ? x0 : make_uint4(0, 0, 0, 0);
+        vr[1] = k1 <= last ? x1 : make_uint4(0, 0, 0, 0);
+      }
     }
   };
-
-  auto store_tile = [&]() {
+  auto store_tile = [&](int s) {
 #pragma unroll
-    for (int i = 0; i < KPT; ++i) {
-      const int c = tid + 256 * i;
-      const int key = c / CPR, dc = c % CPR;
-      *reinterpret_cast<uint4*>(&Ks[key * KS + dc * 8]) = kr[i];
-    }
+    for (int i = 0; i < KPT; ++i) *reinterpret_cast<uint4*>(&Ks[s][k_key[i] * KS + k_dc[i] * 8]) = kr[i];
+    if constexpr (PAGED) {
 #pragma unroll
-    for (int i = 0; i < VPT; ++i) {
-      const int u = tid + 256 * i;
-      const int pr = u % (KT / 2), dc = u / (KT / 2);
-      const int pos = vt_pos(2 * pr);
-      const uint32_t a[4] = {vr[2 * i].x, vr[2 * i].y, vr[2 * i].z, vr[2 * i].w};
-      const uint32_t b[4] = {vr[2 * i + 1].x, vr[2 * i + 1].y, vr[2 * i + 1].z, vr[2 * i + 1].w};
+      for (int i = 0; i < VPT; ++i) {
+        const int u = tid + kThreads * i;
+        const int bi = u / (2 * D), rem = u % (2 * D);
+        const int d = rem >> 1, h = rem & 1;
+        // keys 8h..8h+3 of block bi -> positions 4h..4h+3, keys 8h+4..8h+7 -> 8+4h..
+        uint16_t* row = &Vt[s][d * VS + bi * 16];
+        *reinterpret_cast<uint2*>(row + 4 * h) = make_uint2(vr[i].x, vr[i].y);
+        *reinterpret_cast<uint2*>(row + 8 + 4 * h) = make_uint2(vr[i].z, vr[i].w);
+      }
+    } else if (v_on) {
+      const int pos = vt_pos(2 * v_pr);
+      const uint32_t a[4] = {vr[0].x, vr[0].y, vr[0].z, vr[0].w};
+      const uint32_t b[4] = {vr[1].x, vr[1].y, vr[1].z, vr[1].w};
 #pragma unroll
       for (int m = 0; m < 4; ++m) {
         // d = dc*8 + 2m holds (key 2pr, key 2pr+1) low halves; d+1 the high halves
-        *reinterpret_cast<uint32_t*>(&Vt[(dc * 8 + 2 * m) * VS + pos]) = (a[m] & 0xffffu) | (b[m] << 16);
-        *reinterpret_cast<uint32_t*>(&Vt[(dc * 8 + 2 * m + 1) * VS + pos]) = (a[m] >> 16) | (b[m] & 0xffff0000u);
+        *reinterpret_cast<uint32_t*>(&Vt[s][(v_dc * 8 + 2 * m) * VS + pos]) = (a[m] & 0xffffu) | (b[m] << 16);
+        *reinterpret_cast<uint32_t*>(&Vt[s][(v_dc * 8 + 2 * m + 1) * VS + pos]) = (a[m] >> 16) | (b[m] & 0xffff0000u);
       }
     }
   };
 
-  float m_run[2] = {-INFINITY, -INFINITY};
-  float l_run[2] = {0.f, 0.f};
-  f32x16_t acc[NDB][2];
+  // Tile cursors (wave-uniform): C = tile being computed, L = next to load.
+  struct Cursor {
+    int ri, kt;
+    RangeRec R;
+    bool ok;
+  };
+  auto advance = [&](Cursor& c) {
+    if (++c.kt * KT >= c.R.n_keys) {
+      c.kt = 0;
+      if (++c.ri < w.rng_count)
+        c.R = uniform_range(p.ranges[w.rng_begin + c.ri]);
+      else
+        c.ok = false;
+    }
+  };
+  Cursor C{0, 0, uniform_range(p.ranges[w.rng_begin]), true};
+  Cursor L = C;
+  int lim = 0;
+  auto load_lim = [&]() { lim = C.R.lim_off < 0 ? C.R.n_keys : (valid ? p.lims[C.R.lim_off + tok] : 0); };
+  load_lim();
+
+  float m_run = -INFINITY, l_run = 0.f;
+  f32x16_t acc[NDB];
 #pragma unroll
   for (int db = 0; db < NDB; ++db)
 #pragma unroll
-    for (int nb = 0; nb < 2; ++nb)
-#pragma unroll
-      for (int i = 0; i < 16; ++i) acc[db][nb][i] = 0.f;
-
-  int ri = 0, kt = 0;
-  RangeRec R = p.ranges[w.rng_begin];
-  int lim[2];
-  auto load_lims = [&]() {
-#pragma unroll
-    for (int nb = 0; nb < 2; ++nb)
-      lim[nb] = R.lim_off < 0 ? R.n_keys : (valid[nb] ? p.lims[R.lim_off + tok[nb]] : 0);
-  };
-  load_lims();
-  load_tile(R, 0);
+    for (int i = 0; i < 16; ++i) acc[db][i] = 0.f;
   const float sl2 = p.scale_log2;
 
+  // Prologue: tile 0 into LDS stage 0, tile 1 into registers.
+  int64_t ids[NB] = {};
+  if constexpr (PAGED) fetch_ids(L.R, L.kt, ids);
+  load_tile(L.R, L.kt, ids);
+  advance(L);
+  store_tile(0);
+  bool staged = false;
+  if (L.ok) {
+    if constexpr (PAGED) fetch_ids(L.R, L.kt, ids);
+    load_tile(L.R, L.kt, ids);
+    advance(L);
+    staged = true;
+    if (PAGED && L.ok) fetch_ids(L.R, L.kt, ids);
+  }
+  __syncthreads();
+
+  int s = 0;
   while (true) {
-    __syncthreads();  // every wave is done reading the previous tile
-    store_tile();
-    __syncthreads();
+    const uint16_t* ks = Ks[s];
+    const uint16_t* vt = Vt[s];
+    const int kb = C.kt * KT;
 
-    // Prefetch the next tile into registers while this one is computed.
-    int nri = ri, nkt = kt + 1;
-    RangeRec NR = R;
-    bool has_next = true;
-    if (nkt * KT >= R.n_keys) {
-      nri = ri + 1;
-      nkt = 0;
-      if (nri < w.rng_count)
-        NR = p.ranges[w.rng_begin + nri];
-      else
-        has_next = false;
-    }
-    if (has_next) load_tile(NR, nkt);
-
-    // S^T = K Q^T for 64 keys x 64 columns.
-    f32x16_t S[2][2];
+    // S^T = K Q^T for 64 keys x 32 columns.
+    f32x16_t S[2];
 #pragma unroll
     for (int mb = 0; mb < 2; ++mb)
 #pragma unroll
-      for (int nb = 0; nb < 2; ++nb)
+      for (int i = 0; i < 16; ++i) S[mb][i] = 0.f;
 #pragma unroll
-        for (int i = 0; i < 16; ++i) S[mb][nb][i] = 0.f;
-#pragma unroll
-    for (int kk = 0; kk < NKK; ++kk) {
+    for (int kk = 0; kk < NKK; ++kk)
 #pragma unroll
       for (int mb = 0; mb < 2; ++mb) {
-        const bf16x8_t a = *reinterpret_cast<const bf16x8_t*>(&Ks[(mb * 32 + l32) * KS + kk * 16 + hf * 8]);
-#pragma unroll
-        for (int nb = 0; nb < 2; ++nb)
-          S[mb][nb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, bq[nb][kk], S[mb][nb], 0, 0, 0);
+        const bf16x8_t a = *reinterpret_cast<const bf16x8_t*>(&ks[(mb * 32 + l32) * KS + kk * 16 + hf * 8]);
+        S[mb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, bq[kk], S[mb], 0, 0, 0);
       }
+    if (kb + KT > C.R.min_lim) {
+      // Partial tile: key (mb, i) of this lane is kb + mb*32 + (i/4)*8 + hf*4 + i%4.
+#pragma unroll
+      for (int mb = 0; mb < 2; ++mb)
+#pragma unroll
+        for (int i = 0; i < 16; ++i)
+          if (kb + mb * 32 + (i >> 2) * 8 + hf * 4 + (i & 3) >= lim) S[mb][i] = -INFINITY;
     }
 
-    if ((kt + 1) * KT > R.min_lim) {
-      // Partial tile: key (mb, i) of this lane is
-      // kt*64 + mb*32 + (i/4)*8 + hf*4 + i%4.
+    // Online softmax with a lazily raised reference maximum.
+    float mx = -INFINITY;
 #pragma unroll
-      for (int mb = 0; mb < 2; ++mb)
+    for (int mb = 0; mb < 2; ++mb)
 #pragma unroll
-        for (int nb = 0; nb < 2; ++nb)
+      for (int i = 0; i < 16; i += 2) mx = fmaxf(mx, fmaxf(S[mb][i], S[mb][i + 1]));
+    mx = fmaxf(mx, __shfl_xor(mx, 32)) * sl2;
+    const bool raise = mx > m_run + kRescaleSlack;
+    if (__any(raise)) {
+      // raising lanes: factor 2^(old - new) (0 when nothing was seen yet);
+      // the others keep their reference (factor 1, also when still -inf)
+      const float alpha = raise ? fast_exp2(m_run - mx) : 1.f;
+      m_run = raise ? mx : m_run;
+      l_run *= alpha;
 #pragma unroll
-          for (int i = 0; i < 16; ++i) {
-            const int key = kt * KT + mb * 32 + (i >> 2) * 8 + hf * 4 + (i & 3);
-            if (key >= lim[nb]) S[mb][nb][i] = -INFINITY;
-          }
+      for (int db = 0; db < NDB; ++db) acc[db] *= alpha;
     }
-
-    // Online softmax, one column per lane (shared with lane ^ 32).
+    const float m_sub = m_run == -INFINITY ? 0.f : m_run;
+    float ls = 0.f;
 #pragma unroll
-    for (int nb = 0; nb < 2; ++nb) {
-      float mx = -INFINITY;
+    for (int mb = 0; mb < 2; ++mb)
 #pragma unroll
-      for (int mb = 0; mb < 2; ++mb)
-#pragma unroll
-        for (int i = 0; i < 16; ++i) mx = fmaxf(mx, S[mb][nb][i]);
-      mx = fmaxf(mx, __shfl_xor(mx, 32));
-      const float m_new = fmaxf(m_run[nb], mx * sl2);
-      const float m_sub = m_new == -INFINITY ? 0.f : m_new;
-      const float alpha = fast_exp2(m_run[nb] - m_sub);
-      m_run[nb] = m_new;
-      float ls = 0.f;
-#pragma unroll
-      for (int mb = 0; mb < 2; ++mb)
-#pragma unroll
-        for (int i = 0; i < 16; ++i) {
-          const float e = fast_exp2(fmaf(S[mb][nb][i], sl2, -m_sub));
-          S[mb][nb][i] = e;
-          ls += e;
-        }
-      l_run[nb] = fmaf(l_run[nb], alpha, ls);
-#pragma unroll
-      for (int db = 0; db < NDB; ++db) acc[db][nb] *= alpha;
-    }
+      for (int i = 0; i < 16; ++i) {
+        const float e = fast_exp2(fmaf(S[mb][i], sl2, -m_sub));
+        S[mb][i] = e;
+        ls += e;
+      }
+    l_run += ls;
 
     // O^T += V^T P^T, 16 keys per MFMA: keys mb*32 + 16j + [0,16).
 #pragma unroll
-    for (int mb = 0; mb < 2; ++mb) {
+    for (int mb = 0; mb < 2; ++mb)
 #pragma unroll
       for (int j = 0; j < 2; ++j) {
-        bf16x8_t pb[2];
+        f32x8_t x;
 #pragma unroll
-        for (int nb = 0; nb < 2; ++nb) {
-          f32x8_t x;
-#pragma unroll
-          for (int s = 0; s < 8; ++s) x[s] = S[mb][nb][8 * j + s];
-          pb[nb] = __builtin_convertvector(x, bf16x8_t);
-        }
+        for (int e = 0; e < 8; ++e) x[e] = S[mb][8 * j + e];
+        const bf16x8_t pb = __builtin_convertvector(x, bf16x8_t);
 #pragma unroll
         for (int db = 0; db < NDB; ++db) {
-          const bf16x8_t a =
-              *reinterpret_cast<const bf16x8_t*>(&Vt[(db * 32 + l32) * VS + mb * 32 + 16 * j + hf * 8]);
-#pragma unroll
-          for (int nb = 0; nb < 2; ++nb)
-            acc[db][nb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, pb[nb], acc[db][nb], 0, 0, 0);
+          const bf16x8_t a = *reinterpret_cast<const bf16x8_t*>(&vt[(db * 32 + l32) * VS + mb * 32 + 16 * j + hf * 8]);
+          acc[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, pb, acc[db], 0, 0, 0);
         }
       }
-    }
 
-    if (!has_next) break;
-    if (nri != ri) {
-      R = NR;
-      ri = nri;
-      load_lims();
+    // Stage the next tile into the other buffer (last read before the
+    // previous barrier) and start loading the one after.
+    if (staged) {
+      store_tile(s ^ 1);
+      staged = false;
     }
-    kt = nkt;
+    if (L.ok) {
+      load_tile(L.R, L.kt, ids);
+      advance(L);
+      staged = true;
+      if (PAGED && L.ok) fetch_ids(L.R, L.kt, ids);
+    }
+    __syncthreads();
+
+    const int ri_before = C.ri;
+    advance(C);
+    if (!C.ok) break;
+    if (C.ri != ri_before) load_lim();
+    s ^= 1;
   }
 
   // Epilogue.  Lane (column, hf) holds d = db*32 + (i/4)*8 + hf*4 + i%4.
+  const float lt = l_run + __shfl_xor(l_run, 32);
+  if (!valid) return;
+  if constexpr (PARTIAL) {
+    const int64_t slot = (int64_t)w.out_base + col;
+    float* op = p.part_o + slot * D;
 #pragma unroll
-  for (int nb = 0; nb < 2; ++nb) {
-    const float lt = l_run[nb] + __shfl_xor(l_run[nb], 32);
-    if (!valid[nb]) continue;
-    if constexpr (PARTIAL) {
-      const int64_t slot = (int64_t)w.out_base + wave * 64 + nb * 32 + l32;
-      float* op = p.part_o + slot * D;
+    for (int db = 0; db < NDB; ++db)
 #pragma unroll
-      for (int db = 0; db < NDB; ++db)
-#pragma unroll
-        for (int i4 = 0; i4 < 4; ++i4) {
-          const int d0 = db * 32 + i4 * 8 + hf * 4;
-          *reinterpret_cast<float4*>(op + d0) = make_float4(acc[db][nb][4 * i4], acc[db][nb][4 * i4 + 1],
-                                                            acc[db][nb][4 * i4 + 2], acc[db][nb][4 * i4 + 3]);
-        }
-      if (hf == 0) {
-        p.part_ml[2 * slot] = m_run[nb];
-        p.part_ml[2 * slot + 1] = lt;
+      for (int i4 = 0; i4 < 4; ++i4) {
+        const int d0 = db * 32 + i4 * 8 + hf * 4;
+        *reinterpret_cast<float4*>(op + d0) =
+            make_float4(acc[db][4 * i4], acc[db][4 * i4 + 1], acc[db][4 * i4 + 2], acc[db][4 * i4 + 3]);
       }
-    } else {
-      const float inv = 1.f / lt;
-      uint16_t* op = static_cast<uint16_t*>(p.o) + ((int64_t)qrow[nb] * p.Hq + hq[nb]) * D;
-#pragma unroll
-      for (int db = 0; db < NDB; ++db)
-#pragma unroll
-        for (int i4 = 0; i4 < 4; ++i4) {
-          const int d0 = db * 32 + i4 * 8 + hf * 4;
-          uint2 pk;
-          pk.x = (uint32_t)f32_to_bf16_bits(acc[db][nb][4 * i4] * inv) |
-                 ((uint32_t)f32_to_bf16_bits(acc[db][nb][4 * i4 + 1] * inv) << 16);
-          pk.y = (uint32_t)f32_to_bf16_bits(acc[db][nb][4 * i4 + 2] * inv) |
-                 ((uint32_t)f32_to_bf16_bits(acc[db][nb][4 * i4 + 3] * inv) << 16);
-          *reinterpret_cast<uint2*>(op + d0) = pk;
-        }
-      if (hf == 0) p.lse[(int64_t)qrow[nb] * p.Hq + hq[nb]] = (m_run[nb] + __log2f(lt)) * kLn2;
+    if (hf == 0) {
+      p.part_ml[2 * slot] = m_run;
+      p.part_ml[2 * slot + 1] = lt;
     }
+  } else {
+    const float inv = 1.f / lt;
+    uint16_t* op = static_cast<uint16_t*>(p.o) + ((int64_t)qrow * p.Hq + hq) * D;
+#pragma unroll
+    for (int db = 0; db < NDB; ++db)
+#pragma unroll
+      for (int i4 = 0; i4 < 4; ++i4) {
+        const int d0 = db * 32 + i4 * 8 + hf * 4;
+        uint2 pk;
+        pk.x = (uint32_t)f32_to_bf16_bits(acc[db][4 * i4] * inv) |
+               ((uint32_t)f32_to_bf16_bits(acc[db][4 * i4 + 1] * inv) << 16);
+        pk.y = (uint32_t)f32_to_bf16_bits(acc[db][4 * i4 + 2] * inv) |
+               ((uint32_t)f32_to_bf16_bits(acc[db][4 * i4 + 3] * inv) << 16);
+        *reinterpret_cast<uint2*>(op + d0) = pk;
+      }
+    if (hf == 0) p.lse[(int64_t)qrow * p.Hq + hq] = (m_run + __log2f(lt)) * kLn2;
   }
 }
 
-hipError_t launch_tile_mfma_bf16(const TileParams& p, int n_work, int D, hipStream_t stream) {
-  const dim3 grid(n_work), block(256);
-  if (D == 64)
-    hipLaunchKernelGGL((tile_mfma_bf16_kernel<64, false, false>), grid, block, 0, stream, p);
-  else
-    hipLaunchKernelGGL((tile_mfma_bf16_kernel<128, false, false>), grid, block, 0, stream, p);
+}  // namespace
+
+hipError_t launch_tile_mfma_bf16(const TileParams& p, int n_work, int D, bool paged, hipStream_t stream) {
+  if (n_work <= 0) return hipSuccess;
+  const dim3 grid(n_work), block(kThreads);
+  if (D == 64) {
+    if (paged) hipLaunchKernelGGL((tile_mfma_bf16_kernel<64, true, true>), grid, block, 0, stream, p);
+    else hipLaunchKernelGGL((tile_mfma_bf16_kernel<64, false, false>), grid, block, 0, stream, p);
+  } else {
+    if (paged) hipLaunchKernelGGL((tile_mfma_bf16_kernel<128, true, true>), grid, block, 0, stream, p);
+    else hipLaunchKernelGGL((tile_mfma_bf16_kernel<128, false, false>), grid, block, 0, stream, p);
+  }
   return hipGetLastError();
 }
 

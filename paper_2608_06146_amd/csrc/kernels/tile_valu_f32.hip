@@ -1,10 +1,9 @@
 // fp32 tile kernel: one thread per (query token, head) column of a work item,
 // keys visited one by one with an exact online softmax in fp32 on the vector
 // ALUs.  This is the fp32 path of both entry points (the MFMA paths are
-// bf16); it reads the same schedules as the bf16 kernels: packed forward
-// items of up to 256 columns (one per workgroup), decode wave items of up to
-// 32 columns (eight per workgroup, one per wavefront) over the paged cache
-// (K blocks [16][d], V blocks d-major [d][16]).
+// bf16); it reads the same schedules as the bf16 kernels, one workgroup per
+// work item (columns col0 .. col0+ncol-1 of the item's task), over packed
+// K/V or the paged cache (K blocks [16][d], V blocks d-major [d][16]).
 //
 // Per column and visible key j (App. E Attn equation, with the scale applied
 // in log2 units): s = scale*log2(e) * q.k_j; m' = max(m, s);
@@ -14,14 +13,14 @@
 namespace padoc {
 
 template <int D, bool PAGED>
-__global__ __launch_bounds__(512) void tile_valu_f32_kernel(TileParams p) {
+__global__ __launch_bounds__(256) void tile_valu_f32_kernel(TileParams p) {
   constexpr bool PARTIAL = PAGED;  // decode plans write split-KV partials
-  if (!PAGED && threadIdx.x >= kTileCols) return;
-  const WorkRec w = PAGED ? p.work[blockIdx.x * kDecodeWaves + (threadIdx.x >> 6)] : p.work[blockIdx.x];
-  const int c = PAGED ? (threadIdx.x & 63) : threadIdx.x;
+  const WorkRec w = p.work[blockIdx.x];
+  if ((int)threadIdx.x >= w.ncol) return;  // no barriers below
+  const int c = w.col0 + threadIdx.x;
   const int t = c / p.G;
   const int h = c - t * p.G;
-  if (t >= w.ntok) return;  // no barriers below
+  if (t >= w.ntok) return;
   const int32_t qrow = p.toks[w.tok_begin + t];
   const int32_t hq = w.kvh * p.G + h;
   const float4* qp = reinterpret_cast<const float4*>(static_cast<const float*>(p.q) + ((int64_t)qrow * p.Hq + hq) * D);
@@ -97,8 +96,7 @@ __global__ __launch_bounds__(512) void tile_valu_f32_kernel(TileParams p) {
 }
 
 hipError_t launch_tile_valu_f32(const TileParams& p, int n_work, int D, bool paged, hipStream_t stream) {
-  const dim3 grid(paged ? (n_work + kDecodeWaves - 1) / kDecodeWaves : n_work),
-      block(paged ? 64 * kDecodeWaves : kTileCols);
+  const dim3 grid(n_work), block(kTileCols);
   if (D == 64) {
     if (paged) hipLaunchKernelGGL((tile_valu_f32_kernel<64, true>), grid, block, 0, stream, p);
     else hipLaunchKernelGGL((tile_valu_f32_kernel<64, false>), grid, block, 0, stream, p);

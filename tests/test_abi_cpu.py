@@ -36,7 +36,7 @@ def test_library_exports_every_declared_symbol():
 
 def test_struct_layouts_match_header():
     assert C.sizeof(_lib.Segment) == 32 and pa.SEGMENT_DTYPE.itemsize == 32
-    assert _lib.WORK_DTYPE.itemsize == 32 and _lib.RANGE_DTYPE.itemsize == 32
+    assert _lib.WORK_DTYPE.itemsize == 48 and _lib.RANGE_DTYPE.itemsize == 32
 
 
 # ---------------------------------------------------------------- tree -> segments
@@ -109,7 +109,7 @@ def _check_forward(segs, G, Hkv):
     row_tok = _token_of_row(nodes, segs["q_off"])
     seen = {g: {} for g in range(Hkv)}
     for w in ex["work"]:
-        assert w["ntok"] * G <= ex["tile_cols"]
+        assert w["ntok"] * G <= ex["tile_cols"] and w["col0"] == 0 and w["ncol"] == w["ntok"] * G
         toks, cover = _item_coverage(ex, w, G)
         for i, row in enumerate(toks):
             assert int(row) not in seen[int(w["kvh"])], "query row scheduled twice for one KV head"
@@ -156,10 +156,14 @@ def _check_decode(segs, G, Hkv, chunk=0, read_once=False):
     assert ex["kind"] == 1
     row_tok = _token_of_row(nodes, segs["q_off"])
     slot_cover = {}
-    for w in ex["work"]:
-        if w["ntok"] == 0:
-            continue  # idle wave of a partly filled workgroup
-        assert w["ntok"] * G <= 32 and w["nblk"] == 1
+    slot_item = {}
+    cols_of = {}
+    fin_rows = set()
+    for idx, w in enumerate(ex["work"]):
+        width = 256 if idx < ex["n_work_shared"] else 16
+        assert 0 < w["ncol"] <= width and w["col0"] % width == 0
+        assert w["col0"] + w["ncol"] <= w["ntok"] * G
+        cols_of.setdefault(int(w["out_base"]), []).extend(range(w["col0"], w["col0"] + w["ncol"]))
         toks, cover = _item_coverage(ex, w, G)
         for r in range(w["rng_begin"], w["rng_begin"] + w["rng_count"]):
             R = ex["ranges"][r]
@@ -169,6 +173,13 @@ def _check_decode(segs, G, Hkv, chunk=0, read_once=False):
                 assert R["n_keys"] <= chunk
         for i in range(w["ntok"]):
             slot_cover[int(w["out_base"]) + i * G] = (int(toks[i]), int(w["kvh"]), cover[i])
+            slot_item.setdefault(int(w["out_base"]) + i * G, set()).add(idx)
+            if w["fin"]:
+                fin_rows.add(int(toks[i]) * Hkv + int(w["kvh"]))
+        if w["fin"]:
+            assert idx >= ex["n_work_shared"], "only private items finish rows"
+    for base, cols in cols_of.items():
+        assert sorted(cols) == list(range(len(cols))), "task columns not covered exactly once"
     n_q = int(sum(n[3] for n in nodes))
     assert len(ex["comb_ptr"]) == n_q * Hkv + 1
     for row, (s, p) in row_tok.items():
@@ -181,20 +192,30 @@ def _check_decode(segs, G, Hkv, chunk=0, read_once=False):
                 keys += cov
             assert len(keys) == len(set(keys)), "a key is combined twice"
             assert set(keys) == _visible_keys(nodes, s, p)
+    # a row finished by a private item: that item's slot is the row's last
+    # entry and every other entry is a shared item's (computed before it);
+    # the combine kernel visits exactly the other rows that have entries
+    for rk in fin_rows:
+        ents = [int(e) for e in ex["comb_slot"][ex["comb_ptr"][rk]: ex["comb_ptr"][rk + 1]]]
+        assert ents and all(ex["work"]["fin"][i] for i in slot_item[ents[-1]])
+        for e in ents[:-1]:
+            assert all(i < ex["n_work_shared"] for i in slot_item[e])
+    nonempty = {rk for rk in range(n_q * Hkv) if ex["comb_ptr"][rk + 1] > ex["comb_ptr"][rk]}
+    assert list(ex["comb_rows"]) == sorted(nonempty - fin_rows)
     # slots the combine does not read belong to tokens that see no key there
     used = set(int(e) for e in ex["comb_slot"])
     for slot, (_, _, cov) in slot_cover.items():
         assert (slot in used) == (len(cov) > 0)
     if read_once:
-        # every key is streamed by exactly one workgroup per KV head: sibling
-        # waves of a workgroup share the loads
+        # every key is streamed by exactly one task per KV head (siblings
+        # share the task's tiles)
         owner = {}
         for i, w in enumerate(ex["work"]):
             for r in range(w["rng_begin"], w["rng_begin"] + w["rng_count"]):
                 R = ex["ranges"][r]
                 for j in range(int(R["n_keys"])):
                     key = (int(w["kvh"]), int(R["seg"]), int(R["key_begin"]) + j)
-                    assert owner.setdefault(key, i // 8) == i // 8
+                    assert owner.setdefault(key, int(w["out_base"])) == int(w["out_base"])
     return ex
 
 
@@ -223,8 +244,8 @@ def test_decode_schedule_mixed_step_structure():
 
 def test_concurrent_decode_read_once():
     """64 pages x 24 branches: every cached key is streamed by exactly one
-    workgroup per KV head (the page's 25 streams are sibling waves of
-    one workgroup of seven waves), and every cached key is streamed."""
+    work item per KV head (the page's 25 streams share one 200-column tile
+    item for the prefix and stream), and every cached key is streamed."""
     wl = syn.make_workload("concurrent_decode_64pages")
     segs = pa.segments_from_pages(wl.pages, 16)
     nb = int(sum(-(-int(s["len"]) // 16) for s in segs))
@@ -233,13 +254,13 @@ def test_concurrent_decode_read_once():
     for g in range(2):
         owner = [np.full(int(sg["len"]), -1, dtype=np.int64) for sg in segs]
         for i, w in enumerate(ex["work"]):
-            if w["ntok"] == 0 or w["kvh"] != g:
+            if w["kvh"] != g:
                 continue
             for r in range(w["rng_begin"], w["rng_begin"] + w["rng_count"]):
                 R = ex["ranges"][r]
                 o = owner[int(R["seg"])][int(R["key_begin"]): int(R["key_begin"]) + int(R["n_keys"])]
-                assert ((o == -1) | (o == i // 8)).all(), "a key is streamed by two workgroups"
-                o[:] = i // 8
+                assert ((o == -1) | (o == i)).all(), "a key is streamed by two work items"
+                o[:] = i
         assert all((o >= 0).all() for o in owner), "a cached key is never streamed"
 
 

@@ -213,3 +213,16 @@ def test_dense_page_mixed_step_full_size_sampled():
     nq = syn.count_queries(wl.pages)
     rows = sorted(set(rng.choice(nq, 60, replace=False).tolist()) | {0, nq - 1})
     decode_case(wl.pages, 28, 4, 128, "bf16", 0, pool_extra=3000, rows=rows)
+
+
+@pytest.mark.parametrize("heads", [(40, 2), (64, 1)])
+def test_decode_wide_gqa_groups(heads):
+    """G = 20 and G = 64 heads per KV head: a private stream's columns are
+    split across several 16-column wavefront items."""
+    Hq, Hkv = heads
+    rng = np.random.default_rng(11)
+    br = tuple(syn.Branch(int(f), int(L), int(q)) for f, L, q in
+               zip(np.sort(rng.integers(1, 40, 6)), rng.integers(1, 120, 6), (1, 1, 2, 1, 3, 1)))
+    pages = [syn.Page(150, 0, 40, 1, br)]
+    decode_case(pages, Hq, Hkv, 128, "bf16", 3)
+    decode_case(pages, Hq, Hkv, 64, "f32", 3)
