@@ -84,6 +84,7 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(2, 2))) void
 
   uint4 kf[2][2][NDS];  // [set][M block][K-slice]
   uint4 vf[2][NDM];     // [set][16-row d block]
+  int vkeep[2];
   int64_t blk[2][2];    // [set][block of the step's first/second 16 keys]
 
   auto load_k = [&](const Cursor& c, int X) {
@@ -94,12 +95,10 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(2, 2))) void
 #pragma unroll
     for (int mb = 0; mb < 2; ++mb) {
       const int key = step_key(mb, n);
-      const bool ok = kb + key < nk;
       const uint16_t* kp = Kc + ((blk[X][key >> 4] * Hkv + kvh) * kBlock + (key & 15)) * D + 8 * g;
 #pragma unroll
       for (int ds = 0; ds < NDS; ++ds) {
-        const uint4 x = *reinterpret_cast<const uint4*>(kp + ds * 32);
-        kf[X][mb][ds] = ok ? x : make_uint4(0, 0, 0, 0);
+        kf[X][mb][ds] = load_stream16(kp + ds * 32);
       }
     }
   };
@@ -108,7 +107,8 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(2, 2))) void
     const uint16_t* vp = Vc + ((blk[X][g >> 1] * Hkv + kvh) * D + n) * kBlock + 8 * (g & 1);
 #pragma unroll
     for (int dm = 0; dm < NDM; ++dm)
-      vf[X][dm] = keep_first(*reinterpret_cast<const uint4*>(vp + dm * 16 * kBlock), keep);
+      vf[X][dm] = load_stream16(vp + dm * 16 * kBlock);
+    vkeep[X] = keep;
   };
 
   float m_run = -INFINITY, l_part = 0.f;
@@ -174,7 +174,7 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(2, 2))) void
 #pragma unroll
     for (int dm = 0; dm < NDM; ++dm) {
       acc[dm] *= alpha;
-      acc[dm] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf16x8(vf[X][dm]), pb, acc[dm], 0, 0, 0);
+      acc[dm] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf16x8(keep_first(vf[X][dm], vkeep[X])), pb, acc[dm], 0, 0, 0);
     }
     if (more) {
       load_v(L, X);  // set X's V is consumed

@@ -24,7 +24,48 @@ __device__ __forceinline__ int64_t key_offset(const RangeRec& r, int32_t j, int3
   }
 }
 
+// 16-byte load with the non-temporal hint: for K/V that a kernel reads once
+// (paged decode), so the caches do not keep lines nobody will read again.
+__device__ __forceinline__ uint4 load_stream16(const void* p) {
+  typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
+  const u32x4 t = __builtin_nontemporal_load(static_cast<const u32x4*>(p));
+  return make_uint4(t.x, t.y, t.z, t.w);
+}
+
 __device__ __forceinline__ float fast_exp2(float x) { return __builtin_amdgcn_exp2f(x); }
+
+// max(a, b, c) as one v_max3_f32.  Written as an instruction so the compiler
+// does not first canonicalise each operand (it cannot prove that values
+// merged from masked and unmasked paths are canonical); inputs here are
+// finite or -inf.
+__device__ __forceinline__ float max3f(float a, float b, float c) {
+  float r;
+  asm("v_max3_f32 %0, %1, %2, %3" : "=v"(r) : "v"(a), "v"(b), "v"(c));
+  return r;
+}
+
+// Maximum of x over lanes l and l^32 (in every lane): v_permlane32_swap of
+// two copies leaves one holding the low half's values in both halves and the
+// other the high half's.
+__device__ __forceinline__ float max_lane_halves(float x) {
+  const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  return max3f(x, __uint_as_float(r[0]), __uint_as_float(r[1]));
+}
+
+// Maximum of x over lanes l and l^16 (rows of 16 lanes): v_permlane16_swap
+// of two copies pairs each row with its neighbour.
+__device__ __forceinline__ float max_lane_rows(float x) {
+  const auto r = __builtin_amdgcn_permlane16_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  return max3f(x, __uint_as_float(r[0]), __uint_as_float(r[1]));
+}
+
+typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
+
+// acc + x.lo + x.hi for two bf16 values (one v_dot2c_f32_bf16 against 1.0).
+__device__ __forceinline__ float add_bf16x2(bf16x2_t x, float acc) {
+  const bf16x2_t one = {(__bf16)1.0f, (__bf16)1.0f};
+  return __builtin_amdgcn_fdot2_f32_bf16(x, one, acc, false);
+}
 
 // Round-to-nearest-even fp32 -> bf16 bits (inputs here are finite).
 __device__ __forceinline__ uint16_t f32_to_bf16_bits(float f) {

@@ -14,12 +14,15 @@
 //   O^T += V^T P^T      P^T comes straight from the S^T registers
 // (App. E Attn equation; App. C tree-varlen relation).  Only tiles of ancestor
 // prefixes and the own causal range are visited: the planner lists no other
-// segment.  Tiles wholly below every column's limit skip the mask; keys past
-// a range's end are zeroed in LDS so no stale or sentinel memory enters a
-// product.
+// segment.  Tiles wholly below every column's limit skip the mask.  Keys
+// past a range's end never contribute: their K/V rows are copies of the
+// range's last row (finite), their scores are masked to -inf, and paged V
+// chunks past the end are zeroed in LDS, so no stale or sentinel memory
+// enters a product.
 //
 // Accumulation is fp32 and scores are in log2 units, so each probability is
-// one v_exp_f32.  The reference maximum of a column is raised only when a
+// one v_exp_f32; the softmax denominator sums the bf16-rounded probabilities
+// that enter the PV product, so O is their exact weighted mean.  The reference maximum of a column is raised only when a
 // tile's maximum exceeds it by more than 2^8 (probabilities stay <= 256); the
 // accumulator is rescaled only then.  Any reference gives the same O and LSE.
 // O is rounded to bf16 (RNE) at the end.
@@ -41,6 +44,7 @@ typedef float f32x16_t __attribute__((ext_vector_type(16)));
 
 constexpr int kWaves = 8;
 constexpr int kThreads = 64 * kWaves;
+constexpr int kStages = 3;
 constexpr float kRescaleSlack = 8.0f;  // log2 units: probabilities <= 2^8
 
 // Position of key r (0..63) inside a transposed V row.  Within each group of
@@ -77,8 +81,8 @@ __global__ __launch_bounds__(kThreads) void tile_mfma_bf16_kernel(TileParams p) 
   constexpr int VPT = PAGED ? 8 * D / kThreads : 1;  // V loads per thread (paged chunks / packed pairs)
   constexpr int NB = KT / kBlock;                    // blocks per tile (paged)
 
-  __shared__ __attribute__((aligned(16))) uint16_t Ks[2][KT * KS];
-  __shared__ __attribute__((aligned(16))) uint16_t Vt[2][D * VS];
+  __shared__ __attribute__((aligned(16))) uint16_t Ks[kStages][KT * KS];
+  __shared__ __attribute__((aligned(16))) uint16_t Vt[kStages][D * VS];
 
   const WorkRec w = p.work[blockIdx.x];
   if (w.rng_count <= 0) return;
@@ -122,6 +126,7 @@ __global__ __launch_bounds__(kThreads) void tile_mfma_bf16_kernel(TileParams p) 
   const bool v_on = PAGED || v_dc < CPR;
 
   uint4 kr[KPT], vr[2 * VPT];
+  int vkeep[PAGED ? VPT : 1];  // paged V: keys of each chunk inside the range
 
   auto fetch_ids = [&](const RangeRec& R, int kt, int64_t (&ids)[NB]) {
     const int kbase = kt * KT;
@@ -129,8 +134,10 @@ __global__ __launch_bounds__(kThreads) void tile_mfma_bf16_kernel(TileParams p) 
     for (int bi = 0; bi < NB; ++bi)
       ids[bi] = p.block_table[R.kv_start + (kbase >> 4) + ((kbase + bi * kBlock < R.n_keys) ? bi : 0)];
   };
-  // Global -> registers, branch-free: rows past the range end are read from
-  // a clamped valid row and zeroed.
+  // Global -> registers, branch-free.  Rows past the range end are read from
+  // the range's last row (finite data whose scores the mask removes); paged
+  // V chunks, which may reach into unwritten slots, are zeroed past the end
+  // when they are stored, a tile later, so no load is waited for early.
   auto load_tile = [&](const RangeRec& R, int kt, const int64_t (&ids)[NB]) {
     const int kbase = kt * KT;
     const int last = R.n_keys - 1 - kbase;  // >= 0
@@ -143,8 +150,8 @@ __global__ __launch_bounds__(kThreads) void tile_mfma_bf16_kernel(TileParams p) 
         off = ((ids[kc >> 4] * Hkv + kvh) * kBlock + (kc & 15)) * (int64_t)D;
       else
         off = ((R.kv_start + kbase + kc) * Hkv + kvh) * (int64_t)D;
-      const uint4 x = *reinterpret_cast<const uint4*>(Kg + off + k_dc[i] * 8);
-      kr[i] = key <= last ? x : make_uint4(0, 0, 0, 0);
+      const uint4 x = PAGED ? load_stream16(Kg + off + k_dc[i] * 8) : *reinterpret_cast<const uint4*>(Kg + off + k_dc[i] * 8);
+      kr[i] = x;
     }
     if constexpr (PAGED) {
 #pragma unroll
@@ -154,7 +161,8 @@ __global__ __launch_bounds__(kThreads) void tile_mfma_bf16_kernel(TileParams p) 
         const int d = rem >> 1, h = rem & 1;
         const int keep = R.n_keys - (kbase + bi * kBlock + h * 8);
         const int64_t blk = ids[keep > 0 ? bi : 0];
-        vr[i] = keep_first(*reinterpret_cast<const uint4*>(Vg + ((blk * Hkv + kvh) * D + d) * kBlock + h * 8), keep);
+        vr[i] = load_stream16(Vg + ((blk * Hkv + kvh) * D + d) * kBlock + h * 8);
+        vkeep[i] = keep;
       }
     } else {
       if (v_on) {
@@ -162,8 +170,8 @@ __global__ __launch_bounds__(kThreads) void tile_mfma_bf16_kernel(TileParams p) 
         const int c0 = k0 <= last ? k0 : last, c1 = k1 <= last ? k1 : last;
         const uint4 x0 = *reinterpret_cast<const uint4*>(Vg + ((R.kv_start + kbase + c0) * Hkv + kvh) * D + v_dc * 8);
         const uint4 x1 = *reinterpret_cast<const uint4*>(Vg + ((R.kv_start + kbase + c1) * Hkv + kvh) * D + v_dc * 8);
-        vr[0] = k0 <= last ? x0 : make_uint4(0, 0, 0, 0);
-        vr[1] = k1 <= last ? x1 : make_uint4(0, 0, 0, 0);
+        vr[0] = x0;
+        vr[1] = x1;
       }
     }
   };
@@ -178,8 +186,9 @@ __global__ __launch_bounds__(kThreads) void tile_mfma_bf16_kernel(TileParams p) 
         const int d = rem >> 1, h = rem & 1;
         // keys 8h..8h+3 of block bi -> positions 4h..4h+3, keys 8h+4..8h+7 -> 8+4h..
         uint16_t* row = &Vt[s][d * VS + bi * 16];
-        *reinterpret_cast<uint2*>(row + 4 * h) = make_uint2(vr[i].x, vr[i].y);
-        *reinterpret_cast<uint2*>(row + 8 + 4 * h) = make_uint2(vr[i].z, vr[i].w);
+        const uint4 x = keep_first(vr[i], vkeep[i]);
+        *reinterpret_cast<uint2*>(row + 4 * h) = make_uint2(x.x, x.y);
+        *reinterpret_cast<uint2*>(row + 8 + 4 * h) = make_uint2(x.z, x.w);
       }
     } else if (v_on) {
       const int pos = vt_pos(2 * v_pr);
@@ -212,7 +221,13 @@ __global__ __launch_bounds__(kThreads) void tile_mfma_bf16_kernel(TileParams p) 
   Cursor C{0, 0, uniform_range(p.ranges[w.rng_begin]), true};
   Cursor L = C;
   int lim = 0;
-  auto load_lim = [&]() { lim = C.R.lim_off < 0 ? C.R.n_keys : (valid ? p.lims[C.R.lim_off + tok] : 0); };
+  auto load_lim = [&]() {
+    // one unconditional load (of a valid int when the range has no limits),
+    // so the compiler's wait counts for the tile loads stay exact
+    const int32_t* lp = C.R.lim_off < 0 ? &p.work[blockIdx.x].ntok : p.lims + C.R.lim_off + (valid ? tok : 0);
+    const int32_t lv = *lp;
+    lim = C.R.lim_off < 0 ? C.R.n_keys : (valid ? lv : 0);
+  };
   load_lim();
 
   float m_run = -INFINITY, l_run = 0.f;
@@ -223,7 +238,8 @@ __global__ __launch_bounds__(kThreads) void tile_mfma_bf16_kernel(TileParams p) 
     for (int i = 0; i < 16; ++i) acc[db][i] = 0.f;
   const float sl2 = p.scale_log2;
 
-  // Prologue: tile 0 into LDS stage 0, tile 1 into registers.
+  // Prologue: tile 0 into LDS stage 0, tile 1 into registers.  Tile t lives
+  // in stage t % 3.
   int64_t ids[NB] = {};
   if constexpr (PAGED) fetch_ids(L.R, L.kt, ids);
   load_tile(L.R, L.kt, ids);
@@ -239,10 +255,46 @@ __global__ __launch_bounds__(kThreads) void tile_mfma_bf16_kernel(TileParams p) 
   }
   __syncthreads();
 
+  // O^T += V^T P^T, 16 keys per MFMA: key group g = (mb, j) holds keys
+  // mb*32 + 16j + [0,16).  The V^T fragments of group g+1 are read while the
+  // products of group g run; group 0's are read by the caller (vf0), ahead of
+  // the softmax.
+  auto vfrag = [&](const uint16_t* vt, int g, bf16x8_t (&a)[NDB]) {
+#pragma unroll
+    for (int db = 0; db < NDB; ++db)
+      a[db] = *reinterpret_cast<const bf16x8_t*>(&vt[(db * 32 + l32) * VS + (g >> 1) * 32 + 16 * (g & 1) + hf * 8]);
+  };
+  auto pv = [&](const uint16_t* vt, bf16x8_t (&vf0)[NDB], const bf16x8_t (&P)[2][2]) {
+    bf16x8_t vf1[NDB];
+#pragma unroll
+    for (int g = 0; g < 4; ++g) {
+      bf16x8_t(&cur)[NDB] = (g & 1) ? vf1 : vf0;
+      bf16x8_t(&nxt)[NDB] = (g & 1) ? vf0 : vf1;
+      if (g < 3) vfrag(vt, g + 1, nxt);
+#pragma unroll
+      for (int db = 0; db < NDB; ++db)
+        acc[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(cur[db], P[g >> 1][g & 1], acc[db], 0, 0, 0);
+    }
+  };
+
+  // The two wavefronts sharing a SIMD are offset by a phase: waves of the
+  // second half apply a tile's PV product at the start of the next
+  // iteration, so while one wavefront of a pair exponentiates, the other
+  // keeps the matrix core busy (and their LDS reads spread out).  A tile's V
+  // therefore stays in LDS one iteration longer: three stages.
+  const bool lag = wave >= kWaves / 2;
+  bf16x8_t held[2][2];  // lagging waves: P^T of the previous tile
+  int s_held = 0;
+  bool have_held = false;
+
   int s = 0;
+  bf16x8_t vf0[NDB];
   while (true) {
+    if (lag && have_held) {
+      vfrag(Vt[s_held], 0, vf0);
+      pv(Vt[s_held], vf0, held);
+    }
     const uint16_t* ks = Ks[s];
-    const uint16_t* vt = Vt[s];
     const int kb = C.kt * KT;
 
     // S^T = K Q^T for 64 keys x 32 columns.
@@ -258,22 +310,26 @@ __global__ __launch_bounds__(kThreads) void tile_mfma_bf16_kernel(TileParams p) 
         const bf16x8_t a = *reinterpret_cast<const bf16x8_t*>(&ks[(mb * 32 + l32) * KS + kk * 16 + hf * 8]);
         S[mb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, bq[kk], S[mb], 0, 0, 0);
       }
+    if (!lag) vfrag(Vt[s], 0, vf0);  // lands during the softmax
     if (kb + KT > C.R.min_lim) {
-      // Partial tile: key (mb, i) of this lane is kb + mb*32 + (i/4)*8 + hf*4 + i%4.
+      // Partial tile: key (mb, i) of this lane is kb + hf*4 + mb*32 + (i/4)*8 + i%4;
+      // it is visible iff the constant part is below rel.
+      const int rel = lim - kb - hf * 4;
 #pragma unroll
       for (int mb = 0; mb < 2; ++mb)
 #pragma unroll
         for (int i = 0; i < 16; ++i)
-          if (kb + mb * 32 + (i >> 2) * 8 + hf * 4 + (i & 3) >= lim) S[mb][i] = -INFINITY;
+          if (mb * 32 + (i >> 2) * 8 + (i & 3) >= rel) S[mb][i] = -INFINITY;
     }
 
     // Online softmax with a lazily raised reference maximum.
-    float mx = -INFINITY;
+    float m0 = max3f(S[0][0], S[0][1], S[0][2]), m1 = max3f(S[1][0], S[1][1], S[1][2]);
 #pragma unroll
-    for (int mb = 0; mb < 2; ++mb)
-#pragma unroll
-      for (int i = 0; i < 16; i += 2) mx = fmaxf(mx, fmaxf(S[mb][i], S[mb][i + 1]));
-    mx = fmaxf(mx, __shfl_xor(mx, 32)) * sl2;
+    for (int i = 3; i < 15; i += 2) {
+      m0 = max3f(m0, S[0][i], S[0][i + 1]);
+      m1 = max3f(m1, S[1][i], S[1][i + 1]);
+    }
+    const float mx = max_lane_halves(max3f(max3f(m0, S[0][15], S[1][15]), m1, m1)) * sl2;
     const bool raise = mx > m_run + kRescaleSlack;
     if (__any(raise)) {
       // raising lanes: factor 2^(old - new) (0 when nothing was seen yet);
@@ -285,37 +341,41 @@ __global__ __launch_bounds__(kThreads) void tile_mfma_bf16_kernel(TileParams p) 
       for (int db = 0; db < NDB; ++db) acc[db] *= alpha;
     }
     const float m_sub = m_run == -INFINITY ? 0.f : m_run;
-    float ls = 0.f;
-#pragma unroll
-    for (int mb = 0; mb < 2; ++mb)
-#pragma unroll
-      for (int i = 0; i < 16; ++i) {
-        const float e = fast_exp2(fmaf(S[mb][i], sl2, -m_sub));
-        S[mb][i] = e;
-        ls += e;
-      }
-    l_run += ls;
-
-    // O^T += V^T P^T, 16 keys per MFMA: keys mb*32 + 16j + [0,16).
+    // The row sum adds the bf16 probabilities the PV product uses.
+    float ls0 = 0.f, ls1 = 0.f;
+    bf16x8_t P[2][2];
 #pragma unroll
     for (int mb = 0; mb < 2; ++mb)
 #pragma unroll
       for (int j = 0; j < 2; ++j) {
         f32x8_t x;
 #pragma unroll
-        for (int e = 0; e < 8; ++e) x[e] = S[mb][8 * j + e];
-        const bf16x8_t pb = __builtin_convertvector(x, bf16x8_t);
+        for (int e = 0; e < 8; ++e) x[e] = fast_exp2(fmaf(S[mb][8 * j + e], sl2, -m_sub));
+        P[mb][j] = __builtin_convertvector(x, bf16x8_t);
 #pragma unroll
-        for (int db = 0; db < NDB; ++db) {
-          const bf16x8_t a = *reinterpret_cast<const bf16x8_t*>(&vt[(db * 32 + l32) * VS + mb * 32 + 16 * j + hf * 8]);
-          acc[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, pb, acc[db], 0, 0, 0);
+        for (int e = 0; e < 8; e += 4) {
+          ls0 = add_bf16x2(bf16x2_t{P[mb][j][e], P[mb][j][e + 1]}, ls0);
+          ls1 = add_bf16x2(bf16x2_t{P[mb][j][e + 2], P[mb][j][e + 3]}, ls1);
         }
       }
+    l_run += ls0 + ls1;
 
-    // Stage the next tile into the other buffer (last read before the
-    // previous barrier) and start loading the one after.
+    if (!lag) {
+      pv(Vt[s], vf0, P);
+    } else {
+#pragma unroll
+      for (int mb = 0; mb < 2; ++mb)
+#pragma unroll
+        for (int j = 0; j < 2; ++j) held[mb][j] = P[mb][j];
+      s_held = s;
+      have_held = true;
+    }
+
+    // Stage the next tile (its stage was last read by the lagging waves
+    // before the previous barrier) and start loading the one after.
+    const int s1 = s == kStages - 1 ? 0 : s + 1;
     if (staged) {
-      store_tile(s ^ 1);
+      store_tile(s1);
       staged = false;
     }
     if (L.ok) {
@@ -330,7 +390,11 @@ __global__ __launch_bounds__(kThreads) void tile_mfma_bf16_kernel(TileParams p) 
     advance(C);
     if (!C.ok) break;
     if (C.ri != ri_before) load_lim();
-    s ^= 1;
+    s = s1;
+  }
+  if (lag && have_held) {
+    vfrag(Vt[s_held], 0, vf0);
+    pv(Vt[s_held], vf0, held);
   }
 
   // Epilogue.  Lane (column, hf) holds d = db*32 + (i/4)*8 + hf*4 + i%4.
