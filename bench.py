@@ -7,16 +7,18 @@ A step is one decode step of masked parallel decoding over the paged cache of
 the concurrent-decode workload (64 pages x [prefix 3072, layout stream 256,
 24 branches with lengths U[1,1024]]; 1600 live streams, Hq=16, Hkv=2, d=128,
 bf16, 16-token blocks shuffled across a pool that fills most of HBM): the
-decode plan is uploaded, the split-KV tile kernel runs and the partials are
-combined.  Inputs (Q, the paged K/V cache, the block table) are resident in
+decode plan is uploaded, the shared-key tile kernel and the private-key
+streaming kernel run, and the remaining split partials are combined.  Inputs (Q, the paged K/V cache, the block table) are resident in
 HBM before timing starts.  The headline value is branch tokens (queries) per
 second of one attention-layer call.  The same run also times the packed
 forward of the 8-page training/branch-creation workload (TFLOP/s), and the
 CPU oracle on a bounded sample of the decode workload.
 
 One JSON line is printed (rank 0, one GPU).  Kernel durations for the
-roofline come from HIP events the library records around its tile kernel on
-the launch stream.
+roofline come from HIP events the library records around all kernels of a
+call on the launch stream; `roofline.traffic` comes from the committed
+rocprofv3 counter summary in profiles/ while it matches the library sources
+(`--summarize-profile` writes it).
 """
 from __future__ import annotations
 
@@ -35,6 +37,14 @@ if ROOT not in sys.path:
 METRIC = "branch-decode tokens/s + HBM GB/s; packed tree-attn TFLOP/s (% roofline)"
 HBM_PEAK_GBS = 8000.0
 BF16_PEAK_TFLOPS = 2516.6
+PROFILE_TAG = "concurrent_decode_64pages_packed_forward_8pages"
+TRACE_SUMMARY = os.path.join(ROOT, "profiles", f"kernel_trace_{PROFILE_TAG}.md")
+TRAFFIC_SUMMARY = os.path.join(ROOT, "profiles", f"hbm_traffic_{PROFILE_TAG}.txt")
+DECODE_KERNELS = ("tile_mfma_bf16_kernel<128, true, true>", "decode_private_kernel<128>",
+                  "lse_combine_kernel<128, true>")
+FORWARD_KERNEL = "tile_mfma_bf16_kernel<128, false, false>"
+COPY_KERNEL = "__amd_rocclr_copyBuffer"
+COPY_BYTES = 1 << 30
 
 
 def log(msg: str) -> None:
@@ -60,6 +70,8 @@ def parse_args(argv=None):
                     help="decode plan: workgroups the planner aims for when it chooses chunks (0 = default)")
     ap.add_argument("--calibrate-copy", action="store_true",
                     help="only run a plain 1 GiB device-to-device copy three times (reference for HBM counters)")
+    ap.add_argument("--summarize-profile", metavar="DIR",
+                    help="only summarize rocprofv3 outputs under DIR into profiles/ (no GPU needed)")
     return ap.parse_args(argv)
 
 
@@ -126,6 +138,125 @@ def alloc_pools(torch, n_blocks_needed, Hkv, d, pool_gib, dev):
     n = n_blocks_needed
     return (torch.empty((n, Hkv, 16, d), dtype=torch.bfloat16, device=dev),
             torch.empty((n, Hkv, d, 16), dtype=torch.bfloat16, device=dev), n)
+
+
+# ---------------------------------------------------------------- profile summaries
+
+def source_digest() -> str:
+    """SHA-256 over the library sources (kernels, planner, C ABI header):
+    a counter summary applies only to the sources it was taken on."""
+    import glob
+    import hashlib
+    files = sorted(f for f in glob.glob(os.path.join(ROOT, "paper_2608_06146_amd", "csrc", "**", "*"), recursive=True)
+                   if f.endswith((".hip", ".hpp", ".cpp", ".h")))
+    files.append(os.path.join(ROOT, "include", "padoc_attn.h"))
+    h = hashlib.sha256()
+    for f in files:
+        h.update(os.path.relpath(f, ROOT).encode())
+        with open(f, "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()
+
+
+def short_kernel_name(name: str) -> str:
+    n = name.replace("void ", "").replace("padoc::(anonymous namespace)::", "").replace("padoc::", "")
+    return n.split("(")[0].strip()
+
+
+def measured_traffic():
+    """HBM bytes per decode call and per forward launch from the committed
+    counter summary, or (None, None) when it was taken on other sources."""
+    try:
+        with open(TRAFFIC_SUMMARY) as fh:
+            kv = dict(line.split(":", 1) for line in fh if ":" in line and not line.startswith("#"))
+    except OSError:
+        return None, None
+    kv = {k.strip(): v.strip() for k, v in kv.items()}
+    if kv.get("sources_sha256") != source_digest():
+        return None, None
+    return float(kv["decode_call_bytes"]), float(kv["forward_launch_bytes"])
+
+
+PROFILE_COMMANDS = """\
+    R=<repository root>; cd /tmp && export TMPDIR=/tmp
+    rocprofv3 --kernel-trace --stats -d $R/gpurun_out/prof/trace -o bench -- \\
+        python3 $R/bench.py --steps 5 --warmup 1 --no-cpu-baseline > $R/gpurun_out/prof/trace/bench.json
+    rocprofv3 --pmc FETCH_SIZE --kernel-include-regex padoc -f csv -d $R/gpurun_out/prof/fetch -o p -- \\
+        python3 $R/bench.py --steps 5 --warmup 1 --no-cpu-baseline
+    rocprofv3 --pmc WRITE_SIZE --kernel-include-regex padoc -f csv -d $R/gpurun_out/prof/write -o p -- \\
+        python3 $R/bench.py --steps 5 --warmup 1 --no-cpu-baseline
+    rocprofv3 --pmc FETCH_SIZE -f csv -d $R/gpurun_out/prof/copy_fetch -o c -- python3 $R/bench.py --calibrate-copy
+    rocprofv3 --pmc WRITE_SIZE -f csv -d $R/gpurun_out/prof/copy_write -o c -- python3 $R/bench.py --calibrate-copy
+    python3 $R/bench.py --summarize-profile $R/gpurun_out/prof
+"""
+
+
+def summarize_profile(d: str) -> None:
+    """Write the kernel-trace table and the HBM-traffic summary under
+    profiles/ from the outputs of the profiling commands above."""
+    import csv
+    import glob
+    import sqlite3
+    import statistics
+
+    db = sorted(glob.glob(os.path.join(d, "trace", "**", "*.db"), recursive=True))[0]
+    con = sqlite3.connect(db)
+    rows = con.execute("select name, count(*), avg(duration), min(duration), max(duration), max(lds_size), "
+                       "max(grid_x), max(workgroup_x) from kernels "
+                       "where name like '%padoc%' group by name order by avg(duration) desc").fetchall()
+    ev = {}
+    try:
+        with open(os.path.join(d, "trace", "bench.json")) as fh:
+            ev = json.loads(fh.read().strip().splitlines()[-1])
+    except (OSError, ValueError, IndexError):
+        pass
+
+    def counter(sub, name):
+        out = {}
+        for f in glob.glob(os.path.join(d, sub, "**", "*counter_collection.csv"), recursive=True):
+            with open(f) as fh:
+                for r in csv.DictReader(fh):
+                    if r["Counter_Name"] == name:
+                        out.setdefault(short_kernel_name(r["Kernel_Name"]), []).append(float(r["Counter_Value"]))
+        return {k: statistics.mean(v) for k, v in out.items()}
+
+    fetch, write = counter("fetch", "FETCH_SIZE"), counter("write", "WRITE_SIZE")
+    fetch_factor = COPY_BYTES / 1024 / counter("copy_fetch", "FETCH_SIZE")[COPY_KERNEL]
+    write_factor = COPY_BYTES / 1024 / counter("copy_write", "WRITE_SIZE")[COPY_KERNEL]
+
+    def traffic(k):
+        return (fetch[k] * fetch_factor + write[k] * write_factor) * 1024
+
+    dec_bytes = sum(traffic(k) for k in DECODE_KERNELS)
+    fwd_bytes = traffic(FORWARD_KERNEL)
+    lines = [f"# Kernel trace: bench.py default run (concurrent decode, 64 pages x 24 branches; packed forward, 8 pages)",
+             "", "Commands (GPU host, repository root as $R):", "", PROFILE_COMMANDS,
+             "| kernel | calls | avg us | min us | max us | LDS B | workgroups | threads |",
+             "|---|---|---|---|---|---|---|---|"]
+    for name, n, avg, mn, mx, lds, gx, wx in rows:
+        lines.append(f"| `{short_kernel_name(name)}` | {n} | {avg / 1e3:.1f} | {mn / 1e3:.1f} | {mx / 1e3:.1f} | "
+                     f"{lds} | {gx // max(wx, 1)} | {wx} |")
+    dec_avg = sum(r[2] for r in rows if short_kernel_name(r[0]) in DECODE_KERNELS) / 1e3
+    lines += ["", f"Decode call (sum of the three decode kernels' averages): {dec_avg:.1f} us."]
+    if ev:
+        lines.append(f"Same run, HIP events around each call (bench.py): decode call "
+                     f"{ev['decode']['kernel_ms'] * 1e3:.1f} us, forward {ev['forward']['kernel_ms'] * 1e3:.1f} us.")
+    lines += ["", f"HBM traffic per launch (FETCH_SIZE x {fetch_factor:.3f} + WRITE_SIZE x {write_factor:.3f}, factors "
+              f"from a 1 GiB device copy): see {os.path.basename(TRAFFIC_SUMMARY)}.", ""]
+    with open(TRACE_SUMMARY, "w") as fh:
+        fh.write("\n".join(lines))
+    tl = ["# HBM traffic from rocprofv3 FETCH_SIZE / WRITE_SIZE (KiB per dispatch), scaled by a 1 GiB copy.",
+          "# Commands: as in " + os.path.basename(TRACE_SUMMARY) + ". bench.py reports these bytes as",
+          "# roofline.traffic only while sources_sha256 matches the library sources.",
+          f"sources_sha256: {source_digest()}",
+          f"fetch_factor: {fetch_factor:.4f}", f"write_factor: {write_factor:.4f}"]
+    for k in DECODE_KERNELS + (FORWARD_KERNEL,):
+        tl.append(f"kernel {k} fetch_kib: {fetch[k]:.1f}")
+        tl.append(f"kernel {k} write_kib: {write[k]:.1f}")
+    tl += [f"decode_call_bytes: {dec_bytes:.0f}", f"forward_launch_bytes: {fwd_bytes:.0f}", ""]
+    with open(TRAFFIC_SUMMARY, "w") as fh:
+        fh.write("\n".join(tl))
+    print(f"wrote {TRACE_SUMMARY} and {TRAFFIC_SUMMARY}")
 
 
 # ---------------------------------------------------------------- decode leg
@@ -250,7 +381,8 @@ def run_forward(args, torch, np, syn, pa, dev):
         "ms_per_step": ms, "kernel_ms": k_ms, "tflops": flops / (ms * 1e-3) / 1e12,
         "kernel_tflops": flops / (k_ms * 1e-3) / 1e12, "plan_ms": plan_ms,
         "roofline": {"bound": "mfma", "achieved": flops / (k_ms * 1e-3) / 1e12, "peak": BF16_PEAK_TFLOPS,
-                     "unit": "TFLOP/s", "frac": flops / (k_ms * 1e-3) / 1e12 / BF16_PEAK_TFLOPS, "traffic": None},
+                     "unit": "TFLOP/s", "frac": flops / (k_ms * 1e-3) / 1e12 / BF16_PEAK_TFLOPS,
+                     "traffic": measured_traffic()[1], "kernel": FORWARD_KERNEL},
     }
 
 
@@ -290,6 +422,9 @@ def main(argv=None) -> int:
               "independent trees, so several GPUs would shard by page with no exchange -- not built here.",
               file=sys.stderr)
         return 2
+    if args.summarize_profile:
+        summarize_profile(args.summarize_profile)
+        return 0
     import numpy as np
     import torch
 
@@ -335,9 +470,8 @@ def main(argv=None) -> int:
                    "Hkv": dec["Hkv"], "d": dec["d"], "block": 16, "pool_gib": round(dec["pool_gib"], 1)},
         "hbm_gbps": dec["step_gbps"],
         "roofline": {"bound": "hbm", "achieved": dec["kernel_gbps"], "peak": HBM_PEAK_GBS, "unit": "GB/s",
-                     "frac": dec["kernel_gbps"] / HBM_PEAK_GBS, "traffic": None,
-                     "kernel": "decode call: tile_mfma_kernel<128,paged> (shared keys) + "
-                               "decode_private_kernel<128> + lse_combine_kernel<128,bf16>",
+                     "frac": dec["kernel_gbps"] / HBM_PEAK_GBS, "traffic": measured_traffic()[0],
+                     "kernel": "decode call: " + " + ".join(DECODE_KERNELS),
                      "kernel_ms": dec["kernel_ms"],
                      "bytes_per_launch": dec["kernel_bytes"]},
         "cpu_baseline": cpu,
