@@ -127,7 +127,7 @@ def alloc_pools(torch, n_blocks_needed, Hkv, d, pool_gib, dev):
     while want > 0:
         n = max(n_blocks_needed, want // block_bytes)
         try:
-            kc = torch.empty((n, Hkv, 16, d), dtype=torch.bfloat16, device=dev)
+            kc = torch.empty((n, Hkv, d // 8, 16, 8), dtype=torch.bfloat16, device=dev)  # chunk-major K blocks
             vc = torch.empty((n, Hkv, d, 16), dtype=torch.bfloat16, device=dev)  # d-major V blocks
             return kc, vc, n
         except RuntimeError:
@@ -136,7 +136,7 @@ def alloc_pools(torch, n_blocks_needed, Hkv, d, pool_gib, dev):
                 break
             want -= 8 << 30
     n = n_blocks_needed
-    return (torch.empty((n, Hkv, 16, d), dtype=torch.bfloat16, device=dev),
+    return (torch.empty((n, Hkv, d // 8, 16, 8), dtype=torch.bfloat16, device=dev),
             torch.empty((n, Hkv, d, 16), dtype=torch.bfloat16, device=dev), n)
 
 
@@ -301,7 +301,10 @@ def run_decode(args, torch, np, syn, pa, dev):
         slot[r0:r0 + L] = t % 16
     bi = torch.as_tensor(blk, device=dev)
     si = torch.as_tensor(slot, device=dev)
-    kc[bi, :, si, :] = k
+    # K blocks are chunk-major: token t's 8-dim piece c at [c][slot], slot =
+    # t with bits 2 and 3 exchanged (the library's documented cache layout)
+    ci = (si & 3) | ((si >> 3) & 1) << 2 | ((si >> 2) & 1) << 3
+    kc[bi, :, :, ci, :] = k.reshape(T, Hkv, d // 8, 8)
     vc[bi, :, :, si] = v
     del k, v, bi, si
     bt = torch.as_tensor(ids, device=dev)

@@ -31,11 +31,17 @@
  *   Q, O     [n_q_rows, Hq, d]        segment s's queries = its LAST q_len
  *                                     tokens, at rows q_off .. q_off+q_len-1
  *   K, V     packed: [num_kv_rows, Hkv, d], segment s's token j at row kv_off+j
- *   K cache  paged:  [num_blocks, Hkv, 16, d]  (16 token rows per block)
+ *   K cache  paged:  [num_blocks, Hkv, d/8, 16, 8]  (chunk-major: element
+ *                    (slot t, dim c) of a block at [c/8][kslot(t)][c%8],
+ *                    kslot(t) = t with bits 2 and 3 swapped, i.e.
+ *                    (t & 3) | (t & 4) << 1 | (t & 8) >> 1; 8 consecutive
+ *                    dims of a token are one piece, the 16 tokens' pieces of
+ *                    one chunk are contiguous, and tokens {0-3, 8-11} and
+ *                    {4-7, 12-15} each fill one 128-byte line per chunk)
  *   V cache  paged:  [num_blocks, Hkv, d, 16]  (d-major: the 16 tokens of a
  *                    block are contiguous for each d)
  *            segment s's token j lives in block block_table[kv_off + j/16],
- *            slot j%16, of both caches
+ *            slot t = j%16, of both caches
  *   LSE      float32 [n_q_rows, Hq], natural log
  *   GQA      query head h reads KV head h / (Hq/Hkv)
  *   dtype    Q, K, V and O share one dtype (bf16 or fp32); accumulation is
@@ -124,8 +130,11 @@ typedef struct {
   int64_t block_table_len;       /* paged: entries in the block table           */
   int32_t max_chunk_keys;        /* decode: split keys into chunks of at most
                                     this many (multiple of 64); 0 = automatic */
-  int32_t target_workgroups;     /* decode: aim for about this many work items
-                                    when choosing chunks; 0 = 512              */
+  int32_t target_workgroups;     /* decode chunk sizes (0 = 1024): shared keys
+                                    are cut into about this / 4 tile items
+                                    (8 wavefronts each), private keys into
+                                    about 2x this many wavefront items; both
+                                    chunk sizes clamped to [512, 8192] keys   */
 } padoc_tree_desc;
 
 typedef struct padoc_plan padoc_plan;
@@ -216,7 +225,8 @@ padoc_status padoc_tree_attn_fwd(const padoc_plan* plan, const void* q, const vo
                                  size_t workspace_bytes, hipStream_t stream);
 
 /* Decode step over a paged cache.  Needs a plan with block_size == 16.
-   block_table is the device copy of the table the plan was built for
+   k_cache / v_cache follow the paged layouts above (chunk-major K, d-major
+   V).  block_table is the device copy of the table the plan was built for
    (block_table_len int32 entries, every id < num_kv_rows). */
 padoc_status padoc_branch_decode(const padoc_plan* plan, const void* q, const void* k_cache,
                                  const void* v_cache, const int32_t* block_table, void* o,

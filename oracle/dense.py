@@ -46,7 +46,7 @@ import numpy as np
 __all__ = [
     "page_nodes", "canonical_layout", "ancestors", "visible_counts", "page_of",
     "dense_mask", "masked_attention", "tree_attention", "tree_attention_paged",
-    "gather_paged", "paged_slots", "simulate_masked_parallel_decoding",
+    "gather_paged", "paged_slots", "chunk_slot", "simulate_masked_parallel_decoding",
     "visible_pair_count",
 ]
 
@@ -302,33 +302,58 @@ def paged_slots(nodes, block_table, block_size: int, bt_off=None):
     return np.concatenate(blk), np.concatenate(slot)
 
 
-def gather_paged(nodes, pool, block_table, block_size: int, bt_off=None, d_major: bool = False) -> np.ndarray:
+def chunk_slot(t):
+    """Slot of token ``t`` (0..15) inside a chunk-major K block: bits 2 and 3
+    of ``t`` exchanged (the cache layout the library documents)."""
+    t = np.asarray(t)
+    return (t & 3) | ((t >> 3) & 1) << 2 | ((t >> 2) & 1) << 3
+
+
+def gather_paged(nodes, pool, block_table, block_size: int, bt_off=None, d_major: bool = False,
+                 layout: str = None) -> np.ndarray:
     """Read a paged cache back into packed token order ``[T, Hkv, d]``
-    (fp64).  Row-major blocks: ``pool [num_blocks, Hkv, block_size, d]``;
-    d-major blocks (``d_major``): ``pool [num_blocks, Hkv, d, block_size]``."""
+    (fp64).  ``layout``:
+
+    * ``"rows"``: ``pool [num_blocks, Hkv, block_size, d]``;
+    * ``"d_major"`` (or ``d_major=True``): ``pool [num_blocks, Hkv, d, block_size]``;
+    * ``"chunked"``: ``pool [num_blocks, Hkv, d/8, 16, 8]``, token ``t``'s dims
+      ``[8c, 8c+8)`` at ``[c, chunk_slot(t), :]``."""
+    layout = layout or ("d_major" if d_major else "rows")
     blk, slot = paged_slots(nodes, block_table, block_size, bt_off)
+    if layout == "chunked":
+        slot = chunk_slot(slot)
     try:
         import torch
         if isinstance(pool, torch.Tensor):
             bi = torch.as_tensor(blk, device=pool.device)
             si = torch.as_tensor(slot, device=pool.device)
-            got = pool[bi, :, :, si] if d_major else pool[bi, :, si, :]
+            if layout == "d_major":
+                got = pool[bi, :, :, si]
+            elif layout == "chunked":
+                got = pool[bi, :, :, si, :].reshape(len(blk), pool.shape[1], -1)
+            else:
+                got = pool[bi, :, si, :]
             return got.to("cpu", torch.float64).numpy()
     except ImportError:  # pragma: no cover
         pass
     p = _f64(pool)
-    return p[blk, :, :, slot] if d_major else p[blk, :, slot, :]
+    if layout == "d_major":
+        return p[blk, :, :, slot]
+    if layout == "chunked":
+        return p[blk, :, :, slot, :].reshape(len(blk), p.shape[1], -1)
+    return p[blk, :, slot, :]
 
 
 def tree_attention_paged(nodes, q, k_pool, v_pool, block_table, scale: float,
                          num_heads_q: int, num_heads_kv: int, block_size: int = 16,
                          bt_off=None, q_off=None, rows=None):
     """Decode form: K/V in a paged cache, the library's cache format: K blocks
-    row-major ``[num_blocks, Hkv, 16, d]``, V blocks d-major
-    ``[num_blocks, Hkv, d, 16]``.  Gathers every segment back into packed
-    order with :func:`gather_paged`, then applies :func:`tree_attention`."""
+    chunk-major ``[num_blocks, Hkv, d/8, 16, 8]`` (see :func:`chunk_slot`), V
+    blocks d-major ``[num_blocks, Hkv, d, 16]``.  Gathers every segment back
+    into packed order with :func:`gather_paged`, then applies
+    :func:`tree_attention`."""
     nodes = _as_nodes(nodes)
-    k = gather_paged(nodes, k_pool, block_table, block_size, bt_off)
+    k = gather_paged(nodes, k_pool, block_table, block_size, bt_off, layout="chunked")
     v = gather_paged(nodes, v_pool, block_table, block_size, bt_off, d_major=True)
     kv_off, qo = canonical_layout(nodes, 0)
     return tree_attention(nodes, q, k, v, scale, num_heads_q, num_heads_kv,

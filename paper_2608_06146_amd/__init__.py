@@ -209,8 +209,9 @@ def tree_attn_fwd(q, k, v, plan: TreePlan, out=None, lse=None, workspace=None, s
 def branch_decode(q, k_cache, v_cache, block_table, plan: TreePlan, out=None, lse=None, workspace=None,
                   stream=None):
     """Decode step over a paged cache (``padoc_branch_decode``).  q ``[n_q,
-    Hq, d]``; caches ``[blocks, Hkv, 16, d]``; block_table int32 on the
-    device; returns ``(O, LSE)``."""
+    Hq, d]``; K cache chunk-major ``[blocks, Hkv, d/8, 16, 8]``, V cache
+    d-major ``[blocks, Hkv, d, 16]`` (layouts in ``padoc_attn.h``);
+    block_table int32 on the device; returns ``(O, LSE)``."""
     import torch
     dt = _torch_dtype(plan)
     dev = q.device

@@ -352,27 +352,30 @@ void build_decode(padoc_plan& P, Builder& B, const std::vector<std::vector<std::
       }
     }
   }
-  // Work estimate in key-steps of one wavefront (a shared item keeps four
-  // wavefronts busy) for the chunk size.
+  // Chunk sizes.  Shared keys: about one tile item (a whole compute unit's
+  // worth of wavefronts) per target_workgroups / 4, since every extra chunk
+  // costs a round of split partials.  Private keys: about
+  // target_workgroups x 2 wavefronts' worth of equal pieces.
   std::vector<std::vector<VisRange>> svis, pvis;
-  int64_t total = 0;
+  int64_t total_s = 0, total_p = 0;
   for (const Task& t : stasks) {
     svis.push_back(B.visible(t, shared));
-    for (const auto& r : svis.back()) total += 4 * round_up(r.n_keys, 64) * P.Hkv;
+    for (const auto& r : svis.back()) total_s += round_up(r.n_keys, 64) * P.Hkv;
   }
   for (const Task& t : ptasks) {
     pvis.push_back(B.visible(t, priv));
     const int64_t splits = ceil_div((int64_t)t.seg.size() * G, kPrivateCols);
-    for (const auto& r : pvis.back()) total += round_up(r.n_keys, 32) * P.Hkv * splits;
+    for (const auto& r : pvis.back()) total_p += round_up(r.n_keys, 32) * P.Hkv * splits;
   }
-  int64_t CH = d->max_chunk_keys;
-  if (CH == 0) {
-    // about target_workgroups x 4 wavefronts' worth of equal pieces
-    const int64_t target = 4 * (d->target_workgroups > 0 ? d->target_workgroups : 1024);
-    CH = round_up(std::max<int64_t>(1, ceil_div(total, target)), 64);
-    CH = std::min<int64_t>(std::max<int64_t>(CH, 512), 8192);
-  }
-  auto cut = [&](const std::vector<VisRange>& vis) {
+  const int64_t tw = d->target_workgroups > 0 ? d->target_workgroups : 1024;
+  auto chunk_keys = [&](int64_t total, int64_t pieces) {
+    if (d->max_chunk_keys > 0) return (int64_t)d->max_chunk_keys;
+    const int64_t ch = round_up(std::max<int64_t>(1, ceil_div(total, pieces)), 64);
+    return std::min<int64_t>(std::max<int64_t>(ch, 512), 8192);
+  };
+  const int64_t CHs = chunk_keys(total_s, std::max<int64_t>(1, tw / 4));
+  const int64_t CHp = chunk_keys(total_p, 2 * tw);
+  auto cut = [&](const std::vector<VisRange>& vis, int64_t CH) {
     std::vector<std::vector<Piece>> chunks(1);
     int64_t room = CH;
     for (const auto& r : vis) {
@@ -423,7 +426,7 @@ void build_decode(padoc_plan& P, Builder& B, const std::vector<std::vector<std::
   };
   for (size_t i = 0; i < stasks.size(); ++i) {
     const int32_t tb = B.add_tokens(stasks[i]);
-    for (const auto& chunk : cut(svis[i])) emit(stasks[i], tb, chunk, kTileCols, sitems);
+    for (const auto& chunk : cut(svis[i], CHs)) emit(stasks[i], tb, chunk, kTileCols, sitems);
   }
   // A private task cut into a single chunk finishes its rows in the
   // streaming kernel (bf16): every other partial of those rows comes from a
@@ -431,7 +434,7 @@ void build_decode(padoc_plan& P, Builder& B, const std::vector<std::vector<std::
   std::vector<char> finished((size_t)P.num_q_rows * P.Hkv, 0);
   for (size_t i = 0; i < ptasks.size(); ++i) {
     const int32_t tb = B.add_tokens(ptasks[i]);
-    const auto chunks = cut(pvis[i]);
+    const auto chunks = cut(pvis[i], CHp);
     const size_t first = pitems.size();
     for (const auto& chunk : chunks) emit(ptasks[i], tb, chunk, kPrivateCols, pitems);
     if (P.dtype == PADOC_BF16 && chunks.size() == 1) {

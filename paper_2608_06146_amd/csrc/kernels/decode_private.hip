@@ -5,7 +5,9 @@
 // of the live streams; Attn equation with the ancestor mask).
 //
 // Per step, with v_mfma_f32_16x16x32_bf16 (lane l: row/column l%16, group
-// g = l/16 holding eight consecutive K-dimension elements):
+// g = l/16 holding eight consecutive K-dimension elements; K blocks are
+// chunk-major, so every 16-byte K load of a lane group is part of a full
+// 128-byte line):
 //   S^T = K Q^T     two 16-key M blocks; row m of block mb holds key
 //                   8*(m/4) + 4*mb + m%4, so each lane's eight scores are the
 //                   keys 8g .. 8g+7 of the step
@@ -94,12 +96,12 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(2, 2))) void
     blk[X][1] = bt[base + ((kb + 16 < nk) ? 1 : 0)];
 #pragma unroll
     for (int mb = 0; mb < 2; ++mb) {
+      // dims ds*32 + 8g .. +7 = chunk 4ds + g; with the chunk-major block
+      // layout the 16 lanes of a group read two full 128-byte lines
       const int key = step_key(mb, n);
-      const uint16_t* kp = Kc + ((blk[X][key >> 4] * Hkv + kvh) * kBlock + (key & 15)) * D + 8 * g;
+      const uint16_t* kp = Kc + paged_k_offset<D>(blk[X][key >> 4], kvh, (int32_t)Hkv, key & 15, g);
 #pragma unroll
-      for (int ds = 0; ds < NDS; ++ds) {
-        kf[X][mb][ds] = load_stream16(kp + ds * 32);
-      }
+      for (int ds = 0; ds < NDS; ++ds) kf[X][mb][ds] = load_stream16(kp + ds * 4 * (kBlock * 8));
     }
   };
   auto load_v = [&](const Cursor& c, int X) {

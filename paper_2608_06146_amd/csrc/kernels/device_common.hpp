@@ -10,18 +10,17 @@ namespace padoc {
 
 constexpr float kLn2 = 0.693147180559945309f;
 
-// Device address of key `j` of a range for KV head `kvh` (element offset).
-// Packed K/V: [T, Hkv, D] rows; paged: [blocks, Hkv, 16, D] with the block
-// taken from the block table.
-template <int D, bool PAGED>
-__device__ __forceinline__ int64_t key_offset(const RangeRec& r, int32_t j, int32_t kvh, int32_t Hkv,
-                                              const int32_t* __restrict__ block_table) {
-  if constexpr (PAGED) {
-    const int64_t blk = block_table[r.kv_start + (j >> 4)];
-    return ((blk * Hkv + kvh) * kBlock + (j & 15)) * (int64_t)D;
-  } else {
-    return ((r.kv_start + j) * Hkv + kvh) * (int64_t)D;
-  }
+// Paged K blocks are chunk-major, [Hkv][D/8][16 slots][8]: token t of a
+// block lives in slot kslot(t) (bits 2 and 3 of t swapped), so one 8-dim
+// chunk of the tokens {0-3, 8-11} (or {4-7, 12-15}) is one 128-byte line.
+// kslot is its own inverse.
+__device__ __forceinline__ int kslot(int t) { return (t & 3) | ((t & 4) << 1) | ((t & 8) >> 1); }
+
+// Element offset of dims [8c, 8c+8) of token t (0..15) in paged K block blk
+// for KV head kvh.
+template <int D>
+__device__ __forceinline__ int64_t paged_k_offset(int64_t blk, int32_t kvh, int32_t Hkv, int t, int c) {
+  return ((blk * Hkv + kvh) * (D / 8) + c) * (kBlock * 8) + kslot(t) * 8;
 }
 
 // 16-byte load with the non-temporal hint: for K/V that a kernel reads once

@@ -27,11 +27,11 @@
 // accumulator is rescaled only then.  Any reference gives the same O and LSE.
 // O is rounded to bf16 (RNE) at the end.
 //
-// Paged K/V: K blocks [16 tokens][d] are read like packed rows through the
-// block table; V blocks are d-major ([d][16 tokens]), so a 16-byte load holds
-// 8 consecutive keys of one d row and lands in the transposed LDS tile as two
-// 8-byte stores.  A tile's block ids are wave-uniform scalars fetched one tile
-// ahead of its K/V loads.
+// Paged K/V: K blocks are chunk-major ([d/8][16 slots][8]) and land in the
+// row-major LDS tile piece by piece; V blocks are d-major ([d][16 tokens]),
+// so a 16-byte load holds 8 consecutive keys of one d row and lands in the
+// transposed LDS tile as two 8-byte stores.  A tile's block ids are
+// wave-uniform scalars fetched one tile ahead of its K/V loads.
 #include "device_common.hpp"
 
 namespace padoc {
@@ -114,12 +114,21 @@ __global__ __launch_bounds__(kThreads) void tile_mfma_bf16_kernel(TileParams p) 
   const uint16_t* Vg = static_cast<const uint16_t*>(p.v);
 
   // Per-thread load geometry (independent of the tile).
+  // K piece u (16 bytes): packed K rows are read row by row; paged K blocks
+  // are chunk-major, so consecutive threads take consecutive slots of one
+  // chunk (token kslot(slot)).  Either way a wave reads 1 KB contiguous.
   int k_key[KPT], k_dc[KPT];
 #pragma unroll
   for (int i = 0; i < KPT; ++i) {
     const int u = tid + kThreads * i;
-    k_key[i] = u / CPR;
-    k_dc[i] = u % CPR;
+    if constexpr (PAGED) {
+      const int bi = u / (kBlock * CPR), rem = u % (kBlock * CPR);
+      k_key[i] = bi * kBlock + kslot(rem % kBlock);
+      k_dc[i] = rem / kBlock;
+    } else {
+      k_key[i] = u / CPR;
+      k_dc[i] = u % CPR;
+    }
   }
   // packed V: key pair (2pr, 2pr+1) and 16-byte chunk dc (threads >= 32*CPR idle)
   const int v_pr = tid % (KT / 2), v_dc = tid / (KT / 2);
@@ -145,12 +154,9 @@ __global__ __launch_bounds__(kThreads) void tile_mfma_bf16_kernel(TileParams p) 
     for (int i = 0; i < KPT; ++i) {
       const int key = k_key[i];
       const int kc = key <= last ? key : last;
-      int64_t off;
-      if constexpr (PAGED)
-        off = ((ids[kc >> 4] * Hkv + kvh) * kBlock + (kc & 15)) * (int64_t)D;
-      else
-        off = ((R.kv_start + kbase + kc) * Hkv + kvh) * (int64_t)D;
-      const uint4 x = PAGED ? load_stream16(Kg + off + k_dc[i] * 8) : *reinterpret_cast<const uint4*>(Kg + off + k_dc[i] * 8);
+      const uint4 x = PAGED ? load_stream16(Kg + paged_k_offset<D>(ids[kc >> 4], kvh, (int32_t)Hkv, kc & 15, k_dc[i]))
+                            : *reinterpret_cast<const uint4*>(Kg + ((R.kv_start + kbase + kc) * Hkv + kvh) * (int64_t)D +
+                                                              k_dc[i] * 8);
       kr[i] = x;
     }
     if constexpr (PAGED) {

@@ -43,12 +43,21 @@ __global__ __launch_bounds__(256) void tile_valu_f32_kernel(TileParams p) {
     const RangeRec R = p.ranges[w.rng_begin + r];
     const int lim = R.lim_off < 0 ? R.n_keys : p.lims[R.lim_off + t];
     for (int j = 0; j < lim; ++j) {
-      const int64_t off = key_offset<D, PAGED>(R, j, w.kvh, p.Hkv, p.block_table);
-      const float4* kp = reinterpret_cast<const float4*>(K + off);
+      // K row j: packed [T, Hkv, D]; paged chunk-major blocks (8 dims per piece)
+      int64_t off;
+      int64_t blk = 0;
+      if constexpr (PAGED) {
+        blk = p.block_table[R.kv_start + (j >> 4)];
+        off = paged_k_offset<D>(blk, w.kvh, p.Hkv, j & 15, 0);
+      } else {
+        off = ((R.kv_start + j) * p.Hkv + w.kvh) * (int64_t)D;
+      }
       float s = 0.f;
 #pragma unroll
       for (int i = 0; i < D / 4; ++i) {
-        const float4 x = kp[i];
+        // dims 4i..4i+3: chunk i/2, half i%2 of the piece
+        const int64_t ko = PAGED ? off + (i >> 1) * (kBlock * 8) + 4 * (i & 1) : off + 4 * i;
+        const float4 x = *reinterpret_cast<const float4*>(K + ko);
         s = fmaf(q[4 * i], x.x, s);
         s = fmaf(q[4 * i + 1], x.y, s);
         s = fmaf(q[4 * i + 2], x.z, s);
@@ -58,7 +67,6 @@ __global__ __launch_bounds__(256) void tile_valu_f32_kernel(TileParams p) {
       // V row j: packed [T, Hkv, D]; paged d-major blocks [Hkv][D][16]
       int64_t voff, vstride;
       if constexpr (PAGED) {
-        const int64_t blk = p.block_table[R.kv_start + (j >> 4)];
         voff = (blk * p.Hkv + w.kvh) * (int64_t)D * kBlock + (j & 15);
         vstride = kBlock;
       } else {

@@ -83,18 +83,19 @@ def forward_case(pages_or_nodes, Hq, Hkv, d, dtype, seed, prescale=False, kv_off
 
 
 def fill_pool(nodes, k_packed, v_packed, n_pool, seed, device="cuda", sentinel=float("nan")):
-    """Paged caches (K [n_pool, Hkv, 16, d], V d-major [n_pool, Hkv, d, 16])
-    holding the packed K/V at the block ids drawn by the generator; every
-    other slot holds `sentinel`."""
+    """Paged caches (K chunk-major [n_pool, Hkv, d/8, 16, 8], V d-major
+    [n_pool, Hkv, d, 16]) holding the packed K/V at the block ids drawn by the
+    generator; every other slot holds `sentinel`."""
     nb = int(sum(-(-n[2] // 16) for n in nodes))
     ids = syn.draw_block_ids(nb, n_pool, seed)
     Hkv, d = k_packed.shape[1], k_packed.shape[2]
-    kc = torch.full((n_pool, Hkv, 16, d), sentinel, dtype=k_packed.dtype, device=device)
+    kc = torch.full((n_pool, Hkv, d // 8, 16, 8), sentinel, dtype=k_packed.dtype, device=device)
     vc = torch.full((n_pool, Hkv, d, 16), sentinel, dtype=v_packed.dtype, device=device)
     blk, slot = od.paged_slots(nodes, ids, 16)
     bi = torch.as_tensor(blk, device=device)
     si = torch.as_tensor(slot, device=device)
-    kc[bi, :, si, :] = k_packed.to(device)
+    ci = torch.as_tensor(od.chunk_slot(slot), device=device)
+    kc[bi, :, :, ci, :] = k_packed.to(device).reshape(len(slot), Hkv, d // 8, 8)
     vc[bi, :, :, si] = v_packed.to(device)
     return kc, vc, ids
 

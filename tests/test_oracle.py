@@ -387,12 +387,46 @@ def test_P8_paged_equals_packed():
         nb = int(sum(-(-n[2] // 16) for n in nodes))
         pool_n = nb + 7
         ids = syn.draw_block_ids(nb, pool_n, seed)
-        pool_k = np.full((pool_n, Hkv, 16, d), np.nan)
+        pool_k = np.full((pool_n, Hkv, d // 8, 16, 8), np.nan)  # K blocks are chunk-major
         pool_v = np.full((pool_n, Hkv, d, 16), np.nan)      # V blocks are d-major
         blk, slot = ot.paged_slots(nodes, ids, 16)
-        pool_k[blk, :, slot, :] = k
+        pool_k[blk, :, :, ot.chunk_slot(slot), :] = k.reshape(len(slot), Hkv, d // 8, 8)
         pool_v[blk, :, :, slot] = v
         O_d, L_d = oracle.tree_attention_paged(nodes, q, pool_k, pool_v, ids, 0.3, 4, Hkv, 16)
         np.testing.assert_allclose(O_d, O_p, atol=1e-12)
         np.testing.assert_allclose(L_d, L_p, atol=1e-12)
         assert np.isfinite(O_d).all()
+
+
+def test_chunk_major_k_layout():
+    """Chunk-major paged K blocks: the slot table written out, its own
+    inverse, the two 128-byte line groups, and a gather read element by
+    element from a pool whose values encode their own position."""
+    s = ot.chunk_slot(np.arange(16))
+    assert list(s) == [0, 1, 2, 3, 8, 9, 10, 11, 4, 5, 6, 7, 12, 13, 14, 15]
+    assert list(ot.chunk_slot(s)) == list(range(16))
+    assert set(np.arange(16)[s < 8]) == {0, 1, 2, 3, 8, 9, 10, 11}
+    nodes = [(-1, 0, 37, 0), (0, 20, 9, 1)]
+    Hkv, d = 2, 16
+    nb = 3 + 1
+    ids = np.array([5, 2, 7, 0], dtype=np.int32)
+    pool = np.zeros((8, Hkv, d // 8, 16, 8))
+    for b in range(8):
+        for h in range(Hkv):
+            for c in range(d // 8):
+                for sl in range(16):
+                    for e in range(8):
+                        pool[b, h, c, sl, e] = b * 1e6 + h * 1e4 + c * 1e3 + sl * 10 + e
+    got = ot.gather_paged(nodes, pool, ids, 16, layout="chunked")
+    assert got.shape == (37 + 9, Hkv, d)
+    bt_off, _ = ot.canonical_layout(nodes, 16)
+    row = 0
+    for seg, (_, _, ln, _) in enumerate(nodes):
+        for j in range(ln):
+            b = ids[bt_off[seg] + j // 16]
+            t = j % 16
+            for h in range(Hkv):
+                for dim in range(d):
+                    c, e = divmod(dim, 8)
+                    assert got[row, h, dim] == b * 1e6 + h * 1e4 + c * 1e3 + int(ot.chunk_slot(t)) * 10 + e
+            row += 1
