@@ -67,10 +67,12 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(2, 2))) void
 
   // Step cursors over the item's ranges: C = step being computed, L = next
   // step to load (two ahead of C once the pipeline is full).
+  // No implicit padding: copies of a padded struct keep the padding in
+  // memory (the compiler would place it in LDS).
   struct Cursor {
     int ri, st;
     RangeRec R;
-    bool ok;
+    int ok, unused;
   };
   auto advance = [&](Cursor& c) {
     if (++c.st * 32 >= c.R.n_keys) {
@@ -78,10 +80,10 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(2, 2))) void
       if (++c.ri < w.rng_count)
         c.R = p.ranges[w.rng_begin + c.ri];
       else
-        c.ok = false;
+        c.ok = 0;
     }
   };
-  Cursor C{0, 0, p.ranges[w.rng_begin], true};
+  Cursor C{0, 0, p.ranges[w.rng_begin], 1, 0};
   Cursor L = C;
 
   uint4 kf[2][2][NDS];  // [set][M block][K-slice]

@@ -30,8 +30,10 @@
 // Paged K/V: K blocks are chunk-major ([d/8][16 slots][8]) and land in the
 // row-major LDS tile piece by piece; V blocks are d-major ([d][16 tokens]),
 // so a 16-byte load holds 8 consecutive keys of one d row and lands in the
-// transposed LDS tile as two 8-byte stores.  A tile's block ids are
-// wave-uniform scalars fetched one tile ahead of its K/V loads.
+// transposed LDS tile as two 8-byte stores.  A tile's block ids come from one
+// vector load issued a tile ahead of its K/V loads.
+#include <type_traits>
+
 #include "device_common.hpp"
 
 namespace padoc {
@@ -134,20 +136,29 @@ __global__ __launch_bounds__(kThreads) void tile_mfma_bf16_kernel(TileParams p) 
   const int v_pr = tid % (KT / 2), v_dc = tid / (KT / 2);
   const bool v_on = PAGED || v_dc < CPR;
 
-  uint4 kr[KPT], vr[2 * VPT];
-  int vkeep[PAGED ? VPT : 1];  // paged V: keys of each chunk inside the range
+  // Two staging register sets: a tile's global loads are issued two
+  // iterations before its LDS store.
+  uint4 kr[2][KPT], vr[2][2 * VPT];
+  int vkeep[2][PAGED ? VPT : 1];  // paged V: keys of each chunk inside the range
 
-  auto fetch_ids = [&](const RangeRec& R, int kt, int64_t (&ids)[NB]) {
-    const int kbase = kt * KT;
-#pragma unroll
-    for (int bi = 0; bi < NB; ++bi)
-      ids[bi] = p.block_table[R.kv_start + (kbase >> 4) + ((kbase + bi * kBlock < R.n_keys) ? bi : 0)];
+  // Block ids of a tile: lane l (mod NB) loads the id of block l with a
+  // vector load.  Scalar loads would share the LDS wait counter (and return
+  // out of order), so every LDS wait would also wait for the block table.
+  auto fetch_idv = [&](const RangeRec& R, int kt) -> int {
+    const int kbase = kt * KT, bi = lane & (NB - 1);
+    return p.block_table[R.kv_start + (kbase >> 4) + ((kbase + bi * kBlock < R.n_keys) ? bi : 0)];
   };
   // Global -> registers, branch-free.  Rows past the range end are read from
   // the range's last row (finite data whose scores the mask removes); paged
   // V chunks, which may reach into unwritten slots, are zeroed past the end
   // when they are stored, a tile later, so no load is waited for early.
-  auto load_tile = [&](const RangeRec& R, int kt, const int64_t (&ids)[NB]) {
+  auto load_tile = [&](auto xc, const RangeRec& R, int kt, int idv) {
+    constexpr int X = decltype(xc)::value;
+    int64_t ids[NB] = {};
+    if constexpr (PAGED) {
+#pragma unroll
+      for (int bi = 0; bi < NB; ++bi) ids[bi] = __builtin_amdgcn_readlane(idv, bi);
+    }
     const int kbase = kt * KT;
     const int last = R.n_keys - 1 - kbase;  // >= 0
 #pragma unroll
@@ -157,7 +168,7 @@ __global__ __launch_bounds__(kThreads) void tile_mfma_bf16_kernel(TileParams p) 
       const uint4 x = PAGED ? load_stream16(Kg + paged_k_offset<D>(ids[kc >> 4], kvh, (int32_t)Hkv, kc & 15, k_dc[i]))
                             : *reinterpret_cast<const uint4*>(Kg + ((R.kv_start + kbase + kc) * Hkv + kvh) * (int64_t)D +
                                                               k_dc[i] * 8);
-      kr[i] = x;
+      kr[X][i] = x;
     }
     if constexpr (PAGED) {
 #pragma unroll
@@ -167,8 +178,8 @@ __global__ __launch_bounds__(kThreads) void tile_mfma_bf16_kernel(TileParams p) 
         const int d = rem >> 1, h = rem & 1;
         const int keep = R.n_keys - (kbase + bi * kBlock + h * 8);
         const int64_t blk = ids[keep > 0 ? bi : 0];
-        vr[i] = load_stream16(Vg + ((blk * Hkv + kvh) * D + d) * kBlock + h * 8);
-        vkeep[i] = keep;
+        vr[X][i] = load_stream16(Vg + ((blk * Hkv + kvh) * D + d) * kBlock + h * 8);
+        vkeep[X][i] = keep;
       }
     } else {
       if (v_on) {
@@ -176,14 +187,15 @@ __global__ __launch_bounds__(kThreads) void tile_mfma_bf16_kernel(TileParams p) 
         const int c0 = k0 <= last ? k0 : last, c1 = k1 <= last ? k1 : last;
         const uint4 x0 = *reinterpret_cast<const uint4*>(Vg + ((R.kv_start + kbase + c0) * Hkv + kvh) * D + v_dc * 8);
         const uint4 x1 = *reinterpret_cast<const uint4*>(Vg + ((R.kv_start + kbase + c1) * Hkv + kvh) * D + v_dc * 8);
-        vr[0] = x0;
-        vr[1] = x1;
+        vr[X][0] = x0;
+        vr[X][1] = x1;
       }
     }
   };
-  auto store_tile = [&](int s) {
+  auto store_tile = [&](auto xc, int s) {
+    constexpr int X = decltype(xc)::value;
 #pragma unroll
-    for (int i = 0; i < KPT; ++i) *reinterpret_cast<uint4*>(&Ks[s][k_key[i] * KS + k_dc[i] * 8]) = kr[i];
+    for (int i = 0; i < KPT; ++i) *reinterpret_cast<uint4*>(&Ks[s][k_key[i] * KS + k_dc[i] * 8]) = kr[X][i];
     if constexpr (PAGED) {
 #pragma unroll
       for (int i = 0; i < VPT; ++i) {
@@ -192,14 +204,14 @@ __global__ __launch_bounds__(kThreads) void tile_mfma_bf16_kernel(TileParams p) 
         const int d = rem >> 1, h = rem & 1;
         // keys 8h..8h+3 of block bi -> positions 4h..4h+3, keys 8h+4..8h+7 -> 8+4h..
         uint16_t* row = &Vt[s][d * VS + bi * 16];
-        const uint4 x = keep_first(vr[i], vkeep[i]);
+        const uint4 x = keep_first(vr[X][i], vkeep[X][i]);
         *reinterpret_cast<uint2*>(row + 4 * h) = make_uint2(x.x, x.y);
         *reinterpret_cast<uint2*>(row + 8 + 4 * h) = make_uint2(x.z, x.w);
       }
     } else if (v_on) {
       const int pos = vt_pos(2 * v_pr);
-      const uint32_t a[4] = {vr[0].x, vr[0].y, vr[0].z, vr[0].w};
-      const uint32_t b[4] = {vr[1].x, vr[1].y, vr[1].z, vr[1].w};
+      const uint32_t a[4] = {vr[X][0].x, vr[X][0].y, vr[X][0].z, vr[X][0].w};
+      const uint32_t b[4] = {vr[X][1].x, vr[X][1].y, vr[X][1].z, vr[X][1].w};
 #pragma unroll
       for (int m = 0; m < 4; ++m) {
         // d = dc*8 + 2m holds (key 2pr, key 2pr+1) low halves; d+1 the high halves
@@ -210,31 +222,34 @@ __global__ __launch_bounds__(kThreads) void tile_mfma_bf16_kernel(TileParams p) 
   };
 
   // Tile cursors (wave-uniform): C = tile being computed, L = next to load.
+  // No implicit padding: copies of a padded struct keep the padding in
+  // memory (the compiler would place it in LDS).
   struct Cursor {
     int ri, kt;
     RangeRec R;
-    bool ok;
+    int ok, unused;
   };
   auto advance = [&](Cursor& c) {
     if (++c.kt * KT >= c.R.n_keys) {
       c.kt = 0;
       if (++c.ri < w.rng_count)
-        c.R = uniform_range(p.ranges[w.rng_begin + c.ri]);
+        c.R = uniform_range(p.ranges[__builtin_amdgcn_readfirstlane(w.rng_begin + c.ri)]);  // scalar loads
       else
-        c.ok = false;
+        c.ok = 0;
     }
   };
-  Cursor C{0, 0, uniform_range(p.ranges[w.rng_begin]), true};
+  Cursor C{0, 0, uniform_range(p.ranges[w.rng_begin]), 1, 0};
   Cursor L = C;
-  int lim = 0;
-  auto load_lim = [&]() {
-    // one unconditional load (of a valid int when the range has no limits),
-    // so the compiler's wait counts for the tile loads stay exact
-    const int32_t* lp = C.R.lim_off < 0 ? &p.work[blockIdx.x].ntok : p.lims + C.R.lim_off + (valid ? tok : 0);
-    const int32_t lv = *lp;
-    lim = C.R.lim_off < 0 ? C.R.n_keys : (valid ? lv : 0);
+  // This column's limit entry for a cursor's range: one unconditional load
+  // (of a valid int when the range has no limits), interpreted only in the
+  // mask.  Loads are never skipped or copied right after being issued, so
+  // the compiler's wait counts stay exact across iterations.
+  auto fetch_lim = [&](int32_t lim_off) -> int {
+    const int32_t* lp = lim_off < 0 ? &p.work[blockIdx.x].ntok : p.lims + lim_off + (valid ? tok : 0);
+    return *lp;
   };
-  load_lim();
+  int limr[2];  // [t % 2]: limit entry of tile t's range
+  limr[0] = fetch_lim(C.R.lim_off);
 
   float m_run = -INFINITY, l_run = 0.f;
   f32x16_t acc[NDB];
@@ -244,34 +259,47 @@ __global__ __launch_bounds__(kThreads) void tile_mfma_bf16_kernel(TileParams p) 
     for (int i = 0; i < 16; ++i) acc[db][i] = 0.f;
   const float sl2 = p.scale_log2;
 
-  // Prologue: tile 0 into LDS stage 0, tile 1 into registers.  Tile t lives
-  // in stage t % 3.
-  int64_t ids[NB] = {};
-  if constexpr (PAGED) fetch_ids(L.R, L.kt, ids);
-  load_tile(L.R, L.kt, ids);
-  advance(L);
-  store_tile(0);
-  bool staged = false;
-  if (L.ok) {
-    if constexpr (PAGED) fetch_ids(L.R, L.kt, ids);
-    load_tile(L.R, L.kt, ids);
-    advance(L);
-    staged = true;
-    if (PAGED && L.ok) fetch_ids(L.R, L.kt, ids);
-  }
+  // Prologue: tile 0 into LDS stage 0, tiles 1 and 2 into register sets 0
+  // and 1.  Tile t lives in stage t % 3; `ids` holds the block ids of L's
+  // tile.
+  using Set0 = std::integral_constant<int, 0>;
+  using Set1 = std::integral_constant<int, 1>;
+  // load_next(X) loads L's tile into staging set X using the block ids in
+  // idv[X^1] and requests the ids of the tile after it into idv[X] first, so
+  // waiting for ids never waits for the newest tile's data.  Past the item's
+  // last tile the loader re-reads a valid tile of its last range (not
+  // staged), so every iteration issues the same loads.
+  int idv[2] = {0, 0};
+  bool staged[2] = {false, false};  // register set holds a loaded tile not yet in LDS
+  auto load_next = [&](auto xc) {
+    constexpr int X = decltype(xc)::value;
+    const bool real = L.ok;
+    Cursor nx = L;
+    advance(nx);
+    if constexpr (PAGED) idv[X] = fetch_idv(nx.R, nx.kt);
+    load_tile(xc, L.R, L.kt, idv[X ^ 1]);
+    L = nx;
+    staged[X] = real;
+  };
+  if constexpr (PAGED) idv[0] = fetch_idv(L.R, L.kt);
+  load_next(Set1{});  // tile 0 (set 1, ids in idv[0])
+  store_tile(Set1{}, 0);
+  staged[1] = false;
+  load_next(Set0{});  // tile 1
+  load_next(Set1{});  // tile 2
   __syncthreads();
 
   // O^T += V^T P^T, 16 keys per MFMA: key group g = (mb, j) holds keys
   // mb*32 + 16j + [0,16).  The V^T fragments of group g+1 are read while the
-  // products of group g run; group 0's are read by the caller (vf0), ahead of
-  // the softmax.
+  // products of group g run.
   auto vfrag = [&](const uint16_t* vt, int g, bf16x8_t (&a)[NDB]) {
 #pragma unroll
     for (int db = 0; db < NDB; ++db)
       a[db] = *reinterpret_cast<const bf16x8_t*>(&vt[(db * 32 + l32) * VS + (g >> 1) * 32 + 16 * (g & 1) + hf * 8]);
   };
-  auto pv = [&](const uint16_t* vt, bf16x8_t (&vf0)[NDB], const bf16x8_t (&P)[2][2]) {
-    bf16x8_t vf1[NDB];
+  auto pv = [&](const uint16_t* vt, const bf16x8_t (&P)[2][2]) {
+    bf16x8_t vf0[NDB], vf1[NDB];
+    vfrag(vt, 0, vf0);
 #pragma unroll
     for (int g = 0; g < 4; ++g) {
       bf16x8_t(&cur)[NDB] = (g & 1) ? vf1 : vf0;
@@ -294,14 +322,18 @@ __global__ __launch_bounds__(kThreads) void tile_mfma_bf16_kernel(TileParams p) 
   bool have_held = false;
 
   int s = 0;
-  bf16x8_t vf0[NDB];
-  while (true) {
-    if (lag && have_held) {
-      vfrag(Vt[s_held], 0, vf0);
-      pv(Vt[s_held], vf0, held);
-    }
+  // Iteration t (register set X = t % 2) consumes tile t, stores tile t+1
+  // (loaded two iterations ago into set X) and loads tile t+3 into set X.
+  auto iter = [&](auto xc) -> bool {
+    constexpr int X = decltype(xc)::value;
+    if (lag && have_held) pv(Vt[s_held], held);
     const uint16_t* ks = Ks[s];
     const int kb = C.kt * KT;
+    // the next tile's cursor, and its limit entry (requested before this
+    // iteration's tile loads)
+    Cursor cn = C;
+    advance(cn);
+    limr[X ^ 1] = fetch_lim(cn.ok ? cn.R.lim_off : C.R.lim_off);
 
     // S^T = K Q^T for 64 keys x 32 columns.
     f32x16_t S[2];
@@ -316,10 +348,10 @@ __global__ __launch_bounds__(kThreads) void tile_mfma_bf16_kernel(TileParams p) 
         const bf16x8_t a = *reinterpret_cast<const bf16x8_t*>(&ks[(mb * 32 + l32) * KS + kk * 16 + hf * 8]);
         S[mb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, bq[kk], S[mb], 0, 0, 0);
       }
-    if (!lag) vfrag(Vt[s], 0, vf0);  // lands during the softmax
     if (kb + KT > C.R.min_lim) {
       // Partial tile: key (mb, i) of this lane is kb + hf*4 + mb*32 + (i/4)*8 + i%4;
       // it is visible iff the constant part is below rel.
+      const int lim = C.R.lim_off < 0 ? C.R.n_keys : (valid ? limr[X] : 0);
       const int rel = lim - kb - hf * 4;
 #pragma unroll
       for (int mb = 0; mb < 2; ++mb)
@@ -367,7 +399,7 @@ __global__ __launch_bounds__(kThreads) void tile_mfma_bf16_kernel(TileParams p) 
     l_run += ls0 + ls1;
 
     if (!lag) {
-      pv(Vt[s], vf0, P);
+      pv(Vt[s], P);
     } else {
 #pragma unroll
       for (int mb = 0; mb < 2; ++mb)
@@ -378,30 +410,23 @@ __global__ __launch_bounds__(kThreads) void tile_mfma_bf16_kernel(TileParams p) 
     }
 
     // Stage the next tile (its stage was last read by the lagging waves
-    // before the previous barrier) and start loading the one after.
+    // before the previous barrier) and start loading the one three ahead.
     const int s1 = s == kStages - 1 ? 0 : s + 1;
-    if (staged) {
-      store_tile(s1);
-      staged = false;
+    if (staged[X]) {
+      store_tile(xc, s1);
+      staged[X] = false;
     }
-    if (L.ok) {
-      load_tile(L.R, L.kt, ids);
-      advance(L);
-      staged = true;
-      if (PAGED && L.ok) fetch_ids(L.R, L.kt, ids);
-    }
+    load_next(xc);
     __syncthreads();
 
-    const int ri_before = C.ri;
-    advance(C);
-    if (!C.ok) break;
-    if (C.ri != ri_before) load_lim();
+    C = cn;
+    if (!C.ok) return false;
     s = s1;
+    return true;
+  };
+  while (iter(Set0{}) && iter(Set1{})) {
   }
-  if (lag && have_held) {
-    vfrag(Vt[s_held], 0, vf0);
-    pv(Vt[s_held], vf0, held);
-  }
+  if (lag && have_held) pv(Vt[s_held], held);
 
   // Epilogue.  Lane (column, hf) holds d = db*32 + (i/4)*8 + hf*4 + i%4.
   const float lt = l_run + __shfl_xor(l_run, 32);
