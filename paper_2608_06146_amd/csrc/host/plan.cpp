@@ -176,6 +176,8 @@ padoc_status validate(const padoc_tree_desc* d) {
     return set_error(PADOC_ERR_SHAPE, "Hq/Hkv=%d exceeds 64", d->num_heads_q / d->num_heads_kv);
   if (d->head_dim != 64 && d->head_dim != 128)
     return set_error(PADOC_ERR_SHAPE, "head_dim=%d is not 64 or 128", d->head_dim);
+  if (d->num_heads_kv > 4096)  // kernels address a 64-key K/V tile with 32-bit offsets
+    return set_error(PADOC_ERR_SHAPE, "Hkv=%d exceeds 4096", d->num_heads_kv);
   if (!std::isfinite(d->softmax_scale) || !(d->softmax_scale > 0.f))
     return set_error(PADOC_ERR_ARG, "softmax_scale must be positive and finite");
   if (d->block_size != 0 && d->block_size != kBlock)

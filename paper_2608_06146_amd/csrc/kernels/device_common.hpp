@@ -31,6 +31,18 @@ __device__ __forceinline__ uint4 load_stream16(const void* p) {
   return make_uint4(t.x, t.y, t.z, t.w);
 }
 
+// Plain 16-byte load and store as one vector value (a uint4 struct copy
+// would become a memory-to-memory copy through a stack slot).
+__device__ __forceinline__ uint4 load16(const void* p) {
+  typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
+  const u32x4 t = *static_cast<const u32x4*>(p);
+  return make_uint4(t.x, t.y, t.z, t.w);
+}
+__device__ __forceinline__ void store16(void* p, const uint4& v) {
+  typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
+  *static_cast<u32x4*>(p) = u32x4{v.x, v.y, v.z, v.w};
+}
+
 __device__ __forceinline__ float fast_exp2(float x) { return __builtin_amdgcn_exp2f(x); }
 
 // max(a, b, c) as one v_max3_f32.  Written as an instruction so the compiler

@@ -5,29 +5,36 @@
 //
 // An item is up to 256 columns (query token x head of one KV-head group: the
 // G heads of a token share every K/V tile) against the item's key ranges, 64
-// keys per tile.  K tiles are staged row-major and V tiles transposed in a
-// two-stage LDS ring with one barrier per tile; a tile's global loads are
-// issued two tiles before its LDS store (two staging register sets).  Each
-// wavefront owns 32 columns and, per tile:
+// keys per tile.  Each wavefront owns 32 columns; per tile t it computes
 //   S^T = K Q^T         v_mfma_f32_32x32x16_bf16, keys on M, columns on N
 //                       (a lane owns one column and 16 of 32 key rows of a
-//                       half; the other 16 rows sit in lane^32), both 32-key
-//                       halves issued back to back
-//   online softmax      per half: half 0's runs while half 1's products are
-//                       in flight, half 1's while half 0's PV products run
+//                       half; the other 16 rows sit in lane^32)
+//   online softmax      VALU: mask, row max, exponentials, bf16 P^T
 //   O^T += V^T P^T      P^T comes straight from the score registers
 // (App. E Attn equation; App. C tree-varlen relation).  Only tiles of
 // ancestor prefixes and the own causal range are visited: the planner lists
 // no other segment.  Tiles wholly below every column's limit skip the mask.
-// Keys past a range's end never contribute: their K/V rows are copies of the
-// range's last row (finite), their scores are masked to -inf, and paged V
-// chunks past the end are zeroed in LDS, so no stale or sentinel memory
-// enters a product.
+//
+// Ping-pong schedule.  Wavefronts w and w+4 share a SIMD.  Each wavefront
+// alternates a matrix-core phase (PV of tile t-1, then S of tile t) and a
+// vector phase (softmax of tile t, LDS staging, global loads), and the two
+// halves of the workgroup run them half a step apart: while waves 0-3 issue
+// MFMAs, waves 4-7 exponentiate, and the reverse, separated by two
+// workgroup barriers per tile.  So each SIMD's matrix core has a wavefront
+// with independent work while the other one runs its softmax.
+//
+// LDS holds two K stages and two V^T stages.  Step t reads K(t) and V(t-1)
+// and stores K(t+1) and V(t) into the stages last read at step t-1; global
+// loads for the stores of step t+2 (K(t+3), V(t+2)) are issued in step t, so
+// every load has two steps to land.  Keys past a range's end never
+// contribute: their K/V rows are copies of the range's last row (finite),
+// their scores are masked to -inf, and paged V chunks past the end are zeroed
+// when stored, so no stale or sentinel memory enters a product.
 //
 // Accumulation is fp32 and scores are in log2 units, so each probability is
 // one v_exp_f32; the softmax denominator sums the bf16-rounded probabilities
 // that enter the PV product, so O is their exact weighted mean.  The
-// reference maximum of a column is raised only when a half's maximum exceeds
+// reference maximum of a column is raised only when a tile's maximum exceeds
 // it by more than 2^8 (probabilities stay <= 256); the accumulator is
 // rescaled only then.  Any reference gives the same O and LSE.  O is rounded
 // to bf16 (RNE) at the end.
@@ -36,7 +43,7 @@
 // row-major LDS tile piece by piece; V blocks are d-major ([d][16 tokens]),
 // so a 16-byte load holds 8 consecutive keys of one d row and lands in the
 // transposed LDS tile as two 8-byte stores.  A tile's block ids come from one
-// vector load issued a tile ahead of its K/V loads.
+// vector load issued a step ahead of its K (or V) loads.
 #pragma once
 
 #include <type_traits>
@@ -52,7 +59,6 @@ typedef float f32x16_t __attribute__((ext_vector_type(16)));
 
 constexpr int kWaves = 8;
 constexpr int kThreads = 64 * kWaves;
-constexpr int kStages = 2;
 constexpr float kRescaleSlack = 8.0f;  // log2 units: probabilities <= 2^8
 
 // Position of key r (0..63) inside a transposed V row.  Within each group of
@@ -77,6 +83,18 @@ __device__ __forceinline__ RangeRec uniform_range(RangeRec r) {
   return r;
 }
 
+// f(integral_constant<int, i>) for i = 0 .. N-1: constant indices into the
+// staging register arrays, so they stay registers (a loop index that is
+// still a variable when the optimizer first looks would place them in
+// scratch memory).
+template <int N, int I = 0, class F>
+__device__ __forceinline__ void static_for(F&& f) {
+  if constexpr (I < N) {
+    f(std::integral_constant<int, I>{});
+    static_for<N, I + 1>(f);
+  }
+}
+
 // One work item (up to 256 columns) on the 8 wavefronts of a workgroup.
 template <int D, bool PAGED, bool PARTIAL>
 __device__ __forceinline__ void tile_item(const TileParams& p, int item) {
@@ -90,8 +108,8 @@ __device__ __forceinline__ void tile_item(const TileParams& p, int item) {
   constexpr int VPT = PAGED ? 8 * D / kThreads : 1;  // V loads per thread (paged chunks / packed pairs)
   constexpr int NB = KT / kBlock;                    // blocks per tile (paged)
 
-  __shared__ __attribute__((aligned(16))) uint16_t Ks[kStages][KT * KS];
-  __shared__ __attribute__((aligned(16))) uint16_t Vt[kStages][D * VS];
+  __shared__ __attribute__((aligned(16))) uint16_t Ks[2][KT * KS];
+  __shared__ __attribute__((aligned(16))) uint16_t Vt[2][D * VS];
 
   const WorkRec w = p.work[item];
   if (w.rng_count <= 0) return;
@@ -100,6 +118,12 @@ __device__ __forceinline__ void tile_item(const TileParams& p, int item) {
   const int G = p.G;
   const int kvh = w.kvh;
   const int64_t Hkv = p.Hkv;
+
+  // Tiles of the item (wave-uniform).
+  int n_tiles = 0;
+  for (int r = 0; r < w.rng_count; ++r)
+    n_tiles += (p.ranges[__builtin_amdgcn_readfirstlane(w.rng_begin + r)].n_keys + KT - 1) / KT;
+  n_tiles = __builtin_amdgcn_readfirstlane(n_tiles);
 
   // This lane's column.
   const int col = wave * 32 + l32;
@@ -122,120 +146,62 @@ __device__ __forceinline__ void tile_item(const TileParams& p, int item) {
   const uint16_t* Kg = static_cast<const uint16_t*>(p.k);
   const uint16_t* Vg = static_cast<const uint16_t*>(p.v);
 
-  // Per-thread load geometry (independent of the tile).
+  // Per-thread load geometry (independent of the tile).  Every global load
+  // is a wave-uniform (scalar) tile or block base plus a per-thread 32-bit
+  // element offset, so a load costs no 64-bit vector address arithmetic.
   // K piece u (16 bytes): packed K rows are read row by row; paged K blocks
   // are chunk-major, so consecutive threads take consecutive slots of one
-  // chunk (token kslot(slot)).  Either way a wave reads 1 KB contiguous.
-  int k_key[KPT], k_dc[KPT];
+  // chunk (token kslot(slot)).  Either way a wave reads 1 KB contiguous, and
+  // a wave's paged pieces all lie in one block (k_blk, wave-uniform).
+  const uint32_t HD = (uint32_t)Hkv * D;  // elements per packed K/V row
+  int k_key[KPT], k_dc[KPT], k_blk[KPT];
+  uint32_t k_off[KPT];
 #pragma unroll
   for (int i = 0; i < KPT; ++i) {
     const int u = tid + kThreads * i;
     if constexpr (PAGED) {
       const int bi = u / (kBlock * CPR), rem = u % (kBlock * CPR);
-      k_key[i] = bi * kBlock + kslot(rem % kBlock);
+      const int slot = rem % kBlock;
+      k_key[i] = bi * kBlock + kslot(slot);
       k_dc[i] = rem / kBlock;
+      k_blk[i] = __builtin_amdgcn_readfirstlane(bi);
+      k_off[i] = ((uint32_t)kvh * (D / 8) + k_dc[i]) * (kBlock * 8) + slot * 8;
     } else {
       k_key[i] = u / CPR;
       k_dc[i] = u % CPR;
+      k_blk[i] = 0;
+      k_off[i] = (uint32_t)kvh * D + k_dc[i] * 8;
     }
   }
-  // packed V: key pair (2pr, 2pr+1) and 16-byte chunk dc (threads >= 32*CPR idle)
-  const int v_pr = tid % (KT / 2), v_dc = tid / (KT / 2);
-  const bool v_on = PAGED || v_dc < CPR;
+  // paged V: chunk i of a thread is d row d, keys 8h .. 8h+7 of block bi
+  // (bi wave-uniform).  packed V: key pair (2pr, 2pr+1) and 16-byte chunk
+  // dc; with fewer chunks than thread groups (d = 64) the extra threads load
+  // a duplicate chunk and store nothing: every thread issues the same loads,
+  // so the compiler's load wait counts stay exact.
+  int v_blk[VPT], v_d[VPT], v_h[VPT];
+  uint32_t v_off[VPT];
+#pragma unroll
+  for (int i = 0; i < VPT; ++i) {
+    const int u = tid + kThreads * i;
+    const int bi = u / (2 * D), rem = u % (2 * D);
+    v_blk[i] = __builtin_amdgcn_readfirstlane(bi);
+    v_d[i] = rem >> 1;
+    v_h[i] = rem & 1;
+    v_off[i] = ((uint32_t)kvh * D + v_d[i]) * kBlock + v_h[i] * 8;
+  }
+  const int v_pr = tid % (KT / 2), v_dc = (tid / (KT / 2)) % CPR;
+  const bool v_on = PAGED || tid / (KT / 2) < CPR;
+  const uint32_t v_poff = (uint32_t)kvh * D + v_dc * 8;  // packed V: offset within a row
 
-  // Two staging register sets: a tile's global loads are issued two
-  // iterations before its LDS store.
-  uint4 kr[2][KPT], vr[2][2 * VPT];
-  int vkeep[2][PAGED ? VPT : 1];  // paged V: keys of each chunk inside the range
-
-  // Block ids of a tile: lane l (mod NB) loads the id of block l with a
-  // vector load.  Scalar loads would share the LDS wait counter (and return
-  // out of order), so every LDS wait would also wait for the block table.
-  auto fetch_idv = [&](const RangeRec& R, int kt) -> int {
-    const int kbase = kt * KT, bi = lane & (NB - 1);
-    return p.block_table[R.kv_start + (kbase >> 4) + ((kbase + bi * kBlock < R.n_keys) ? bi : 0)];
-  };
-  // Global -> registers, branch-free.  Rows past the range end are read from
-  // the range's last row (finite data whose scores the mask removes); paged
-  // V chunks, which may reach into unwritten slots, are zeroed past the end
-  // when they are stored, a tile later, so no load is waited for early.
-  auto load_tile = [&](auto xc, const RangeRec& R, int kt, int idv) {
-    constexpr int X = decltype(xc)::value;
-    int64_t ids[NB] = {};
-    if constexpr (PAGED) {
-#pragma unroll
-      for (int bi = 0; bi < NB; ++bi) ids[bi] = __builtin_amdgcn_readlane(idv, bi);
-    }
-    const int kbase = kt * KT;
-    const int last = R.n_keys - 1 - kbase;  // >= 0
-#pragma unroll
-    for (int i = 0; i < KPT; ++i) {
-      const int key = k_key[i];
-      const int kc = key <= last ? key : last;
-      const uint4 x = PAGED ? load_stream16(Kg + paged_k_offset<D>(ids[kc >> 4], kvh, (int32_t)Hkv, kc & 15, k_dc[i]))
-                            : *reinterpret_cast<const uint4*>(Kg + ((R.kv_start + kbase + kc) * Hkv + kvh) * (int64_t)D +
-                                                              k_dc[i] * 8);
-      kr[X][i] = x;
-    }
-    if constexpr (PAGED) {
-#pragma unroll
-      for (int i = 0; i < VPT; ++i) {
-        const int u = tid + kThreads * i;
-        const int bi = u / (2 * D), rem = u % (2 * D);
-        const int d = rem >> 1, h = rem & 1;
-        const int keep = R.n_keys - (kbase + bi * kBlock + h * 8);
-        const int64_t blk = ids[keep > 0 ? bi : 0];
-        vr[X][i] = load_stream16(Vg + ((blk * Hkv + kvh) * D + d) * kBlock + h * 8);
-        vkeep[X][i] = keep;
-      }
-    } else {
-      if (v_on) {
-        const int k0 = 2 * v_pr, k1 = k0 + 1;
-        const int c0 = k0 <= last ? k0 : last, c1 = k1 <= last ? k1 : last;
-        const uint4 x0 = *reinterpret_cast<const uint4*>(Vg + ((R.kv_start + kbase + c0) * Hkv + kvh) * D + v_dc * 8);
-        const uint4 x1 = *reinterpret_cast<const uint4*>(Vg + ((R.kv_start + kbase + c1) * Hkv + kvh) * D + v_dc * 8);
-        vr[X][0] = x0;
-        vr[X][1] = x1;
-      }
-    }
-  };
-  auto store_tile = [&](auto xc, int s) {
-    constexpr int X = decltype(xc)::value;
-#pragma unroll
-    for (int i = 0; i < KPT; ++i) *reinterpret_cast<uint4*>(&Ks[s][k_key[i] * KS + k_dc[i] * 8]) = kr[X][i];
-    if constexpr (PAGED) {
-#pragma unroll
-      for (int i = 0; i < VPT; ++i) {
-        const int u = tid + kThreads * i;
-        const int bi = u / (2 * D), rem = u % (2 * D);
-        const int d = rem >> 1, h = rem & 1;
-        // keys 8h..8h+3 of block bi -> positions 4h..4h+3, keys 8h+4..8h+7 -> 8+4h..
-        uint16_t* row = &Vt[s][d * VS + bi * 16];
-        const uint4 x = keep_first(vr[X][i], vkeep[X][i]);
-        *reinterpret_cast<uint2*>(row + 4 * h) = make_uint2(x.x, x.y);
-        *reinterpret_cast<uint2*>(row + 8 + 4 * h) = make_uint2(x.z, x.w);
-      }
-    } else if (v_on) {
-      const int pos = vt_pos(2 * v_pr);
-      const uint32_t a[4] = {vr[X][0].x, vr[X][0].y, vr[X][0].z, vr[X][0].w};
-      const uint32_t b[4] = {vr[X][1].x, vr[X][1].y, vr[X][1].z, vr[X][1].w};
-#pragma unroll
-      for (int m = 0; m < 4; ++m) {
-        // d = dc*8 + 2m holds (key 2pr, key 2pr+1) low halves; d+1 the high halves
-        *reinterpret_cast<uint32_t*>(&Vt[s][(v_dc * 8 + 2 * m) * VS + pos]) = (a[m] & 0xffffu) | (b[m] << 16);
-        *reinterpret_cast<uint32_t*>(&Vt[s][(v_dc * 8 + 2 * m + 1) * VS + pos]) = (a[m] >> 16) | (b[m] & 0xffff0000u);
-      }
-    }
-  };
-
-  // Tile cursors (wave-uniform): C = tile being computed, L = next to load.
-  // No implicit padding: copies of a padded struct keep the padding in
-  // memory (the compiler would place it in LDS).
+  // Tile cursors (wave-uniform).  No implicit padding: copies of a padded
+  // struct keep the padding in memory (the compiler would place it in LDS).
   struct Cursor {
     int ri, kt;
     RangeRec R;
     int ok, unused;
   };
+  // Past the item's last tile a cursor keeps pointing at a valid tile of the
+  // last range (kt * KT < n_keys always holds), so loads stay in bounds.
   auto advance = [&](Cursor& c) {
     if (++c.kt * KT >= c.R.n_keys) {
       c.kt = 0;
@@ -245,12 +211,118 @@ __device__ __forceinline__ void tile_item(const TileParams& p, int item) {
         c.ok = 0;
     }
   };
-  Cursor C{0, 0, uniform_range(p.ranges[w.rng_begin]), 1, 0};
-  Cursor L = C;
-  // This column's limit entry for a cursor's range: one unconditional load
-  // (of a valid int when the range has no limits), interpreted only in the
-  // mask.  Loads are never skipped or copied right after being issued, so
-  // the compiler's wait counts stay exact across iterations.
+
+  // Staging registers: set b%2 holds bundle b = K(b) and V(b-1).
+  uint4 kr[2][KPT], vr[2][2 * VPT];
+  int vkeep[2][PAGED ? VPT : 1];  // paged V: keys of each chunk inside the range
+
+  // Block ids of a tile: lane l (mod NB) loads the id of block l with a
+  // vector load.  Scalar loads would share the LDS wait counter (and return
+  // out of order), so every LDS wait would also wait for the block table.
+  auto fetch_idv = [&](const Cursor& c) -> int {
+    const int kbase = c.kt * KT, bi = lane & (NB - 1);
+    return p.block_table[c.R.kv_start + (kbase >> 4) + ((kbase + bi * kBlock < c.R.n_keys) ? bi : 0)];
+  };
+  // Global -> registers, branch-free.  Packed rows past the range end are
+  // read from the range's last row (the buffer may end there).  Paged slots
+  // past the end are read as they are (their block exists: the block ids of
+  // blocks wholly past the end are the tile's first block): their scores are
+  // masked and their V chunks zeroed when stored.
+  auto load_k = [&](auto xc, const Cursor& c, int idv) {
+    constexpr int X = decltype(xc)::value;
+    const int kbase = c.kt * KT;
+    static_for<KPT>([&](auto ic) {
+      constexpr int i = decltype(ic)::value;
+      if constexpr (PAGED) {
+        const int64_t blk = __builtin_amdgcn_readlane(idv, k_blk[i]);
+        kr[X][i] = load_stream16(Kg + blk * (int64_t)(HD * kBlock) + k_off[i]);
+      } else {
+        const int last = c.R.n_keys - 1 - kbase;  // >= 0
+        const int kc = k_key[i] <= last ? k_key[i] : last;
+        const uint16_t* tb = Kg + (c.R.kv_start + kbase) * (int64_t)HD;
+        kr[X][i] = load16(tb + (__umul24((uint32_t)kc, HD) + k_off[i]));
+      }
+    });
+  };
+  auto load_v = [&](auto xc, const Cursor& c, int idv) {
+    constexpr int X = decltype(xc)::value;
+    const int kbase = c.kt * KT;
+    if constexpr (PAGED) {
+      static_for<VPT>([&](auto ic) {
+        constexpr int i = decltype(ic)::value;
+        const int64_t blk = __builtin_amdgcn_readlane(idv, v_blk[i]);
+        vr[X][i] = load_stream16(Vg + blk * (int64_t)(HD * kBlock) + v_off[i]);
+        vkeep[X][i] = c.R.n_keys - (kbase + v_blk[i] * kBlock + v_h[i] * 8);
+      });
+    } else {
+      const int last = c.R.n_keys - 1 - kbase;
+      const int k0 = 2 * v_pr, k1 = k0 + 1;
+      const int c0 = k0 <= last ? k0 : last, c1 = k1 <= last ? k1 : last;
+      const uint16_t* tb = Vg + (c.R.kv_start + kbase) * (int64_t)HD;
+      vr[X][0] = load16(tb + (__umul24((uint32_t)c0, HD) + v_poff));
+      vr[X][1] = load16(tb + (__umul24((uint32_t)c1, HD) + v_poff));
+    }
+  };
+  auto store_k = [&](auto xc, uint16_t* ks) {
+    constexpr int X = decltype(xc)::value;
+    static_for<KPT>([&](auto ic) {
+      constexpr int i = decltype(ic)::value;
+      store16(&ks[k_key[i] * KS + k_dc[i] * 8], kr[X][i]);
+    });
+  };
+  auto store_v = [&](auto xc, uint16_t* vt) {
+    constexpr int X = decltype(xc)::value;
+    if constexpr (PAGED) {
+      static_for<VPT>([&](auto ic) {
+        constexpr int i = decltype(ic)::value;
+        // keys 8h..8h+3 of block bi -> positions 4h..4h+3, keys 8h+4..8h+7 -> 8+4h..
+        uint16_t* row = &vt[v_d[i] * VS + v_blk[i] * 16];
+        const uint4 x = keep_first(vr[X][i], vkeep[X][i]);
+        *reinterpret_cast<uint2*>(row + 4 * v_h[i]) = make_uint2(x.x, x.y);
+        *reinterpret_cast<uint2*>(row + 8 + 4 * v_h[i]) = make_uint2(x.z, x.w);
+      });
+    } else if (v_on) {
+      const int pos = vt_pos(2 * v_pr);
+      const uint32_t a[4] = {vr[X][0].x, vr[X][0].y, vr[X][0].z, vr[X][0].w};
+      const uint32_t b[4] = {vr[X][1].x, vr[X][1].y, vr[X][1].z, vr[X][1].w};
+#pragma unroll
+      for (int m = 0; m < 4; ++m) {
+        // d = dc*8 + 2m holds (key 2pr, key 2pr+1) low halves; d+1 the high
+        // halves (one byte permute each)
+        *reinterpret_cast<uint32_t*>(&vt[(v_dc * 8 + 2 * m) * VS + pos]) = __builtin_amdgcn_perm(b[m], a[m], 0x05040100u);
+        *reinterpret_cast<uint32_t*>(&vt[(v_dc * 8 + 2 * m + 1) * VS + pos]) =
+            __builtin_amdgcn_perm(b[m], a[m], 0x07060302u);
+      }
+    }
+  };
+
+  // Bundle loader: K from cursor Lk (tile b), V from cursor Lv (tile b-1,
+  // the previous Lk).  Block ids of the next K and V tiles are requested
+  // first, into the other id slot, so waiting for ids never waits for the
+  // newest tile data.  Past the item's end the cursors re-read a valid tile
+  // (never stored), so every step issues the same loads.
+  const RangeRec R0 = uniform_range(p.ranges[w.rng_begin]);
+  Cursor Lk{0, 0, R0, 1, 0};
+  Cursor Lv = Lk;
+  int idk[2] = {0, 0}, idv[2] = {0, 0};  // [slot]: block ids of a K / V tile
+  auto load_bundle = [&](auto xc) {
+    constexpr int X = decltype(xc)::value;
+    Cursor nk = Lk;
+    advance(nk);
+    if constexpr (PAGED) {
+      idk[X] = fetch_idv(nk);
+      idv[X] = fetch_idv(Lk);
+    }
+    load_k(xc, Lk, idk[X ^ 1]);
+    load_v(xc, Lv, idv[X ^ 1]);
+    Lv = Lk;
+    Lk = nk;
+  };
+
+  // Compute cursor (tile of the next S product) and this column's limit
+  // entry per tile: one unconditional load per tile (of a valid int when
+  // the range has no limits), interpreted only in the mask.
+  Cursor C{0, 0, R0, 1, 0};
   auto fetch_lim = [&](int32_t lim_off) -> int {
     const int32_t* lp = lim_off < 0 ? &p.work[item].ntok : p.lims + lim_off + (valid ? tok : 0);
     return *lp;
@@ -266,112 +338,54 @@ __device__ __forceinline__ void tile_item(const TileParams& p, int item) {
     for (int i = 0; i < 16; ++i) acc[db][i] = 0.f;
   const float sl2 = p.scale_log2;
 
-  // Prologue: tile 0 into LDS stage 0, tiles 1 and 2 into register sets 0
-  // and 1.  Tile t lives in stage t % 2.
-  using Set0 = std::integral_constant<int, 0>;
-  using Set1 = std::integral_constant<int, 1>;
-  // load_next(X) loads L's tile into staging set X using the block ids in
-  // idv[X^1] and requests the ids of the tile after it into idv[X] first, so
-  // waiting for ids never waits for the newest tile's data.  Past the item's
-  // last tile the loader re-reads a valid tile of its last range (not
-  // staged), so every iteration issues the same loads.
-  int idv[2] = {0, 0};
-  bool staged[2] = {false, false};  // register set holds a loaded tile not yet in LDS
-  auto load_next = [&](auto xc) {
-    constexpr int X = decltype(xc)::value;
-    const bool real = L.ok;
-    Cursor nx = L;
-    advance(nx);
-    if constexpr (PAGED) idv[X] = fetch_idv(nx.R, nx.kt);
-    load_tile(xc, L.R, L.kt, idv[X ^ 1]);
-    L = nx;
-    staged[X] = real;
-  };
-  if constexpr (PAGED) idv[0] = fetch_idv(L.R, L.kt);
-  load_next(Set1{});  // tile 0 (set 1, ids in idv[0])
-  store_tile(Set1{}, 0);
-  staged[1] = false;
-  load_next(Set0{});  // tile 1
-  load_next(Set1{});  // tile 2
-  __syncthreads();
+  f32x16_t S[2];     // scores of the last S product (two 32-key halves)
+  bf16x8_t P[2][2];  // probabilities of the last softmax
+#pragma unroll
+  for (int g = 0; g < 4; ++g)
+#pragma unroll
+    for (int e = 0; e < 8; ++e) P[g >> 1][g & 1][e] = (__bf16)0.f;
+  // mask data of the tile in S: whether any column is cut, and this lane's
+  // limit relative to the tile (keys of the lane's rows at or past it are
+  // masked)
+  int s_rel = 0;
+  bool s_partial = false;
 
-  // O^T += V^T P^T, 16 keys per MFMA: key group g = (mb, j) holds keys
-  // mb*32 + 16j + [0,16).
-  auto vfrag = [&](const uint16_t* vt, int g, bf16x8_t (&a)[NDB]) {
+  // Online softmax of the tile in S with a lazily raised reference maximum.
+  auto softmax = [&]() {
+    if (s_partial) {
 #pragma unroll
-    for (int db = 0; db < NDB; ++db)
-      a[db] = *reinterpret_cast<const bf16x8_t*>(&vt[(db * 32 + l32) * VS + (g >> 1) * 32 + 16 * (g & 1) + hf * 8]);
-  };
-  // PV products of half mb (key groups 2mb and 2mb+1).
-  auto pv_half = [&](const uint16_t* vt, int mb, const bf16x8_t (&P)[2][2]) {
-    bf16x8_t vf0[NDB], vf1[NDB];
-    vfrag(vt, 2 * mb, vf0);
-    vfrag(vt, 2 * mb + 1, vf1);
-#pragma unroll
-    for (int db = 0; db < NDB; ++db)
-      acc[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf0[db], P[mb][0], acc[db], 0, 0, 0);
-#pragma unroll
-    for (int db = 0; db < NDB; ++db)
-      acc[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf1[db], P[mb][1], acc[db], 0, 0, 0);
-  };
-
-  int s = 0;
-  // Iteration t (register set X = t % 2) consumes tile t, stores tile t+1
-  // (loaded two iterations ago into set X) and loads tile t+3 into set X.
-  auto iter = [&](auto xc) -> bool {
-    constexpr int X = decltype(xc)::value;
-    const uint16_t* ks = Ks[s];
-    const int kb = C.kt * KT;
-    // the next tile's cursor, and its limit entry (requested before this
-    // iteration's tile loads)
-    Cursor cn = C;
-    advance(cn);
-    limr[X ^ 1] = fetch_lim(cn.ok ? cn.R.lim_off : C.R.lim_off);
-
-    // S^T = K Q^T for 64 keys x 32 columns, as two 32-key halves (M blocks);
-    // half 1's products are issued before half 0's softmax, and half 0's PV
-    // products before half 1's softmax, so the matrix core has independent
-    // work while the vector units exponentiate.
-    f32x16_t S[2];
-#pragma unroll
-    for (int mb = 0; mb < 2; ++mb) {
-#pragma unroll
-      for (int i = 0; i < 16; ++i) S[mb][i] = 0.f;
-#pragma unroll
-      for (int kk = 0; kk < NKK; ++kk) {
-        const bf16x8_t a = *reinterpret_cast<const bf16x8_t*>(&ks[(mb * 32 + l32) * KS + kk * 16 + hf * 8]);
-        S[mb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, bq[kk], S[mb], 0, 0, 0);
-      }
-    }
-    const bool partial = kb + KT > C.R.min_lim;
-    // key of element i of half mb for this lane: kb + hf*4 + mb*32 + (i/4)*8 + i%4
-    const int rel = (C.R.lim_off < 0 ? C.R.n_keys : (valid ? limr[X] : 0)) - kb - hf * 4;
-    bf16x8_t P[2][2];
-    // Online softmax of one half with a lazily raised reference maximum.
-    auto softmax_half = [&](auto mbc) {
-      constexpr int mb = decltype(mbc)::value;
-      if (partial) {
+      for (int mb = 0; mb < 2; ++mb)
 #pragma unroll
         for (int i = 0; i < 16; ++i)
-          if (mb * 32 + (i >> 2) * 8 + (i & 3) >= rel) S[mb][i] = -INFINITY;
-      }
-      float m = max3f(S[mb][0], S[mb][1], S[mb][2]);
+          if (mb * 32 + (i >> 2) * 8 + (i & 3) >= s_rel) S[mb][i] = -INFINITY;
+    }
+    // row maximum as a tree of v_max3 (depth 4)
+    float t1[11];
 #pragma unroll
-      for (int i = 3; i < 15; i += 2) m = max3f(m, S[mb][i], S[mb][i + 1]);
-      const float mx = max_lane_halves(max3f(m, S[mb][15], S[mb][15])) * sl2;
-      const bool raise = mx > m_run + kRescaleSlack;
-      if (__any(raise)) {
-        // raising lanes: factor 2^(old - new) (0 when nothing was seen yet);
-        // the others keep their reference (factor 1, also when still -inf)
-        const float alpha = raise ? fast_exp2(m_run - mx) : 1.f;
-        m_run = raise ? mx : m_run;
-        l_run *= alpha;
+    for (int j = 0; j < 10; ++j) {
+      const int e = 3 * j;
+      t1[j] = max3f(S[e >> 4][e & 15], S[(e + 1) >> 4][(e + 1) & 15], S[(e + 2) >> 4][(e + 2) & 15]);
+    }
+    t1[10] = max3f(S[1][14], S[1][15], S[1][15]);
+    const float t2a = max3f(t1[0], t1[1], t1[2]), t2b = max3f(t1[3], t1[4], t1[5]);
+    const float t2c = max3f(t1[6], t1[7], t1[8]), t2d = max3f(t1[9], t1[10], t1[10]);
+    const float m = max3f(max3f(t2a, t2b, t2c), t2d, t2d);
+    const float mx = max_lane_halves(m) * sl2;
+    const bool raise = mx > m_run + kRescaleSlack;
+    if (__any(raise)) {
+      // raising lanes: factor 2^(old - new) (0 when nothing was seen yet);
+      // the others keep their reference (factor 1, also when still -inf)
+      const float alpha = raise ? fast_exp2(m_run - mx) : 1.f;
+      m_run = raise ? mx : m_run;
+      l_run *= alpha;
 #pragma unroll
-        for (int db = 0; db < NDB; ++db) acc[db] *= alpha;
-      }
-      const float m_sub = m_run == -INFINITY ? 0.f : m_run;
-      // the row sum adds the bf16 probabilities the PV product uses
-      float ls0 = 0.f, ls1 = 0.f;
+      for (int db = 0; db < NDB; ++db) acc[db] *= alpha;
+    }
+    const float m_sub = m_run == -INFINITY ? 0.f : m_run;
+    // the row sum adds the bf16 probabilities the PV product uses
+    float ls0 = 0.f, ls1 = 0.f;
+#pragma unroll
+    for (int mb = 0; mb < 2; ++mb)
 #pragma unroll
       for (int j = 0; j < 2; ++j) {
         f32x8_t x;
@@ -384,29 +398,128 @@ __device__ __forceinline__ void tile_item(const TileParams& p, int item) {
           ls1 = add_bf16x2(bf16x2_t{P[mb][j][e + 2], P[mb][j][e + 3]}, ls1);
         }
       }
-      l_run += ls0 + ls1;
-    };
-    softmax_half(std::integral_constant<int, 0>{});
-    pv_half(Vt[s], 0, P);
-    softmax_half(std::integral_constant<int, 1>{});
-    pv_half(Vt[s], 1, P);
-
-    // Stage the next tile (its stage held tile t-1, last read before the
-    // previous barrier) and start loading the one three ahead.
-    const int s1 = s == kStages - 1 ? 0 : s + 1;
-    if (staged[X]) {
-      store_tile(xc, s1);
-      staged[X] = false;
-    }
-    load_next(xc);
-    __syncthreads();
-
-    C = cn;
-    if (!C.ok) return false;
-    s = s1;
-    return true;
+    l_run += ls0 + ls1;
   };
-  while (iter(Set0{}) && iter(Set1{})) {
+
+  // Matrix-core phase: PV of the previous tile (V^T stage vt, P), then S of
+  // the current one (K stage ks).  The A operands (16-byte LDS fragments)
+  // stream through a ring of kPrefetch registers, so each MFMA's fragment
+  // was requested kPrefetch MFMAs earlier.  No scalar loads are in flight
+  // here (the barrier before drained them), so the LDS waits are exact.  At
+  // the first step P is zero and V^T stage 1 is zeroed, so the PV adds
+  // nothing; after the last tile the S product reads a stale stage and its
+  // result is never used.
+  constexpr int NPV = 4 * NDB, NMF = NPV + 2 * NKK, kPrefetch = PAGED ? 6 : 8;
+  auto mfma_phase = [&](const uint16_t* ks, const uint16_t* vt) {
+    // fragment of MFMA i: PV key group g = i / NDB (keys (g/2)*32 + 16(g%2)
+    // + [0,16)) and d block i % NDB; then S K-slice kk = j / 2 of half j % 2
+    auto frag = [&](int i) -> bf16x8_t {
+      if (i < NPV) {
+        const int g = i / NDB, db = i % NDB;
+        return *reinterpret_cast<const bf16x8_t*>(&vt[(db * 32 + l32) * VS + (g >> 1) * 32 + 16 * (g & 1) + hf * 8]);
+      }
+      const int j = i - NPV, kk = j >> 1, mb = j & 1;
+      return *reinterpret_cast<const bf16x8_t*>(&ks[(mb * 32 + l32) * KS + kk * 16 + hf * 8]);
+    };
+    bf16x8_t f[kPrefetch];
+#pragma unroll
+    for (int i = 0; i < kPrefetch; ++i) f[i] = frag(i);
+#pragma unroll
+    for (int mb = 0; mb < 2; ++mb)
+#pragma unroll
+      for (int e = 0; e < 16; ++e) S[mb][e] = 0.f;
+    // the scheduler may not sink the reads back towards their uses
+    __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+    for (int i = 0; i < NMF; ++i) {
+      const bf16x8_t a = f[i % kPrefetch];
+      if (i < NPV) {
+        const int g = i / NDB, db = i % NDB;
+        acc[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, P[g >> 1][g & 1], acc[db], 0, 0, 0);
+      } else {
+        const int j = i - NPV, kk = j >> 1, mb = j & 1;
+        S[mb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, bq[kk], S[mb], 0, 0, 0);
+      }
+      if (i + kPrefetch < NMF) f[i % kPrefetch] = frag(i + kPrefetch);
+      __builtin_amdgcn_sched_barrier(0);
+    }
+  };
+
+  // Vector phase of tile c (parity Y): mask data from the compute cursor and
+  // the tile's limit entry limr[Y], softmax, then the cursor moves to tile
+  // c+1 and that tile's limit entry is requested into limr[Y^1].
+  auto valu_phase = [&](auto yc) {
+    constexpr int Y = decltype(yc)::value;
+    const int kb = C.kt * KT;
+    s_partial = kb + KT > C.R.min_lim;
+    // key of element i of half mb for this lane: kb + hf*4 + mb*32 + (i/4)*8 + i%4
+    s_rel = (C.R.lim_off < 0 ? C.R.n_keys : (valid ? limr[Y] : 0)) - kb - hf * 4;
+    softmax();
+    Cursor cn = C;
+    advance(cn);
+    limr[Y ^ 1] = fetch_lim(cn.ok ? cn.R.lim_off : C.R.lim_off);
+    C = cn;
+  };
+
+  // Staging of step t: store bundle t+1 (K(t+1) into K stage (t+1)%2, V(t)
+  // into V stage t%2; both stages were last read at step t-1) from register
+  // set (t+1)%2, then load bundle t+3 into the same set.  Past the item's end
+  // the stores write re-read tiles into stages nobody reads again.
+  auto staging = [&](auto xc) {
+    constexpr int X = decltype(xc)::value;  // t % 2
+    using Next = std::integral_constant<int, X ^ 1>;
+    store_k(Next{}, Ks[X ^ 1]);
+    store_v(Next{}, Vt[X]);
+    load_bundle(Next{});
+  };
+
+  // Prologue: bundle 0 (K(0)) into LDS, bundles 1 and 2 into register sets.
+  using Set0 = std::integral_constant<int, 0>;
+  using Set1 = std::integral_constant<int, 1>;
+  if constexpr (PAGED) {
+    idk[1] = fetch_idv(Lk);
+    idv[1] = idk[1];
+  }
+  load_bundle(Set0{});  // bundle 0: K(0) (its V part re-reads tile 0, unused)
+  store_k(Set0{}, Ks[0]);
+  for (int i = tid; i < D * VS / 8; i += kThreads) reinterpret_cast<uint4*>(Vt[1])[i] = make_uint4(0, 0, 0, 0);
+  load_bundle(Set1{});  // bundle 1: K(1), V(0)
+  load_bundle(Set0{});  // bundle 2: K(2), V(1)
+  __syncthreads();
+
+  // Step t: leading half (waves 0-3): matrix phase, barrier, vector phase,
+  // barrier.  Lagging half (waves 4-7): vector phase of step t-1's scores,
+  // barrier, matrix phase, barrier.  Both halves pass the same barriers.
+  if (wave < 4) {
+    auto step = [&](auto xc, int t) {
+      constexpr int X = decltype(xc)::value;
+      mfma_phase(Ks[X], Vt[X ^ 1]);
+      __syncthreads();
+      if (t < n_tiles) valu_phase(xc);  // tile t
+      staging(xc);
+      __syncthreads();
+    };
+    for (int t = 0;;) {
+      step(Set0{}, t);
+      if (++t > n_tiles) break;
+      step(Set1{}, t);
+      if (++t > n_tiles) break;
+    }
+  } else {
+    auto step = [&](auto xc, int t) {
+      constexpr int X = decltype(xc)::value;
+      if (t >= 1) valu_phase(std::integral_constant<int, X ^ 1>{});  // tile t-1
+      staging(xc);
+      __syncthreads();
+      mfma_phase(Ks[X], Vt[X ^ 1]);
+      __syncthreads();
+    };
+    for (int t = 0;;) {
+      step(Set0{}, t);
+      if (++t > n_tiles) break;
+      step(Set1{}, t);
+      if (++t > n_tiles) break;
+    }
   }
 
   // Epilogue.  Lane (column, hf) holds d = db*32 + (i/4)*8 + hf*4 + i%4.
