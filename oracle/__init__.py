@@ -5,3 +5,4 @@ leg.  See :mod:`oracle.dense` for the definitions it follows.
 """
 from .dense import *  # noqa: F401,F403
 from .dense import __all__  # noqa: F401
+from .backward import masked_attention_backward, tree_attention_backward  # noqa: F401,E402
