@@ -26,6 +26,11 @@
  *                           paged KV cache: every live stream's newest
  *                           q_len tokens query their ancestors + own history;
  *                           keys shared by sibling streams are read once.
+ *   padoc_tree_attn_bwd  -- gradient of the packed forward (the paper trains
+ *                           with the tree-varlen backend, App. C): dQ, dK, dV
+ *                           of sum(dO * O); a key shared by several segments
+ *                           (page prefix, layout stream) receives the sum over
+ *                           every query that sees it.
  *
  * Layouts (row-major, head dimension innermost, everything contiguous):
  *   Q, O     [n_q_rows, Hq, d]        segment s's queries = its LAST q_len
@@ -179,6 +184,18 @@ typedef struct {
   int32_t n_keys, min_lim, lim_off, seg, key_begin, reserved;
 } padoc_range_view;
 
+/* Backward key-major item (packed bf16 plans): keys key_row0 .. +n_keys-1
+   (K/V rows of one segment, n_keys <= 128) of KV head kvh against the query
+   tokens btoks[tok_begin .. tok_begin+ntok) (Q rows), of which token i sees
+   the item's keys [0, blims[lim_begin + i]) (relative to key_row0); the item
+   computes columns col0 .. col0+ncol-1 (column c = token c/G, head c%G) and
+   adds their dK/dV contributions.  Items of one key range that split its
+   columns add into the same rows. */
+typedef struct {
+  int64_t key_row0;
+  int32_t n_keys, tok_begin, ntok, lim_begin, col0, ncol, kvh, cost;
+} padoc_bwd_view;
+
 typedef struct {
   int32_t kind;                  /* 0 = forward (final O), 1 = decode (partials) */
   int32_t tile_cols, tile_keys;  /* columns per work item, keys per key tile     */
@@ -192,6 +209,9 @@ typedef struct {
   int64_t n_comb;     const int32_t* comb_slot;
   int64_t n_comb_rows; const int32_t* comb_rows; /* (row*Hkv + kv head) merged
                                                     by the combine kernel     */
+  int32_t n_bwd; const padoc_bwd_view* bwd;      /* backward items (packed bf16) */
+  int64_t n_btok; const int32_t* btoks;
+  int64_t n_blim; const int32_t* blims;
   int64_t n_slots;
   size_t workspace_bytes;
 } padoc_schedule_view;
@@ -232,6 +252,22 @@ padoc_status padoc_branch_decode(const padoc_plan* plan, const void* q, const vo
                                  const void* v_cache, const int32_t* block_table, void* o,
                                  float* lse, void* workspace, size_t workspace_bytes,
                                  hipStream_t stream);
+
+/* Backward of the packed forward (bf16 plans with block_size == 0).
+   Given the forward's inputs q, k, v, its outputs o and lse, and the
+   upstream gradient dout ([n_q, Hq, d], same dtype), writes dq [n_q, Hq, d]
+   and dk, dv [num_kv_rows, Hkv, d] (bf16, rounded to nearest-even from fp32
+   accumulation; rows that no query sees get zero).  The gradient is that of
+   sum(dout * O) with O = softmax(scale * q K^T + mask) V.  Rows of dk/dv
+   whose keys are seen by more than 1024 query columns sum contributions in
+   an order that depends on scheduling (fp32 rounding differences only).
+   workspace: a device buffer of at least padoc_plan_backward_workspace_bytes
+   bytes (256-byte aligned); fp32 plans return PADOC_ERR_DTYPE. */
+padoc_status padoc_plan_backward_workspace_bytes(const padoc_plan* plan, size_t* bytes);
+padoc_status padoc_tree_attn_bwd(const padoc_plan* plan, const void* q, const void* k,
+                                 const void* v, const void* o, const float* lse,
+                                 const void* dout, void* dq, void* dk, void* dv,
+                                 void* workspace, size_t workspace_bytes, hipStream_t stream);
 
 /* Thread-local description of the last error on this thread ("" if none). */
 const char* padoc_last_error(void);

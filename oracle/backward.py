@@ -20,7 +20,11 @@ closed form, written out here per query row i over its visible keys j
 * ``dS_ij = P_ij (dP_ij - D_i)``,
 * ``dQ_i = c sum_j dS_ij k_j``, ``dK_j = c sum_i dS_ij q_i``.
 
-Masked pairs enter no sum.  With grouped heads (query head h reads KV head
+Masked pairs enter no sum.  ``D_i`` equals ``dO_i . O_i``; a backward that
+receives the forward's stored output (rounded to the forward's dtype)
+computes D from that stored O, so both functions take an optional ``o``: when
+given, ``D_i = dO_i . o_i`` (fp64 sum of the given values), else the exact
+``sum_j P_ij dP_ij``.  With grouped heads (query head h reads KV head
 ``h // G``), dK and dV of a KV head sum over its G query heads; a key shared by
 several segments (a page prefix, a layout stream) sums over every query of
 every descendant that sees it.  Everything is fp64 (bf16 inputs are exact in
@@ -37,17 +41,20 @@ from .dense import _as_nodes, _f64, ancestors, canonical_layout, masked_attentio
 __all__ = ["masked_attention_backward", "tree_attention_backward"]
 
 
-def masked_attention_backward(q, k, v, mask, scale: float, dout):
+def masked_attention_backward(q, k, v, mask, scale: float, dout, o=None):
     """Gradient of one head of masked softmax attention, fp64.
 
     ``q [nq, d]``, ``k, v [nk, d]``, ``mask [nq, nk]`` (True = visible),
-    ``dout [nq, dv]``.  Returns ``(dq, dk, dv)`` by the closed form in the
-    module docstring."""
+    ``dout [nq, dv]``, optional stored output ``o [nq, dv]`` for D.  Returns
+    ``(dq, dk, dv)`` by the closed form in the module docstring."""
     q, k, v, dout = _f64(q), _f64(k), _f64(v), _f64(dout)
     _, _, p = masked_attention(q, k, v, mask, scale, return_probs=True)
     dv = p.T @ dout
     dp = dout @ v.T
-    dd = np.sum(p * dp, axis=1, keepdims=True)
+    if o is None:
+        dd = np.sum(p * dp, axis=1, keepdims=True)
+    else:
+        dd = np.sum(dout * _f64(o), axis=1, keepdims=True)
     ds = np.where(mask, p * (dp - dd), 0.0)
     dq = scale * (ds @ k)
     dk = scale * (ds.T @ q)
@@ -55,17 +62,19 @@ def masked_attention_backward(q, k, v, mask, scale: float, dout):
 
 
 def tree_attention_backward(nodes, q, k, v, dout, scale: float, num_heads_q: int, num_heads_kv: int,
-                            kv_off=None, q_off=None):
+                            kv_off=None, q_off=None, o=None):
     """Backward of packed tree attention by definition.
 
     Layouts as in :func:`oracle.dense.tree_attention`: ``q, dout [n_q, Hq, d]``,
     ``k, v [T, Hkv, d]``.  Returns fp64 ``(dQ [n_q, Hq, d], dK [T, Hkv, d],
-    dV [T, Hkv, d])``; K/V rows no query sees get zero gradient."""
+    dV [T, Hkv, d])``; K/V rows no query sees get zero gradient.  ``o [n_q,
+    Hq, d]``, when given, is the stored forward output D is computed from."""
     nodes = _as_nodes(nodes)
     if num_heads_q % num_heads_kv:
         raise ValueError("Hq must be a multiple of Hkv")
     G = num_heads_q // num_heads_kv
     q64, k64, v64, do64 = _f64(q), _f64(k), _f64(v), _f64(dout)
+    o64 = None if o is None else _f64(o)
     if kv_off is None or q_off is None:
         ko, qo = canonical_layout(nodes, 0)
         kv_off = ko if kv_off is None else kv_off
@@ -100,7 +109,8 @@ def tree_attention_backward(nodes, q, k, v, dout, scale: float, num_heads_q: int
         for h in range(num_heads_q):
             g = h // G
             dq, dk, dv = masked_attention_backward(q64[qr, h, :], k64[kv_rows, g, :], v64[kv_rows, g, :], mask,
-                                                   scale, do64[qr, h, :])
+                                                   scale, do64[qr, h, :],
+                                                   None if o64 is None else o64[qr, h, :])
             dQ[qr, h, :] = dq
             dK[kv_rows, g, :] += dk
             dV[kv_rows, g, :] += dv

@@ -18,9 +18,9 @@ from typing import Optional, Sequence
 import numpy as np
 
 from . import _lib
-from ._lib import PadocError, SEGMENT_DTYPE, WORK_DTYPE, RANGE_DTYPE
+from ._lib import PadocError, SEGMENT_DTYPE, WORK_DTYPE, RANGE_DTYPE, BWD_DTYPE
 
-__all__ = ["TreePlan", "segments_from_pages", "segments_layout", "tree_attn_fwd", "branch_decode",
+__all__ = ["TreePlan", "segments_from_pages", "segments_layout", "tree_attn_fwd", "tree_attn_bwd", "branch_decode",
            "PadocError", "SEGMENT_DTYPE", "version", "set_kernel_events", "make_workspace"]
 
 _DTYPES = {"f32": _lib.F32, "fp32": _lib.F32, "float32": _lib.F32, "bf16": _lib.BF16, "bfloat16": _lib.BF16}
@@ -143,8 +143,25 @@ class TreePlan:
             "tile_class_off": arr(v.tile_class_off, v.n_range, np.int64),
             "comb_ptr": arr(v.comb_ptr, v.n_comb_ptr, np.int32), "comb_slot": arr(v.comb_slot, v.n_comb, np.int32),
             "comb_rows": arr(v.comb_rows, v.n_comb_rows, np.int32),
+            "bwd": arr(v.bwd, v.n_bwd, BWD_DTYPE), "btoks": arr(v.btoks, v.n_btok, np.int32),
+            "blims": arr(v.blims, v.n_blim, np.int32),
             "n_slots": v.n_slots, "workspace_bytes": v.workspace_bytes,
         }
+
+    def backward_workspace_bytes(self) -> int:
+        n = C.c_size_t(0)
+        _lib.check(_lib.lib().padoc_plan_backward_workspace_bytes(self.handle, C.byref(n)))
+        return int(n.value)
+
+    def backward_workspace(self, device):
+        """A cached device workspace for the backward (256-byte aligned)."""
+        import torch
+        if getattr(self, "_bws", None) is None or self._bws[0] != torch.device(device):
+            nb = self.backward_workspace_bytes()
+            raw = torch.empty(nb + 256, dtype=torch.uint8, device=device)
+            off = (-raw.data_ptr()) % 256
+            self._bws = (torch.device(device), raw, raw[off: off + nb])
+        return self._bws[2]
 
     def workspace(self, device):
         """A cached device workspace of the plan's size (256-byte aligned)."""
@@ -225,6 +242,31 @@ def branch_decode(q, k_cache, v_cache, block_table, plan: TreePlan, out=None, ls
                                               _ptr(out), _ptr(lse), _ptr(ws), ws.numel(),
                                               C.c_void_p(s.cuda_stream)))
     return out, lse
+
+
+def tree_attn_bwd(q, k, v, o, lse, dout, plan: TreePlan, dq=None, dk=None, dv=None, workspace=None, stream=None):
+    """Backward of the packed forward (``padoc_tree_attn_bwd``, bf16 plans).
+    q, o, dout ``[n_q, Hq, d]``; k, v ``[T, Hkv, d]``; lse float32 ``[n_q,
+    Hq]`` (the forward's outputs); returns ``(dQ, dK, dV)``."""
+    import torch
+    dt = _torch_dtype(plan)
+    dev = q.device
+    for name, t in (("q", q), ("k", k), ("v", v), ("o", o), ("dout", dout)):
+        _check_tensor(name, t, dt, dev)
+    _check_tensor("lse", lse, torch.float32, dev)
+    dq = torch.empty_like(q) if dq is None else dq
+    dk = torch.empty_like(k) if dk is None else dk
+    dv = torch.empty_like(v) if dv is None else dv
+    for name, t, ref in (("dq", dq, q), ("dk", dk, k), ("dv", dv, v)):
+        _check_tensor(name, t, dt, dev)
+        if t.shape != ref.shape:
+            raise ValueError(f"{name} has shape {tuple(t.shape)}, expected {tuple(ref.shape)}")
+    ws = plan.backward_workspace(dev) if workspace is None else workspace
+    s = torch.cuda.current_stream(dev) if stream is None else stream
+    _lib.check(_lib.lib().padoc_tree_attn_bwd(plan.handle, _ptr(q), _ptr(k), _ptr(v), _ptr(o), _ptr(lse), _ptr(dout),
+                                              _ptr(dq), _ptr(dk), _ptr(dv), _ptr(ws), ws.numel(),
+                                              C.c_void_p(s.cuda_stream)))
+    return dq, dk, dv
 
 
 def set_kernel_events(before=None, after=None):

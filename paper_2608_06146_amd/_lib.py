@@ -25,6 +25,8 @@ SEGMENT_DTYPE = np.dtype([("parent", "<i4"), ("fork", "<i4"), ("len", "<i4"), ("
 WORK_DTYPE = np.dtype([("tok_begin", "<i4"), ("ntok", "<i4"), ("rng_begin", "<i4"), ("rng_count", "<i4"),
                        ("kvh", "<i4"), ("out_base", "<i4"), ("cost", "<i4"), ("col0", "<i4"),
                        ("ncol", "<i4"), ("fin", "<i4"), ("reserved", "<i4", (2,))])
+BWD_DTYPE = np.dtype([("key_row0", "<i8"), ("n_keys", "<i4"), ("tok_begin", "<i4"), ("ntok", "<i4"),
+                      ("lim_begin", "<i4"), ("col0", "<i4"), ("ncol", "<i4"), ("kvh", "<i4"), ("cost", "<i4")])
 RANGE_DTYPE = np.dtype([("kv_start", "<i8"), ("n_keys", "<i4"), ("min_lim", "<i4"), ("lim_off", "<i4"),
                         ("seg", "<i4"), ("key_begin", "<i4"), ("reserved", "<i4")])
 
@@ -59,6 +61,9 @@ class ScheduleView(C.Structure):
                 ("n_comb_ptr", C.c_int64), ("comb_ptr", C.c_void_p),
                 ("n_comb", C.c_int64), ("comb_slot", C.c_void_p),
                 ("n_comb_rows", C.c_int64), ("comb_rows", C.c_void_p),
+                ("n_bwd", C.c_int32), ("bwd", C.c_void_p),
+                ("n_btok", C.c_int64), ("btoks", C.c_void_p),
+                ("n_blim", C.c_int64), ("blims", C.c_void_p),
                 ("n_slots", C.c_int64), ("workspace_bytes", C.c_size_t)]
 
 
@@ -66,6 +71,7 @@ EXPORTED = [
     "padoc_tree_from_pages", "padoc_tree_layout", "padoc_plan_create", "padoc_plan_workspace_bytes",
     "padoc_plan_export", "padoc_plan_destroy", "padoc_tree_attn_fwd", "padoc_branch_decode",
     "padoc_last_error", "padoc_set_kernel_events", "padoc_version",
+    "padoc_plan_backward_workspace_bytes", "padoc_tree_attn_bwd",
 ]
 
 _lib = None
@@ -90,13 +96,16 @@ def lib():
     L.padoc_plan_destroy.restype = None
     L.padoc_tree_attn_fwd.argtypes = [vp, vp, vp, vp, vp, vp, vp, sz, vp]
     L.padoc_branch_decode.argtypes = [vp, vp, vp, vp, vp, vp, vp, vp, sz, vp]
+    L.padoc_plan_backward_workspace_bytes.argtypes = [vp, C.POINTER(sz)]
+    L.padoc_tree_attn_bwd.argtypes = [vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, sz, vp]
     L.padoc_last_error.argtypes = []
     L.padoc_last_error.restype = C.c_char_p
     L.padoc_set_kernel_events.argtypes = [vp, vp]
     L.padoc_version.argtypes = []
     L.padoc_version.restype = C.c_char_p
     for name in ("padoc_tree_from_pages", "padoc_tree_layout", "padoc_plan_create", "padoc_plan_workspace_bytes",
-                 "padoc_plan_export", "padoc_tree_attn_fwd", "padoc_branch_decode", "padoc_set_kernel_events"):
+                 "padoc_plan_export", "padoc_tree_attn_fwd", "padoc_branch_decode", "padoc_set_kernel_events",
+                 "padoc_plan_backward_workspace_bytes", "padoc_tree_attn_bwd"):
         getattr(L, name).restype = C.c_int
     _lib = L
     return L

@@ -29,12 +29,12 @@ SOURCES = [
     "csrc/kernels/decode_private.hip",
     "csrc/kernels/tile_valu_f32.hip",
     "csrc/kernels/lse_combine.hip",
+    "csrc/kernels/bwd.hip",
 ]
-HEADERS = [
-    "csrc/schedule.hpp",
-    "csrc/host/plan.hpp",
-    "csrc/kernels/device_common.hpp",
-]
+# Every header under csrc/ (and the public header) enters each object's
+# digest, so an edit to any of them rebuilds every object.
+HEADERS = sorted(os.path.relpath(os.path.join(d, f), PKG)
+                 for d, _, fs in os.walk(os.path.join(PKG, "csrc")) for f in fs if f.endswith((".hpp", ".h")))
 
 # Packed fp32 VALU forms are kept out of device code on purpose: the
 # compiler must not form v_pk_{add,mul,fma}_f32 from scalar fp32 code.

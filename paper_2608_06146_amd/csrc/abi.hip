@@ -11,6 +11,7 @@ hipError_t launch_tile_mfma_bf16(const TileParams& p, int n_work, int D, bool pa
 hipError_t launch_decode_private_bf16(const TileParams& p, int n_items, int D, hipStream_t s);
 hipError_t launch_tile_valu_f32(const TileParams& p, int n_work, int D, bool paged, hipStream_t s);
 hipError_t launch_lse_combine(const CombineParams& p, int D, bool bf16, hipStream_t s);
+hipError_t launch_tree_attn_bwd(const BwdParams& p, int n_work, int n_bwd, int D, hipStream_t s);
 
 namespace {
 thread_local hipEvent_t t_ev_before = nullptr;
@@ -54,6 +55,18 @@ const void* pinned_blob(const padoc_plan* P) {
     P->pin_status = (int)e;
   });
   return P->pinned ? P->pinned : P->blob.data();
+}
+
+// The plan's backward schedule in pinned host memory (made once per plan).
+const void* pinned_bwd_blob(const padoc_plan* P) {
+  std::call_once(P->bpin_once, [P] {
+    void* h = nullptr;
+    if (hipHostMalloc(&h, P->bwd_blob.size(), hipHostMallocDefault) == hipSuccess) {
+      std::memcpy(h, P->bwd_blob.data(), P->bwd_blob.size());
+      P->bpinned = h;
+    }
+  });
+  return P->bpinned ? P->bpinned : P->bwd_blob.data();
 }
 
 padoc_status run(const padoc_plan* P, const void* q, const void* k, const void* v, const int32_t* bt, void* o,
@@ -154,9 +167,78 @@ extern "C" padoc_status padoc_branch_decode(const padoc_plan* plan, const void* 
   return run(plan, q, k_cache, v_cache, block_table, o, lse, workspace, stream);
 }
 
+extern "C" padoc_status padoc_tree_attn_bwd(const padoc_plan* plan, const void* q, const void* k, const void* v,
+                                            const void* o, const float* lse, const void* dout, void* dq, void* dk,
+                                            void* dv, void* workspace, size_t workspace_bytes, hipStream_t stream) {
+  clear_error();
+  if (!plan) return set_error(PADOC_ERR_ARG, "plan is null");
+  if (plan->kind != 0)
+    return set_error(PADOC_ERR_MODE, "the backward needs a packed plan (block_size 0)");
+  if (plan->dtype != PADOC_BF16) return set_error(PADOC_ERR_DTYPE, "the backward supports bf16 plans only");
+  if (!workspace) return set_error(PADOC_ERR_WORKSPACE, "workspace is null");
+  if (((uintptr_t)workspace) & 255) return set_error(PADOC_ERR_WORKSPACE, "workspace must be 256-byte aligned");
+  if (workspace_bytes < plan->bws_bytes)
+    return set_error(PADOC_ERR_WORKSPACE, "workspace of %zu bytes is smaller than the %zu the backward needs",
+                     workspace_bytes, plan->bws_bytes);
+  const bool any_q = plan->num_q_rows > 0, any_kv = plan->num_kv_rows > 0;
+  if ((any_q && (!q || !o || !lse || !dout || !dq)) || (any_kv && (!k || !v || !dk || !dv)))
+    return set_error(PADOC_ERR_ARG, "a tensor pointer is null");
+  if (((uintptr_t)q | (uintptr_t)k | (uintptr_t)v | (uintptr_t)o | (uintptr_t)dout | (uintptr_t)dq |
+       (uintptr_t)dk | (uintptr_t)dv) & 15)
+    return set_error(PADOC_ERR_ARG, "q, k, v, o, dout, dq, dk and dv must be 16-byte aligned");
+  if (((uintptr_t)lse) & 3) return set_error(PADOC_ERR_ARG, "lse must be 4-byte aligned");
+  if (!any_q && !any_kv) return PADOC_OK;
+  char* ws = static_cast<char*>(workspace);
+  hipError_t e = hipSuccess;
+  if (!plan->blob.empty()) e = hipMemcpyAsync(ws, pinned_blob(plan), plan->blob.size(), hipMemcpyHostToDevice, stream);
+  if (e == hipSuccess && !plan->bwd_blob.empty())
+    e = hipMemcpyAsync(ws + plan->bws_off_blob, pinned_bwd_blob(plan), plan->bwd_blob.size(), hipMemcpyHostToDevice,
+                       stream);
+  if (e != hipSuccess) return hip_fail("hipMemcpyAsync(schedule)", e);
+  BwdParams bp{};
+  bp.q = q;
+  bp.k = k;
+  bp.v = v;
+  bp.o = o;
+  bp.lse = lse;
+  bp.dout = dout;
+  bp.dq = dq;
+  bp.dk = dk;
+  bp.dv = dv;
+  bp.dd = reinterpret_cast<float*>(ws + plan->bws_off_dd);
+  bp.dk_acc = reinterpret_cast<float*>(ws + plan->bws_off_dk);
+  bp.dv_acc = reinterpret_cast<float*>(ws + plan->bws_off_dv);
+  bp.work = at<WorkRec>(ws, plan->off_work);
+  bp.ranges = at<RangeRec>(ws, plan->off_ranges);
+  bp.lims = at<int32_t>(ws, plan->off_lims);
+  bp.toks = at<int32_t>(ws, plan->off_toks);
+  bp.bwd = at<BwdRec>(ws, plan->bws_off_blob + plan->boff_bwd);
+  bp.btoks = at<int32_t>(ws, plan->bws_off_blob + plan->boff_btoks);
+  bp.blims = at<int32_t>(ws, plan->bws_off_blob + plan->boff_blims);
+  bp.n_q = plan->num_q_rows;
+  bp.T = plan->num_kv_rows;
+  bp.Hq = plan->Hq;
+  bp.Hkv = plan->Hkv;
+  bp.G = plan->G;
+  bp.scale = plan->scale;
+  bp.scale_log2 = plan->scale * 1.4426950408889634f;
+  if (t_ev_before && t_ev_after) {
+    e = hipEventRecord(t_ev_before, stream);
+    if (e != hipSuccess) return hip_fail("hipEventRecord", e);
+  }
+  e = launch_tree_attn_bwd(bp, (int)plan->work.size(), (int)plan->bwd.size(), plan->D, stream);
+  if (e != hipSuccess) return hip_fail("backward kernel launch", e);
+  if (t_ev_before && t_ev_after) {
+    e = hipEventRecord(t_ev_after, stream);
+    if (e != hipSuccess) return hip_fail("hipEventRecord", e);
+  }
+  return PADOC_OK;
+}
+
 extern "C" void padoc_plan_destroy(padoc_plan* plan) {
   if (!plan) return;
   if (plan->pinned) (void)hipHostFree(plan->pinned);
+  if (plan->bpinned) (void)hipHostFree(plan->bpinned);
   delete plan;
 }
 

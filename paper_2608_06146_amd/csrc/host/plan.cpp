@@ -292,6 +292,64 @@ void build_forward(padoc_plan& P, Builder& B) {
   }
 }
 
+// Backward (packed bf16): key-major items.  For each segment t and each run of
+// up to kBwdKeys of its keys [kb, kb+nk), the query tokens that see any of
+// them: t's own queries at positions p >= kb (they see keys <= p), and every
+// query of every descendant s whose fork offset into t, F(s, t), exceeds kb
+// (they see keys < F).  Each token's limit is stored relative to kb and
+// clipped to nk.  The tokens' columns (token x head) are cut into items of
+// at most kBwdCols columns per KV head; items of one key run add into the
+// same dK/dV rows.
+void build_backward(padoc_plan& P, const std::vector<std::vector<std::pair<int32_t, int32_t>>>& anc) {
+  const int32_t n = (int32_t)P.seg.size();
+  std::vector<std::vector<std::pair<int32_t, int32_t>>> desc(n);  // (s, F(s, t)) per t
+  for (int32_t s = 0; s < n; ++s)
+    for (const auto& a : anc[s]) desc[a.first].push_back({s, a.second});
+  auto qrow = [&](int32_t s, int32_t p) {
+    const padoc_segment& sg = P.seg[s];
+    return (int32_t)(sg.q_off + (p - (sg.len - sg.q_len)));
+  };
+  for (int32_t t = 0; t < n; ++t) {
+    const padoc_segment& tg = P.seg[t];
+    for (int32_t kb = 0; kb < tg.len; kb += kBwdKeys) {
+      const int32_t nk = std::min(kBwdKeys, tg.len - kb);
+      const int32_t tok_begin = (int32_t)P.btoks.size(), lim_begin = (int32_t)P.blims.size();
+      for (int32_t p = std::max(kb, tg.len - tg.q_len); p < tg.len; ++p) {
+        P.btoks.push_back(qrow(t, p));
+        P.blims.push_back(std::min(p + 1 - kb, nk));
+      }
+      for (const auto& d : desc[t]) {
+        const padoc_segment& sg = P.seg[d.first];
+        if (d.second <= kb || sg.q_len == 0) continue;
+        for (int32_t p = sg.len - sg.q_len; p < sg.len; ++p) {
+          P.btoks.push_back(qrow(d.first, p));
+          P.blims.push_back(std::min(d.second - kb, nk));
+        }
+      }
+      const int32_t ntok = (int32_t)P.btoks.size() - tok_begin;
+      if (ntok == 0) continue;
+      const int64_t cols = (int64_t)ntok * P.G;
+      for (int64_t c0 = 0; c0 < cols; c0 += kBwdCols) {
+        for (int32_t g = 0; g < P.Hkv; ++g) {
+          padoc::BwdRec b{};
+          b.key_row0 = tg.kv_off + kb;
+          b.n_keys = nk;
+          b.tok_begin = tok_begin;
+          b.ntok = ntok;
+          b.lim_begin = lim_begin;
+          b.col0 = (int32_t)c0;
+          b.ncol = (int32_t)std::min<int64_t>(kBwdCols, cols - c0);
+          b.kvh = g;
+          b.cost = (int32_t)ceil_div(b.ncol, 32);
+          P.bwd.push_back(b);
+        }
+      }
+    }
+  }
+  std::stable_sort(P.bwd.begin(), P.bwd.end(),
+                   [](const padoc::BwdRec& a, const padoc::BwdRec& b) { return a.cost > b.cost; });
+}
+
 // Decode.  A segment is shared when a query token of another segment sees
 // any of it (page prefix, layout stream), private otherwise (a branch seen
 // only by its own queries).  Shared keys are processed by the matrix-core
@@ -467,6 +525,26 @@ void put(std::vector<unsigned char>& blob, size_t off, const std::vector<T>& v) 
   if (!v.empty()) std::memcpy(blob.data() + off, v.data(), v.size() * sizeof(T));
 }
 
+// Backward workspace: the forward schedule (dQ items), the backward
+// schedule, then sum(dO * O) per (row, head) and the fp32 dK / dV
+// accumulators.
+void serialise_backward(padoc_plan& P) {
+  P.boff_bwd = 0;
+  P.boff_btoks = align256(P.boff_bwd + P.bwd.size() * sizeof(padoc::BwdRec));
+  P.boff_blims = align256(P.boff_btoks + P.btoks.size() * 4);
+  const size_t bytes = P.boff_blims + P.blims.size() * 4;
+  P.bwd_blob.assign(bytes, 0);
+  put(P.bwd_blob, P.boff_bwd, P.bwd);
+  put(P.bwd_blob, P.boff_btoks, P.btoks);
+  put(P.bwd_blob, P.boff_blims, P.blims);
+  P.bws_off_blob = align256(P.blob.size());
+  P.bws_off_dd = align256(P.bws_off_blob + bytes);
+  P.bws_off_dk = align256(P.bws_off_dd + (size_t)P.num_q_rows * P.Hq * 4);
+  const size_t acc = (size_t)P.num_kv_rows * P.Hkv * P.D * 4;
+  P.bws_off_dv = align256(P.bws_off_dk + acc);
+  P.bws_bytes = std::max<size_t>(256, align256(P.bws_off_dv + acc));
+}
+
 void serialise(padoc_plan& P) {
   P.off_work = 0;
   P.off_ranges = align256(P.off_work + P.work.size() * sizeof(padoc::WorkRec));
@@ -586,6 +664,12 @@ extern "C" padoc_status padoc_plan_create(const padoc_tree_desc* d, padoc_plan**
       std::stable_sort(P->work.begin(), P->work.end(),
                        [](const padoc::WorkRec& a, const padoc::WorkRec& b) { return a.cost > b.cost; });
     serialise(*P);
+    if (P->kind == 0 && P->dtype == PADOC_BF16) {
+      build_backward(*P, anc);
+      if ((int64_t)P->btoks.size() > kI32Max || (int64_t)P->bwd.size() > kI32Max)
+        return set_error(PADOC_ERR_ARG, "backward schedule too large");
+      serialise_backward(*P);
+    }
     *out = P.release();
   } catch (const std::bad_alloc&) {
     return set_error(PADOC_ERR_ARG, "out of host memory while planning");
@@ -597,6 +681,15 @@ extern "C" padoc_status padoc_plan_workspace_bytes(const padoc_plan* plan, size_
   clear_error();
   if (!plan || !bytes) return set_error(PADOC_ERR_ARG, "null argument");
   *bytes = plan->ws_bytes;
+  return PADOC_OK;
+}
+
+extern "C" padoc_status padoc_plan_backward_workspace_bytes(const padoc_plan* plan, size_t* bytes) {
+  clear_error();
+  if (!plan || !bytes) return set_error(PADOC_ERR_ARG, "null argument");
+  if (plan->kind != 0) return set_error(PADOC_ERR_MODE, "the backward needs a packed plan (block_size 0)");
+  if (plan->dtype != PADOC_BF16) return set_error(PADOC_ERR_DTYPE, "the backward supports bf16 plans only");
+  *bytes = plan->bws_bytes;
   return PADOC_OK;
 }
 
@@ -625,6 +718,12 @@ extern "C" padoc_status padoc_plan_export(const padoc_plan* P, padoc_schedule_vi
   v->comb_slot = P->comb_slot.data();
   v->n_comb_rows = (int64_t)P->comb_rows.size();
   v->comb_rows = P->comb_rows.data();
+  v->n_bwd = (int32_t)P->bwd.size();
+  v->bwd = P->bwd.data();
+  v->n_btok = (int64_t)P->btoks.size();
+  v->btoks = P->btoks.data();
+  v->n_blim = (int64_t)P->blims.size();
+  v->blims = P->blims.data();
   v->n_slots = P->n_slots;
   v->workspace_bytes = P->ws_bytes;
   return PADOC_OK;

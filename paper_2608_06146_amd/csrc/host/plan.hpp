@@ -36,6 +36,15 @@ struct padoc_plan {
   std::vector<int32_t> comb_rows;  // (row*Hkv + kvh) pairs the combine kernel merges
   int64_t n_slots = 0;
 
+  // Backward (packed bf16 plans): key-major items and their token lists.
+  std::vector<padoc::BwdRec> bwd;
+  std::vector<int32_t> btoks, blims;
+  std::vector<unsigned char> bwd_blob;  // bwd, btoks, blims (uploaded by padoc_tree_attn_bwd)
+  size_t boff_bwd = 0, boff_btoks = 0, boff_blims = 0;
+  size_t bws_off_blob = 0, bws_off_dd = 0, bws_off_dk = 0, bws_off_dv = 0, bws_bytes = 0;
+  mutable std::once_flag bpin_once;
+  mutable void* bpinned = nullptr;
+
   // Serialised schedule (uploaded into the workspace before every launch).
   std::vector<unsigned char> blob;
   size_t off_work = 0, off_ranges = 0, off_lims = 0, off_toks = 0;

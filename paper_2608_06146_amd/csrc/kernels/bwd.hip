@@ -1,0 +1,479 @@
+// Backward of the packed tree forward (bf16, gfx950 matrix cores).
+//
+// The gradient of sum(dO * O) with O = softmax(scale * q K^T + A_M) V over
+// each query's visible keys (App. E Attn equation with the ancestor mask;
+// App. C tree-varlen relation, the backend the paper trains with), written
+// per query row i and visible key j:
+//   P_ij  = exp(scale q_i.k_j - LSE_i)      (recomputed from the forward LSE)
+//   dV_j  = sum_i P_ij dO_i
+//   dP_ij = dO_i . v_j,   D_i = dO_i . O_i
+//   dS_ij = P_ij (dP_ij - D_i)
+//   dQ_i  = scale sum_j dS_ij k_j,   dK_j = scale sum_i dS_ij q_i
+// Four kernels:
+//   bwd_prep   D per (row, head); zero the fp32 dK / dV accumulators
+//   bwd_dq     query-major: the forward's work items (256 columns x the
+//              item's key ranges); per 64-key tile S^T, dP^T, dS^T and
+//              dQ^T += K^T dS^T; dQ is complete per item and written directly
+//   bwd_dkdv   key-major: up to 128 keys of one segment against the query
+//              columns that see them, 32 columns per step; waves 0-3 compute
+//              dV^T += dO^T P for 32 keys each, waves 4-7 dK^T += Q^T dS for
+//              the same keys; results are added into fp32 accumulators
+//   bwd_finalize  fp32 accumulators -> bf16 dK, dV (round to nearest even)
+// All products are v_mfma_f32_32x32x16_bf16 with fp32 accumulation.  The
+// operand whose contraction index is not contiguous in memory (K^T for dQ,
+// dO^T and Q^T for dV and dK) is staged transposed in LDS with the column
+// permutation that makes a lane's 8 values one 16-byte read against the
+// matrix-core layout of the probabilities (the same permutation as the
+// forward's V^T).
+#include <algorithm>
+
+#include "device_common.hpp"
+
+namespace padoc {
+
+namespace {
+
+typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
+typedef float f32x16_t __attribute__((ext_vector_type(16)));
+
+constexpr int kThreads = 512;
+constexpr float kLog2e = 1.4426950408889634f;
+
+__device__ __forceinline__ bf16x8_t as_bf16x8(const uint4& u) { return *reinterpret_cast<const bf16x8_t*>(&u); }
+
+// Position of column / key r inside a transposed row (see the file comment).
+__device__ __forceinline__ int perm_pos(int r) {
+  const int q = r & 15;
+  return (r & ~15) + ((q >> 2) & 1) * 8 + (q >> 3) * 4 + (q & 3);
+}
+
+// ------------------------------------------------------------------ prep
+
+template <int D>
+__global__ __launch_bounds__(256) void bwd_prep_kernel(BwdParams p, int64_t n_rows, int64_t n_acc4) {
+  const int lane = threadIdx.x & 63;
+  const int64_t nwaves = (int64_t)gridDim.x * 4;
+  for (int64_t r = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6); r < n_rows; r += nwaves) {
+    const uint16_t* o = static_cast<const uint16_t*>(p.o) + r * D;
+    const uint16_t* g = static_cast<const uint16_t*>(p.dout) + r * D;
+    float acc = 0.f;
+#pragma unroll
+    for (int e = lane; e < D; e += 64) acc = fmaf(bf16_bits_to_f32(o[e]), bf16_bits_to_f32(g[e]), acc);
+#pragma unroll
+    for (int m = 32; m >= 1; m >>= 1) acc += __shfl_xor(acc, m);
+    if (lane == 0) p.dd[r] = acc;
+  }
+  const int64_t nth = (int64_t)gridDim.x * 256;
+  for (int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x; i < n_acc4; i += nth) {
+    reinterpret_cast<float4*>(p.dk_acc)[i] = make_float4(0.f, 0.f, 0.f, 0.f);
+    reinterpret_cast<float4*>(p.dv_acc)[i] = make_float4(0.f, 0.f, 0.f, 0.f);
+  }
+}
+
+// ------------------------------------------------------------------ dQ
+
+template <int D>
+__global__ __launch_bounds__(kThreads) void bwd_dq_kernel(BwdParams p) {
+  constexpr int KT = kTileKeys;  // 64 keys per tile
+  constexpr int KS = D + 8;      // row stride of the row-major K and V tiles
+  constexpr int TS = KT + 8;     // row stride of the transposed K tile
+  constexpr int NKK = D / 16;
+  constexpr int NDB = D / 32;
+  constexpr int CPR = D / 8;
+  constexpr int KPT = KT * CPR / kThreads;  // row pieces per thread (2 or 1)
+
+  __shared__ __attribute__((aligned(16))) uint16_t Ks[KT * KS];
+  __shared__ __attribute__((aligned(16))) uint16_t Vs[KT * KS];
+  __shared__ __attribute__((aligned(16))) uint16_t Kt[D * TS];
+
+  const WorkRec w = p.work[blockIdx.x];
+  if (w.rng_count <= 0) return;
+  const int tid = threadIdx.x;
+  const int wave = tid >> 6, lane = tid & 63, l32 = lane & 31, hf = lane >> 5;
+  const int G = p.G, kvh = w.kvh;
+  const int64_t Hkv = p.Hkv;
+  const int col = wave * 32 + l32;
+  const int tok = col / G;
+  const bool valid = tok < w.ntok;
+  const int32_t qrow = valid ? p.toks[w.tok_begin + tok] : 0;
+  const int32_t hq = kvh * G + (col - tok * G);
+  const int64_t qoff = ((int64_t)qrow * p.Hq + hq) * D;
+
+  bf16x8_t bq[NKK], bdo[NKK];
+  {
+    const uint16_t* qp = static_cast<const uint16_t*>(p.q) + qoff + hf * 8;
+    const uint16_t* gp = static_cast<const uint16_t*>(p.dout) + qoff + hf * 8;
+#pragma unroll
+    for (int kk = 0; kk < NKK; ++kk) {
+      bq[kk] = as_bf16x8(valid ? load16(qp + kk * 16) : make_uint4(0, 0, 0, 0));
+      bdo[kk] = as_bf16x8(valid ? load16(gp + kk * 16) : make_uint4(0, 0, 0, 0));
+    }
+  }
+  const float lse2 = valid ? p.lse[(int64_t)qrow * p.Hq + hq] * kLog2e : 0.f;
+  const float dcol = valid ? p.dd[(int64_t)qrow * p.Hq + hq] : 0.f;
+  const float sl2 = p.scale_log2;
+
+  const uint16_t* Kg = static_cast<const uint16_t*>(p.k);
+  const uint16_t* Vg = static_cast<const uint16_t*>(p.v);
+  // row pieces (key, 16-byte chunk) and key pairs for the transposed K tile
+  int r_key[KPT], r_dc[KPT];
+#pragma unroll
+  for (int i = 0; i < KPT; ++i) {
+    const int u = tid + kThreads * i;
+    r_key[i] = u / CPR;
+    r_dc[i] = u % CPR;
+  }
+  const int t_pr = tid % (KT / 2), t_dc = (tid / (KT / 2)) % CPR;
+  const bool t_on = tid / (KT / 2) < CPR;
+
+  struct Cursor {
+    int ri, kt;
+    RangeRec R;
+    int ok, unused;
+  };
+  auto advance = [&](Cursor& c) {
+    if (++c.kt * KT >= c.R.n_keys) {
+      c.kt = 0;
+      if (++c.ri < w.rng_count)
+        c.R = p.ranges[w.rng_begin + c.ri];
+      else
+        c.ok = 0;
+    }
+  };
+  uint4 kr[KPT], vr[KPT], tr[2];
+  // Tile loads: rows past the range end repeat its last row (finite values
+  // whose scores the mask removes).
+  auto load = [&](const Cursor& c) {
+    const int kbase = c.kt * KT, last = c.R.n_keys - 1 - kbase;
+    const int64_t row0 = c.R.kv_start + kbase;
+#pragma unroll
+    for (int i = 0; i < KPT; ++i) {
+      const int kc = r_key[i] <= last ? r_key[i] : last;
+      const int64_t off = ((row0 + kc) * Hkv + kvh) * D + r_dc[i] * 8;
+      kr[i] = load16(Kg + off);
+      vr[i] = load16(Vg + off);
+    }
+    const int k0 = 2 * t_pr, k1 = k0 + 1;
+    const int c0 = k0 <= last ? k0 : last, c1 = k1 <= last ? k1 : last;
+    tr[0] = load16(Kg + ((row0 + c0) * Hkv + kvh) * D + t_dc * 8);
+    tr[1] = load16(Kg + ((row0 + c1) * Hkv + kvh) * D + t_dc * 8);
+  };
+  auto store = [&]() {
+#pragma unroll
+    for (int i = 0; i < KPT; ++i) {
+      store16(&Ks[r_key[i] * KS + r_dc[i] * 8], kr[i]);
+      store16(&Vs[r_key[i] * KS + r_dc[i] * 8], vr[i]);
+    }
+    if (t_on) {
+      const int pos = perm_pos(2 * t_pr);
+      const uint32_t a[4] = {tr[0].x, tr[0].y, tr[0].z, tr[0].w};
+      const uint32_t b[4] = {tr[1].x, tr[1].y, tr[1].z, tr[1].w};
+#pragma unroll
+      for (int m = 0; m < 4; ++m) {
+        *reinterpret_cast<uint32_t*>(&Kt[(t_dc * 8 + 2 * m) * TS + pos]) = __builtin_amdgcn_perm(b[m], a[m], 0x05040100u);
+        *reinterpret_cast<uint32_t*>(&Kt[(t_dc * 8 + 2 * m + 1) * TS + pos]) =
+            __builtin_amdgcn_perm(b[m], a[m], 0x07060302u);
+      }
+    }
+  };
+  auto lim_of = [&](const RangeRec& R) -> int {
+    return R.lim_off < 0 ? R.n_keys : (valid ? p.lims[R.lim_off + tok] : 0);
+  };
+
+  f32x16_t acc[NDB];
+#pragma unroll
+  for (int db = 0; db < NDB; ++db)
+#pragma unroll
+    for (int i = 0; i < 16; ++i) acc[db][i] = 0.f;
+
+  Cursor C{0, 0, p.ranges[w.rng_begin], 1, 0};
+  Cursor L = C;
+  load(L);
+  advance(L);
+  int lim = lim_of(C.R);
+  for (;;) {
+    store();
+    __syncthreads();
+    if (L.ok) load(L);  // next tile, in flight during this one
+    const int kb = C.kt * KT;
+    const bool partial = kb + KT > C.R.min_lim;
+    const int rel = lim - kb - hf * 4;
+#pragma unroll
+    for (int mb = 0; mb < 2; ++mb) {
+      f32x16_t S, dP;
+#pragma unroll
+      for (int i = 0; i < 16; ++i) {
+        S[i] = 0.f;
+        dP[i] = 0.f;
+      }
+#pragma unroll
+      for (int kk = 0; kk < NKK; ++kk) {
+        const int off = (mb * 32 + l32) * KS + kk * 16 + hf * 8;
+        S = __builtin_amdgcn_mfma_f32_32x32x16_bf16(*reinterpret_cast<const bf16x8_t*>(&Ks[off]), bq[kk], S, 0, 0, 0);
+        dP = __builtin_amdgcn_mfma_f32_32x32x16_bf16(*reinterpret_cast<const bf16x8_t*>(&Vs[off]), bdo[kk], dP, 0, 0, 0);
+      }
+      // element i: key mb*32 + (i/4)*8 + hf*4 + i%4 of the tile, this lane's column
+      bf16x8_t ds[2];
+#pragma unroll
+      for (int i = 0; i < 16; ++i) {
+        const bool vis = !partial || mb * 32 + (i >> 2) * 8 + (i & 3) < rel;
+        const float pr = vis ? fast_exp2(fmaf(S[i], sl2, -lse2)) : 0.f;
+        ds[i >> 3][i & 7] = (__bf16)(pr * (dP[i] - dcol));
+      }
+#pragma unroll
+      for (int j = 0; j < 2; ++j)
+#pragma unroll
+        for (int db = 0; db < NDB; ++db) {
+          const bf16x8_t a =
+              *reinterpret_cast<const bf16x8_t*>(&Kt[(db * 32 + l32) * TS + mb * 32 + 16 * j + hf * 8]);
+          acc[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, ds[j], acc[db], 0, 0, 0);
+        }
+    }
+    __syncthreads();
+    const int ri_before = C.ri;
+    advance(C);
+    if (!C.ok) break;
+    if (C.ri != ri_before) lim = lim_of(C.R);
+    advance(L);
+  }
+
+  if (!valid) return;
+  const float sc = p.scale;
+  uint16_t* op = static_cast<uint16_t*>(p.dq) + qoff;
+#pragma unroll
+  for (int db = 0; db < NDB; ++db)
+#pragma unroll
+    for (int i4 = 0; i4 < 4; ++i4) {
+      const int d0 = db * 32 + i4 * 8 + hf * 4;
+      uint2 pk;
+      pk.x = (uint32_t)f32_to_bf16_bits(acc[db][4 * i4] * sc) | ((uint32_t)f32_to_bf16_bits(acc[db][4 * i4 + 1] * sc) << 16);
+      pk.y = (uint32_t)f32_to_bf16_bits(acc[db][4 * i4 + 2] * sc) |
+             ((uint32_t)f32_to_bf16_bits(acc[db][4 * i4 + 3] * sc) << 16);
+      *reinterpret_cast<uint2*>(op + d0) = pk;
+    }
+}
+
+// ------------------------------------------------------------------ dK, dV
+
+template <int D>
+__global__ __launch_bounds__(kThreads) void bwd_dkdv_kernel(BwdParams p) {
+  constexpr int QS = D + 8;   // row stride of the row-major Q / dO blocks
+  constexpr int TS = 32 + 8;  // row stride of the transposed blocks
+  constexpr int NKK = D / 16;
+  constexpr int NDB = D / 32;
+  constexpr int CPR = D / 8;
+
+  __shared__ __attribute__((aligned(16))) uint16_t Qs[32 * QS];
+  __shared__ __attribute__((aligned(16))) uint16_t Gs[32 * QS];
+  __shared__ __attribute__((aligned(16))) uint16_t Qt[D * TS];
+  __shared__ __attribute__((aligned(16))) uint16_t Gt[D * TS];
+  __shared__ __attribute__((aligned(16))) float Ls[32];  // LSE * log2(e)
+  __shared__ __attribute__((aligned(16))) float Dd[32];  // dO . O
+  __shared__ __attribute__((aligned(16))) int Lm[32];    // visible keys of the item
+
+  const BwdRec b = p.bwd[blockIdx.x];
+  const int tid = threadIdx.x;
+  const int wave = tid >> 6, lane = tid & 63, l32 = lane & 31, hf = lane >> 5;
+  const bool kwave = wave >= 4;          // waves 4-7: dK; 0-3: dV
+  const int key = (wave & 3) * 32 + l32;  // this lane's key within the item
+  const int G = p.G, kvh = b.kvh;
+  const int64_t Hkv = p.Hkv;
+
+  // B operands of S = Q K^T and dP = dO V^T: this lane's key, d = kk*16 + hf*8 ..
+  bf16x8_t bk[NKK], bv[NKK];
+  {
+    const int kc = key < b.n_keys ? key : b.n_keys - 1;
+    const int64_t off = ((b.key_row0 + kc) * Hkv + kvh) * D + hf * 8;
+#pragma unroll
+    for (int kk = 0; kk < NKK; ++kk) {
+      bk[kk] = as_bf16x8(load16(static_cast<const uint16_t*>(p.k) + off + kk * 16));
+      bv[kk] = as_bf16x8(kwave ? load16(static_cast<const uint16_t*>(p.v) + off + kk * 16) : make_uint4(0, 0, 0, 0));
+    }
+  }
+
+  // Staging geometry: thread -> (column, 16-byte chunk) of a 32-column block;
+  // with d = 64 the upper half of the threads repeats the lower half's loads
+  // and stores nothing.
+  const int s_col = (tid / CPR) % 32, s_dc = tid % CPR;
+  const bool s_on = tid < 32 * CPR;
+  uint4 qr, gr;
+  float lr = 0.f, dr = 0.f;
+  int mr = 0;
+  auto load = [&](int c0) {
+    const int cabs = c0 + s_col;
+    const bool ok = cabs < b.col0 + b.ncol;
+    const int t = cabs / G;
+    const int32_t row = ok ? p.btoks[b.tok_begin + t] : 0;
+    const int64_t off = ((int64_t)row * p.Hq + kvh * G + (cabs - t * G)) * D + s_dc * 8;
+    qr = ok ? load16(static_cast<const uint16_t*>(p.q) + off) : make_uint4(0, 0, 0, 0);
+    gr = ok ? load16(static_cast<const uint16_t*>(p.dout) + off) : make_uint4(0, 0, 0, 0);
+    if (tid < 32) {  // per-column scalars of column tid
+      const int cc = c0 + tid;
+      const bool okc = cc < b.col0 + b.ncol;
+      const int tc = cc / G;
+      const int32_t rc = okc ? p.btoks[b.tok_begin + tc] : 0;
+      const int64_t li = (int64_t)rc * p.Hq + kvh * G + (cc - tc * G);
+      lr = okc ? p.lse[li] * kLog2e : 0.f;
+      dr = okc ? p.dd[li] : 0.f;
+      mr = okc ? p.blims[b.lim_begin + tc] : 0;
+    }
+  };
+  auto store = [&]() {
+    if (s_on) {
+      store16(&Qs[s_col * QS + s_dc * 8], qr);
+      store16(&Gs[s_col * QS + s_dc * 8], gr);
+      const int pos = perm_pos(s_col);
+      const uint32_t a[4] = {qr.x, qr.y, qr.z, qr.w};
+      const uint32_t g[4] = {gr.x, gr.y, gr.z, gr.w};
+#pragma unroll
+      for (int m = 0; m < 4; ++m) {
+        Qt[(s_dc * 8 + 2 * m) * TS + pos] = (uint16_t)(a[m] & 0xffffu);
+        Qt[(s_dc * 8 + 2 * m + 1) * TS + pos] = (uint16_t)(a[m] >> 16);
+        Gt[(s_dc * 8 + 2 * m) * TS + pos] = (uint16_t)(g[m] & 0xffffu);
+        Gt[(s_dc * 8 + 2 * m + 1) * TS + pos] = (uint16_t)(g[m] >> 16);
+      }
+    }
+    if (tid < 32) {
+      Ls[tid] = lr;
+      Dd[tid] = dr;
+      Lm[tid] = mr;
+    }
+  };
+
+  f32x16_t acc[NDB];
+#pragma unroll
+  for (int db = 0; db < NDB; ++db)
+#pragma unroll
+    for (int i = 0; i < 16; ++i) acc[db][i] = 0.f;
+  const float sl2 = p.scale_log2;
+
+  const int c_end = b.col0 + b.ncol;
+  load(b.col0);
+  for (int c0 = b.col0; c0 < c_end; c0 += 32) {
+    store();
+    __syncthreads();
+    if (c0 + 32 < c_end) load(c0 + 32);  // next block, in flight during this one
+
+    // S = Q K^T: columns on M, this wave's 32 keys on N.  Element i of a lane
+    // is column (i/4)*8 + hf*4 + i%4 of the block and key `key`.
+    f32x16_t S;
+#pragma unroll
+    for (int i = 0; i < 16; ++i) S[i] = 0.f;
+#pragma unroll
+    for (int kk = 0; kk < NKK; ++kk)
+      S = __builtin_amdgcn_mfma_f32_32x32x16_bf16(*reinterpret_cast<const bf16x8_t*>(&Qs[l32 * QS + kk * 16 + hf * 8]),
+                                                  bk[kk], S, 0, 0, 0);
+    float pr[16];
+#pragma unroll
+    for (int q4 = 0; q4 < 4; ++q4) {
+      const int cb = q4 * 8 + hf * 4;  // columns cb .. cb+3 = elements 4*q4 .. 4*q4+3
+      const float4 l4 = *reinterpret_cast<const float4*>(&Ls[cb]);
+      const int4 m4 = *reinterpret_cast<const int4*>(&Lm[cb]);
+      const float lv[4] = {l4.x, l4.y, l4.z, l4.w};
+      const int mv[4] = {m4.x, m4.y, m4.z, m4.w};
+#pragma unroll
+      for (int e = 0; e < 4; ++e) pr[4 * q4 + e] = key < mv[e] ? fast_exp2(fmaf(S[4 * q4 + e], sl2, -lv[e])) : 0.f;
+    }
+    if (!kwave) {
+      // dV^T += dO^T P: d on M (block db), keys on N, columns on K
+#pragma unroll
+      for (int j = 0; j < 2; ++j) {
+        bf16x8_t pb;
+#pragma unroll
+        for (int e = 0; e < 8; ++e) pb[e] = (__bf16)pr[8 * j + e];
+#pragma unroll
+        for (int db = 0; db < NDB; ++db) {
+          const bf16x8_t a = *reinterpret_cast<const bf16x8_t*>(&Gt[(db * 32 + l32) * TS + 16 * j + hf * 8]);
+          acc[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, pb, acc[db], 0, 0, 0);
+        }
+      }
+    } else {
+      // dP = dO V^T; dS = P (dP - D); dK^T += Q^T dS
+      f32x16_t dP;
+#pragma unroll
+      for (int i = 0; i < 16; ++i) dP[i] = 0.f;
+#pragma unroll
+      for (int kk = 0; kk < NKK; ++kk)
+        dP = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
+            *reinterpret_cast<const bf16x8_t*>(&Gs[l32 * QS + kk * 16 + hf * 8]), bv[kk], dP, 0, 0, 0);
+      float dsv[16];
+#pragma unroll
+      for (int q4 = 0; q4 < 4; ++q4) {
+        const float4 d4 = *reinterpret_cast<const float4*>(&Dd[q4 * 8 + hf * 4]);
+        const float dv[4] = {d4.x, d4.y, d4.z, d4.w};
+#pragma unroll
+        for (int e = 0; e < 4; ++e) dsv[4 * q4 + e] = pr[4 * q4 + e] * (dP[4 * q4 + e] - dv[e]);
+      }
+#pragma unroll
+      for (int j = 0; j < 2; ++j) {
+        bf16x8_t sb;
+#pragma unroll
+        for (int e = 0; e < 8; ++e) sb[e] = (__bf16)dsv[8 * j + e];
+#pragma unroll
+        for (int db = 0; db < NDB; ++db) {
+          const bf16x8_t a = *reinterpret_cast<const bf16x8_t*>(&Qt[(db * 32 + l32) * TS + 16 * j + hf * 8]);
+          acc[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, sb, acc[db], 0, 0, 0);
+        }
+      }
+    }
+    __syncthreads();
+  }
+
+  if (key >= b.n_keys) return;
+  // acc[db] element i: d = db*32 + (i/4)*8 + hf*4 + i%4, key `key`
+  float* dst = (kwave ? p.dk_acc : p.dv_acc) + ((b.key_row0 + key) * Hkv + kvh) * D;
+  const float sc = kwave ? p.scale : 1.f;
+#pragma unroll
+  for (int db = 0; db < NDB; ++db)
+#pragma unroll
+    for (int i = 0; i < 16; ++i) atomicAdd(dst + db * 32 + (i >> 2) * 8 + hf * 4 + (i & 3), acc[db][i] * sc);
+}
+
+// ------------------------------------------------------------------ finalize
+
+__global__ __launch_bounds__(256) void bwd_finalize_kernel(BwdParams p, int64_t n4) {
+  const int64_t nth = (int64_t)gridDim.x * 256;
+  for (int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x; i < n4; i += nth) {
+    const float4 a = reinterpret_cast<const float4*>(p.dk_acc)[i];
+    const float4 c = reinterpret_cast<const float4*>(p.dv_acc)[i];
+    uint2 ka, va;
+    ka.x = (uint32_t)f32_to_bf16_bits(a.x) | ((uint32_t)f32_to_bf16_bits(a.y) << 16);
+    ka.y = (uint32_t)f32_to_bf16_bits(a.z) | ((uint32_t)f32_to_bf16_bits(a.w) << 16);
+    va.x = (uint32_t)f32_to_bf16_bits(c.x) | ((uint32_t)f32_to_bf16_bits(c.y) << 16);
+    va.y = (uint32_t)f32_to_bf16_bits(c.z) | ((uint32_t)f32_to_bf16_bits(c.w) << 16);
+    reinterpret_cast<uint2*>(p.dk)[i] = ka;
+    reinterpret_cast<uint2*>(p.dv)[i] = va;
+  }
+}
+
+}  // namespace
+
+hipError_t launch_tree_attn_bwd(const BwdParams& p, int n_work, int n_bwd, int D, hipStream_t stream) {
+  const int64_t n_rows = p.n_q * p.Hq;
+  const int64_t n_acc4 = p.T * p.Hkv * D / 4;
+  const int64_t want = (std::max(n_rows / 4, n_acc4 / 256) + 1);
+  const dim3 prep_grid((unsigned)std::min<int64_t>(want, 4096)), blk256(256), blk512(kThreads);
+  if (D == 64)
+    hipLaunchKernelGGL((bwd_prep_kernel<64>), prep_grid, blk256, 0, stream, p, n_rows, n_acc4);
+  else
+    hipLaunchKernelGGL((bwd_prep_kernel<128>), prep_grid, blk256, 0, stream, p, n_rows, n_acc4);
+  if (n_work > 0) {
+    if (D == 64)
+      hipLaunchKernelGGL((bwd_dq_kernel<64>), dim3(n_work), blk512, 0, stream, p);
+    else
+      hipLaunchKernelGGL((bwd_dq_kernel<128>), dim3(n_work), blk512, 0, stream, p);
+  }
+  if (n_bwd > 0) {
+    if (D == 64)
+      hipLaunchKernelGGL((bwd_dkdv_kernel<64>), dim3(n_bwd), blk512, 0, stream, p);
+    else
+      hipLaunchKernelGGL((bwd_dkdv_kernel<128>), dim3(n_bwd), blk512, 0, stream, p);
+  }
+  if (n_acc4 > 0) {
+    const dim3 fin_grid((unsigned)std::min<int64_t>(n_acc4 / 256 + 1, 4096));
+    hipLaunchKernelGGL(bwd_finalize_kernel, fin_grid, blk256, 0, stream, p, n_acc4);
+  }
+  return hipGetLastError();
+}
+
+}  // namespace padoc

@@ -13,14 +13,18 @@ namespace padoc {
 
 using WorkRec = padoc_work_view;    // 48 bytes
 using RangeRec = padoc_range_view;  // 32 bytes
+using BwdRec = padoc_bwd_view;      // 40 bytes
 static_assert(sizeof(WorkRec) == 48, "work record is 48 bytes");
 static_assert(sizeof(RangeRec) == 32, "range record is 32 bytes");
+static_assert(sizeof(BwdRec) == 40, "backward record is 40 bytes");
 
 // Key tile of every kernel (keys staged per step) and columns per work item.
 constexpr int kTileKeys = 64;
 constexpr int kTileCols = 256;
 constexpr int kBlock = 16;  // paged KV block (tokens)
 constexpr int kPrivateCols = 16;  // columns of a private decode item (one wavefront)
+constexpr int kBwdKeys = 128;     // keys of a backward key-major item (4 x 32)
+constexpr int kBwdCols = 1024;    // query columns per backward item (32 blocks of 32)
 
 // Everything a tile kernel needs.  Pointers are device pointers.
 struct TileParams {
@@ -40,6 +44,32 @@ struct TileParams {
   const int32_t* comb_slot;  // ... merged by items with fin = 1
   int32_t Hq, Hkv, G;
   float scale_log2;       // softmax_scale * log2(e)
+};
+
+// Backward of the packed forward (bf16).
+struct BwdParams {
+  const void* q;     // [n_q, Hq, D]
+  const void* k;     // [T, Hkv, D]
+  const void* v;
+  const void* o;     // [n_q, Hq, D]
+  const float* lse;  // [n_q, Hq]
+  const void* dout;  // [n_q, Hq, D]
+  void* dq;          // [n_q, Hq, D]
+  void* dk;          // [T, Hkv, D]
+  void* dv;
+  float* dd;         // workspace [n_q, Hq]: sum_d dout * o
+  float* dk_acc;     // workspace [T, Hkv, D] fp32
+  float* dv_acc;
+  const WorkRec* work;  // the forward's query-major items (dQ)
+  const RangeRec* ranges;
+  const int32_t* lims;
+  const int32_t* toks;
+  const BwdRec* bwd;    // key-major items (dK, dV)
+  const int32_t* btoks;
+  const int32_t* blims;
+  int64_t n_q, T;
+  int32_t Hq, Hkv, G;
+  float scale, scale_log2;
 };
 
 struct CombineParams {

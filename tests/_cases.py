@@ -130,3 +130,66 @@ def decode_case(pages_or_nodes, Hq, Hkv, d, dtype, seed, pool_extra=7, check=Tru
     O_ref, LSE_ref = oracle.tree_attention_paged(nodes, q, kc, vc, ids, 1.0 / math.sqrt(d), Hq, Hkv, 16, rows=rows)
     errs = compare(f"decode seed={seed}", o, lse, O_ref, LSE_ref, dtype, rows=rows)
     return o, lse, plan, errs
+
+
+# Backward tolerance.  Gradients have no unit scale (a prefix key's dK sums
+# over every query below it), so the stated bf16 bounds (max 1.5e-2, mean
+# 2e-3) are applied in units of the gradient's scale: for the max, the larger
+# of the tensor's RMS and the RMS of the element's own row (a key seen by
+# every query of a page sums thousands of terms, each carrying the half-ulp
+# bf16 rounding of its P or dS operand, so its error grows with its own
+# magnitude), plus one bf16 ulp of the element's value (2^-8 |g|: the output
+# is rounded to nearest-even after fp32 accumulation); for the mean, the
+# tensor's RMS.
+BWD_TOL = (1.5e-2, 2e-3)
+BWD_ULP = 2.0 ** -8
+
+
+def backward_case(pages_or_nodes, Hq, Hkv, d, seed, device="cuda", check=True):
+    """Packed forward then backward on seeded bf16 inputs, against the fp64
+    backward oracle on the same values (dO drawn like the inputs)."""
+    if len(pages_or_nodes) and isinstance(pages_or_nodes[0], syn.Page):
+        segs = pa.segments_from_pages(pages_or_nodes, 0)
+        nodes = od.page_nodes(pages_or_nodes)
+    else:
+        nodes = [tuple(n) if isinstance(n, tuple) else (n.parent, n.fork, n.length, n.q_len) for n in pages_or_nodes]
+        segs = pa.segments_layout(nodes, 0)
+    ref_kv, ref_q = od.canonical_layout(nodes, 0)
+    T = int(sum(n[2] for n in nodes))
+    nq = int(sum(n[3] for n in nodes))
+    q = syn.draw_normal((nq, Hq, d), seed, 1, "bf16", device=device)
+    k = syn.draw_normal((T, Hkv, d), seed, 2, "bf16", device=device)
+    v = syn.draw_normal((T, Hkv, d), seed, 3, "bf16", device=device)
+    do = syn.draw_normal((nq, Hq, d), seed, 4, "bf16", device=device)
+    plan = pa.TreePlan(segs, Hq, Hkv, d, "bf16", 0, num_kv_rows=T, num_q_rows=nq)
+    ex = plan.export()
+    print(f"[case] backward T={T} nq={nq} Hq={Hq} Hkv={Hkv} d={d} seed={seed} work={len(ex['work'])} "
+          f"bwd={len(ex['bwd'])}", flush=True)
+    scale = 1.0 / math.sqrt(d)
+    if not check:
+        o, lse = pa.tree_attn_fwd(q, k, v, plan)
+        return pa.tree_attn_bwd(q, k, v, o, lse, do, plan), plan
+    # Both sides get the same stored forward output: the oracle's O rounded
+    # to bf16 (what a bf16 forward stores) and its LSE in fp32; D = dO . O is
+    # then formed from the same values on both sides.
+    O_ref, LSE_ref = oracle.tree_attention(nodes, q, k, v, scale, Hq, Hkv, kv_off=ref_kv, q_off=ref_q)
+    o = torch.tensor(O_ref, dtype=torch.float64).to(torch.bfloat16).to(device)
+    lse = torch.tensor(LSE_ref, dtype=torch.float64).to(torch.float32).to(device)
+    dq, dk, dv = pa.tree_attn_bwd(q, k, v, o, lse, do, plan)
+    torch.cuda.synchronize()
+    ref = oracle.tree_attention_backward(nodes, q, k, v, do, scale, Hq, Hkv, kv_off=ref_kv, q_off=ref_q, o=o)
+    errs = {}
+    for name, g, r in zip(("dq", "dk", "dv"), (dq, dk, dv), ref):
+        x = g.detach().to("cpu", torch.float64).numpy()
+        assert np.isfinite(x).all(), f"{name}: non-finite gradient"
+        s = float(np.sqrt(np.mean(r * r))) if r.size else 1.0
+        s = s if s > 0 else 1.0
+        err = np.abs(x - r)
+        s_el = np.maximum(s, np.sqrt(np.mean(r * r, axis=2, keepdims=True)))
+        e_max = float(np.max(np.maximum(err - BWD_ULP * np.abs(r), 0.0) / s_el)) if r.size else 0.0
+        e_mean = float(err.mean() / s) if r.size else 0.0
+        errs[name] = (e_max, e_mean, s)
+        print(f"  {name}: rms {s:.3e} (max-err - ulp)/scale {e_max:.3e} mean-err/rms {e_mean:.3e}", flush=True)
+        assert e_max <= BWD_TOL[0], f"{name}: (max-abs - ulp)/scale {e_max:.3e} > {BWD_TOL[0]}"
+        assert e_mean <= BWD_TOL[1], f"{name}: mean-abs/rms {e_mean:.3e} > {BWD_TOL[1]}"
+    return errs, plan

@@ -396,3 +396,66 @@ def test_block_ids_distinct_and_in_range():
     assert len(set(ids.tolist())) == 5000 and ids.min() >= 0 and ids.max() < (1 << 24)
     ids = syn.draw_block_ids(100, 150, 3)
     assert len(set(ids.tolist())) == 100 and ids.max() < 150
+
+
+def _check_backward(nodes, G, Hkv):
+    """Backward key-major items cover every visible (key row, query row,
+    head) exactly once: no pair is missed (a gradient term lost) or added
+    twice (counted twice in the sum)."""
+    segs = pa.segments_layout(nodes, 0)
+    T = int(sum(n[2] for n in nodes))
+    nq = int(sum(n[3] for n in nodes))
+    plan = pa.TreePlan(segs, G * Hkv, Hkv, 128, "bf16", 0, num_kv_rows=T, num_q_rows=nq)
+    ex = plan.export()
+    row_tok = _token_of_row(nodes, segs["q_off"])
+    want = {}
+    for row, (s, p) in row_tok.items():
+        for (t, j) in _visible_keys(nodes, s, p):
+            krow = int(segs["kv_off"][t]) + j
+            for g in range(Hkv):
+                for h in range(G):
+                    want[(krow, g, row, g * G + h)] = 1
+    got = {}
+    for b in ex["bwd"]:
+        assert 0 < b["n_keys"] <= 128 and 0 < b["ncol"] <= 1024 and b["col0"] % 1024 == 0
+        assert b["col0"] + b["ncol"] <= b["ntok"] * G
+        assert b["cost"] == -(-b["ncol"] // 32)
+        for c in range(b["col0"], b["col0"] + b["ncol"]):
+            t, h = divmod(c, G)
+            row = int(ex["btoks"][b["tok_begin"] + t])
+            lim = int(ex["blims"][b["lim_begin"] + t])
+            assert 0 < lim <= b["n_keys"]
+            for j in range(lim):
+                key = (int(b["key_row0"]) + j, int(b["kvh"]), row, int(b["kvh"]) * G + h)
+                got[key] = got.get(key, 0) + 1
+    assert got == want
+    costs = list(ex["bwd"]["cost"])
+    assert costs == sorted(costs, reverse=True)
+    return ex
+
+
+@pytest.mark.parametrize("G,Hkv", [(1, 1), (8, 2), (7, 4)])
+def test_backward_schedule_random_trees(G, Hkv):
+    for seed in range(3):
+        nodes = [(a.parent, a.fork, a.length, a.q_len)
+                 for a in syn.random_tree(seed + 40, n_pages=2, max_depth=4, max_len=70, q_mode="some", max_nodes=10)]
+        _check_backward(nodes, G, Hkv)
+
+
+def test_backward_schedule_split_runs():
+    # 200 queries x G=8 see the prefix: 1600 columns -> two items per key run
+    nodes = [(-1, 0, 130, 0), (0, 130, 100, 100), (1, 50, 60, 60), (1, 100, 40, 40)]
+    ex = _check_backward(nodes, 8, 1)
+    assert (ex["bwd"]["col0"] == 1024).any()
+
+
+def test_backward_workspace_and_modes():
+    nodes = [(-1, 0, 10, 10)]
+    segs = pa.segments_layout(nodes, 0)
+    plan = pa.TreePlan(segs, 2, 1, 64, "bf16", 0, num_kv_rows=10, num_q_rows=10)
+    nb = plan.backward_workspace_bytes()
+    assert nb >= 10 * 2 * 4 + 2 * 10 * 1 * 64 * 4 and nb % 256 == 0
+    f32 = pa.TreePlan(segs, 2, 1, 64, "f32", 0, num_kv_rows=10, num_q_rows=10)
+    with pytest.raises(_lib.PadocError) as e:
+        f32.backward_workspace_bytes()
+    assert e.value.status == _lib.ERR_DTYPE

@@ -14,6 +14,9 @@ one branch only -- fails at least one of:
 * B3  exact invariants: per KV head, sum_j dK_j = 0 (softmax gradients sum to
       zero over each row's keys) and sum_j dV_j = sum of dO over the group's
       query rows (probabilities sum to one)
+* B4  the stored-output form: D from a given O equals the exact form when O
+      is the exact forward output, and a perturbation dO_i . delta of the
+      stored O_i shifts dQ_i by exactly -c * delta_D * sum_j P_ij k_j
 """
 import numpy as np
 import pytest
@@ -136,3 +139,27 @@ def test_B3_gradient_invariants():
         np.testing.assert_allclose(dk[:, g, :].sum(axis=0), 0.0, atol=1e-11)
         np.testing.assert_allclose(dv[:, g, :].sum(axis=0), do[:, g * G:(g + 1) * G, :].sum(axis=(0, 1)),
                                    rtol=1e-12, atol=1e-11)
+
+
+def test_B4_stored_output_form():
+    nodes = _tiny_nodes()
+    Hq, Hkv, d, scale = 4, 2, 8, 0.37
+    ko, qo, q, k, v, do = _problem(nodes, Hq, Hkv, d, 21)
+    O, _ = ot.tree_attention(nodes, q, k, v, scale, Hq, Hkv, kv_off=ko, q_off=qo)
+    exact = oracle.tree_attention_backward(nodes, q, k, v, do, scale, Hq, Hkv, kv_off=ko, q_off=qo)
+    stored = oracle.tree_attention_backward(nodes, q, k, v, do, scale, Hq, Hkv, kv_off=ko, q_off=qo, o=O)
+    for a, b in zip(exact, stored):
+        np.testing.assert_allclose(a, b, rtol=1e-10, atol=1e-12)
+    # perturb one stored row: dQ of that row moves by -c * dD * (P k) (P k = O
+    # computed with K in place of V), other rows' dQ stay
+    row, h = 3, 1
+    delta = _rand((d,), 77) * 1e-3
+    O2 = O.copy()
+    O2[row, h] += delta
+    dq2, _, dv2 = oracle.tree_attention_backward(nodes, q, k, v, do, scale, Hq, Hkv, kv_off=ko, q_off=qo, o=O2)
+    dD = float(do[row, h] @ delta)
+    Pk, _ = ot.tree_attention(nodes, q, k, k, scale, Hq, Hkv, kv_off=ko, q_off=qo)
+    want = exact[0].copy()
+    want[row, h] -= scale * dD * Pk[row, h]
+    np.testing.assert_allclose(dq2, want, rtol=1e-10, atol=1e-12)
+    np.testing.assert_allclose(dv2, exact[2], rtol=1e-12, atol=1e-12)
