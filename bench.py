@@ -43,6 +43,7 @@ TRAFFIC_SUMMARY = os.path.join(ROOT, "profiles", f"hbm_traffic_{PROFILE_TAG}.txt
 DECODE_KERNELS = ("tile_mfma_bf16_kernel<128, true, true>", "decode_private_kernel<128>",
                   "lse_combine_kernel<128, true>")
 FORWARD_KERNEL = "tile_mfma_bf16_kernel<128, false, false>"
+BACKWARD_KERNELS = ("bwd_prep_kernel<128>", "bwd_dq_kernel<128>", "bwd_dkdv_kernel<128>", "bwd_finalize_kernel")
 COPY_KERNEL = "__amd_rocclr_copyBuffer"
 COPY_BYTES = 1 << 30
 
@@ -63,6 +64,7 @@ def parse_args(argv=None):
     ap.add_argument("--pool-gib", type=float, default=0.0,
                     help="bytes of each of the K and V pools in GiB (0: 45%% of HBM each, backing off on failure)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-backward", action="store_true", help="skip the backward of the forward workload")
     ap.add_argument("--cpu-pages", type=int, default=64, help="pages of the decode workload the oracle times")
     ap.add_argument("--decode-chunk", type=int, default=0,
                     help="decode plan: max keys per work item (0 = planner's choice)")
@@ -379,6 +381,27 @@ def run_forward(args, torch, np, syn, pa, dev):
     k_ms = statistics.mean(kms)
     pairs = visible_pairs_of(segs)
     flops = 4 * d * Hq * pairs
+    bwd = None
+    if not args.no_backward and wl.dtype == "bf16":
+        # Backward of the same forward: dO drawn like the inputs; algorithmic
+        # flops = 5 products per visible pair (S recomputed, dP, dV, dQ, dK).
+        dout = syn.draw_normal((nq, Hq, d), args.seed, 4, wl.dtype, device=dev)
+        dq, dk, dv = torch.empty_like(q), torch.empty_like(k), torch.empty_like(v)
+        bws = plan.backward_workspace(dev)
+
+        def bstep():
+            pa.tree_attn_bwd(q, k, v, o, lse, dout, plan, dq=dq, dk=dk, dv=dv, workspace=bws)
+
+        log("backward of the forward workload")
+        bms, bkms = timed_steps(bstep, max(5, args.steps // 2), args.warmup, torch, pa)
+        bk = statistics.mean(bkms)
+        bflops = 10 * d * Hq * pairs
+        ex = plan.export()
+        bwd = {"ms_per_step": bms, "kernel_ms": bk, "flops": bflops, "kernel_tflops": bflops / (bk * 1e-3) / 1e12,
+               "dkdv_items": int(len(ex["bwd"])), "dq_items": int(len(ex["work"])),
+               "roofline": {"bound": "mfma", "achieved": bflops / (bk * 1e-3) / 1e12, "peak": BF16_PEAK_TFLOPS,
+                            "unit": "TFLOP/s", "frac": bflops / (bk * 1e-3) / 1e12 / BF16_PEAK_TFLOPS,
+                            "kernel": "backward call: " + " + ".join(BACKWARD_KERNELS)}}
     return {
         "workload": wl.name, "tokens": T, "visible_pairs": pairs, "flops": flops,
         "ms_per_step": ms, "kernel_ms": k_ms, "tflops": flops / (ms * 1e-3) / 1e12,
@@ -386,6 +409,7 @@ def run_forward(args, torch, np, syn, pa, dev):
         "roofline": {"bound": "mfma", "achieved": flops / (k_ms * 1e-3) / 1e12, "peak": BF16_PEAK_TFLOPS,
                      "unit": "TFLOP/s", "frac": flops / (k_ms * 1e-3) / 1e12 / BF16_PEAK_TFLOPS,
                      "traffic": measured_traffic()[1], "kernel": FORWARD_KERNEL},
+        "backward": bwd,
     }
 
 

@@ -188,9 +188,9 @@ typedef struct {
    (K/V rows of one segment, n_keys <= 128) of KV head kvh against the query
    tokens btoks[tok_begin .. tok_begin+ntok) (Q rows), of which token i sees
    the item's keys [0, blims[lim_begin + i]) (relative to key_row0); the item
-   computes columns col0 .. col0+ncol-1 (column c = token c/G, head c%G) and
-   adds their dK/dV contributions.  Items of one key range that split its
-   columns add into the same rows. */
+   computes columns col0 .. col0+ncol-1 (column c = token c/G, head c%G).  An
+   item with all ntok*G columns stores its rows' dK/dV; the items of a key
+   run split into column pieces (multiples of 32) add into the same rows. */
 typedef struct {
   int64_t key_row0;
   int32_t n_keys, tok_begin, ntok, lim_begin, col0, ncol, kvh, cost;
@@ -259,8 +259,10 @@ padoc_status padoc_branch_decode(const padoc_plan* plan, const void* q, const vo
    and dk, dv [num_kv_rows, Hkv, d] (bf16, rounded to nearest-even from fp32
    accumulation; rows that no query sees get zero).  The gradient is that of
    sum(dout * O) with O = softmax(scale * q K^T + mask) V.  Rows of dk/dv
-   whose keys are seen by more than 1024 query columns sum contributions in
-   an order that depends on scheduling (fp32 rounding differences only).
+   whose key run is split over several items (runs seen by more query
+   columns than about one compute unit's share of the whole backward) sum the
+   pieces in an order that depends on scheduling (fp32 rounding differences
+   only); all other results are deterministic.
    workspace: a device buffer of at least padoc_plan_backward_workspace_bytes
    bytes (256-byte aligned); fp32 plans return PADOC_ERR_DTYPE. */
 padoc_status padoc_plan_backward_workspace_bytes(const padoc_plan* plan, size_t* bytes);

@@ -297,10 +297,13 @@ void build_forward(padoc_plan& P, Builder& B) {
 // them: t's own queries at positions p >= kb (they see keys <= p), and every
 // query of every descendant s whose fork offset into t, F(s, t), exceeds kb
 // (they see keys < F).  Each token's limit is stored relative to kb and
-// clipped to nk.  The tokens' columns (token x head) are cut into items of
-// at most kBwdCols columns per KV head; items of one key run add into the
-// same dK/dV rows.
-void build_backward(padoc_plan& P, const std::vector<std::vector<std::pair<int32_t, int32_t>>>& anc) {
+// clipped to nk.  A run's columns (token x head) form one item per KV head,
+// except that runs longer than about one compute unit's share of all the
+// 32-column blocks (total / (target_workgroups / 4), at least 64 blocks) are
+// cut into equal block-aligned pieces, whose items add into the same dK/dV
+// rows; whole runs store their rows.
+void build_backward(padoc_plan& P, const std::vector<std::vector<std::pair<int32_t, int32_t>>>& anc,
+                    int32_t target_workgroups) {
   const int32_t n = (int32_t)P.seg.size();
   std::vector<std::vector<std::pair<int32_t, int32_t>>> desc(n);  // (s, F(s, t)) per t
   for (int32_t s = 0; s < n; ++s)
@@ -309,6 +312,12 @@ void build_backward(padoc_plan& P, const std::vector<std::vector<std::pair<int32
     const padoc_segment& sg = P.seg[s];
     return (int32_t)(sg.q_off + (p - (sg.len - sg.q_len)));
   };
+  struct Run {
+    int64_t key_row0;
+    int32_t nk, tok_begin, ntok, lim_begin;
+  };
+  std::vector<Run> runs;
+  int64_t total_blocks = 0;
   for (int32_t t = 0; t < n; ++t) {
     const padoc_segment& tg = P.seg[t];
     for (int32_t kb = 0; kb < tg.len; kb += kBwdKeys) {
@@ -328,21 +337,30 @@ void build_backward(padoc_plan& P, const std::vector<std::vector<std::pair<int32
       }
       const int32_t ntok = (int32_t)P.btoks.size() - tok_begin;
       if (ntok == 0) continue;
-      const int64_t cols = (int64_t)ntok * P.G;
-      for (int64_t c0 = 0; c0 < cols; c0 += kBwdCols) {
-        for (int32_t g = 0; g < P.Hkv; ++g) {
-          padoc::BwdRec b{};
-          b.key_row0 = tg.kv_off + kb;
-          b.n_keys = nk;
-          b.tok_begin = tok_begin;
-          b.ntok = ntok;
-          b.lim_begin = lim_begin;
-          b.col0 = (int32_t)c0;
-          b.ncol = (int32_t)std::min<int64_t>(kBwdCols, cols - c0);
-          b.kvh = g;
-          b.cost = (int32_t)ceil_div(b.ncol, 32);
-          P.bwd.push_back(b);
-        }
+      runs.push_back({tg.kv_off + kb, nk, tok_begin, ntok, lim_begin});
+      total_blocks += ceil_div((int64_t)ntok * P.G, 32) * P.Hkv;
+    }
+  }
+  const int64_t tw = target_workgroups > 0 ? target_workgroups : 1024;
+  const int64_t cap = std::max<int64_t>(64, ceil_div(total_blocks * 4, tw));
+  for (const Run& r : runs) {
+    const int64_t cols = (int64_t)r.ntok * P.G;
+    const int64_t blocks = ceil_div(cols, 32);
+    const int64_t pieces = ceil_div(blocks, cap);
+    const int64_t step = ceil_div(blocks, pieces) * 32;
+    for (int64_t c0 = 0; c0 < cols; c0 += step) {
+      for (int32_t g = 0; g < P.Hkv; ++g) {
+        padoc::BwdRec b{};
+        b.key_row0 = r.key_row0;
+        b.n_keys = r.nk;
+        b.tok_begin = r.tok_begin;
+        b.ntok = r.ntok;
+        b.lim_begin = r.lim_begin;
+        b.col0 = (int32_t)c0;
+        b.ncol = (int32_t)std::min<int64_t>(step, cols - c0);
+        b.kvh = g;
+        b.cost = (int32_t)ceil_div(b.ncol, 32);
+        P.bwd.push_back(b);
       }
     }
   }
@@ -665,7 +683,7 @@ extern "C" padoc_status padoc_plan_create(const padoc_tree_desc* d, padoc_plan**
                        [](const padoc::WorkRec& a, const padoc::WorkRec& b) { return a.cost > b.cost; });
     serialise(*P);
     if (P->kind == 0 && P->dtype == PADOC_BF16) {
-      build_backward(*P, anc);
+      build_backward(*P, anc, d->target_workgroups);
       if ((int64_t)P->btoks.size() > kI32Max || (int64_t)P->bwd.size() > kI32Max)
         return set_error(PADOC_ERR_ARG, "backward schedule too large");
       serialise_backward(*P);

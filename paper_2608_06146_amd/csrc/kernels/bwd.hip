@@ -17,7 +17,8 @@
 //   bwd_dkdv   key-major: up to 128 keys of one segment against the query
 //              columns that see them, 32 columns per step; waves 0-3 compute
 //              dV^T += dO^T P for 32 keys each, waves 4-7 dK^T += Q^T dS for
-//              the same keys; results are added into fp32 accumulators
+//              the same keys; results go to fp32 rows (stored by an item that
+//              holds the whole run, added by the pieces of a split run)
 //   bwd_finalize  fp32 accumulators -> bf16 dK, dV (round to nearest even)
 // All products are v_mfma_f32_32x32x16_bf16 with fp32 accumulation.  The
 // operand whose contraction index is not contiguous in memory (K^T for dQ,
@@ -420,13 +421,25 @@ __global__ __launch_bounds__(kThreads) void bwd_dkdv_kernel(BwdParams p) {
   }
 
   if (key >= b.n_keys) return;
-  // acc[db] element i: d = db*32 + (i/4)*8 + hf*4 + i%4, key `key`
+  // acc[db] element i: d = db*32 + (i/4)*8 + hf*4 + i%4, key `key`.  An item
+  // that holds all of its key run's columns stores its rows; the pieces of a
+  // split run add into them (rows start at zero).
   float* dst = (kwave ? p.dk_acc : p.dv_acc) + ((b.key_row0 + key) * Hkv + kvh) * D;
   const float sc = kwave ? p.scale : 1.f;
+  if (b.col0 == 0 && b.ncol == b.ntok * G) {
 #pragma unroll
-  for (int db = 0; db < NDB; ++db)
+    for (int db = 0; db < NDB; ++db)
 #pragma unroll
-    for (int i = 0; i < 16; ++i) atomicAdd(dst + db * 32 + (i >> 2) * 8 + hf * 4 + (i & 3), acc[db][i] * sc);
+      for (int i4 = 0; i4 < 4; ++i4)
+        *reinterpret_cast<float4*>(dst + db * 32 + i4 * 8 + hf * 4) =
+            make_float4(acc[db][4 * i4] * sc, acc[db][4 * i4 + 1] * sc, acc[db][4 * i4 + 2] * sc,
+                        acc[db][4 * i4 + 3] * sc);
+  } else {
+#pragma unroll
+    for (int db = 0; db < NDB; ++db)
+#pragma unroll
+      for (int i = 0; i < 16; ++i) atomicAdd(dst + db * 32 + (i >> 2) * 8 + hf * 4 + (i & 3), acc[db][i] * sc);
+  }
 }
 
 // ------------------------------------------------------------------ finalize

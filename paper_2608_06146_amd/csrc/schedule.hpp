@@ -24,7 +24,6 @@ constexpr int kTileCols = 256;
 constexpr int kBlock = 16;  // paged KV block (tokens)
 constexpr int kPrivateCols = 16;  // columns of a private decode item (one wavefront)
 constexpr int kBwdKeys = 128;     // keys of a backward key-major item (4 x 32)
-constexpr int kBwdCols = 1024;    // query columns per backward item (32 blocks of 32)
 
 // Everything a tile kernel needs.  Pointers are device pointers.
 struct TileParams {

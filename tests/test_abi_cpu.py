@@ -417,7 +417,7 @@ def _check_backward(nodes, G, Hkv):
                     want[(krow, g, row, g * G + h)] = 1
     got = {}
     for b in ex["bwd"]:
-        assert 0 < b["n_keys"] <= 128 and 0 < b["ncol"] <= 1024 and b["col0"] % 1024 == 0
+        assert 0 < b["n_keys"] <= 128 and 0 < b["ncol"] and b["col0"] % 32 == 0
         assert b["col0"] + b["ncol"] <= b["ntok"] * G
         assert b["cost"] == -(-b["ncol"] // 32)
         for c in range(b["col0"], b["col0"] + b["ncol"]):
@@ -443,10 +443,12 @@ def test_backward_schedule_random_trees(G, Hkv):
 
 
 def test_backward_schedule_split_runs():
-    # 200 queries x G=8 see the prefix: 1600 columns -> two items per key run
-    nodes = [(-1, 0, 130, 0), (0, 130, 100, 100), (1, 50, 60, 60), (1, 100, 40, 40)]
+    # 500 queries x G=8 see the prefix: 4000 columns = 125 blocks, more than
+    # the 64-block minimum piece -> two equal pieces per key run
+    nodes = [(-1, 0, 130, 0), (0, 130, 300, 300), (1, 50, 120, 120), (1, 100, 80, 80)]
     ex = _check_backward(nodes, 8, 1)
-    assert (ex["bwd"]["col0"] == 1024).any()
+    pre = ex["bwd"][ex["bwd"]["key_row0"] < 130]
+    assert (pre["col0"] == 2016).any() and (pre["ncol"] == 2016).any()
 
 
 def test_backward_workspace_and_modes():
