@@ -264,13 +264,18 @@ __global__ __launch_bounds__(kThreads) void bwd_dkdv_kernel(BwdParams p) {
   constexpr int NDB = D / 32;
   constexpr int CPR = D / 8;
 
-  __shared__ __attribute__((aligned(16))) uint16_t Qs[32 * QS];
-  __shared__ __attribute__((aligned(16))) uint16_t Gs[32 * QS];
-  __shared__ __attribute__((aligned(16))) uint16_t Qt[D * TS];
-  __shared__ __attribute__((aligned(16))) uint16_t Gt[D * TS];
-  __shared__ __attribute__((aligned(16))) float Ls[32];  // LSE * log2(e)
-  __shared__ __attribute__((aligned(16))) float Dd[32];  // dO . O
-  __shared__ __attribute__((aligned(16))) int Lm[32];    // visible keys of the item
+  // Two stages: block i is computed from stage i%2 while block i+1 is stored
+  // into the other one (one barrier per block).
+  struct Stage {
+    uint16_t q[32 * QS];  // Q rows (column-major block: row = column)
+    uint16_t g[32 * QS];  // dO rows
+    uint16_t qt[D * TS];  // Q transposed, columns permuted
+    uint16_t gt[D * TS];  // dO transposed, columns permuted
+    float ls[32];         // LSE * log2(e) per column
+    float dd[32];         // dO . O per column
+    int lm[32];           // keys of the item the column sees
+  };
+  __shared__ __attribute__((aligned(16))) Stage st[2];
 
   const BwdRec b = p.bwd[blockIdx.x];
   const int tid = threadIdx.x;
@@ -292,52 +297,82 @@ __global__ __launch_bounds__(kThreads) void bwd_dkdv_kernel(BwdParams p) {
     }
   }
 
-  // Staging geometry: thread -> (column, 16-byte chunk) of a 32-column block;
-  // with d = 64 the upper half of the threads repeats the lower half's loads
-  // and stores nothing.
-  const int s_col = (tid / CPR) % 32, s_dc = tid % CPR;
+  // Staging geometry: thread -> (column, 16-byte chunk) of a 32-column block,
+  // columns fastest: the transposed stores of a wave then spread over 32
+  // banks (chunk-fastest lanes would hit rows 8 * TS apart, two banks); with
+  // d = 64 the upper half of the threads repeats the lower half's loads and
+  // stores nothing.  Every thread also loads the per-column scalars of column
+  // tid % 32 (threads < 32 store them), so all threads issue the same loads
+  // and the compiler's load wait counts stay exact.
+  const int s_col = tid % 32, s_dc = (tid / 32) % CPR;
   const bool s_on = tid < 32 * CPR;
-  uint4 qr, gr;
-  float lr = 0.f, dr = 0.f;
-  int mr = 0;
-  auto load = [&](int c0) {
-    const int cabs = c0 + s_col;
-    const bool ok = cabs < b.col0 + b.ncol;
-    const int t = cabs / G;
-    const int32_t row = ok ? p.btoks[b.tok_begin + t] : 0;
-    const int64_t off = ((int64_t)row * p.Hq + kvh * G + (cabs - t * G)) * D + s_dc * 8;
-    qr = ok ? load16(static_cast<const uint16_t*>(p.q) + off) : make_uint4(0, 0, 0, 0);
-    gr = ok ? load16(static_cast<const uint16_t*>(p.dout) + off) : make_uint4(0, 0, 0, 0);
-    if (tid < 32) {  // per-column scalars of column tid
-      const int cc = c0 + tid;
-      const bool okc = cc < b.col0 + b.ncol;
-      const int tc = cc / G;
-      const int32_t rc = okc ? p.btoks[b.tok_begin + tc] : 0;
-      const int64_t li = (int64_t)rc * p.Hq + kvh * G + (cc - tc * G);
-      lr = okc ? p.lse[li] * kLog2e : 0.f;
-      dr = okc ? p.dd[li] : 0.f;
-      mr = okc ? p.blims[b.lim_begin + tc] : 0;
-    }
+  const int c_end = b.col0 + b.ncol;
+  const int c_last = b.col0 + ((b.ncol - 1) & ~31);  // first column of the last block
+  // Register sets [i % 2]: Q / dO pieces and column scalars of a block
+  // loaded two blocks ahead of its LDS store; the Q rows of its columns are
+  // fetched one block before that.
+  uint4 qr[2], gr[2];
+  float lr[2], dr[2];
+  int mr[2];
+  int rq[2], rc[2];  // Q rows of this thread's piece column and scalar column
+  auto fetch_rows = [&](auto xc, int c0) {
+    constexpr int X = decltype(xc)::value;
+    c0 = c0 <= c_last ? c0 : c_last;  // past the end: re-read the last block
+    const int ca = c0 + s_col, cb = c0 + (tid & 31);
+    rq[X] = p.btoks[b.tok_begin + (ca < c_end ? ca : c_end - 1) / G];
+    rc[X] = p.btoks[b.tok_begin + (cb < c_end ? cb : c_end - 1) / G];
   };
-  auto store = [&]() {
+  auto load = [&](auto xc, int c0) {
+    constexpr int X = decltype(xc)::value;
+    c0 = c0 <= c_last ? c0 : c_last;
+    const int ca = c0 + s_col;
+    const bool ok = ca < c_end;
+    const int ha = kvh * G + ca % G;
+    const int64_t off = ((int64_t)rq[X] * p.Hq + ha) * D + s_dc * 8;
+    const uint4 q = load16(static_cast<const uint16_t*>(p.q) + off);
+    const uint4 g = load16(static_cast<const uint16_t*>(p.dout) + off);
+    qr[X] = ok ? q : make_uint4(0, 0, 0, 0);
+    gr[X] = ok ? g : make_uint4(0, 0, 0, 0);
+    const int cb = c0 + (tid & 31);
+    const bool okc = cb < c_end;
+    const int64_t li = (int64_t)rc[X] * p.Hq + kvh * G + cb % G;
+    const float l = p.lse[li], dd = p.dd[li];
+    const int m = p.blims[b.lim_begin + (okc ? cb : c_end - 1) / G];
+    lr[X] = okc ? l * kLog2e : 0.f;
+    dr[X] = okc ? dd : 0.f;
+    mr[X] = okc ? m : 0;
+  };
+  auto store = [&](auto xc, Stage& S) {
+    constexpr int X = decltype(xc)::value;
+    // Transposed stores as 32-bit words of a column pair: lanes 2c and 2c+1
+    // (columns 2c, 2c+1, adjacent in the permuted order) swap halves; the
+    // even lane writes the even d rows, the odd lane the odd ones.
+    const uint32_t a[4] = {qr[X].x, qr[X].y, qr[X].z, qr[X].w};
+    const uint32_t g[4] = {gr[X].x, gr[X].y, gr[X].z, gr[X].w};
+    uint32_t an[4], gn[4];
+#pragma unroll
+    for (int m = 0; m < 4; ++m) {
+      an[m] = (uint32_t)__shfl_xor((int)a[m], 1);
+      gn[m] = (uint32_t)__shfl_xor((int)g[m], 1);
+    }
     if (s_on) {
-      store16(&Qs[s_col * QS + s_dc * 8], qr);
-      store16(&Gs[s_col * QS + s_dc * 8], gr);
-      const int pos = perm_pos(s_col);
-      const uint32_t a[4] = {qr.x, qr.y, qr.z, qr.w};
-      const uint32_t g[4] = {gr.x, gr.y, gr.z, gr.w};
+      store16(&S.q[s_col * QS + s_dc * 8], qr[X]);
+      store16(&S.g[s_col * QS + s_dc * 8], gr[X]);
+      const int odd = s_col & 1;
+      const int pos = perm_pos(s_col & ~1);
 #pragma unroll
       for (int m = 0; m < 4; ++m) {
-        Qt[(s_dc * 8 + 2 * m) * TS + pos] = (uint16_t)(a[m] & 0xffffu);
-        Qt[(s_dc * 8 + 2 * m + 1) * TS + pos] = (uint16_t)(a[m] >> 16);
-        Gt[(s_dc * 8 + 2 * m) * TS + pos] = (uint16_t)(g[m] & 0xffffu);
-        Gt[(s_dc * 8 + 2 * m + 1) * TS + pos] = (uint16_t)(g[m] >> 16);
+        const int row = s_dc * 8 + 2 * m + odd;
+        const uint32_t wq = odd ? __builtin_amdgcn_perm(a[m], an[m], 0x07060302u) : __builtin_amdgcn_perm(an[m], a[m], 0x05040100u);
+        const uint32_t wg = odd ? __builtin_amdgcn_perm(g[m], gn[m], 0x07060302u) : __builtin_amdgcn_perm(gn[m], g[m], 0x05040100u);
+        *reinterpret_cast<uint32_t*>(&S.qt[row * TS + pos]) = wq;
+        *reinterpret_cast<uint32_t*>(&S.gt[row * TS + pos]) = wg;
       }
     }
     if (tid < 32) {
-      Ls[tid] = lr;
-      Dd[tid] = dr;
-      Lm[tid] = mr;
+      S.ls[tid] = lr[X];
+      S.dd[tid] = dr[X];
+      S.lm[tid] = mr[X];
     }
   };
 
@@ -348,59 +383,65 @@ __global__ __launch_bounds__(kThreads) void bwd_dkdv_kernel(BwdParams p) {
     for (int i = 0; i < 16; ++i) acc[db][i] = 0.f;
   const float sl2 = p.scale_log2;
 
-  const int c_end = b.col0 + b.ncol;
-  load(b.col0);
-  for (int c0 = b.col0; c0 < c_end; c0 += 32) {
-    store();
-    __syncthreads();
-    if (c0 + 32 < c_end) load(c0 + 32);  // next block, in flight during this one
-
+  // Block computation from one stage.  Fragments of each product group are
+  // requested together before its matrix products.
+  auto compute = [&](const Stage& S) {
     // S = Q K^T: columns on M, this wave's 32 keys on N.  Element i of a lane
     // is column (i/4)*8 + hf*4 + i%4 of the block and key `key`.
-    f32x16_t S;
+    bf16x8_t fa[NKK];
 #pragma unroll
-    for (int i = 0; i < 16; ++i) S[i] = 0.f;
+    for (int kk = 0; kk < NKK; ++kk) fa[kk] = *reinterpret_cast<const bf16x8_t*>(&S.q[l32 * QS + kk * 16 + hf * 8]);
+    f32x16_t sc;
 #pragma unroll
-    for (int kk = 0; kk < NKK; ++kk)
-      S = __builtin_amdgcn_mfma_f32_32x32x16_bf16(*reinterpret_cast<const bf16x8_t*>(&Qs[l32 * QS + kk * 16 + hf * 8]),
-                                                  bk[kk], S, 0, 0, 0);
+    for (int i = 0; i < 16; ++i) sc[i] = 0.f;
+#pragma unroll
+    for (int kk = 0; kk < NKK; ++kk) sc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[kk], bk[kk], sc, 0, 0, 0);
     float pr[16];
 #pragma unroll
     for (int q4 = 0; q4 < 4; ++q4) {
       const int cb = q4 * 8 + hf * 4;  // columns cb .. cb+3 = elements 4*q4 .. 4*q4+3
-      const float4 l4 = *reinterpret_cast<const float4*>(&Ls[cb]);
-      const int4 m4 = *reinterpret_cast<const int4*>(&Lm[cb]);
+      const float4 l4 = *reinterpret_cast<const float4*>(&S.ls[cb]);
+      const int4 m4 = *reinterpret_cast<const int4*>(&S.lm[cb]);
       const float lv[4] = {l4.x, l4.y, l4.z, l4.w};
       const int mv[4] = {m4.x, m4.y, m4.z, m4.w};
 #pragma unroll
-      for (int e = 0; e < 4; ++e) pr[4 * q4 + e] = key < mv[e] ? fast_exp2(fmaf(S[4 * q4 + e], sl2, -lv[e])) : 0.f;
+      for (int e = 0; e < 4; ++e) pr[4 * q4 + e] = key < mv[e] ? fast_exp2(fmaf(sc[4 * q4 + e], sl2, -lv[e])) : 0.f;
     }
+    bf16x8_t fb[2 * NDB];
     if (!kwave) {
       // dV^T += dO^T P: d on M (block db), keys on N, columns on K
+#pragma unroll
+      for (int j = 0; j < 2; ++j)
+#pragma unroll
+        for (int db = 0; db < NDB; ++db)
+          fb[j * NDB + db] = *reinterpret_cast<const bf16x8_t*>(&S.gt[(db * 32 + l32) * TS + 16 * j + hf * 8]);
 #pragma unroll
       for (int j = 0; j < 2; ++j) {
         bf16x8_t pb;
 #pragma unroll
         for (int e = 0; e < 8; ++e) pb[e] = (__bf16)pr[8 * j + e];
 #pragma unroll
-        for (int db = 0; db < NDB; ++db) {
-          const bf16x8_t a = *reinterpret_cast<const bf16x8_t*>(&Gt[(db * 32 + l32) * TS + 16 * j + hf * 8]);
-          acc[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, pb, acc[db], 0, 0, 0);
-        }
+        for (int db = 0; db < NDB; ++db)
+          acc[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fb[j * NDB + db], pb, acc[db], 0, 0, 0);
       }
     } else {
       // dP = dO V^T; dS = P (dP - D); dK^T += Q^T dS
+#pragma unroll
+      for (int kk = 0; kk < NKK; ++kk) fa[kk] = *reinterpret_cast<const bf16x8_t*>(&S.g[l32 * QS + kk * 16 + hf * 8]);
+#pragma unroll
+      for (int j = 0; j < 2; ++j)
+#pragma unroll
+        for (int db = 0; db < NDB; ++db)
+          fb[j * NDB + db] = *reinterpret_cast<const bf16x8_t*>(&S.qt[(db * 32 + l32) * TS + 16 * j + hf * 8]);
       f32x16_t dP;
 #pragma unroll
       for (int i = 0; i < 16; ++i) dP[i] = 0.f;
 #pragma unroll
-      for (int kk = 0; kk < NKK; ++kk)
-        dP = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
-            *reinterpret_cast<const bf16x8_t*>(&Gs[l32 * QS + kk * 16 + hf * 8]), bv[kk], dP, 0, 0, 0);
+      for (int kk = 0; kk < NKK; ++kk) dP = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[kk], bv[kk], dP, 0, 0, 0);
       float dsv[16];
 #pragma unroll
       for (int q4 = 0; q4 < 4; ++q4) {
-        const float4 d4 = *reinterpret_cast<const float4*>(&Dd[q4 * 8 + hf * 4]);
+        const float4 d4 = *reinterpret_cast<const float4*>(&S.dd[q4 * 8 + hf * 4]);
         const float dv[4] = {d4.x, d4.y, d4.z, d4.w};
 #pragma unroll
         for (int e = 0; e < 4; ++e) dsv[4 * q4 + e] = pr[4 * q4 + e] * (dP[4 * q4 + e] - dv[e]);
@@ -411,13 +452,41 @@ __global__ __launch_bounds__(kThreads) void bwd_dkdv_kernel(BwdParams p) {
 #pragma unroll
         for (int e = 0; e < 8; ++e) sb[e] = (__bf16)dsv[8 * j + e];
 #pragma unroll
-        for (int db = 0; db < NDB; ++db) {
-          const bf16x8_t a = *reinterpret_cast<const bf16x8_t*>(&Qt[(db * 32 + l32) * TS + 16 * j + hf * 8]);
-          acc[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, sb, acc[db], 0, 0, 0);
-        }
+        for (int db = 0; db < NDB; ++db)
+          acc[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fb[j * NDB + db], sb, acc[db], 0, 0, 0);
       }
     }
+  };
+
+  // Block i is computed from stage i % 2 and its pieces sit in register set
+  // i % 2 until stored (at step i-1); step i stores block i+1, loads block
+  // i+2 into set i % 2 and fetches the rows of block i+3 into row set
+  // (i+1) % 2.
+  using Set0 = std::integral_constant<int, 0>;
+  using Set1 = std::integral_constant<int, 1>;
+  fetch_rows(Set0{}, b.col0);
+  load(Set0{}, b.col0);
+  fetch_rows(Set1{}, b.col0 + 32);
+  load(Set1{}, b.col0 + 32);
+  store(Set0{}, st[0]);
+  fetch_rows(Set0{}, b.col0 + 64);
+  __syncthreads();
+  auto step = [&](auto xc, int c0) {
+    constexpr int X = decltype(xc)::value;
+    using Y = std::integral_constant<int, X ^ 1>;
+    compute(st[X]);
+    if (c0 + 32 < c_end) store(Y{}, st[X ^ 1]);  // that stage was last read before the previous barrier
+    load(xc, c0 + 64);
+    fetch_rows(Y{}, c0 + 96);
     __syncthreads();
+  };
+  for (int c0 = b.col0;;) {
+    step(Set0{}, c0);
+    c0 += 32;
+    if (c0 >= c_end) break;
+    step(Set1{}, c0);
+    c0 += 32;
+    if (c0 >= c_end) break;
   }
 
   if (key >= b.n_keys) return;
