@@ -215,6 +215,7 @@ __device__ __forceinline__ void tile_item(const TileParams& p, int item) {
   // Staging registers: set b%2 holds bundle b = K(b) and V(b-1).
   uint4 kr[2][KPT], vr[2][2 * VPT];
   int vkeep[2][PAGED ? VPT : 1];  // paged V: keys of each chunk inside the range
+  bool vfull[2] = {true, true};     // paged V: the whole tile lies inside the range
 
   // Block ids of a tile: lane l (mod NB) loads the id of block l with a
   // vector load.  Scalar loads would share the LDS wait counter (and return
@@ -253,6 +254,7 @@ __device__ __forceinline__ void tile_item(const TileParams& p, int item) {
         const int64_t blk = __builtin_amdgcn_readlane(idv, v_blk[i]);
         vr[X][i] = load_stream16(Vg + blk * (int64_t)(HD * kBlock) + v_off[i]);
         vkeep[X][i] = c.R.n_keys - (kbase + v_blk[i] * kBlock + v_h[i] * 8);
+        vfull[X] = c.R.n_keys - kbase >= KT;
       });
     } else {
       const int last = c.R.n_keys - 1 - kbase;
@@ -277,7 +279,7 @@ __device__ __forceinline__ void tile_item(const TileParams& p, int item) {
         constexpr int i = decltype(ic)::value;
         // keys 8h..8h+3 of block bi -> positions 4h..4h+3, keys 8h+4..8h+7 -> 8+4h..
         uint16_t* row = &vt[v_d[i] * VS + v_blk[i] * 16];
-        const uint4 x = keep_first(vr[X][i], vkeep[X][i]);
+        const uint4 x = vfull[X] ? vr[X][i] : keep_first(vr[X][i], vkeep[X][i]);
         *reinterpret_cast<uint2*>(row + 4 * v_h[i]) = make_uint2(x.x, x.y);
         *reinterpret_cast<uint2*>(row + 8 + 4 * v_h[i]) = make_uint2(x.z, x.w);
       });
