@@ -52,114 +52,184 @@ int64_t ceil_div(int64_t a, int64_t b) { return (a + b - 1) / b; }
 int64_t round_up(int64_t a, int64_t b) { return ceil_div(a, b) * b; }
 size_t align256(size_t x) { return (x + 255) & ~size_t(255); }
 
-// A set of query tokens processed together (one work item per KV head and
-// key chunk).
-struct Task {
-  std::vector<int32_t> seg, pos;
+// Proper ancestors of every segment as (ancestor, fork offset into it)
+// pairs, root first, stored flat.
+struct AncList {
+  using Pair = std::pair<int32_t, int32_t>;
+  struct Span {
+    const Pair *b, *e;
+    const Pair* begin() const { return b; }
+    const Pair* end() const { return e; }
+  };
+  std::vector<int64_t> off;  // n + 1 entries
+  std::vector<Pair> a;
+  Span operator[](int32_t s) const { return {a.data() + off[s], a.data() + off[s + 1]}; }
 };
 
-// A visible segment of a task with each token's limit.
+// A set of query tokens processed together (one work item per KV head and
+// key chunk): entries begin .. begin+count-1 of the builder's token list.
+struct Task {
+  int32_t begin, count;
+};
+
+// A visible segment of a task: each token's limit (keys [0, lim) visible)
+// is at the builder's vlim[lim_off + i].
 struct VisRange {
   int32_t t;
-  std::vector<int32_t> lim;
   int32_t n_keys;  // max lim
+  int64_t lim_off;
 };
 
-// A key chunk [kb, kb+len) of one VisRange.
+// A key chunk [kb, kb+len) of the VisRange with index r.
 struct Piece {
-  const VisRange* r;
-  int32_t kb, len;
+  int32_t r, kb, len;
 };
+
+// Sort work items by cost, highest first, keeping the order of equal costs.
+void sort_by_cost(std::vector<padoc::WorkRec>& w, std::vector<padoc::WorkRec>& tmp) {
+  int32_t mx = 0;
+  for (const auto& x : w) mx = std::max(mx, x.cost);
+  if (mx > (1 << 16)) {
+    std::stable_sort(w.begin(), w.end(), [](const padoc::WorkRec& a, const padoc::WorkRec& b) { return a.cost > b.cost; });
+    return;
+  }
+  std::vector<int32_t> start(mx + 2, 0);
+  for (const auto& x : w) ++start[mx - x.cost + 1];
+  for (int32_t c = 0; c <= mx; ++c) start[c + 1] += start[c];
+  tmp.assign(w.begin(), w.end());
+  for (const auto& x : tmp) w[start[mx - x.cost]++] = x;
+}
+
+// Working vectors of the planner, kept per thread so that repeated planning
+// (a new schedule every decode step) reuses their memory.
+struct Scratch {
+  std::vector<int32_t> tseg, tpos, vlim, slot, touched, l;
+  std::vector<char> sees, finished;
+  AncList anc;
+  std::vector<int64_t> viewers;
+  std::vector<int32_t> root, at, fill;
+  std::vector<Task> tasks, stasks, ptasks;
+  std::vector<VisRange> vis, svis, pvis;
+  std::vector<size_t> svis_at, pvis_at;
+  std::vector<Piece> pieces;
+  std::vector<std::pair<size_t, int32_t>> parts;
+  std::vector<padoc::WorkRec> sitems, pitems, tmp;
+};
+thread_local Scratch t_scratch;
 
 class Builder {
  public:
-  Builder(padoc_plan& p, const std::vector<std::vector<std::pair<int32_t, int32_t>>>& anc)
-      : P(p), anc_(anc) {}
+  Builder(padoc_plan& p, Scratch& s)
+      : P(p), S(s), tseg(s.tseg), tpos(s.tpos), vlim(s.vlim), sees(s.sees), anc_(s.anc), slot_(s.slot),
+        touched_(s.touched), l_(s.l) {
+    tseg.clear();
+    tpos.clear();
+    vlim.clear();
+    slot_.assign(p.seg.size(), -1);
+  }
 
-  // Segments visible to any token of `task` for which include(t) holds.
+  padoc_plan& P;
+  Scratch& S;
+  // Token list of all tasks: segment and position of each query token.
+  std::vector<int32_t>&tseg, &tpos;
+  // Per-token limits of the visible ranges.
+  std::vector<int32_t>& vlim;
+  // Tokens of the last emit_ranges call that see at least one key.
+  std::vector<char>& sees;
+
+  // Appends to `out` the segments visible to any token of `task` for which
+  // include(t) holds, in ascending segment order.
   template <class Pred>
-  std::vector<VisRange> visible(const Task& task, Pred include) const {
-    const int32_t nt = (int32_t)task.seg.size();
-    std::map<int32_t, std::vector<int32_t>> per;
-    auto put = [&](int32_t t, int32_t i, int32_t lim) {
-      auto it = per.find(t);
-      if (it == per.end()) it = per.emplace(t, std::vector<int32_t>(nt, 0)).first;
-      it->second[i] = lim;
-    };
-    for (int32_t i = 0; i < nt; ++i) {
-      const int32_t s = task.seg[i], p = task.pos[i];
+  void visible(const Task& task, Pred include, std::vector<VisRange>& out) {
+    touched_.clear();
+    const int32_t e = task.begin + task.count;
+    for (int32_t i = task.begin; i < e; ++i) {
+      const int32_t s = tseg[i];
       for (const auto& a : anc_[s])
-        if (a.second > 0 && include(a.first)) put(a.first, i, a.second);
-      if (include(s)) put(s, i, p + 1);
+        if (a.second > 0 && include(a.first)) touch(a.first);
+      if (include(s)) touch(s);
     }
-    std::vector<VisRange> out;
-    for (auto& kv : per) {
-      VisRange r;
-      r.t = kv.first;
-      r.lim = std::move(kv.second);
-      r.n_keys = *std::max_element(r.lim.begin(), r.lim.end());
-      if (r.n_keys > 0) out.push_back(std::move(r));
+    std::sort(touched_.begin(), touched_.end());
+    for (int32_t t : touched_) {
+      slot_[t] = (int32_t)out.size();
+      out.push_back({t, 0, (int64_t)vlim.size()});
+      vlim.resize(vlim.size() + task.count, 0);
     }
-    return out;
+    for (int32_t i = task.begin; i < e; ++i) {
+      const int32_t s = tseg[i], k = i - task.begin;
+      for (const auto& a : anc_[s])
+        if (a.second > 0 && include(a.first)) set(out[slot_[a.first]], k, a.second);
+      if (include(s)) set(out[slot_[s]], k, tpos[i] + 1);
+    }
+    for (int32_t t : touched_) slot_[t] = -1;
   }
 
   int32_t add_tokens(const Task& task) {
     const int32_t begin = (int32_t)P.toks.size();
-    for (size_t i = 0; i < task.seg.size(); ++i) {
-      const padoc_segment& s = P.seg[task.seg[i]];
-      const int32_t p = task.pos[i];
-      P.toks.push_back((int32_t)(s.q_off + (p - (s.len - s.q_len))));
+    for (int32_t i = task.begin; i < task.begin + task.count; ++i) {
+      const padoc_segment& s = P.seg[tseg[i]];
+      P.toks.push_back((int32_t)(s.q_off + (tpos[i] - (s.len - s.q_len))));
     }
     return begin;
   }
 
-  // Emit the range records of `pieces`; returns {rng_begin, rng_count, cost}
-  // and marks in `sees` the tokens that see at least one key.
-  void emit_ranges(const std::vector<Piece>& pieces, int32_t ntok, int32_t& rng_begin,
-                   int32_t& rng_count, int32_t& cost, std::vector<char>& sees) {
+  // Emit the range records of pieces[0 .. n_pieces) (ranges of `vis`);
+  // returns {rng_begin, rng_count, cost} and marks in sees[] the tokens that
+  // see at least one key.
+  void emit_ranges(const std::vector<VisRange>& vis, const Piece* pieces, size_t n_pieces, int32_t ntok,
+                   int32_t& rng_begin, int32_t& rng_count, int32_t& cost) {
     rng_begin = (int32_t)P.ranges.size();
     rng_count = 0;
     cost = 1;
     sees.assign(ntok, 0);
-    std::vector<int32_t> l(ntok);
-    for (const Piece& pc : pieces) {
+    l_.resize(ntok);
+    for (size_t k = 0; k < n_pieces; ++k) {
+      const Piece& pc = pieces[k];
+      const VisRange& r = vis[pc.r];
+      const int32_t* lim = vlim.data() + r.lim_off;
       int32_t mx = 0, mn = std::numeric_limits<int32_t>::max();
       for (int32_t i = 0; i < ntok; ++i) {
-        int32_t v = pc.r->lim[i] - pc.kb;
+        int32_t v = lim[i] - pc.kb;
         v = v < 0 ? 0 : (v > pc.len ? pc.len : v);
-        l[i] = v;
+        l_[i] = v;
         mx = std::max(mx, v);
         mn = std::min(mn, v);
         if (v > 0) sees[i] = 1;
       }
       if (mx == 0) continue;
-      const padoc_segment& t = P.seg[pc.r->t];
+      const padoc_segment& t = P.seg[r.t];
       padoc::RangeRec rr{};
       rr.kv_start = P.block_size ? t.kv_off + pc.kb / P.block_size : t.kv_off + pc.kb;
       rr.n_keys = mx;
       rr.min_lim = mn;
-      rr.seg = pc.r->t;
+      rr.seg = r.t;
       rr.key_begin = pc.kb;
       if (mn == mx) {
         rr.lim_off = -1;
       } else {
         rr.lim_off = (int32_t)P.lims.size();
-        P.lims.insert(P.lims.end(), l.begin(), l.end());
+        P.lims.insert(P.lims.end(), l_.begin(), l_.end());
       }
-      P.tile_class_off.push_back((int64_t)P.tile_class.size());
-      const int32_t nkt = (int32_t)ceil_div(mx, P.tile_keys);
-      for (int32_t kt = 0; kt < nkt; ++kt)
-        P.tile_class.push_back((int64_t)(kt + 1) * P.tile_keys <= mn ? 1 : 2);
       P.ranges.push_back(rr);
       ++rng_count;
-      cost += nkt;
+      cost += (int32_t)ceil_div(mx, P.tile_keys);
     }
   }
 
-  padoc_plan& P;
-
  private:
-  const std::vector<std::vector<std::pair<int32_t, int32_t>>>& anc_;
+  void touch(int32_t t) {
+    if (slot_[t] == -1) {
+      slot_[t] = -2;
+      touched_.push_back(t);
+    }
+  }
+  void set(VisRange& r, int32_t k, int32_t lim) {
+    vlim[r.lim_off + k] = lim;
+    r.n_keys = std::max(r.n_keys, lim);
+  }
+
+  const AncList& anc_;
+  std::vector<int32_t>&slot_, &touched_, &l_;
 };
 
 padoc_status validate(const padoc_tree_desc* d) {
@@ -243,14 +313,13 @@ void build_forward(padoc_plan& P, Builder& B) {
   // Tokens are packed into tasks of tile_tokens; consecutive siblings share
   // tasks (their ancestor ranges coincide), a root starts its own.
   const int32_t n = (int32_t)P.seg.size();
-  std::vector<Task> tasks;
-  Task cur;
+  auto& tasks = B.S.tasks;
+  tasks.clear();
+  Task cur{0, 0};
   int64_t group = std::numeric_limits<int64_t>::min();
   auto flush = [&] {
-    if (!cur.seg.empty()) {
-      tasks.push_back(std::move(cur));
-      cur = Task();
-    }
+    if (cur.count > 0) tasks.push_back(cur);
+    cur = {(int32_t)B.tseg.size(), 0};
   };
   for (int32_t s = 0; s < n; ++s) {
     const padoc_segment& sg = P.seg[s];
@@ -261,32 +330,34 @@ void build_forward(padoc_plan& P, Builder& B) {
       group = g;
     }
     for (int32_t p = sg.len - sg.q_len; p < sg.len; ++p) {
-      cur.seg.push_back(s);
-      cur.pos.push_back(p);
-      if ((int32_t)cur.seg.size() == P.tile_tokens) flush();
+      B.tseg.push_back(s);
+      B.tpos.push_back(p);
+      if (++cur.count == P.tile_tokens) flush();
     }
   }
   flush();
-  std::vector<char> sees;
+  auto& vis = B.S.vis;
+  auto& pieces = B.S.pieces;
   for (const Task& task : tasks) {
-    auto vis = B.visible(task, [](int32_t) { return true; });
-    std::vector<Piece> pieces;
-    for (const auto& r : vis) pieces.push_back({&r, 0, r.n_keys});
-    const int32_t ntok = (int32_t)task.seg.size();
+    vis.clear();
+    B.vlim.clear();
+    B.visible(task, [](int32_t) { return true; }, vis);
+    pieces.clear();
+    for (size_t r = 0; r < vis.size(); ++r) pieces.push_back({(int32_t)r, 0, vis[r].n_keys});
     const int32_t tok_begin = B.add_tokens(task);
     int32_t rb, rc, cost;
-    B.emit_ranges(pieces, ntok, rb, rc, cost, sees);
+    B.emit_ranges(vis, pieces.data(), pieces.size(), task.count, rb, rc, cost);
     for (int32_t g = 0; g < P.Hkv; ++g) {
       padoc::WorkRec w{};
       w.tok_begin = tok_begin;
-      w.ntok = ntok;
+      w.ntok = task.count;
       w.rng_begin = rb;
       w.rng_count = rc;
       w.kvh = g;
       w.out_base = 0;
       w.cost = cost;
       w.col0 = 0;
-      w.ncol = ntok * P.G;
+      w.ncol = task.count * P.G;
       P.work.push_back(w);
     }
   }
@@ -302,8 +373,7 @@ void build_forward(padoc_plan& P, Builder& B) {
 // 32-column blocks (total / (target_workgroups / 4), at least 64 blocks) are
 // cut into equal block-aligned pieces, whose items add into the same dK/dV
 // rows; whole runs store their rows.
-void build_backward(padoc_plan& P, const std::vector<std::vector<std::pair<int32_t, int32_t>>>& anc,
-                    int32_t target_workgroups) {
+void build_backward(padoc_plan& P, const AncList& anc, int32_t target_workgroups) {
   const int32_t n = (int32_t)P.seg.size();
   std::vector<std::vector<std::pair<int32_t, int32_t>>> desc(n);  // (s, F(s, t)) per t
   for (int32_t s = 0; s < n; ++s)
@@ -376,57 +446,72 @@ void build_backward(padoc_plan& P, const std::vector<std::vector<std::pair<int32
 // HBM once per item and key chunk).  Private keys are streamed by wavefront
 // items of 16 columns.  Both kinds write split partials; the combine map lists
 // them per (query row, KV head) in creation order.
-void build_decode(padoc_plan& P, Builder& B, const std::vector<std::vector<std::pair<int32_t, int32_t>>>& anc,
-                  const padoc_tree_desc* d) {
+void build_decode(padoc_plan& P, Builder& B, const AncList& anc, const padoc_tree_desc* d) {
   const int32_t n = (int32_t)P.seg.size();
   const int32_t G = P.G;
   const int32_t NTs = std::max(1, kTileCols / G);
   const int32_t NTp = std::max(1, kPrivateCols / G);
-  std::vector<int64_t> viewers(n, 0);
+  Scratch& S = B.S;
+  auto& viewers = S.viewers;
+  viewers.assign(n, 0);
   for (int32_t s = 0; s < n; ++s)
     if (P.seg[s].q_len > 0)
       for (const auto& a : anc[s])
         if (a.second > 0) viewers[a.first] += P.seg[s].q_len;
   auto shared = [&](int32_t t) { return viewers[t] > 0; };
   auto priv = [&](int32_t t) { return viewers[t] == 0; };
-  std::vector<int32_t> root(n);
+  auto& root = S.root;
+  root.resize(n);
   for (int32_t s = 0; s < n; ++s) root[s] = P.seg[s].parent < 0 ? s : root[P.seg[s].parent];
 
-  std::vector<Task> stasks, ptasks;
+  // Shared tasks: per page (ascending root), the query tokens of every
+  // segment that sees a shared key, in segment then position order, cut
+  // into tasks of NTs tokens.  Private tasks: NTp consecutive query tokens
+  // of one private segment.
+  auto& stasks = S.stasks;
+  auto& ptasks = S.ptasks;
+  stasks.clear();
+  ptasks.clear();
   {
-    std::map<int32_t, Task> per_page;
+    auto sees_shared = [&](int32_t s) {
+      if (P.seg[s].q_len == 0) return false;
+      if (shared(s)) return true;
+      for (const auto& a : anc[s])
+        if (a.second > 0) return true;
+      return false;
+    };
+    auto& at = S.at;
+    at.assign(n + 1, 0);
+    for (int32_t s = 0; s < n; ++s)
+      if (sees_shared(s)) at[root[s] + 1] += P.seg[s].q_len;
+    for (int32_t r = 0; r < n; ++r) at[r + 1] += at[r];
+    const int32_t total = at[n];
+    B.tseg.resize(total);
+    B.tpos.resize(total);
+    auto& fill = S.fill;
+    fill.assign(at.begin(), at.end() - 1);
     for (int32_t s = 0; s < n; ++s) {
+      if (!sees_shared(s)) continue;
       const padoc_segment& sg = P.seg[s];
-      if (sg.q_len == 0) continue;
-      bool any_anc = false;
-      for (const auto& a : anc[s]) any_anc |= a.second > 0;
-      if (!any_anc && !shared(s)) continue;
-      Task& t = per_page[root[s]];
       for (int32_t p = sg.len - sg.q_len; p < sg.len; ++p) {
-        t.seg.push_back(s);
-        t.pos.push_back(p);
+        const int32_t i = fill[root[s]]++;
+        B.tseg[i] = s;
+        B.tpos[i] = p;
       }
     }
-    for (auto& kv : per_page) {
-      const Task& all = kv.second;
-      for (size_t b = 0; b < all.seg.size(); b += NTs) {
-        Task t;
-        const size_t e = std::min(all.seg.size(), b + (size_t)NTs);
-        t.seg.assign(all.seg.begin() + b, all.seg.begin() + e);
-        t.pos.assign(all.pos.begin() + b, all.pos.begin() + e);
-        stasks.push_back(std::move(t));
-      }
-    }
+    for (int32_t r = 0; r < n; ++r)
+      for (int32_t b = at[r]; b < at[r + 1]; b += NTs) stasks.push_back({b, std::min(NTs, at[r + 1] - b)});
     for (int32_t s = 0; s < n; ++s) {
       const padoc_segment& sg = P.seg[s];
       if (sg.q_len == 0 || shared(s)) continue;
       for (int32_t b = sg.len - sg.q_len; b < sg.len; b += NTp) {
-        Task t;
+        Task t{(int32_t)B.tseg.size(), 0};
         for (int32_t p = b; p < std::min(sg.len, b + NTp); ++p) {
-          t.seg.push_back(s);
-          t.pos.push_back(p);
+          B.tseg.push_back(s);
+          B.tpos.push_back(p);
+          ++t.count;
         }
-        ptasks.push_back(std::move(t));
+        ptasks.push_back(t);
       }
     }
   }
@@ -434,16 +519,25 @@ void build_decode(padoc_plan& P, Builder& B, const std::vector<std::vector<std::
   // worth of wavefronts) per target_workgroups / 4, since every extra chunk
   // costs a round of split partials.  Private keys: about
   // target_workgroups x 2 wavefronts' worth of equal pieces.
-  std::vector<std::vector<VisRange>> svis, pvis;
+  auto& svis = S.svis;
+  auto& pvis = S.pvis;
+  auto& svis_at = S.svis_at;
+  auto& pvis_at = S.pvis_at;
+  svis.clear();
+  pvis.clear();
+  svis_at.assign(1, 0);
+  pvis_at.assign(1, 0);
   int64_t total_s = 0, total_p = 0;
   for (const Task& t : stasks) {
-    svis.push_back(B.visible(t, shared));
-    for (const auto& r : svis.back()) total_s += round_up(r.n_keys, 64) * P.Hkv;
+    B.visible(t, shared, svis);
+    for (size_t r = svis_at.back(); r < svis.size(); ++r) total_s += round_up(svis[r].n_keys, 64) * P.Hkv;
+    svis_at.push_back(svis.size());
   }
   for (const Task& t : ptasks) {
-    pvis.push_back(B.visible(t, priv));
-    const int64_t splits = ceil_div((int64_t)t.seg.size() * G, kPrivateCols);
-    for (const auto& r : pvis.back()) total_p += round_up(r.n_keys, 32) * P.Hkv * splits;
+    B.visible(t, priv, pvis);
+    const int64_t splits = ceil_div((int64_t)t.count * G, kPrivateCols);
+    for (size_t r = pvis_at.back(); r < pvis.size(); ++r) total_p += round_up(pvis[r].n_keys, 32) * P.Hkv * splits;
+    pvis_at.push_back(pvis.size());
   }
   const int64_t tw = d->target_workgroups > 0 ? d->target_workgroups : 1024;
   auto chunk_keys = [&](int64_t total, int64_t pieces) {
@@ -453,39 +547,24 @@ void build_decode(padoc_plan& P, Builder& B, const std::vector<std::vector<std::
   };
   const int64_t CHs = chunk_keys(total_s, std::max<int64_t>(1, tw / 4));
   const int64_t CHp = chunk_keys(total_p, 2 * tw);
-  auto cut = [&](const std::vector<VisRange>& vis, int64_t CH) {
-    std::vector<std::vector<Piece>> chunks(1);
-    int64_t room = CH;
-    for (const auto& r : vis) {
-      int32_t kb = 0;
-      while (kb < r.n_keys) {
-        if (room <= 0) {
-          chunks.emplace_back();
-          room = CH;
-        }
-        const int32_t take = (int32_t)std::min<int64_t>(r.n_keys - kb, room);
-        chunks.back().push_back({&r, kb, take});
-        kb += take;
-        room -= round_up(take, 64);
-      }
-    }
-    if (chunks.back().empty()) chunks.pop_back();
-    return chunks;
-  };
 
-  std::vector<std::vector<int32_t>> comb((size_t)P.num_q_rows * P.Hkv);
-  std::vector<char> sees;
-  std::vector<padoc::WorkRec> sitems, pitems;
-  auto emit = [&](const Task& task, int32_t tok_begin, const std::vector<Piece>& pieces, int32_t width,
-                  std::vector<padoc::WorkRec>& out) {
-    const int32_t ntok = (int32_t)task.seg.size();
+  // (row * Hkv + kvh, slot) of every partial, in creation order.
+  auto& parts = S.parts;
+  auto& sitems = S.sitems;
+  auto& pitems = S.pitems;
+  parts.clear();
+  sitems.clear();
+  pitems.clear();
+  auto emit = [&](const Task& task, int32_t tok_begin, const std::vector<VisRange>& vis, const Piece* pieces,
+                  size_t n_pieces, int32_t width, std::vector<padoc::WorkRec>& out) {
+    const int32_t ntok = task.count;
     int32_t rb, rc, cost;
-    B.emit_ranges(pieces, ntok, rb, rc, cost, sees);
+    B.emit_ranges(vis, pieces, n_pieces, ntok, rb, rc, cost);
     if (rc == 0) return;
     for (int32_t kvh = 0; kvh < P.Hkv; ++kvh) {
       const int32_t base = (int32_t)P.n_slots;
       for (int32_t i = 0; i < ntok; ++i)
-        if (sees[i]) comb[(size_t)P.toks[tok_begin + i] * P.Hkv + kvh].push_back(base + i * G);
+        if (B.sees[i]) parts.push_back({(size_t)P.toks[tok_begin + i] * P.Hkv + kvh, base + i * G});
       P.n_slots += (int64_t)ntok * G;
       for (int32_t c0 = 0; c0 < ntok * G; c0 += width) {
         padoc::WorkRec w{};
@@ -502,20 +581,50 @@ void build_decode(padoc_plan& P, Builder& B, const std::vector<std::vector<std::
       }
     }
   };
+  // Cut the visible ranges vis[r0 .. r1) into chunks of at most CH keys
+  // (each piece counted rounded up to 64) and emit each chunk; returns the
+  // number of chunks.
+  auto& chunk = S.pieces;
+  auto cut_emit = [&](const Task& task, int32_t tok_begin, const std::vector<VisRange>& vis, size_t r0, size_t r1,
+                      int64_t CH, int32_t width, std::vector<padoc::WorkRec>& out) {
+    int32_t n_chunks = 0;
+    int64_t room = CH;
+    chunk.clear();
+    for (size_t r = r0; r < r1; ++r) {
+      int32_t kb = 0;
+      while (kb < vis[r].n_keys) {
+        if (room <= 0) {
+          emit(task, tok_begin, vis, chunk.data(), chunk.size(), width, out);
+          ++n_chunks;
+          chunk.clear();
+          room = CH;
+        }
+        const int32_t take = (int32_t)std::min<int64_t>(vis[r].n_keys - kb, room);
+        chunk.push_back({(int32_t)r, kb, take});
+        kb += take;
+        room -= round_up(take, 64);
+      }
+    }
+    if (!chunk.empty()) {
+      emit(task, tok_begin, vis, chunk.data(), chunk.size(), width, out);
+      ++n_chunks;
+    }
+    return n_chunks;
+  };
   for (size_t i = 0; i < stasks.size(); ++i) {
     const int32_t tb = B.add_tokens(stasks[i]);
-    for (const auto& chunk : cut(svis[i], CHs)) emit(stasks[i], tb, chunk, kTileCols, sitems);
+    cut_emit(stasks[i], tb, svis, svis_at[i], svis_at[i + 1], CHs, kTileCols, sitems);
   }
   // A private task cut into a single chunk finishes its rows in the
   // streaming kernel (bf16): every other partial of those rows comes from a
   // shared item, which runs earlier on the same stream.
-  std::vector<char> finished((size_t)P.num_q_rows * P.Hkv, 0);
+  auto& finished = S.finished;
+  finished.assign((size_t)P.num_q_rows * P.Hkv, 0);
   for (size_t i = 0; i < ptasks.size(); ++i) {
     const int32_t tb = B.add_tokens(ptasks[i]);
-    const auto chunks = cut(pvis[i], CHp);
     const size_t first = pitems.size();
-    for (const auto& chunk : chunks) emit(ptasks[i], tb, chunk, kPrivateCols, pitems);
-    if (P.dtype == PADOC_BF16 && chunks.size() == 1) {
+    const int32_t n_chunks = cut_emit(ptasks[i], tb, pvis, pvis_at[i], pvis_at[i + 1], CHp, kPrivateCols, pitems);
+    if (P.dtype == PADOC_BF16 && n_chunks == 1) {
       for (size_t j = first; j < pitems.size(); ++j) {
         pitems[j].fin = 1;
         for (int32_t t = 0; t < pitems[j].ntok; ++t)
@@ -523,19 +632,27 @@ void build_decode(padoc_plan& P, Builder& B, const std::vector<std::vector<std::
       }
     }
   }
-  auto by_cost = [](const padoc::WorkRec& a, const padoc::WorkRec& b) { return a.cost > b.cost; };
-  std::stable_sort(sitems.begin(), sitems.end(), by_cost);
-  std::stable_sort(pitems.begin(), pitems.end(), by_cost);
-  P.work = sitems;
+  sort_by_cost(sitems, S.tmp);
+  sort_by_cost(pitems, S.tmp);
+  P.work.reserve(sitems.size() + pitems.size());
+  P.work.assign(sitems.begin(), sitems.end());
   P.work.insert(P.work.end(), pitems.begin(), pitems.end());
   P.n_work_shared = (int32_t)sitems.size();
 
-  P.comb_ptr.assign(comb.size() + 1, 0);
-  for (size_t r = 0; r < comb.size(); ++r) P.comb_ptr[r + 1] = P.comb_ptr[r] + (int32_t)comb[r].size();
-  P.comb_slot.reserve(P.comb_ptr.back());
-  for (const auto& c : comb) P.comb_slot.insert(P.comb_slot.end(), c.begin(), c.end());
-  for (size_t r = 0; r < comb.size(); ++r)
-    if (!comb[r].empty() && !finished[r]) P.comb_rows.push_back((int32_t)r);
+  // Combine map: slots per (row, KV head) in creation order (stable counting
+  // sort of the partials by row).
+  const size_t n_rows = (size_t)P.num_q_rows * P.Hkv;
+  P.comb_ptr.assign(n_rows + 1, 0);
+  for (const auto& pr : parts) ++P.comb_ptr[pr.first + 1];
+  for (size_t r = 0; r < n_rows; ++r) P.comb_ptr[r + 1] += P.comb_ptr[r];
+  P.comb_slot.resize(parts.size());
+  {
+    auto& fill = S.fill;
+    fill.assign(P.comb_ptr.begin(), P.comb_ptr.end() - 1);
+    for (const auto& pr : parts) P.comb_slot[fill[pr.first]++] = pr.second;
+  }
+  for (size_t r = 0; r < n_rows; ++r)
+    if (P.comb_ptr[r + 1] > P.comb_ptr[r] && !finished[r]) P.comb_rows.push_back((int32_t)r);
 }
 
 template <class T>
@@ -586,6 +703,85 @@ void serialise(padoc_plan& P) {
 }
 
 }  // namespace
+
+padoc_status build_plan(const padoc_tree_desc* d, padoc_plan& P) {
+  padoc_status st = validate(d);
+  if (st != PADOC_OK) return st;
+  try {
+    P.kind = d->block_size == 0 ? 0 : 1;
+    P.Hq = d->num_heads_q;
+    P.Hkv = d->num_heads_kv;
+    P.G = d->num_heads_q / d->num_heads_kv;
+    P.D = d->head_dim;
+    P.scale = d->softmax_scale;
+    P.dtype = d->dtype;
+    P.block_size = d->block_size;
+    P.num_kv_rows = d->num_kv_rows;
+    P.num_q_rows = d->num_q_rows;
+    P.block_table_len = d->block_table_len;
+    P.seg.assign(d->seg, d->seg + d->n_seg);
+    P.tile_cols = kTileCols;
+    P.tile_keys = P.kind == 1 ? 32 : kTileKeys;  // decode ranges are classified per 32-key step
+    P.tile_tokens = std::max(1, P.tile_cols / P.G);
+    P.work.clear();
+    P.n_work_shared = 0;
+    P.ranges.clear();
+    P.lims.clear();
+    P.toks.clear();
+    {
+      std::lock_guard<std::mutex> lk(P.tc_mu);
+      P.tc_built = false;
+      P.tile_class.clear();
+      P.tile_class_off.clear();
+    }
+    P.comb_ptr.clear();
+    P.comb_slot.clear();
+    P.comb_rows.clear();
+    P.n_slots = 0;
+    P.bwd.clear();
+    P.btoks.clear();
+    P.blims.clear();
+    P.bwd_blob.clear();
+    P.blob.clear();
+    Scratch& S = t_scratch;
+    AncList& anc = S.anc;
+    anc.off.assign((size_t)d->n_seg + 1, 0);
+    for (int32_t s = 0; s < d->n_seg; ++s) {
+      const int32_t par = P.seg[s].parent;
+      anc.off[s + 1] = anc.off[s] + (par >= 0 ? anc.off[par + 1] - anc.off[par] + 1 : 0);
+    }
+    anc.a.resize((size_t)anc.off[d->n_seg]);
+    for (int32_t s = 0; s < d->n_seg; ++s) {
+      const int32_t par = P.seg[s].parent;
+      if (par < 0) continue;
+      std::copy(anc.a.begin() + anc.off[par], anc.a.begin() + anc.off[par + 1], anc.a.begin() + anc.off[s]);
+      anc.a[anc.off[s + 1] - 1] = {par, P.seg[s].fork};
+    }
+    Builder B(P, S);
+    if (P.kind == 0)
+      build_forward(P, B);
+    else
+      build_decode(P, B, anc, d);
+    if (P.n_slots > kI32Max) return set_error(PADOC_ERR_ARG, "schedule too large (%lld partial slots)", (long long)P.n_slots);
+    if ((int64_t)P.lims.size() > kI32Max || (int64_t)P.ranges.size() > kI32Max)
+      return set_error(PADOC_ERR_ARG, "schedule too large");
+    // Costliest items first: the hardware dispatcher then assigns work
+    // greedily to the first free compute unit (longest-processing-time
+    // order).  Decode items are already ordered by workgroup.
+    if (P.kind == 0) sort_by_cost(P.work, S.tmp);
+    serialise(P);
+    if (P.kind == 0 && P.dtype == PADOC_BF16) {
+      build_backward(P, anc, d->target_workgroups);
+      if ((int64_t)P.btoks.size() > kI32Max || (int64_t)P.bwd.size() > kI32Max)
+        return set_error(PADOC_ERR_ARG, "backward schedule too large");
+      serialise_backward(P);
+    }
+  } catch (const std::bad_alloc&) {
+    return set_error(PADOC_ERR_ARG, "out of host memory while planning");
+  }
+  return PADOC_OK;
+}
+
 }  // namespace padoc
 
 using namespace padoc;
@@ -641,58 +837,11 @@ extern "C" padoc_status padoc_plan_create(const padoc_tree_desc* d, padoc_plan**
   if (!out) return set_error(PADOC_ERR_ARG, "out is null");
   *out = nullptr;
   if (!d) return set_error(PADOC_ERR_ARG, "desc is null");
-  padoc_status st = validate(d);
-  if (st != PADOC_OK) return st;
-  try {
-    std::unique_ptr<padoc_plan> P(new padoc_plan());
-    P->kind = d->block_size == 0 ? 0 : 1;
-    P->Hq = d->num_heads_q;
-    P->Hkv = d->num_heads_kv;
-    P->G = d->num_heads_q / d->num_heads_kv;
-    P->D = d->head_dim;
-    P->scale = d->softmax_scale;
-    P->dtype = d->dtype;
-    P->block_size = d->block_size;
-    P->num_kv_rows = d->num_kv_rows;
-    P->num_q_rows = d->num_q_rows;
-    P->block_table_len = d->block_table_len;
-    P->seg.assign(d->seg, d->seg + d->n_seg);
-    if (P->kind == 1) P->tile_keys = 32;  // decode ranges are classified per 32-key step
-    P->tile_tokens = std::max(1, P->tile_cols / P->G);
-    std::vector<std::vector<std::pair<int32_t, int32_t>>> anc(d->n_seg);
-    for (int32_t s = 0; s < d->n_seg; ++s) {
-      const int32_t par = P->seg[s].parent;
-      if (par >= 0) {
-        anc[s] = anc[par];
-        anc[s].push_back({par, P->seg[s].fork});
-      }
-    }
-    Builder B(*P, anc);
-    if (P->kind == 0)
-      build_forward(*P, B);
-    else
-      build_decode(*P, B, anc, d);
-    if (P->n_slots > kI32Max) return set_error(PADOC_ERR_ARG, "schedule too large (%lld partial slots)", (long long)P->n_slots);
-    if ((int64_t)P->lims.size() > kI32Max || (int64_t)P->ranges.size() > kI32Max)
-      return set_error(PADOC_ERR_ARG, "schedule too large");
-    // Costliest items first: the hardware dispatcher then assigns work
-    // greedily to the first free compute unit (longest-processing-time
-    // order).  Decode items are already ordered by workgroup.
-    if (P->kind == 0)
-      std::stable_sort(P->work.begin(), P->work.end(),
-                       [](const padoc::WorkRec& a, const padoc::WorkRec& b) { return a.cost > b.cost; });
-    serialise(*P);
-    if (P->kind == 0 && P->dtype == PADOC_BF16) {
-      build_backward(*P, anc, d->target_workgroups);
-      if ((int64_t)P->btoks.size() > kI32Max || (int64_t)P->bwd.size() > kI32Max)
-        return set_error(PADOC_ERR_ARG, "backward schedule too large");
-      serialise_backward(*P);
-    }
-    *out = P.release();
-  } catch (const std::bad_alloc&) {
-    return set_error(PADOC_ERR_ARG, "out of host memory while planning");
-  }
-  return PADOC_OK;
+  std::unique_ptr<padoc_plan> P(new (std::nothrow) padoc_plan());
+  if (!P) return set_error(PADOC_ERR_ARG, "out of host memory while planning");
+  const padoc_status st = padoc::build_plan(d, *P);
+  if (st == PADOC_OK) *out = P.release();
+  return st;
 }
 
 extern "C" padoc_status padoc_plan_workspace_bytes(const padoc_plan* plan, size_t* bytes) {
@@ -727,6 +876,21 @@ extern "C" padoc_status padoc_plan_export(const padoc_plan* P, padoc_schedule_vi
   v->lims = P->lims.data();
   v->n_tok = (int32_t)P->toks.size();
   v->toks = P->toks.data();
+  // Tile classes are derived from the ranges on the first export (the
+  // kernels classify tiles from n_keys and min_lim themselves).
+  {
+    std::lock_guard<std::mutex> lk(P->tc_mu);
+    if (!P->tc_built) {
+      P->tile_class_off.reserve(P->ranges.size());
+      for (const auto& r : P->ranges) {
+        P->tile_class_off.push_back((int64_t)P->tile_class.size());
+        const int32_t nkt = (int32_t)ceil_div(r.n_keys, P->tile_keys);
+        for (int32_t kt = 0; kt < nkt; ++kt)
+          P->tile_class.push_back((int64_t)(kt + 1) * P->tile_keys <= r.min_lim ? 1 : 2);
+      }
+      P->tc_built = true;
+    }
+  }
   v->n_tile_class = (int64_t)P->tile_class.size();
   v->tile_class = P->tile_class.data();
   v->tile_class_off = P->tile_class_off.data();

@@ -29,8 +29,11 @@ struct padoc_plan {
   std::vector<padoc::RangeRec> ranges;
   std::vector<int32_t> lims;
   std::vector<int32_t> toks;
-  std::vector<int8_t> tile_class;
-  std::vector<int64_t> tile_class_off;  // per range: first entry in tile_class
+  // Export only, filled on the first padoc_plan_export after a build.
+  mutable std::vector<int8_t> tile_class;
+  mutable std::vector<int64_t> tile_class_off;  // per range: first entry in tile_class
+  mutable std::mutex tc_mu;
+  mutable bool tc_built = false;
   std::vector<int32_t> comb_ptr;
   std::vector<int32_t> comb_slot;
   std::vector<int32_t> comb_rows;  // (row*Hkv + kvh) pairs the combine kernel merges
@@ -59,6 +62,11 @@ struct padoc_plan {
 };
 
 namespace padoc {
+
+// Validate `desc` and build its schedule into `plan`, replacing what the plan
+// held (its vectors keep their memory, so rebuilding one plan per decode
+// step allocates little).  Host only.
+padoc_status build_plan(const padoc_tree_desc* desc, padoc_plan& plan);
 
 // Thread-local error state shared by every C entry point.
 padoc_status set_error(padoc_status st, const char* fmt, ...);
