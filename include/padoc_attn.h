@@ -271,6 +271,141 @@ padoc_status padoc_tree_attn_bwd(const padoc_plan* plan, const void* q, const vo
                                  const void* dout, void* dq, void* dk, void* dv,
                                  void* workspace, size_t workspace_bytes, hipStream_t stream);
 
+/* ---------------------------------------------------------------------------
+ * Decode session: the step loop of masked parallel decoding (App. E, the
+ * algorithm "Masked parallel decoding": append one input per live stream,
+ * decode every live stream with its mask row, open a content stream when the
+ * layout stream closes a region, retire a stream at its end of sequence).
+ *
+ * A session keeps the token tree of every page being decoded and the
+ * paged-cache blocks its streams occupy.  A stream is one tree segment:
+ * padoc_session_open(parent, fork) starts one whose tokens see the first
+ * `fork` tokens of `parent` (and, through it, what `parent` sees), as a fork
+ * of the fused mask row would (the child's row is the parent's row with
+ * only the first `fork` parent tokens); parent -1 starts a page root.  A
+ * new stream holds no tokens; every step appends tokens to the open streams
+ * and queries the newest of them, so a fork costs no copy of the parent's
+ * cache and no re-prefill: the child reads the parent's blocks in place.
+ *
+ * Typical page: open a root, step once with the prefix as its new tokens
+ * (no queries), open the layout stream (parent = root, fork = prefix
+ * length), close the root (its blocks stay while a descendant is open),
+ * then step with one new token and one query per open stream; when the
+ * layout stream closes a region, open a content stream with parent = the
+ * layout stream and fork = the layout stream's current length; close a
+ * stream at its end of sequence.
+ *
+ * Each step is two calls.  padoc_session_prepare (host only) appends
+ * n_new[i] tokens to open stream i (rows in ascending stream id), takes
+ * blocks from the pool for them, and builds the step's attention schedule
+ * for the last n_query[i] of them.  padoc_session_launch writes the new
+ * tokens' K/V rows into the caches and updates the device block table, then
+ * runs the attention of padoc_branch_decode on the step's tree, all on the
+ * caller's stream.  Between a prepare and its launch (or
+ * padoc_session_commit) no other session call may change the tree.
+ *
+ * Memory: the caller owns the paged K and V caches (layouts as for
+ * padoc_branch_decode, num_blocks blocks) and a device int32 block table of
+ * block_table_capacity entries; the session only writes into them.  The
+ * session keeps a pinned host staging buffer for its uploads (two of them,
+ * reused once the upload two launches back has completed).  A stream's
+ * blocks return to the pool when it is closed and no stream below it is
+ * still kept; its block-table entries live in a power-of-two region of the
+ * table that moves (copied by the next launch) when the stream outgrows it.
+ * A session is not thread-safe; a session's launches must be ordered on the
+ * device (one stream, or events).
+ * ------------------------------------------------------------------------- */
+typedef struct padoc_session padoc_session;
+
+typedef struct {
+  int32_t num_heads_q, num_heads_kv, head_dim;  /* as in padoc_tree_desc      */
+  float softmax_scale;
+  padoc_dtype dtype;                 /* of the caches and the step's tensors   */
+  int64_t num_blocks;                /* blocks in each cache (the pool)        */
+  int64_t block_table_capacity;      /* int32 entries of the device block table */
+  void* k_cache;                     /* device, may be NULL for host-only use  */
+  void* v_cache;                     /* (then padoc_session_launch is refused) */
+  int32_t* block_table;
+  int32_t max_chunk_keys, target_workgroups;  /* decode schedule, as in
+                                                 padoc_tree_desc               */
+} padoc_session_desc;
+
+/* The prepared step, for inspection and for callers that do the device work
+   themselves.  Pointers stay valid until the next session call that changes
+   the tree. */
+typedef struct {
+  int32_t n_seg;
+  const padoc_segment* seg;     /* the step's tree: every kept stream in id
+                                   order, parent as an index into seg,
+                                   kv_off = first block-table entry, len after
+                                   the step's appends, q_len = n_query       */
+  const int32_t* seg_id;        /* stream id of each segment                 */
+  int32_t n_rows;               /* open streams, ascending id                */
+  const int32_t* row_id;
+  const int32_t* new_off;       /* n_rows + 1: new K/V rows of row i are
+                                   new_off[i] .. new_off[i+1]-1              */
+  const int32_t* q_off;         /* n_rows + 1: Q/O/LSE rows, same form       */
+  const int32_t* new_slot;      /* per new K/V row: (block id, slot) pairs   */
+  int32_t n_patch;
+  const int32_t* patch;         /* (block-table entry, block id) pairs the
+                                   launch writes into the device table       */
+  const int32_t* block_table;   /* host copy of the table after the patches
+                                   (block_table_capacity entries; unused
+                                   entries -1)                               */
+  const padoc_plan* plan;       /* the step's schedule (num_q_rows = q_off
+                                   [n_rows]); usable with padoc_branch_decode
+                                   once the patches and K/V rows are written */
+  int64_t free_blocks;          /* pool blocks free after the step           */
+  size_t workspace_bytes;       /* for padoc_session_launch                  */
+} padoc_session_view;
+
+/* Create / destroy.  Destroy waits for nothing: call it after the stream
+   has passed the session's last launch. */
+padoc_status padoc_session_create(const padoc_session_desc* desc, padoc_session** out);
+void padoc_session_destroy(padoc_session* session);
+
+/* Open a stream under `parent` (a kept stream id, or -1 for a new page root)
+   seeing its first `fork` tokens (0 <= fork <= the parent's current length;
+   roots: 0).  *id receives the new stream's id (ids increase from 0). */
+padoc_status padoc_session_open(padoc_session* session, int32_t parent, int32_t fork, int32_t* id);
+
+/* Close (retire) an open stream: it takes part in no later step.  Closed
+   streams with no kept descendant are released at once, with their blocks
+   and block-table region; a closed stream's tokens stay visible to the
+   streams below it until they are released. */
+padoc_status padoc_session_close(padoc_session* session, int32_t id);
+
+/* Prepare the next step (host only).  n_new / n_query: one entry per open
+   stream in ascending id (NULL = 1 each), 0 <= n_query[i] <= n_new[i].  On
+   success *n_kv_rows / *n_q_rows receive the rows of the launch's k_new/v_new
+   and q/o/lse, and *workspace_bytes the launch's workspace.  Fails with
+   PADOC_ERR_BOUNDS, leaving the session as it was, when the pool or the
+   block table cannot hold the step; with PADOC_ERR_MODE when a prepared
+   step has not been launched or committed. */
+padoc_status padoc_session_prepare(padoc_session* session, const int32_t* n_new, const int32_t* n_query,
+                                   int32_t* n_kv_rows, int32_t* n_q_rows, size_t* workspace_bytes);
+
+/* Run the prepared step: k_new, v_new [n_kv_rows, Hkv, d] (device, packed,
+   the rows of open stream i at new_off[i].. in order), q [n_q_rows, Hq, d],
+   o [n_q_rows, Hq, d], lse float [n_q_rows, Hq]; workspace: device, 256-byte
+   aligned, at least workspace_bytes.  Appends the K/V rows to the caches,
+   applies the block-table patches, then computes O and LSE of every query
+   (as padoc_branch_decode).  On an argument or workspace error nothing is
+   enqueued and the step stays prepared; once enqueueing has begun the step
+   is complete on the host (a HIP error then leaves the caches undefined). */
+padoc_status padoc_session_launch(padoc_session* session, const void* q, const void* k_new, const void* v_new,
+                                  void* o, float* lse, void* workspace, size_t workspace_bytes,
+                                  hipStream_t stream);
+
+/* Complete the prepared step without device work, for callers that write
+   the step's K/V rows and block-table patches themselves (from the view)
+   and run padoc_branch_decode on the view's plan. */
+padoc_status padoc_session_commit(padoc_session* session);
+
+/* View of the prepared step (or, when none is prepared, of the tree as it
+   stands: seg/block table only, plan NULL). */
+padoc_status padoc_session_view_get(const padoc_session* session, padoc_session_view* out);
+
 /* Thread-local description of the last error on this thread ("" if none). */
 const char* padoc_last_error(void);
 

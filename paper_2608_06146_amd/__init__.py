@@ -21,7 +21,7 @@ from . import _lib
 from ._lib import PadocError, SEGMENT_DTYPE, WORK_DTYPE, RANGE_DTYPE, BWD_DTYPE
 
 __all__ = ["TreePlan", "segments_from_pages", "segments_layout", "tree_attn_fwd", "tree_attn_bwd", "branch_decode",
-           "PadocError", "SEGMENT_DTYPE", "version", "set_kernel_events", "make_workspace"]
+           "DecodeSession", "PadocError", "SEGMENT_DTYPE", "version", "set_kernel_events", "make_workspace"]
 
 _DTYPES = {"f32": _lib.F32, "fp32": _lib.F32, "float32": _lib.F32, "bf16": _lib.BF16, "bfloat16": _lib.BF16}
 
@@ -126,27 +126,7 @@ class TreePlan:
 
     def export(self) -> dict:
         """Schedule as numpy arrays (copies)."""
-        v = _lib.ScheduleView()
-        _lib.check(_lib.lib().padoc_plan_export(self.handle, C.byref(v)))
-
-        def arr(ptr, n, dt):
-            if n == 0 or not ptr:
-                return np.zeros(0, dtype=dt)
-            buf = (C.c_char * (n * np.dtype(dt).itemsize)).from_address(ptr)
-            return np.frombuffer(buf, dtype=dt).copy()
-
-        return {
-            "kind": v.kind, "tile_cols": v.tile_cols, "tile_keys": v.tile_keys, "n_work_shared": v.n_work_shared,
-            "work": arr(v.work, v.n_work, WORK_DTYPE), "ranges": arr(v.ranges, v.n_range, RANGE_DTYPE),
-            "lims": arr(v.lims, v.n_lim, np.int32), "toks": arr(v.toks, v.n_tok, np.int32),
-            "tile_class": arr(v.tile_class, v.n_tile_class, np.int8),
-            "tile_class_off": arr(v.tile_class_off, v.n_range, np.int64),
-            "comb_ptr": arr(v.comb_ptr, v.n_comb_ptr, np.int32), "comb_slot": arr(v.comb_slot, v.n_comb, np.int32),
-            "comb_rows": arr(v.comb_rows, v.n_comb_rows, np.int32),
-            "bwd": arr(v.bwd, v.n_bwd, BWD_DTYPE), "btoks": arr(v.btoks, v.n_btok, np.int32),
-            "blims": arr(v.blims, v.n_blim, np.int32),
-            "n_slots": v.n_slots, "workspace_bytes": v.workspace_bytes,
-        }
+        return _export_schedule(self.handle)
 
     def backward_workspace_bytes(self) -> int:
         n = C.c_size_t(0)
@@ -171,6 +151,31 @@ class TreePlan:
             off = (-raw.data_ptr()) % 256
             self._ws = (torch.device(device), raw, raw[off: off + self.workspace_bytes])
         return self._ws[2]
+
+
+def _carray(ptr, n, dt):
+    if n == 0 or not ptr:
+        return np.zeros(0, dtype=dt)
+    buf = (C.c_char * (int(n) * np.dtype(dt).itemsize)).from_address(ptr)
+    return np.frombuffer(buf, dtype=dt).copy()
+
+
+def _export_schedule(handle) -> dict:
+    v = _lib.ScheduleView()
+    _lib.check(_lib.lib().padoc_plan_export(handle, C.byref(v)))
+    arr = _carray
+    return {
+        "kind": v.kind, "tile_cols": v.tile_cols, "tile_keys": v.tile_keys, "n_work_shared": v.n_work_shared,
+        "work": arr(v.work, v.n_work, WORK_DTYPE), "ranges": arr(v.ranges, v.n_range, RANGE_DTYPE),
+        "lims": arr(v.lims, v.n_lim, np.int32), "toks": arr(v.toks, v.n_tok, np.int32),
+        "tile_class": arr(v.tile_class, v.n_tile_class, np.int8),
+        "tile_class_off": arr(v.tile_class_off, v.n_range, np.int64),
+        "comb_ptr": arr(v.comb_ptr, v.n_comb_ptr, np.int32), "comb_slot": arr(v.comb_slot, v.n_comb, np.int32),
+        "comb_rows": arr(v.comb_rows, v.n_comb_rows, np.int32),
+        "bwd": arr(v.bwd, v.n_bwd, BWD_DTYPE), "btoks": arr(v.btoks, v.n_btok, np.int32),
+        "blims": arr(v.blims, v.n_blim, np.int32),
+        "n_slots": v.n_slots, "workspace_bytes": v.workspace_bytes,
+    }
 
 
 def make_workspace(plan: TreePlan, device):
@@ -267,6 +272,193 @@ def tree_attn_bwd(q, k, v, o, lse, dout, plan: TreePlan, dq=None, dk=None, dv=No
                                               _ptr(dq), _ptr(dk), _ptr(dv), _ptr(ws), ws.numel(),
                                               C.c_void_p(s.cuda_stream)))
     return dq, dk, dv
+
+
+class DecodeSession:
+    """Decode session (``padoc_session_*``): the step loop of masked parallel
+    decoding (App. E) over caller-owned paged caches.
+
+    ``open(parent, fork)`` starts a stream (``parent=-1``: a page root) that
+    sees the first ``fork`` tokens of ``parent``; ``close(id)`` retires one.
+    A step is ``prepare(n_new, n_query)`` (host: grow every open stream by
+    ``n_new[i]`` tokens, plan the attention of the last ``n_query[i]``) then
+    ``launch(q, k_new, v_new)`` (device: append the K/V rows, patch the block
+    table, attention); rows follow ascending open stream id.  Without caches
+    (``k_cache=None``) the session is host-only: steps are completed with
+    ``commit()`` and inspected with ``view()``."""
+
+    def __init__(self, num_heads_q: int, num_heads_kv: int, head_dim: int, num_blocks: int, dtype: str = "bf16",
+                 k_cache=None, v_cache=None, block_table=None, block_table_capacity: Optional[int] = None,
+                 softmax_scale: Optional[float] = None, max_chunk_keys: int = 0, target_workgroups: int = 0):
+        self.num_heads_q, self.num_heads_kv, self.head_dim = num_heads_q, num_heads_kv, head_dim
+        self.dtype = dtype
+        self.num_blocks = int(num_blocks)
+        self.softmax_scale = 1.0 / math.sqrt(head_dim) if softmax_scale is None else softmax_scale
+        dev = (k_cache, v_cache, block_table)
+        if any(t is not None for t in dev) and any(t is None for t in dev):
+            raise ValueError("pass k_cache, v_cache and block_table together (or none of them)")
+        self.k_cache, self.v_cache, self.block_table = k_cache, v_cache, block_table
+        if block_table is not None:
+            import torch
+            dt = torch.bfloat16 if _DTYPES[dtype] == _lib.BF16 else torch.float32
+            dv = k_cache.device
+            _check_tensor("k_cache", k_cache, dt, dv)
+            _check_tensor("v_cache", v_cache, dt, dv)
+            _check_tensor("block_table", block_table, torch.int32, dv)
+            want_k = (self.num_blocks, num_heads_kv, head_dim // 8, 16, 8)
+            want_v = (self.num_blocks, num_heads_kv, head_dim, 16)
+            if tuple(k_cache.shape) != want_k or tuple(v_cache.shape) != want_v:
+                raise ValueError(f"caches must be K {want_k} and V {want_v}")
+            if block_table_capacity is None:
+                block_table_capacity = block_table.numel()
+            if block_table_capacity > block_table.numel():
+                raise ValueError("block_table_capacity exceeds the block table")
+            self.device = dv
+        else:
+            self.device = None
+        if block_table_capacity is None:
+            block_table_capacity = 2 * self.num_blocks + 1024
+        self.block_table_capacity = int(block_table_capacity)
+        desc = _lib.SessionDesc(num_heads_q, num_heads_kv, head_dim, float(self.softmax_scale), _DTYPES[dtype],
+                                self.num_blocks, self.block_table_capacity,
+                                k_cache.data_ptr() if k_cache is not None else None,
+                                v_cache.data_ptr() if v_cache is not None else None,
+                                block_table.data_ptr() if block_table is not None else None,
+                                int(max_chunk_keys), int(target_workgroups))
+        h = C.c_void_p()
+        _lib.check(_lib.lib().padoc_session_create(C.byref(desc), C.byref(h)))
+        self._h = h
+        self.n_open = 0
+        self.n_kv_rows = self.n_q_rows = 0
+        self.workspace_bytes = 0
+        self._ws = None
+
+    @property
+    def handle(self):
+        if self._h is None:
+            raise ValueError("session is closed")
+        return self._h
+
+    def destroy(self):
+        if getattr(self, "_h", None) is not None:
+            _lib.lib().padoc_session_destroy(self._h)
+            self._h = None
+
+    def __del__(self):
+        try:
+            self.destroy()
+        except Exception:
+            pass
+
+    def open(self, parent: int = -1, fork: int = 0) -> int:
+        i = C.c_int32(0)
+        _lib.check(_lib.lib().padoc_session_open(self.handle, int(parent), int(fork), C.byref(i)))
+        self.n_open += 1
+        return int(i.value)
+
+    def close(self, stream_id: int) -> None:
+        _lib.check(_lib.lib().padoc_session_close(self.handle, int(stream_id)))
+        self.n_open -= 1
+
+    def prepare(self, n_new=None, n_query=None):
+        """Returns ``(n_kv_rows, n_q_rows, workspace_bytes)`` of the step."""
+        arrs = []
+        for a in (n_new, n_query):
+            if a is None:
+                arrs.append(None)
+                continue
+            a = np.ascontiguousarray(a, dtype=np.int32)
+            if a.shape != (self.n_open,):
+                raise ValueError(f"need one entry per open stream ({self.n_open}), got shape {a.shape}")
+            arrs.append(a)
+        if (arrs[0] is None) != (arrs[1] is None):
+            raise ValueError("pass n_new and n_query together (or neither: one token and one query each)")
+        nk, nq, ws = C.c_int32(0), C.c_int32(0), C.c_size_t(0)
+        ptr = [a.ctypes.data if a is not None else None for a in arrs]
+        _lib.check(_lib.lib().padoc_session_prepare(self.handle, ptr[0], ptr[1], C.byref(nk), C.byref(nq),
+                                                    C.byref(ws)))
+        self.n_kv_rows, self.n_q_rows, self.workspace_bytes = int(nk.value), int(nq.value), int(ws.value)
+        return self.n_kv_rows, self.n_q_rows, self.workspace_bytes
+
+    def workspace(self):
+        """A cached device workspace of at least the prepared step's size."""
+        import torch
+        need = max(256, self.workspace_bytes)
+        if self._ws is None or self._ws[2].numel() < need:
+            cap = need + need // 4
+            raw = torch.empty(cap + 256, dtype=torch.uint8, device=self.device)
+            off = (-raw.data_ptr()) % 256
+            self._ws = (self.device, raw, raw[off: off + cap])
+        return self._ws[2]
+
+    def launch(self, q, k_new, v_new, out=None, lse=None, workspace=None, stream=None):
+        """Run the prepared step; q ``[n_q_rows, Hq, d]``, k_new / v_new
+        ``[n_kv_rows, Hkv, d]``.  Returns ``(O, LSE)``."""
+        import torch
+        if self.device is None:
+            raise RuntimeError("host-only session: use commit()")
+        dt = self.k_cache.dtype
+        dev = self.device
+        if self.n_kv_rows:
+            for name, t in (("k_new", k_new), ("v_new", v_new)):
+                _check_tensor(name, t, dt, dev)
+                if tuple(t.shape) != (self.n_kv_rows, self.num_heads_kv, self.head_dim):
+                    raise ValueError(f"{name} must be [{self.n_kv_rows}, {self.num_heads_kv}, {self.head_dim}]")
+        if out is None:
+            out = torch.empty(self.n_q_rows, self.num_heads_q, self.head_dim, dtype=dt, device=dev)
+        if lse is None:
+            lse = torch.empty(self.n_q_rows, self.num_heads_q, dtype=torch.float32, device=dev)
+        if self.n_q_rows:
+            _check_tensor("q", q, dt, dev)
+            if tuple(q.shape) != (self.n_q_rows, self.num_heads_q, self.head_dim):
+                raise ValueError(f"q must be [{self.n_q_rows}, {self.num_heads_q}, {self.head_dim}]")
+            _check_tensor("out", out, dt, dev)
+            _check_tensor("lse", lse, torch.float32, dev)
+            if tuple(out.shape) != tuple(q.shape) or tuple(lse.shape) != tuple(q.shape[:2]):
+                raise ValueError("out / lse shape does not match q")
+        ws = self.workspace() if workspace is None else workspace
+        s = torch.cuda.current_stream(dev) if stream is None else stream
+
+        def p(t, n):
+            return _ptr(t) if n else None
+        _lib.check(_lib.lib().padoc_session_launch(self.handle, p(q, self.n_q_rows), p(k_new, self.n_kv_rows),
+                                                   p(v_new, self.n_kv_rows), p(out, self.n_q_rows),
+                                                   p(lse, self.n_q_rows), _ptr(ws), ws.numel(),
+                                                   C.c_void_p(s.cuda_stream)))
+        return out, lse
+
+    def step(self, q, k_new, v_new, n_new=None, n_query=None, **kw):
+        """``prepare`` then ``launch``."""
+        self.prepare(n_new, n_query)
+        return self.launch(q, k_new, v_new, **kw)
+
+    def commit(self) -> None:
+        _lib.check(_lib.lib().padoc_session_commit(self.handle))
+
+    def view(self, schedule: bool = False) -> dict:
+        """The prepared step (or the tree as it stands) as numpy copies."""
+        v = _lib.SessionView()
+        _lib.check(_lib.lib().padoc_session_view_get(self.handle, C.byref(v)))
+        arr = _carray
+        n = v.n_rows
+        prepared = bool(v.plan)
+        out = {
+            "seg": arr(v.seg, v.n_seg, SEGMENT_DTYPE), "seg_id": arr(v.seg_id, v.n_seg, np.int32),
+            "row_id": arr(v.row_id, n, np.int32),
+            "block_table": arr(v.block_table, self.block_table_capacity, np.int32),
+            "free_blocks": int(v.free_blocks), "prepared": prepared,
+        }
+        if prepared:
+            new_off = arr(v.new_off, n + 1, np.int32)
+            out.update({
+                "new_off": new_off, "q_off": arr(v.q_off, n + 1, np.int32),
+                "new_slot": arr(v.new_slot, 2 * int(new_off[-1]), np.int32).reshape(-1, 2),
+                "patch": arr(v.patch, 2 * v.n_patch, np.int32).reshape(-1, 2),
+                "workspace_bytes": int(v.workspace_bytes), "plan": int(v.plan),
+            })
+            if schedule:
+                out["schedule"] = _export_schedule(C.c_void_p(v.plan))
+        return out
 
 
 def set_kernel_events(before=None, after=None):

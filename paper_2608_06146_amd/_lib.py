@@ -67,11 +67,28 @@ class ScheduleView(C.Structure):
                 ("n_slots", C.c_int64), ("workspace_bytes", C.c_size_t)]
 
 
+class SessionDesc(C.Structure):
+    _fields_ = [("num_heads_q", C.c_int32), ("num_heads_kv", C.c_int32), ("head_dim", C.c_int32),
+                ("softmax_scale", C.c_float), ("dtype", C.c_int32), ("num_blocks", C.c_int64),
+                ("block_table_capacity", C.c_int64), ("k_cache", C.c_void_p), ("v_cache", C.c_void_p),
+                ("block_table", C.c_void_p), ("max_chunk_keys", C.c_int32), ("target_workgroups", C.c_int32)]
+
+
+class SessionView(C.Structure):
+    _fields_ = [("n_seg", C.c_int32), ("seg", C.c_void_p), ("seg_id", C.c_void_p),
+                ("n_rows", C.c_int32), ("row_id", C.c_void_p), ("new_off", C.c_void_p), ("q_off", C.c_void_p),
+                ("new_slot", C.c_void_p), ("n_patch", C.c_int32), ("patch", C.c_void_p),
+                ("block_table", C.c_void_p), ("plan", C.c_void_p), ("free_blocks", C.c_int64),
+                ("workspace_bytes", C.c_size_t)]
+
+
 EXPORTED = [
     "padoc_tree_from_pages", "padoc_tree_layout", "padoc_plan_create", "padoc_plan_workspace_bytes",
     "padoc_plan_export", "padoc_plan_destroy", "padoc_tree_attn_fwd", "padoc_branch_decode",
     "padoc_last_error", "padoc_set_kernel_events", "padoc_version",
     "padoc_plan_backward_workspace_bytes", "padoc_tree_attn_bwd",
+    "padoc_session_create", "padoc_session_destroy", "padoc_session_open", "padoc_session_close",
+    "padoc_session_prepare", "padoc_session_launch", "padoc_session_commit", "padoc_session_view_get",
 ]
 
 _lib = None
@@ -98,6 +115,15 @@ def lib():
     L.padoc_branch_decode.argtypes = [vp, vp, vp, vp, vp, vp, vp, vp, sz, vp]
     L.padoc_plan_backward_workspace_bytes.argtypes = [vp, C.POINTER(sz)]
     L.padoc_tree_attn_bwd.argtypes = [vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, sz, vp]
+    L.padoc_session_create.argtypes = [C.POINTER(SessionDesc), C.POINTER(vp)]
+    L.padoc_session_destroy.argtypes = [vp]
+    L.padoc_session_destroy.restype = None
+    L.padoc_session_open.argtypes = [vp, i32, i32, C.POINTER(i32)]
+    L.padoc_session_close.argtypes = [vp, i32]
+    L.padoc_session_prepare.argtypes = [vp, vp, vp, C.POINTER(i32), C.POINTER(i32), C.POINTER(sz)]
+    L.padoc_session_launch.argtypes = [vp, vp, vp, vp, vp, vp, vp, sz, vp]
+    L.padoc_session_commit.argtypes = [vp]
+    L.padoc_session_view_get.argtypes = [vp, C.POINTER(SessionView)]
     L.padoc_last_error.argtypes = []
     L.padoc_last_error.restype = C.c_char_p
     L.padoc_set_kernel_events.argtypes = [vp, vp]
@@ -105,7 +131,9 @@ def lib():
     L.padoc_version.restype = C.c_char_p
     for name in ("padoc_tree_from_pages", "padoc_tree_layout", "padoc_plan_create", "padoc_plan_workspace_bytes",
                  "padoc_plan_export", "padoc_tree_attn_fwd", "padoc_branch_decode", "padoc_set_kernel_events",
-                 "padoc_plan_backward_workspace_bytes", "padoc_tree_attn_bwd"):
+                 "padoc_plan_backward_workspace_bytes", "padoc_tree_attn_bwd", "padoc_session_create",
+                 "padoc_session_open", "padoc_session_close", "padoc_session_prepare", "padoc_session_launch",
+                 "padoc_session_commit", "padoc_session_view_get"):
         getattr(L, name).restype = C.c_int
     _lib = L
     return L

@@ -24,12 +24,14 @@ ARCH = os.environ.get("PADOC_OFFLOAD_ARCH", "gfx950")
 
 SOURCES = [
     "csrc/host/plan.cpp",
+    "csrc/host/session.cpp",
     "csrc/abi.hip",
     "csrc/kernels/tile_mfma_bf16.hip",
     "csrc/kernels/decode_private.hip",
     "csrc/kernels/tile_valu_f32.hip",
     "csrc/kernels/lse_combine.hip",
     "csrc/kernels/bwd.hip",
+    "csrc/kernels/append.hip",
 ]
 # Every header under csrc/ (and the public header) enters each object's
 # digest, so an edit to any of them rebuilds every object.

@@ -5,6 +5,7 @@
 #include <cstring>
 
 #include "host/plan.hpp"
+#include "host/session.hpp"
 
 namespace padoc {
 hipError_t launch_tile_mfma_bf16(const TileParams& p, int n_work, int D, bool paged, hipStream_t s);
@@ -12,6 +13,9 @@ hipError_t launch_decode_private_bf16(const TileParams& p, int n_items, int D, h
 hipError_t launch_tile_valu_f32(const TileParams& p, int n_work, int D, bool paged, hipStream_t s);
 hipError_t launch_lse_combine(const CombineParams& p, int D, bool bf16, hipStream_t s);
 hipError_t launch_tree_attn_bwd(const BwdParams& p, int n_work, int n_bwd, int D, hipStream_t s);
+hipError_t launch_append_kv(const void* k_new, const void* v_new, void* k_cache, void* v_cache, const int32_t* slots,
+                            int64_t n_rows, int Hkv, int D, bool bf16, const int32_t* patch, int64_t n_patch,
+                            int32_t* block_table, hipStream_t s);
 
 namespace {
 thread_local hipEvent_t t_ev_before = nullptr;
@@ -43,17 +47,28 @@ padoc_status check_common(const padoc_plan* P, const void* q, const void* k, con
   return PADOC_OK;
 }
 
-// The plan's schedule in pinned host memory (made once per plan).
+// The plan's schedule in pinned host memory, copied once per build of the
+// plan.  A plan rebuilt in place (a session's per-step plan) overwrites the
+// copy only after the upload that last read it has completed.
 const void* pinned_blob(const padoc_plan* P) {
-  std::call_once(P->pin_once, [P] {
-    void* h = nullptr;
-    hipError_t e = hipHostMalloc(&h, P->blob.size(), hipHostMallocDefault);
-    if (e == hipSuccess) {
-      std::memcpy(h, P->blob.data(), P->blob.size());
-      P->pinned = h;
+  std::lock_guard<std::mutex> lk(P->pin_mu);
+  if (P->pinned_build != P->build_id) {
+    if (P->pin_ev) (void)hipEventSynchronize(static_cast<hipEvent_t>(P->pin_ev));
+    if (P->pinned && P->pinned_cap < P->blob.size()) {
+      (void)hipHostFree(P->pinned);
+      P->pinned = nullptr;
+      P->pinned_cap = 0;
     }
-    P->pin_status = (int)e;
-  });
+    if (!P->pinned && !P->blob.empty()) {
+      void* h = nullptr;
+      if (hipHostMalloc(&h, P->blob.size(), hipHostMallocDefault) == hipSuccess) {
+        P->pinned = h;
+        P->pinned_cap = P->blob.size();
+      }
+    }
+    if (P->pinned) std::memcpy(P->pinned, P->blob.data(), P->blob.size());
+    P->pinned_build = P->build_id;
+  }
   return P->pinned ? P->pinned : P->blob.data();
 }
 
@@ -69,11 +84,29 @@ const void* pinned_bwd_blob(const padoc_plan* P) {
   return P->bpinned ? P->bpinned : P->bwd_blob.data();
 }
 
+// Launch the attention of plan P.  `upload`: copy the schedule into the
+// workspace first (else the caller already did); `events`: record the
+// profiling events around the kernels.
 padoc_status run(const padoc_plan* P, const void* q, const void* k, const void* v, const int32_t* bt, void* o,
-                 float* lse, void* ws, hipStream_t stream) {
+                 float* lse, void* ws, hipStream_t stream, bool upload = true, bool events = true) {
   if (P->work.empty()) return PADOC_OK;
-  hipError_t e = hipMemcpyAsync(ws, pinned_blob(P), P->blob.size(), hipMemcpyHostToDevice, stream);
-  if (e != hipSuccess) return hip_fail("hipMemcpyAsync(schedule)", e);
+  hipError_t e = hipSuccess;
+  if (upload) {
+    e = hipMemcpyAsync(ws, pinned_blob(P), P->blob.size(), hipMemcpyHostToDevice, stream);
+    if (e != hipSuccess) return hip_fail("hipMemcpyAsync(schedule)", e);
+    if (P->build_id > 1) {
+      // a rebuilt plan: mark when its pinned copy may be overwritten
+      std::lock_guard<std::mutex> lk(P->pin_mu);
+      if (!P->pin_ev) {
+        hipEvent_t ev = nullptr;
+        if (hipEventCreateWithFlags(&ev, hipEventDisableTiming) == hipSuccess) P->pin_ev = ev;
+      }
+      if (P->pin_ev) {
+        e = hipEventRecord(static_cast<hipEvent_t>(P->pin_ev), stream);
+        if (e != hipSuccess) return hip_fail("hipEventRecord", e);
+      }
+    }
+  }
   TileParams tp{};
   tp.q = q;
   tp.k = k;
@@ -96,7 +129,7 @@ padoc_status run(const padoc_plan* P, const void* q, const void* k, const void* 
   const bool paged = P->block_size != 0;
   const bool partial = P->kind == 1;  // decode plans: wave items, split-KV partials
   const int n_work = (int)P->work.size();
-  if (t_ev_before && t_ev_after) {
+  if (events && t_ev_before && t_ev_after) {
     e = hipEventRecord(t_ev_before, stream);
     if (e != hipSuccess) return hip_fail("hipEventRecord", e);
   }
@@ -133,7 +166,7 @@ padoc_status run(const padoc_plan* P, const void* q, const void* k, const void* 
     e = launch_lse_combine(cp, P->D, P->dtype == PADOC_BF16, stream);
     if (e != hipSuccess) return hip_fail("combine kernel launch", e);
   }
-  if (t_ev_before && t_ev_after) {
+  if (events && t_ev_before && t_ev_after) {
     e = hipEventRecord(t_ev_after, stream);
     if (e != hipSuccess) return hip_fail("hipEventRecord", e);
   }
@@ -237,9 +270,110 @@ extern "C" padoc_status padoc_tree_attn_bwd(const padoc_plan* plan, const void* 
 
 extern "C" void padoc_plan_destroy(padoc_plan* plan) {
   if (!plan) return;
+  if (plan->pin_ev) (void)hipEventDestroy(static_cast<hipEvent_t>(plan->pin_ev));
   if (plan->pinned) (void)hipHostFree(plan->pinned);
   if (plan->bpinned) (void)hipHostFree(plan->bpinned);
   delete plan;
+}
+
+// One step of a decode session: upload the step's slot list, block-table
+// patches and schedule in one copy, append the new K/V rows (and patch the
+// table), then the attention kernels.
+extern "C" padoc_status padoc_session_launch(padoc_session* s, const void* q, const void* k_new, const void* v_new,
+                                             void* o, float* lse, void* workspace, size_t workspace_bytes,
+                                             hipStream_t stream) {
+  clear_error();
+  if (!s) return set_error(PADOC_ERR_ARG, "session is null");
+  if (!s->prepared) return set_error(PADOC_ERR_MODE, "no step is prepared");
+  const padoc_session_desc& d = s->desc;
+  if (!d.k_cache || !d.v_cache || !d.block_table)
+    return set_error(PADOC_ERR_ARG, "the session was created without device caches and block table");
+  if (((uintptr_t)d.k_cache | (uintptr_t)d.v_cache) & 15)
+    return set_error(PADOC_ERR_ARG, "the caches must be 16-byte aligned");
+  const int64_t n_new = s->new_off.back(), n_q = s->q_off.back();
+  const size_t esz = d.dtype == PADOC_BF16 ? 2 : 4;
+  if (n_new > 0 && (!k_new || !v_new)) return set_error(PADOC_ERR_ARG, "k_new / v_new is null");
+  if (((uintptr_t)k_new | (uintptr_t)v_new) & (esz - 1))
+    return set_error(PADOC_ERR_ARG, "k_new / v_new are not aligned to their element size");
+  const padoc_plan* P = &s->plan;
+  if (n_q > 0) {
+    if (!q || !o || !lse) return set_error(PADOC_ERR_ARG, "q, o or lse is null");
+    if (((uintptr_t)q | (uintptr_t)o) & 15) return set_error(PADOC_ERR_ARG, "q and o must be 16-byte aligned");
+    if (((uintptr_t)lse) & 3) return set_error(PADOC_ERR_ARG, "lse must be 4-byte aligned");
+  }
+  if (!workspace) return set_error(PADOC_ERR_WORKSPACE, "workspace is null");
+  if (((uintptr_t)workspace) & 255) return set_error(PADOC_ERR_WORKSPACE, "workspace must be 256-byte aligned");
+  if (workspace_bytes < s->ws_bytes)
+    return set_error(PADOC_ERR_WORKSPACE, "workspace of %zu bytes is smaller than the %zu the step needs",
+                     workspace_bytes, s->ws_bytes);
+  const int64_t n_patch = (int64_t)s->patch.size() / 2;
+  const size_t up = s->ws_records + P->blob.size();
+  char* ws = static_cast<char*>(workspace);
+  hipError_t e = hipSuccess;
+  if (up > 0) {
+    const int k = s->stage_next;
+    if (s->stage_ev[k]) {
+      e = hipEventSynchronize(static_cast<hipEvent_t>(s->stage_ev[k]));
+      if (e != hipSuccess) return hip_fail("hipEventSynchronize(staging)", e);
+    } else {
+      hipEvent_t ev = nullptr;
+      e = hipEventCreateWithFlags(&ev, hipEventDisableTiming);
+      if (e != hipSuccess) return hip_fail("hipEventCreateWithFlags", e);
+      s->stage_ev[k] = ev;
+    }
+    if (s->stage_cap[k] < up) {
+      if (s->stage[k]) (void)hipHostFree(s->stage[k]);
+      s->stage[k] = nullptr;
+      s->stage_cap[k] = 0;
+      const size_t cap = up + up / 2;
+      void* h = nullptr;
+      e = hipHostMalloc(&h, cap, hipHostMallocDefault);
+      if (e != hipSuccess) return hip_fail("hipHostMalloc(staging)", e);
+      s->stage[k] = h;
+      s->stage_cap[k] = cap;
+    }
+    char* h = static_cast<char*>(s->stage[k]);
+    if (n_new > 0) std::memcpy(h, s->new_slot.data(), (size_t)n_new * 8);
+    if (n_patch > 0) std::memcpy(h + s->off_patch, s->patch.data(), (size_t)n_patch * 8);
+    if (!P->blob.empty()) std::memcpy(h + s->ws_records, P->blob.data(), P->blob.size());
+    e = hipMemcpyAsync(ws, h, up, hipMemcpyHostToDevice, stream);
+    if (e != hipSuccess) return hip_fail("hipMemcpyAsync(step)", e);
+    e = hipEventRecord(static_cast<hipEvent_t>(s->stage_ev[k]), stream);
+    if (e != hipSuccess) return hip_fail("hipEventRecord", e);
+    s->stage_next = k ^ 1;
+  }
+  // From here on the step is enqueued: it is complete on the host side even
+  // if a later launch fails (the device state is then undefined).
+  s->prepared = false;
+  if (t_ev_before && t_ev_after) {
+    e = hipEventRecord(t_ev_before, stream);
+    if (e != hipSuccess) return hip_fail("hipEventRecord", e);
+  }
+  if (n_new > 0 || n_patch > 0) {
+    e = launch_append_kv(k_new, v_new, d.k_cache, d.v_cache, at<int32_t>(ws, 0), n_new, d.num_heads_kv, d.head_dim,
+                         d.dtype == PADOC_BF16, at<int32_t>(ws, s->off_patch), n_patch, d.block_table, stream);
+    if (e != hipSuccess) return hip_fail("append kernel launch", e);
+  }
+  padoc_status st = run(P, q, d.k_cache, d.v_cache, d.block_table, o, lse, ws + s->ws_records, stream,
+                        /*upload=*/false, /*events=*/false);
+  if (st != PADOC_OK) return st;
+  if (t_ev_before && t_ev_after) {
+    e = hipEventRecord(t_ev_after, stream);
+    if (e != hipSuccess) return hip_fail("hipEventRecord", e);
+  }
+  return PADOC_OK;
+}
+
+extern "C" void padoc_session_destroy(padoc_session* s) {
+  if (!s) return;
+  for (int k = 0; k < 2; ++k) {
+    if (s->stage_ev[k]) (void)hipEventDestroy(static_cast<hipEvent_t>(s->stage_ev[k]));
+    if (s->stage[k]) (void)hipHostFree(s->stage[k]);
+  }
+  if (s->plan.pin_ev) (void)hipEventDestroy(static_cast<hipEvent_t>(s->plan.pin_ev));
+  if (s->plan.pinned) (void)hipHostFree(s->plan.pinned);
+  if (s->plan.bpinned) (void)hipHostFree(s->plan.bpinned);
+  session_free_host(s);
 }
 
 extern "C" padoc_status padoc_set_kernel_events(hipEvent_t before, hipEvent_t after) {

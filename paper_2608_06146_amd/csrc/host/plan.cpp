@@ -708,6 +708,7 @@ padoc_status build_plan(const padoc_tree_desc* d, padoc_plan& P) {
   padoc_status st = validate(d);
   if (st != PADOC_OK) return st;
   try {
+    ++P.build_id;
     P.kind = d->block_size == 0 ? 0 : 1;
     P.Hq = d->num_heads_q;
     P.Hkv = d->num_heads_kv;

@@ -54,11 +54,18 @@ struct padoc_plan {
   size_t off_comb_ptr = 0, off_comb_slot = 0, off_comb_rows = 0, off_part_o = 0, off_part_ml = 0;
   size_t ws_bytes = 0;
 
-  // Pinned host copy of `blob`, made on the first launch so the schedule
-  // upload is a true asynchronous DMA (freed by padoc_plan_destroy).
-  mutable std::once_flag pin_once;
+  // Incremented by every build of the plan (plans rebuilt in place).
+  uint64_t build_id = 0;
+
+  // Pinned host copy of `blob` (made on the first launch after a build, so
+  // the schedule upload is a true asynchronous DMA; freed by
+  // padoc_plan_destroy), the build it holds, and for rebuilt plans an event
+  // (hipEvent_t) after the last upload that read it.
+  mutable std::mutex pin_mu;
   mutable void* pinned = nullptr;
-  mutable int pin_status = 0;  // hipError_t of the pinned allocation
+  mutable size_t pinned_cap = 0;
+  mutable uint64_t pinned_build = 0;
+  mutable void* pin_ev = nullptr;
 };
 
 namespace padoc {

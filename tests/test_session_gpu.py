@@ -1,0 +1,218 @@
+"""Decode session on the GPU: whole steps (append of the new K/V rows,
+block-table patches, attention) against the oracle.
+
+* Alg.-1 replay: pages prefilled and decoded with seeded fork / end events;
+  every query's O and LSE equal masked attention (fp64) over the cache
+  positions the oracle's fused-mask row selects, with K/V values keyed by
+  cache position (so a wrong slot, block or patch shows as a wrong value).
+* Multi-token steps on deep trees (bf16 and fp32): the oracle's packed tree
+  attention over the test's own record of every stream's tokens.
+* Decoupled mode: the caller writes the step's K/V rows and patches itself
+  from the view and runs padoc_branch_decode on the view's plan.
+Tolerances are those of the decode path (bf16: max 1.5e-2, mean 2e-3; fp32:
+1e-5).
+"""
+import ctypes as C
+import math
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import paper_2608_06146_amd as pa
+from paper_2608_06146_amd import _lib
+
+from _cases import TOL
+from _session import Alg1Run, make_decide, oracle_rows
+
+pytestmark = pytest.mark.gpu
+
+
+def _tdt(dtype):
+    return torch.bfloat16 if dtype == "bf16" else torch.float32
+
+
+def _session(Hq, Hkv, d, dtype, n_blocks, cap):
+    dev = "cuda"
+    t = _tdt(dtype)
+    kc = torch.full((n_blocks, Hkv, d // 8, 16, 8), float("nan"), dtype=t, device=dev)
+    vc = torch.full((n_blocks, Hkv, d, 16), float("nan"), dtype=t, device=dev)
+    bt = torch.full((cap,), -1, dtype=torch.int32, device=dev)
+    return pa.DecodeSession(Hq, Hkv, d, n_blocks, dtype, k_cache=kc, v_cache=vc, block_table=bt)
+
+
+def _draw(rng, shape, dtype):
+    x = torch.from_numpy(rng.standard_normal(shape).astype(np.float32)).to(_tdt(dtype))
+    return x, x.to(torch.float64).numpy()
+
+
+def _check(name, o, lse, O_ref, LSE_ref, dtype):
+    o = o.to("cpu", torch.float64).numpy()
+    lse = lse.to("cpu", torch.float64).numpy()
+    assert np.isfinite(o).all() and np.isfinite(lse).all(), f"{name}: non-finite output"
+    eo, el = np.abs(o - O_ref), np.abs(lse - LSE_ref)
+    mx, mn = TOL[dtype]
+    assert eo.max() <= mx and el.max() <= mx, f"{name}: max-abs O {eo.max():.3e} LSE {el.max():.3e}"
+    if dtype == "bf16":
+        assert eo.mean() <= mn and el.mean() <= mn, f"{name}: mean-abs O {eo.mean():.3e} LSE {el.mean():.3e}"
+    return eo.max()
+
+
+@pytest.mark.parametrize("seed,Hq,Hkv,d", [(0, 8, 2, 128), (1, 4, 4, 64), (2, 16, 2, 128)])
+def test_alg1_replay_attention(seed, Hq, Hkv, d):
+    rng = np.random.default_rng(100 + seed)
+    n_pages, steps = 3, 22
+    prefix = [int(x) for x in rng.integers(1, 180, size=n_pages)]
+    decides = [make_decide(seed, pg, steps) for pg in range(n_pages)]
+    sess = _session(Hq, Hkv, d, "bf16", n_blocks=300, cap=2048)
+    scale = 1.0 / math.sqrt(d)
+    run = Alg1Run(sess, prefix, decides)
+    kv = {}   # (page, stream, index) -> (k [Hkv, d], v [Hkv, d]) as fp64
+
+    n_new, n_q = run.prefill_rows()
+    sess.prepare(n_new, n_q)
+    v0 = sess.view()
+    kt, k64 = _draw(rng, (int(n_new.sum()), Hkv, d), "bf16")
+    vt, v64 = _draw(rng, (int(n_new.sum()), Hkv, d), "bf16")
+    for i, sid in enumerate(v0["row_id"]):
+        pg, c = run.tag_of[int(sid)]
+        for j in range(int(v0["new_off"][i]), int(v0["new_off"][i + 1])):
+            kv[(pg, c, j - int(v0["new_off"][i]))] = (k64[j], v64[j])
+    print(f"[case] session alg1 seed={seed} Hq={Hq} Hkv={Hkv} d={d} prefill {list(n_new)}", flush=True)
+    sess.launch(None, kt.cuda(), vt.cuda())
+    run.after_prefill()
+    want = oracle_rows(prefix, decides, max_steps=steps + 12)
+    worst, n_rows = 0.0, 0
+    while sess.n_open:
+        nk, nq, _ = sess.prepare()
+        v = sess.view()
+        rows = run.rows(v["row_id"])
+        qt, q64 = _draw(rng, (nq, Hq, d), "bf16")
+        kt, k64 = _draw(rng, (nk, Hkv, d), "bf16")
+        vt, v64 = _draw(rng, (nk, Hkv, d), "bf16")
+        for r, (pg, c, i) in enumerate(rows):
+            kv[(pg, c, i)] = (k64[r], v64[r])
+        o, lse = sess.launch(qt.cuda(), kt.cuda(), vt.cuda())
+        torch.cuda.synchronize()
+        O_ref = np.zeros((nq, Hq, d))
+        L_ref = np.zeros((nq, Hq))
+        G = Hq // Hkv
+        for r, (pg, c, i) in enumerate(rows):
+            tags, mrows = want[pg]
+            row = mrows[(c, i)]
+            vis = [tags[l] for l in range(row.size) if row[l]]
+            K = np.stack([kv[(pg,) + t][0] for t in vis])
+            V = np.stack([kv[(pg,) + t][1] for t in vis])
+            for h in range(Hq):
+                oo, ll = oracle.masked_attention(q64[r, h][None], K[:, h // G], V[:, h // G],
+                                                 np.ones((1, len(vis)), bool), scale)
+                O_ref[r, h], L_ref[r, h] = oo[0], ll[0]
+        worst = max(worst, _check(f"step {run.step_no}", o, lse, O_ref, L_ref, "bf16"))
+        n_rows += nq
+        run.events(v["row_id"])
+    print(f"[case] session alg1 seed={seed}: {run.step_no} steps, {n_rows} queries, O max-abs {worst:.2e}",
+          flush=True)
+    assert sess.view()["free_blocks"] == 300
+
+
+@pytest.mark.parametrize("dtype", ["bf16", "f32"])
+def test_multi_token_steps_deep_trees(dtype):
+    rng = np.random.default_rng(7 if dtype == "bf16" else 8)
+    Hq, Hkv, d = 8, 2, 64
+    scale = 1.0 / math.sqrt(d)
+    sess = _session(Hq, Hkv, d, dtype, n_blocks=200, cap=1024)
+    streams = {}          # id -> dict(parent, fork, k [n, Hkv, d], v)
+    r = sess.open(-1, 0)
+    streams[r] = {"parent": -1, "fork": 0, "k": np.zeros((0, Hkv, d)), "v": np.zeros((0, Hkv, d))}
+    for step in range(16):
+        ids = [int(x) for x in sess.view()["row_id"]]
+        n_new = rng.integers(0, 40 if step == 0 else 7, size=len(ids)).astype(np.int32)
+        n_q = np.array([rng.integers(0, n + 1) for n in n_new], dtype=np.int32)
+        nk, nq, _ = sess.prepare(n_new, n_q)
+        kt, k64 = _draw(rng, (nk, Hkv, d), dtype)
+        vt, v64 = _draw(rng, (nk, Hkv, d), dtype)
+        qt, q64 = _draw(rng, (nq, Hq, d), dtype)
+        off = 0
+        for i, sid in enumerate(ids):
+            n = int(n_new[i])
+            streams[sid]["k"] = np.concatenate([streams[sid]["k"], k64[off:off + n]])
+            streams[sid]["v"] = np.concatenate([streams[sid]["v"], v64[off:off + n]])
+            off += n
+        print(f"[case] session multi-token {dtype} step {step}: rows {len(ids)} new {nk} queries {nq}", flush=True)
+        o, lse = sess.launch(qt.cuda(), kt.cuda(), vt.cuda())
+        torch.cuda.synchronize()
+        if nq:
+            # the test's own tree: every stream ever opened, in id order
+            order = sorted(streams)
+            qlen = {sid: 0 for sid in order}
+            for i, sid in enumerate(ids):
+                qlen[sid] = int(n_q[i])
+            nodes = [(streams[s]["parent"], streams[s]["fork"], len(streams[s]["k"]), qlen[s]) for s in order]
+            K = np.concatenate([streams[s]["k"] for s in order])
+            V = np.concatenate([streams[s]["v"] for s in order])
+            O_ref, L_ref = oracle.tree_attention(nodes, q64, K, V, scale, Hq, Hkv)
+            _check(f"{dtype} step {step}", o, lse, O_ref, L_ref, dtype)
+        ids = [int(x) for x in sess.view()["row_id"]]
+        if ids and rng.random() < 0.7:
+            p = int(rng.choice(ids))
+            f = int(rng.integers(0, len(streams[p]["k"]) + 1))
+            c = sess.open(p, f)
+            streams[c] = {"parent": p, "fork": f, "k": np.zeros((0, Hkv, d)), "v": np.zeros((0, Hkv, d))}
+        if len(ids) > 2 and rng.random() < 0.3:
+            sess.close(int(rng.choice(ids)))
+
+
+def test_decoupled_mode_with_branch_decode():
+    """prepare / view / caller-side writes / padoc_branch_decode / commit."""
+    rng = np.random.default_rng(21)
+    Hq, Hkv, d = 8, 2, 128
+    sess = _session(Hq, Hkv, d, "bf16", n_blocks=64, cap=256)
+    kc, vc, bt = sess.k_cache, sess.v_cache, sess.block_table
+    r = sess.open(-1, 0)
+    hist_k, hist_v = [], []
+
+    def write(view, k64, v64):
+        slots = view["new_slot"]
+        for j, (b, t) in enumerate(slots):
+            ch = (t & 3) | ((t & 4) << 1) | ((t & 8) >> 1)
+            kc[b, :, :, ch, :] = torch.from_numpy(k64[j]).to(torch.bfloat16).reshape(Hkv, d // 8, 8).cuda()
+            vc[b, :, :, t] = torch.from_numpy(v64[j]).to(torch.bfloat16).cuda()
+        for e, b in view["patch"]:
+            bt[e] = int(b)
+
+    sess.prepare(np.array([50], np.int32), np.array([0], np.int32))
+    v = sess.view()
+    _, k64 = _draw(rng, (50, Hkv, d), "bf16")
+    _, v64 = _draw(rng, (50, Hkv, d), "bf16")
+    write(v, k64, v64)
+    hist_k.append(k64)
+    hist_v.append(v64)
+    sess.commit()
+    for step in range(3):
+        sess.prepare(np.array([3], np.int32), np.array([2], np.int32))
+        v = sess.view()
+        _, k64 = _draw(rng, (3, Hkv, d), "bf16")
+        _, v64 = _draw(rng, (3, Hkv, d), "bf16")
+        qt, q64 = _draw(rng, (2, Hq, d), "bf16")
+        write(v, k64, v64)
+        hist_k.append(k64)
+        hist_v.append(v64)
+        qd = qt.cuda()
+        o = torch.empty_like(qd)
+        lse = torch.empty(2, Hq, dtype=torch.float32, device="cuda")
+        ws = torch.empty(v["workspace_bytes"] + 256, dtype=torch.uint8, device="cuda")
+        off = (-ws.data_ptr()) % 256
+        print(f"[case] session decoupled step {step}", flush=True)
+        _lib.check(_lib.lib().padoc_branch_decode(C.c_void_p(v["plan"]), C.c_void_p(qd.data_ptr()),
+                                                  C.c_void_p(kc.data_ptr()), C.c_void_p(vc.data_ptr()),
+                                                  C.c_void_p(bt.data_ptr()), C.c_void_p(o.data_ptr()),
+                                                  C.c_void_p(lse.data_ptr()), C.c_void_p(ws.data_ptr() + off),
+                                                  ws.numel() - off, None))
+        torch.cuda.synchronize()
+        K = np.concatenate(hist_k)
+        V = np.concatenate(hist_v)
+        nodes = [(-1, 0, len(K), 2)]
+        O_ref, L_ref = oracle.tree_attention(nodes, q64, K, V, 1.0 / math.sqrt(d), Hq, Hkv)
+        _check(f"decoupled step {step}", o, lse, O_ref, L_ref, "bf16")
+        sess.commit()
