@@ -47,7 +47,7 @@ __all__ = [
     "page_nodes", "canonical_layout", "ancestors", "visible_counts", "page_of",
     "dense_mask", "masked_attention", "tree_attention", "tree_attention_paged",
     "gather_paged", "paged_slots", "chunk_slot", "simulate_masked_parallel_decoding",
-    "visible_pair_count",
+    "visible_pair_count", "decoding_depths",
 ]
 
 Node = Tuple[int, int, int, int]   # (parent, fork, length, q_len)
@@ -358,6 +358,39 @@ def tree_attention_paged(nodes, q, k_pool, v_pool, block_table, scale: float,
     kv_off, qo = canonical_layout(nodes, 0)
     return tree_attention(nodes, q, k, v, scale, num_heads_q, num_heads_kv,
                           kv_off=kv_off, q_off=qo if q_off is None else q_off, rows=rows)
+
+
+# --------------------------------------------------------------------------
+# Decoding depth (Sec. 3.1) and forward steps (App. D)
+# --------------------------------------------------------------------------
+
+def decoding_depths(nodes):
+    """Per page root: ``(D_seq, D_crit)``.
+
+    The roots are the page inputs (prefilled, not decoded); every other
+    segment is decoded one token per step.  Sequential decoding emits the
+    decoded segments one after another: ``D_seq`` = the sum of their lengths
+    (Sec. 3.1, layout length plus every content length).  Decoding all
+    streams concurrently, a segment can start once its parent has produced
+    the ``fork`` tokens it conditions on, so it starts at step
+    ``start(s) = start(parent) + fork`` (0 below a root) and finishes at
+    ``start(s) + len(s)``; ``D_crit`` = the latest finish over the page
+    (Sec. 3.1 critical path ``max_k [l(B_<=k) + l(Y_k)]``, also bounded below
+    by the layout length; App. D ``F_PaDoc``).  Returns a dict root ->
+    (D_seq, D_crit)."""
+    nodes = _as_nodes(nodes)
+    root = page_of(nodes)
+    start = {}
+    out = {}
+    for s, (parent, fork, n, _) in enumerate(nodes):
+        r = int(root[s])
+        seq, crit = out.get(r, (0, 0))
+        if parent < 0:
+            out[r] = (seq, crit)
+            continue
+        start[s] = (start[parent] if nodes[parent][0] >= 0 else 0) + (fork if nodes[parent][0] >= 0 else 0)
+        out[r] = (seq + n, max(crit, start[s] + n))
+    return out
 
 
 # --------------------------------------------------------------------------

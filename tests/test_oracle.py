@@ -430,3 +430,39 @@ def test_chunk_major_k_layout():
                     c, e = divmod(dim, 8)
                     assert got[row, h, dim] == b * 1e6 + h * 1e4 + c * 1e3 + int(ot.chunk_slot(t)) * 10 + e
             row += 1
+
+
+# ---------------------------------------------------------------- P9 decoding depths
+
+def test_P9_depths_of_a_worked_page():
+    """Sec. 3.1 by hand: layout 12 tokens; branches (fork 3, 20 tokens),
+    (fork 7, 2), (fork 12, 5).  Sequential: 12 + 20 + 2 + 5 = 39 steps;
+    critical path: max(12, 3 + 20, 7 + 2, 12 + 5) = 23."""
+    nodes = [(-1, 0, 50, 0), (0, 50, 12, 12), (1, 3, 20, 20), (1, 7, 2, 2), (1, 12, 5, 5)]
+    assert ot.decoding_depths(nodes) == {0: (39, 23)}
+    # a branch of a branch starts after its parent's fork tokens: 3 + 4 + 9
+    nodes.append((2, 4, 9, 9))
+    assert ot.decoding_depths(nodes) == {0: (48, 23)}
+    nodes.append((5, 9, 3, 3))      # 3 + 4 + 9 + 3 = 19
+    nodes.append((2, 20, 8, 8))     # 3 + 20 + 8 = 31
+    assert ot.decoding_depths(nodes) == {0: (59, 31)}
+
+
+@pytest.mark.parametrize("seed", range(10))
+def test_P9_depths_equal_alg1_step_counts(seed):
+    """The replay of masked parallel decoding takes exactly D_crit steps and
+    decodes exactly D_seq tokens, on the tree its events produce."""
+    P = 4
+    tags, queries, forks = _run_alg1(seed, P)
+    counts = {}
+    for c, i in tags:
+        counts[c] = max(counts.get(c, 0), i + 1)
+    nodes = [(-1, 0, P, 0), (0, P, counts.get(0, 0), counts.get(0, 0))]
+    for c in sorted(k for k in counts if k > 0):
+        nodes.append((1, forks[c], counts[c], counts[c]))
+    # step of each query: the mask row grows by the live count each step
+    sizes = sorted(set(row.size for _, _, row in queries))
+    steps = len(sizes)
+    d_seq, d_crit = ot.decoding_depths(nodes)[0]
+    assert d_seq == len(queries)
+    assert d_crit == steps
