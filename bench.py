@@ -65,6 +65,8 @@ def parse_args(argv=None):
                     help="bytes of each of the K and V pools in GiB (0: 45%% of HBM each, backing off on failure)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-backward", action="store_true", help="skip the backward of the forward workload")
+    ap.add_argument("--driver-steps", type=int, default=60,
+                    help="decode-session steps timed on the decode workload's streams (0 to skip)")
     ap.add_argument("--cpu-pages", type=int, default=64, help="pages of the decode workload the oracle times")
     ap.add_argument("--decode-chunk", type=int, default=0,
                     help="decode plan: max keys per work item (0 = planner's choice)")
@@ -354,6 +356,141 @@ def run_decode(args, torch, np, syn, pa, dev):
     return res, wl
 
 
+# ---------------------------------------------------------------- session (step driver) leg
+
+def run_driver(args, torch, np, syn, pa, dev, wl):
+    """Masked parallel decoding steps through a DecodeSession (App. E loop):
+    the decode workload's streams are built in the session (prefix prefill,
+    layout stream, 24 content streams per page at their forks), then each
+    timed step prepares (host plan), launches (append of one new token per
+    live stream + attention) and waits for the outputs, as a decoding loop
+    must before it samples; then the step's events are applied: a content
+    stream ends with probability 1/512 (mean length 512, as U[1,1024]), a
+    layout stream opens a content stream with probability 24/512, keeping
+    about 24 per page.  Reported: per-step wall time split into prepare /
+    launch / wait / events, and tokens/s with and without the host work."""
+    Hq, Hkv, d = wl.num_heads_q, wl.num_heads_kv, wl.head_dim
+    steps = args.driver_steps
+    nb = syn.count_blocks(wl.pages)
+    rows0 = syn.count_queries(wl.pages)
+    n_pool = int(nb * 1.25) + (steps + args.warmup + 2) * (rows0 // 16 + 64) + 4096
+    kc = torch.empty((n_pool, Hkv, d // 8, 16, 8), dtype=torch.bfloat16, device=dev)
+    vc = torch.empty((n_pool, Hkv, d, 16), dtype=torch.bfloat16, device=dev)
+    bt = torch.full((4 * n_pool,), -1, dtype=torch.int32, device=dev)
+    sess = pa.DecodeSession(Hq, Hkv, d, n_pool, "bf16", k_cache=kc, v_cache=vc, block_table=bt,
+                            max_chunk_keys=args.decode_chunk, target_workgroups=args.decode_target_wg)
+    gen = torch.Generator(device=dev)
+    gen.manual_seed(args.seed * 1000003 + 17)
+
+    def rows(n, h):
+        return torch.randn((n, h, d), generator=gen, device=dev, dtype=torch.float32).to(torch.bfloat16)
+
+    def build_step(n_new, n_q):
+        nk, nq, _ = sess.prepare(np.asarray(n_new, np.int32), np.asarray(n_q, np.int32))
+        sess.launch(rows(nq, Hq) if nq else None, rows(nk, Hkv), rows(nk, Hkv))
+        torch.cuda.synchronize()
+
+    roots = [sess.open(-1, 0) for _ in wl.pages]
+    build_step([p.prefix_len for p in wl.pages], [0] * len(wl.pages))
+    lay = [sess.open(r, p.prefix_len) for r, p in zip(roots, wl.pages)]
+    for r in roots:
+        sess.close(r)
+    build_step([p.stream_len - 1 for p in wl.pages], [0] * len(wl.pages))
+    kind = {x: ("layout", i) for i, x in enumerate(lay)}
+    for i, p in enumerate(wl.pages):
+        for b in p.branches:
+            kind[sess.open(lay[i], b.fork)] = ("content", i)
+    ids = [int(x) for x in sess.view(block_table=False)["row_id"]]
+    branch_len = {i: iter([b.length - 1 for b in p.branches]) for i, p in enumerate(wl.pages)}
+    build_step([0 if kind[x][0] == "layout" else next(branch_len[kind[x][1]]) for x in ids], [0] * len(ids))
+    lay_len = {x: p.stream_len - 1 for x, p in zip(lay, wl.pages)}
+    live = ids  # open streams, ascending id (the session's row order)
+    log(f"driver: session holds {len(live)} streams, {sess.view(block_table=False)['free_blocks']} of {n_pool} "
+        "blocks free")
+
+    q_buf = rows(rows0 + 4096, Hq)
+    k_buf = rows(rows0 + 4096, Hkv)
+    v_buf = rows(rows0 + 4096, Hkv)
+    o_buf = torch.empty_like(q_buf)
+    l_buf = torch.empty(q_buf.shape[:2], dtype=torch.float32, device=dev)
+    rng = np.random.default_rng(args.seed + 5)
+    rec = []
+    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(steps)]
+    for b, a in ev:
+        b.record()
+        a.record()
+    torch.cuda.synchronize()
+    for s in range(args.warmup + steps):
+        timed = s >= args.warmup
+        if timed:
+            pa.set_kernel_events(*ev[s - args.warmup])
+        t0 = time.perf_counter()
+        nk, nq, _ = sess.prepare()
+        t1 = time.perf_counter()
+        if nq > q_buf.shape[0]:
+            raise RuntimeError("driver: more live streams than the step buffers hold")
+        sess.launch(q_buf[:nq], k_buf[:nk], v_buf[:nk], out=o_buf[:nq], lse=l_buf[:nq])
+        t2 = time.perf_counter()
+        torch.cuda.synchronize()
+        t3 = time.perf_counter()
+        for x in lay_len:
+            lay_len[x] += 1
+        u = rng.random(len(live))
+        ended, born = set(), []
+        for j in np.nonzero(u < 24.0 / 512)[0]:     # only these streams can have an event
+            x = live[j]
+            k_, pg = kind[x]
+            if k_ == "content" and u[j] < 1.0 / 512:
+                sess.close(x)
+                ended.add(x)
+            elif k_ == "layout":
+                c = sess.open(x, lay_len[x])
+                kind[c] = ("content", pg)
+                born.append(c)
+        if ended:
+            live = [x for x in live if x not in ended]
+        live += born
+        t4 = time.perf_counter()
+        if timed:
+            pa.set_kernel_events()
+            rec.append((nq, t1 - t0, t2 - t1, t3 - t2, t4 - t3))
+    gpu = [b.elapsed_time(a) for b, a in ev]
+    n_rows = sum(r[0] for r in rec)
+    wall = sum(r[1] + r[2] + r[3] + r[4] for r in rec)
+    res = {
+        "steps": steps, "rows_per_step": n_rows / steps,
+        "step_ms": wall * 1e3 / steps,
+        "prepare_ms": 1e3 * statistics.mean(r[1] for r in rec),
+        "launch_ms": 1e3 * statistics.mean(r[2] for r in rec),
+        "wait_ms": 1e3 * statistics.mean(r[3] for r in rec),
+        "events_ms": 1e3 * statistics.mean(r[4] for r in rec),
+        "gpu_ms": statistics.mean(gpu),
+        "tokens_per_s": n_rows / wall,
+        "tokens_per_s_gpu": n_rows / (sum(gpu) * 1e-3),
+        "pool_blocks": n_pool, "free_blocks_end": int(sess.view(block_table=False)["free_blocks"]),
+    }
+    sess.destroy()
+    del kc, vc, bt, q_buf, k_buf, v_buf, o_buf
+    torch.cuda.empty_cache()
+    return res
+
+
+# ---------------------------------------------------------------- decoding-depth accounting
+
+def depth_accounting(pa, syn, np, name, seed):
+    """Per-page sequential depth D_seq, concurrent critical path D_crit and
+    forward-step reduction R_step = 1 - D_crit / D_seq (Sec. 3.1, App. D) of
+    a workload's pages, taken as complete decoding traces (the layout stream
+    and every branch at its full length)."""
+    wl = syn.make_workload(name, seed)
+    _, d_seq, d_crit = pa.tree_depths(pa.segments_from_pages(wl.pages, 0))
+    r = 1.0 - d_crit / np.maximum(d_seq, 1)
+    return {"workload": name, "pages": int(len(d_seq)), "d_seq_mean": float(d_seq.mean()),
+            "d_crit_mean": float(d_crit.mean()), "r_step_mean": float(r.mean()),
+            "r_step_median": float(np.median(r)), "r_step_min": float(r.min()), "r_step_max": float(r.max()),
+            "steps_ratio_total": float(d_seq.sum() / max(int(d_crit.sum()), 1))}
+
+
 # ---------------------------------------------------------------- forward leg
 
 def run_forward(args, torch, np, syn, pa, dev):
@@ -474,6 +611,7 @@ def main(argv=None) -> int:
     pa.version()  # loads the library (fails loudly if it was not built)
 
     dec, wl = run_decode(args, torch, np, syn, pa, dev)
+    drv = run_driver(args, torch, np, syn, pa, dev, wl) if args.driver_steps > 0 else None
     fwd = None
     if args.forward_workload != "none":
         fwd = run_forward(args, torch, np, syn, pa, dev)
@@ -503,6 +641,9 @@ def main(argv=None) -> int:
                      "bytes_per_launch": dec["kernel_bytes"]},
         "cpu_baseline": cpu,
         "decode": dec,
+        "driver": drv,
+        "accounting": [depth_accounting(pa, syn, np, n, args.seed)
+                       for n in ("concurrent_decode_64pages", "packed_forward_8pages")],
         "forward": fwd,
     }
     print(json.dumps(line), flush=True)

@@ -230,6 +230,19 @@ padoc_status padoc_tree_from_pages(const padoc_page* pages, int32_t n_pages, int
    read, not checked (padoc_plan_create checks them). */
 padoc_status padoc_tree_layout(padoc_segment* seg, int32_t n, int32_t block_size);
 
+/* Decoding depths of each page (Sec. 3.1 sequential depth vs critical path;
+   App. D forward steps), host only.  Roots are page inputs (prefilled, not
+   decoded); every other segment is decoded one token per step.  For each
+   root r: d_seq[r] = total length of the page's decoded segments (one
+   stream after another); d_crit[r] = steps when all streams run
+   concurrently and a segment starts as soon as its parent has produced the
+   `fork` tokens it conditions on: start(s) = start(parent) + fork (0 for a
+   child of a root), and the page ends at the largest start(s) + len(s).
+   Entries of non-root segments are set to 0.  The per-page forward-step
+   reduction is 1 - d_crit / d_seq.  Checks parent < own index and
+   0 <= fork <= len(parent); PADOC_ERR_TREE otherwise. */
+padoc_status padoc_tree_depths(const padoc_segment* seg, int32_t n, int64_t* d_seq, int64_t* d_crit);
+
 /* Validate the tree and build the schedule (host only; no HIP call). */
 padoc_status padoc_plan_create(const padoc_tree_desc* desc, padoc_plan** out);
 padoc_status padoc_plan_workspace_bytes(const padoc_plan* plan, size_t* bytes);

@@ -21,7 +21,7 @@ from . import _lib
 from ._lib import PadocError, SEGMENT_DTYPE, WORK_DTYPE, RANGE_DTYPE, BWD_DTYPE
 
 __all__ = ["TreePlan", "segments_from_pages", "segments_layout", "tree_attn_fwd", "tree_attn_bwd", "branch_decode",
-           "DecodeSession", "PadocError", "SEGMENT_DTYPE", "version", "set_kernel_events", "make_workspace"]
+           "DecodeSession", "tree_depths", "PadocError", "SEGMENT_DTYPE", "version", "set_kernel_events", "make_workspace"]
 
 _DTYPES = {"f32": _lib.F32, "fp32": _lib.F32, "float32": _lib.F32, "bf16": _lib.BF16, "bfloat16": _lib.BF16}
 
@@ -68,6 +68,20 @@ def segments_layout(nodes, block_size: int = 0) -> np.ndarray:
             out[i] = (n.parent, n.fork, n.length, n.q_len, 0, 0)
     _lib.check(_lib.lib().padoc_tree_layout(out.ctypes.data_as(C.c_void_p), len(out), block_size))
     return out
+
+
+def tree_depths(segments: np.ndarray):
+    """Per page root of a segment tree: ``(root index, D_seq, D_crit)``
+    arrays (``padoc_tree_depths``: sequential decoding depth and concurrent
+    critical path, Sec. 3.1 / App. D); ``R_step = 1 - D_crit / D_seq``."""
+    segs = np.ascontiguousarray(segments, dtype=SEGMENT_DTYPE)
+    n = len(segs)
+    d_seq = np.zeros(n, np.int64)
+    d_crit = np.zeros(n, np.int64)
+    _lib.check(_lib.lib().padoc_tree_depths(segs.ctypes.data if n else None, n, d_seq.ctypes.data,
+                                            d_crit.ctypes.data))
+    roots = np.nonzero(segs["parent"] < 0)[0]
+    return roots, d_seq[roots], d_crit[roots]
 
 
 class TreePlan:
@@ -435,8 +449,9 @@ class DecodeSession:
     def commit(self) -> None:
         _lib.check(_lib.lib().padoc_session_commit(self.handle))
 
-    def view(self, schedule: bool = False) -> dict:
-        """The prepared step (or the tree as it stands) as numpy copies."""
+    def view(self, schedule: bool = False, block_table: bool = True) -> dict:
+        """The prepared step (or the tree as it stands) as numpy copies
+        (``block_table=False`` skips copying the host block table)."""
         v = _lib.SessionView()
         _lib.check(_lib.lib().padoc_session_view_get(self.handle, C.byref(v)))
         arr = _carray
@@ -445,7 +460,7 @@ class DecodeSession:
         out = {
             "seg": arr(v.seg, v.n_seg, SEGMENT_DTYPE), "seg_id": arr(v.seg_id, v.n_seg, np.int32),
             "row_id": arr(v.row_id, n, np.int32),
-            "block_table": arr(v.block_table, self.block_table_capacity, np.int32),
+            "block_table": arr(v.block_table, self.block_table_capacity if block_table else 0, np.int32),
             "free_blocks": int(v.free_blocks), "prepared": prepared,
         }
         if prepared:

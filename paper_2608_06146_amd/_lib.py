@@ -89,6 +89,7 @@ EXPORTED = [
     "padoc_plan_backward_workspace_bytes", "padoc_tree_attn_bwd",
     "padoc_session_create", "padoc_session_destroy", "padoc_session_open", "padoc_session_close",
     "padoc_session_prepare", "padoc_session_launch", "padoc_session_commit", "padoc_session_view_get",
+    "padoc_tree_depths",
 ]
 
 _lib = None
@@ -124,6 +125,7 @@ def lib():
     L.padoc_session_launch.argtypes = [vp, vp, vp, vp, vp, vp, vp, sz, vp]
     L.padoc_session_commit.argtypes = [vp]
     L.padoc_session_view_get.argtypes = [vp, C.POINTER(SessionView)]
+    L.padoc_tree_depths.argtypes = [vp, i32, vp, vp]
     L.padoc_last_error.argtypes = []
     L.padoc_last_error.restype = C.c_char_p
     L.padoc_set_kernel_events.argtypes = [vp, vp]
@@ -133,7 +135,7 @@ def lib():
                  "padoc_plan_export", "padoc_tree_attn_fwd", "padoc_branch_decode", "padoc_set_kernel_events",
                  "padoc_plan_backward_workspace_bytes", "padoc_tree_attn_bwd", "padoc_session_create",
                  "padoc_session_open", "padoc_session_close", "padoc_session_prepare", "padoc_session_launch",
-                 "padoc_session_commit", "padoc_session_view_get"):
+                 "padoc_session_commit", "padoc_session_view_get", "padoc_tree_depths"):
         getattr(L, name).restype = C.c_int
     _lib = L
     return L

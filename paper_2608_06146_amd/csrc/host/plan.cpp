@@ -833,6 +833,38 @@ extern "C" padoc_status padoc_tree_from_pages(const padoc_page* pages, int32_t n
   return padoc_tree_layout(out, k, block_size);
 }
 
+extern "C" padoc_status padoc_tree_depths(const padoc_segment* seg, int32_t n, int64_t* d_seq, int64_t* d_crit) {
+  clear_error();
+  if (n < 0) return set_error(PADOC_ERR_ARG, "n = %d is negative", n);
+  if (n > 0 && (!seg || !d_seq || !d_crit)) return set_error(PADOC_ERR_ARG, "null pointer");
+  try {
+    std::vector<int64_t> start(n, 0);
+    std::vector<int32_t> root(n);
+    for (int32_t s = 0; s < n; ++s) {
+      const padoc_segment& g = seg[s];
+      if (g.len < 0) return set_error(PADOC_ERR_TREE, "segment %d: negative length", s);
+      if (g.parent < -1 || g.parent >= s)
+        return set_error(PADOC_ERR_TREE, "segment %d: parent %d is not an earlier segment", s, g.parent);
+      d_seq[s] = d_crit[s] = 0;
+      if (g.parent < 0) {
+        root[s] = s;
+        continue;
+      }
+      if (g.fork < 0 || g.fork > seg[g.parent].len)
+        return set_error(PADOC_ERR_TREE, "segment %d: fork %d outside [0, %d]", s, g.fork, seg[g.parent].len);
+      root[s] = root[g.parent];
+      // below a root the stream starts at step 0; deeper, after the parent's
+      // first `fork` tokens
+      start[s] = seg[g.parent].parent < 0 ? 0 : start[g.parent] + g.fork;
+      d_seq[root[s]] += g.len;
+      d_crit[root[s]] = std::max(d_crit[root[s]], start[s] + g.len);
+    }
+  } catch (const std::bad_alloc&) {
+    return set_error(PADOC_ERR_ARG, "out of host memory");
+  }
+  return PADOC_OK;
+}
+
 extern "C" padoc_status padoc_plan_create(const padoc_tree_desc* d, padoc_plan** out) {
   clear_error();
   if (!out) return set_error(PADOC_ERR_ARG, "out is null");

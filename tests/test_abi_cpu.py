@@ -461,3 +461,30 @@ def test_backward_workspace_and_modes():
     with pytest.raises(_lib.PadocError) as e:
         f32.backward_workspace_bytes()
     assert e.value.status == _lib.ERR_DTYPE
+
+
+# ---------------------------------------------------------------- decoding depths
+
+def test_tree_depths_match_oracle():
+    cases = [[(a.parent, a.fork, a.length, a.q_len) for a in syn.random_tree(seed, n_pages=3, max_depth=5,
+                                                                              max_len=30)] for seed in range(20)]
+    for name in ("concurrent_decode_64pages", "packed_forward_8pages", "dense_page_mixed_step"):
+        cases.append(od.page_nodes(syn.make_workload(name, 0).pages))
+    for nodes in cases:
+        segs = pa.segments_layout(nodes, 0)
+        roots, d_seq, d_crit = pa.tree_depths(segs)
+        want = od.decoding_depths(nodes)
+        assert sorted(want) == roots.tolist()
+        for r, a, b in zip(roots, d_seq, d_crit):
+            assert (int(a), int(b)) == want[int(r)]
+
+
+def test_tree_depths_errors():
+    L = _lib.lib()
+    bad = _segs([(0, 0, 3, 0, 0, 0)])                 # parent not earlier
+    z = np.zeros(1, np.int64)
+    assert L.padoc_tree_depths(bad.ctypes.data, 1, z.ctypes.data, z.ctypes.data) == _lib.ERR_TREE
+    bad = _segs([(-1, 0, 3, 0, 0, 0), (0, 4, 2, 0, 3, 0)])   # fork beyond the parent
+    z = np.zeros(2, np.int64)
+    assert L.padoc_tree_depths(bad.ctypes.data, 2, z.ctypes.data, z.ctypes.data) == _lib.ERR_TREE
+    assert L.padoc_tree_depths(None, -1, None, None) == _lib.ERR_ARG
