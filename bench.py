@@ -65,6 +65,8 @@ def parse_args(argv=None):
                     help="bytes of each of the K and V pools in GiB (0: 45%% of HBM each, backing off on failure)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-backward", action="store_true", help="skip the backward of the forward workload")
+    ap.add_argument("--no-baselines", action="store_true",
+                    help="skip the baselines (dense-mask SDPA, gather-varlen, per-stream decode)")
     ap.add_argument("--driver-steps", type=int, default=60,
                     help="decode-session steps timed on the decode workload's streams (0 to skip)")
     ap.add_argument("--cpu-pages", type=int, default=64, help="pages of the decode workload the oracle times")
@@ -539,6 +541,13 @@ def run_forward(args, torch, np, syn, pa, dev):
                "roofline": {"bound": "mfma", "achieved": bflops / (bk * 1e-3) / 1e12, "peak": BF16_PEAK_TFLOPS,
                             "unit": "TFLOP/s", "frac": bflops / (bk * 1e-3) / 1e12 / BF16_PEAK_TFLOPS,
                             "kernel": "backward call: " + " + ".join(BACKWARD_KERNELS)}}
+    base = None
+    if not args.no_baselines:
+        log("forward baselines: dense-mask SDPA, tree-varlen")
+        base = forward_baselines(torch, np, segs, q, k, v, o, Hq, Hkv, d, max(3, args.steps // 5))
+        for b in base.values():
+            b["useful_tflops"] = flops / (b.get("total_ms", b["ms"]) * 1e-3) / 1e12
+            b["tree_speedup"] = b.get("total_ms", b["ms"]) / k_ms
     return {
         "workload": wl.name, "tokens": T, "visible_pairs": pairs, "flops": flops,
         "ms_per_step": ms, "kernel_ms": k_ms, "tflops": flops / (ms * 1e-3) / 1e12,
@@ -547,7 +556,219 @@ def run_forward(args, torch, np, syn, pa, dev):
                      "unit": "TFLOP/s", "frac": flops / (k_ms * 1e-3) / 1e12 / BF16_PEAK_TFLOPS,
                      "traffic": measured_traffic()[1], "kernel": FORWARD_KERNEL},
         "backward": bwd,
+        "baselines": base,
     }
+
+
+# ---------------------------------------------------------------- baselines (measurement only)
+
+def _page_row_ranges(segs):
+    """[begin, end) packed rows and segment index range of each page."""
+    out = []
+    n = len(segs)
+    s = 0
+    while s < n:
+        e = s + 1
+        while e < n and int(segs["parent"][e]) >= 0:
+            e += 1
+        a = int(segs["kv_off"][s])
+        b = int(segs["kv_off"][e - 1] + segs["len"][e - 1])
+        out.append((a, b, s, e))
+        s = e
+    return out
+
+
+def _event_ms(torch, fn, reps):
+    fn()
+    torch.cuda.synchronize()
+    b = torch.cuda.Event(enable_timing=True)
+    a = torch.cuda.Event(enable_timing=True)
+    b.record()
+    for _ in range(reps):
+        fn()
+    a.record()
+    torch.cuda.synchronize()
+    return b.elapsed_time(a) / reps
+
+
+def forward_baselines(torch, np, segs, q, k, v, o_tree, Hq, Hkv, d, reps):
+    """The paper's attention backends for the packed tree (App. C), built from
+    PyTorch-ROCm operations on the same inputs: (1) dense SDPA with the
+    materialised Boolean ancestor mask of each page, (2) tree-varlen: one
+    causal problem for prefix + stream and one per branch over the gathered
+    [prefix, stream[:fork], branch] keys with bottom-right causal alignment,
+    run as one variable-length flash-attention call (or, when that entry is
+    missing, one SDPA call per problem).  Each output is compared with the
+    tree kernel's."""
+    import torch.nn.functional as F
+    G = Hq // Hkv
+    scale = 1.0 / math.sqrt(d)
+    pages = _page_row_ranges(segs)
+    res = {}
+    # (1) dense mask per page
+    dev = q.device
+    masks, qs, ks, vs = [], [], [], []
+    t0 = time.perf_counter()
+    for a, b, s0, s1 in pages:
+        ns = s1 - s0
+        lim = np.zeros((ns, ns), np.int64)
+        for s in range(s0, s1):
+            t, child = int(segs["parent"][s]), s
+            while t >= 0:
+                lim[s - s0, t - s0] = int(segs["fork"][child])
+                child, t = t, int(segs["parent"][t])
+        seg_row = np.repeat(np.arange(ns), segs["len"][s0:s1].astype(np.int64))
+        pos_row = np.concatenate([np.arange(int(L)) for L in segs["len"][s0:s1]])
+        sr = torch.as_tensor(seg_row, device=dev)
+        pr = torch.as_tensor(pos_row, device=dev)
+        limt = torch.as_tensor(lim, device=dev)
+        m = pr[None, :] < limt[sr[:, None], sr[None, :]]
+        same = sr[:, None] == sr[None, :]
+        m = torch.where(same, pr[None, :] <= pr[:, None], m)
+        masks.append(m[None, None])
+        qs.append(q[a:b].transpose(0, 1).unsqueeze(0).contiguous())
+        ks.append(k[a:b].repeat_interleave(G, dim=1).transpose(0, 1).unsqueeze(0).contiguous())
+        vs.append(v[a:b].repeat_interleave(G, dim=1).transpose(0, 1).unsqueeze(0).contiguous())
+    torch.cuda.synchronize()
+    mask_ms = (time.perf_counter() - t0) * 1e3
+
+    def dense():
+        return [F.scaled_dot_product_attention(qq, kk, vv, attn_mask=mm, scale=scale)
+                for qq, kk, vv, mm in zip(qs, ks, vs, masks)]
+
+    outs = dense()
+    o_dense = torch.cat([x[0].transpose(0, 1) for x in outs])
+    res["dense_sdpa"] = {"ms": _event_ms(torch, dense, reps), "mask_build_ms": mask_ms,
+                         "mask_bytes": int(sum(m.numel() for m in masks)),
+                         "max_abs_diff_vs_tree": float((o_dense.float() - o_tree.float()).abs().max())}
+    del masks, qs, ks, vs, outs, o_dense
+    torch.cuda.empty_cache()
+
+    # (2) tree-varlen: gather the keys of each causal problem
+    idx_k, cq, ck = [], [0], [0]
+    for a, b, s0, s1 in pages:
+        P, S = int(segs["len"][s0]), int(segs["len"][s0 + 1])
+        m_rows = np.arange(a, a + P + S)
+        idx_k.append(m_rows)
+        cq.append(cq[-1] + P + S)
+        ck.append(ck[-1] + P + S)
+        for s in range(s0 + 2, s1):
+            f, L, r0 = int(segs["fork"][s]), int(segs["len"][s]), int(segs["kv_off"][s])
+            rows = np.concatenate([np.arange(a, a + P + f), np.arange(r0, r0 + L)])
+            idx_k.append(rows)
+            cq.append(cq[-1] + L)
+            ck.append(ck[-1] + len(rows))
+    idx = torch.as_tensor(np.concatenate(idx_k), device=dev)
+    cum_q = torch.as_tensor(np.array(cq, np.int32), device=dev)
+    cum_k = torch.as_tensor(np.array(ck, np.int32), device=dev)
+    max_q = int(np.diff(cq).max())
+    max_k = int(np.diff(ck).max())
+
+    def gather():
+        return (k.index_select(0, idx).repeat_interleave(G, dim=1),
+                v.index_select(0, idx).repeat_interleave(G, dim=1))
+
+    kg, vg = gather()
+    method = "aten._flash_attention_forward (varlen, causal)"
+
+    def varlen():
+        return torch.ops.aten._flash_attention_forward(q, kg, vg, cum_q, cum_k, max_q, max_k, 0.0, True, False,
+                                                        scale=scale)[0]
+
+    from torch.nn.attention.bias import causal_lower_right
+    probs = [(cq[i], cq[i + 1], ck[i], ck[i + 1]) for i in range(len(cq) - 1)]
+
+    def per_problem():
+        out = torch.empty_like(q)
+        for q0, q1, k0, k1 in probs:
+            qq = q[q0:q1].transpose(0, 1).unsqueeze(0)
+            kk = kg[k0:k1].transpose(0, 1).unsqueeze(0)
+            vv = vg[k0:k1].transpose(0, 1).unsqueeze(0)
+            out[q0:q1] = F.scaled_dot_product_attention(
+                qq, kk, vv, attn_mask=causal_lower_right(q1 - q0, k1 - k0), scale=scale)[0].transpose(0, 1)
+        return out
+
+    try:
+        o_var = varlen()
+        torch.cuda.synchronize()
+        bad = float((o_var.float() - o_tree.float()).abs().max())
+        if not bad < 0.05:   # e.g. a top-left causal alignment: not the tree-varlen relation
+            raise ValueError(f"varlen output differs from the tree's by {bad:.3g}")
+    except Exception as e:  # the entry is not built into every PyTorch
+        log(f"varlen flash entry not usable ({type(e).__name__}: {e}); one SDPA call per problem instead")
+        method = "SDPA per problem, causal_lower_right"
+        varlen = per_problem
+        o_var = varlen()
+    res["tree_varlen"] = {"ms": _event_ms(torch, varlen, reps), "gather_ms": _event_ms(torch, gather, reps),
+                          "method": method, "problems": len(cq) - 1, "gathered_key_rows": int(idx.numel()),
+                          "max_abs_diff_vs_tree": float((o_var.float() - o_tree.float()).abs().max())}
+    res["tree_varlen"]["total_ms"] = res["tree_varlen"]["ms"] + res["tree_varlen"]["gather_ms"]
+    return res
+
+
+def decode_baselines(args, torch, np, syn, pa, dev, wl, tree_ms):
+    """The decode step without tree sharing, on the same kernels: every
+    stream as its own sequence (root) holding its whole visible path --
+    (a) with private copies of every block, (b) with prefix blocks reused
+    across the streams of a page (block-granular prefix caching: full blocks
+    of the prefix and of the stream up to the fork are shared, the rest of
+    the path is the stream's own).  The kernels then read each stream's path
+    once per stream."""
+    Hq, Hkv, d = wl.num_heads_q, wl.num_heads_kv, wl.head_dim
+    paths = []   # per stream: (page, prefix tokens, stream tokens seen, own tokens)
+    for pg, p in enumerate(wl.pages):
+        paths.append((pg, p.prefix_len, p.stream_len, 0))   # the layout stream: prefix + its own tokens
+        for b in p.branches:
+            paths.append((pg, p.prefix_len, b.fork, b.length))
+    n = len(paths)
+    lens = np.array([P + f + L for _, P, f, L in paths], np.int64)
+    nodes = [(-1, 0, int(x), 1) for x in lens]
+    segs = pa.segments_layout(nodes, 16)
+    q = torch.randn((n, Hq, d), device=dev).to(torch.bfloat16)
+    out = {}
+    for variant in ("private_copies", "prefix_block_reuse"):
+        if variant == "private_copies":
+            nb = int(sum(-(-int(x) // 16) for x in lens))
+            table = np.arange(nb, dtype=np.int32)
+            n_pool = nb
+        else:
+            # the page's [prefix | stream] tokens fill its own blocks; a
+            # stream's sequence shares the ones entirely inside its first
+            # prefix + fork tokens, the rest of its blocks are its own
+            ids, nxt, page_blocks = [], 0, {}
+            for pg, p in enumerate(wl.pages):
+                nb_pg = -(-(p.prefix_len + p.stream_len) // 16)
+                page_blocks[pg] = np.arange(nxt, nxt + nb_pg)
+                nxt += nb_pg
+            for pg, P, f, L in paths:
+                sh = (P + f) // 16
+                total = -(-(P + f + L) // 16)
+                ids.append(np.concatenate([page_blocks[pg][:sh], np.arange(nxt, nxt + total - sh)]))
+                nxt += total - sh
+            table = np.concatenate(ids).astype(np.int32)
+            n_pool = nxt
+        assert len(table) == int(sum(-(-int(x) // 16) for x in lens))
+        kc = torch.randn((n_pool, Hkv, d // 8, 16, 8), device=dev).to(torch.bfloat16)
+        vc = torch.randn((n_pool, Hkv, d, 16), device=dev).to(torch.bfloat16)
+        bt = torch.as_tensor(table, device=dev)
+        plan = pa.TreePlan(segs, Hq, Hkv, d, "bf16", 16, num_kv_rows=n_pool, num_q_rows=n,
+                           block_table_len=len(table))
+        o = torch.empty_like(q)
+        lse = torch.empty(n, Hq, dtype=torch.float32, device=dev)
+        ws = plan.workspace(dev)
+
+        def step():
+            pa.branch_decode(q, kc, vc, bt, plan, out=o, lse=lse, workspace=ws)
+
+        _, kms = timed_steps(step, max(10, args.steps // 2), args.warmup, torch, pa)
+        km = statistics.mean(kms)
+        path_bytes = int(lens.sum()) * Hkv * d * 2 * 2
+        out[variant] = {"kernel_ms": km, "tokens_per_s": n / (km * 1e-3), "path_kv_bytes": path_bytes,
+                        "pool_bytes": 2 * n_pool * Hkv * 16 * d * 2, "path_gbps": path_bytes / (km * 1e-3) / 1e9,
+                        "tree_speedup": km / tree_ms}
+        del kc, vc, bt, plan, ws
+        torch.cuda.empty_cache()
+    return out
 
 
 # ---------------------------------------------------------------- CPU oracle leg
@@ -612,6 +833,9 @@ def main(argv=None) -> int:
 
     dec, wl = run_decode(args, torch, np, syn, pa, dev)
     drv = run_driver(args, torch, np, syn, pa, dev, wl) if args.driver_steps > 0 else None
+    if not args.no_baselines:
+        log("decode baselines: per-stream sequences without tree sharing")
+        dec["baselines"] = decode_baselines(args, torch, np, syn, pa, dev, wl, dec["kernel_ms"])
     fwd = None
     if args.forward_workload != "none":
         fwd = run_forward(args, torch, np, syn, pa, dev)
