@@ -23,7 +23,7 @@
 // workgroup barriers per tile.  So each SIMD's matrix core has a wavefront
 // with independent work while the other one runs its softmax.
 //
-// LDS holds two K stages and two V^T stages.  Step t reads K(t) and V(t-1)
+// LDS holds two K stages and two V stages.  Step t reads K(t) and V(t-1)
 // and stores K(t+1) and V(t) into the stages last read at step t-1; global
 // loads for the stores of step t+2 (K(t+3), V(t+2)) are issued in step t, so
 // every load has two steps to land.  Keys past a range's end never
@@ -39,6 +39,13 @@
 // rescaled only then.  Any reference gives the same O and LSE.  O is rounded
 // to bf16 (RNE) at the end.
 //
+// Packed K/V rows land in row-major LDS tiles as they are (16-byte pieces).
+// The V^T operand of the PV product is read from the row-major V tile with
+// the transposing LDS read of gfx950 (ds_read_b64_tr_b16: within each group
+// of 16 lanes, lane r supplies the address of 4 consecutive elements, and
+// lane 4a+b receives element b of the pieces of lanes a, 4+a, 8+a and 12+a),
+// two reads per fragment: lane (d, half) gets keys 4*half + 0..3 and
+// 8 + 4*half + 0..3 of a 16-key group for its d, the key order of its P^T.
 // Paged K/V: K blocks are chunk-major ([d/8][16 slots][8]) and land in the
 // row-major LDS tile piece by piece; V blocks are d-major ([d][16 tokens]),
 // so a 16-byte load holds 8 consecutive keys of one d row and lands in the
@@ -61,15 +68,6 @@ constexpr int kWaves = 8;
 constexpr int kThreads = 64 * kWaves;
 constexpr float kRescaleSlack = 8.0f;  // log2 units: probabilities <= 2^8
 
-// Position of key r (0..63) inside a transposed V row.  Within each group of
-// 16 keys, lane half 0 of the 32x32 P^T fragment holds keys
-// {0,1,2,3,8,9,10,11} and half 1 holds {4..7,12..15}; storing them in that
-// order makes each half's 8 keys one contiguous 16-byte LDS read.
-__device__ __forceinline__ int vt_pos(int r) {
-  const int q = r & 15;
-  return (r & ~15) + ((q >> 2) & 1) * 8 + (q >> 3) * 4 + (q & 3);
-}
-
 __device__ __forceinline__ int64_t uniform64(int64_t x) {
   return (int64_t)(((uint64_t)(uint32_t)__builtin_amdgcn_readfirstlane((int)(x >> 32)) << 32) |
                    (uint32_t)__builtin_amdgcn_readfirstlane((int)x));
@@ -81,6 +79,17 @@ __device__ __forceinline__ RangeRec uniform_range(RangeRec r) {
   r.min_lim = __builtin_amdgcn_readfirstlane(r.min_lim);
   r.lim_off = __builtin_amdgcn_readfirstlane(r.lim_off);
   return r;
+}
+
+// Two transposing LDS reads (4 bf16 each) joined into one 8-element MFMA
+// operand: elements 0-3 from the read at lo, 4-7 from the read at hi.
+typedef short i16x4_t __attribute__((ext_vector_type(4)));
+__device__ __forceinline__ bf16x8_t tr_pair(const uint16_t* lo, const uint16_t* hi) {
+  typedef __attribute__((address_space(3))) i16x4_t lds_i16x4;
+  const i16x4_t a = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)(const_cast<uint16_t*>(lo)));
+  const i16x4_t b = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)(const_cast<uint16_t*>(hi)));
+  const short __attribute__((ext_vector_type(8))) ab = __builtin_shufflevector(a, b, 0, 1, 2, 3, 4, 5, 6, 7);
+  return __builtin_bit_cast(bf16x8_t, ab);
 }
 
 // f(integral_constant<int, i>) for i = 0 .. N-1: constant indices into the
@@ -100,16 +109,20 @@ template <int D, bool PAGED, bool PARTIAL>
 __device__ __forceinline__ void tile_item(const TileParams& p, int item) {
   constexpr int KT = kTileKeys;  // 64 keys per tile
   constexpr int KS = D + 8;      // K row stride in LDS (elements); +8 spreads banks
-  constexpr int VS = KT + 8;     // V^T row stride in LDS
+  constexpr int VS = KT + 8;     // paged: V^T row stride in LDS
+  // packed: V row stride in LDS; +32 elements puts the 4 rows one transposing
+  // read touches per pass in disjoint bank windows
+  constexpr int VSR = D + 32;
+  constexpr int VEL = PAGED ? D * VS : KT * VSR;  // elements of one V stage
   constexpr int NKK = D / 16;    // K-slices of the score product
   constexpr int NDB = D / 32;    // 32-row blocks of O^T
   constexpr int CPR = D / 8;     // 16-byte chunks per key row
   constexpr int KPT = KT * CPR / kThreads;           // K chunks per thread (2 or 1)
-  constexpr int VPT = PAGED ? 8 * D / kThreads : 1;  // V loads per thread (paged chunks / packed pairs)
+  constexpr int VPT = PAGED ? 8 * D / kThreads : KPT;  // V loads per thread (paged chunks / packed pieces)
   constexpr int NB = KT / kBlock;                    // blocks per tile (paged)
 
   __shared__ __attribute__((aligned(16))) uint16_t Ks[2][KT * KS];
-  __shared__ __attribute__((aligned(16))) uint16_t Vt[2][D * VS];
+  __shared__ __attribute__((aligned(16))) uint16_t Vt[2][VEL];
 
   const WorkRec w = p.work[item];
   if (w.rng_count <= 0) return;
@@ -174,10 +187,7 @@ __device__ __forceinline__ void tile_item(const TileParams& p, int item) {
     }
   }
   // paged V: chunk i of a thread is d row d, keys 8h .. 8h+7 of block bi
-  // (bi wave-uniform).  packed V: key pair (2pr, 2pr+1) and 16-byte chunk
-  // dc; with fewer chunks than thread groups (d = 64) the extra threads load
-  // a duplicate chunk and store nothing: every thread issues the same loads,
-  // so the compiler's load wait counts stay exact.
+  // (bi wave-uniform).  packed V: the pieces of K (same rows and chunks).
   int v_blk[VPT], v_d[VPT], v_h[VPT];
   uint32_t v_off[VPT];
 #pragma unroll
@@ -189,9 +199,10 @@ __device__ __forceinline__ void tile_item(const TileParams& p, int item) {
     v_h[i] = rem & 1;
     v_off[i] = ((uint32_t)kvh * D + v_d[i]) * kBlock + v_h[i] * 8;
   }
-  const int v_pr = tid % (KT / 2), v_dc = (tid / (KT / 2)) % CPR;
-  const bool v_on = PAGED || tid / (KT / 2) < CPR;
-  const uint32_t v_poff = (uint32_t)kvh * D + v_dc * 8;  // packed V: offset within a row
+  // packed V^T fragments: this lane's element offset of its transposing read
+  // within a 16-key group and 32-row block (lane r of a 16-lane group reads
+  // key row 4*half + r/4, d columns 16*(group&1) + 4*(r%4) .. +3)
+  const int v_tr = (4 * hf + ((lane & 15) >> 2)) * VSR + 16 * ((lane >> 4) & 1) + 4 * (lane & 3);
 
   // Tile cursors (wave-uniform).  No implicit padding: copies of a padded
   // struct keep the padding in memory (the compiler would place it in LDS).
@@ -213,7 +224,7 @@ __device__ __forceinline__ void tile_item(const TileParams& p, int item) {
   };
 
   // Staging registers: set b%2 holds bundle b = K(b) and V(b-1).
-  uint4 kr[2][KPT], vr[2][2 * VPT];
+  uint4 kr[2][KPT], vr[2][VPT];
   int vkeep[2][PAGED ? VPT : 1];  // paged V: keys of each chunk inside the range
   bool vfull[2] = {true, true};     // paged V: the whole tile lies inside the range
 
@@ -258,11 +269,12 @@ __device__ __forceinline__ void tile_item(const TileParams& p, int item) {
       });
     } else {
       const int last = c.R.n_keys - 1 - kbase;
-      const int k0 = 2 * v_pr, k1 = k0 + 1;
-      const int c0 = k0 <= last ? k0 : last, c1 = k1 <= last ? k1 : last;
       const uint16_t* tb = Vg + (c.R.kv_start + kbase) * (int64_t)HD;
-      vr[X][0] = load16(tb + (__umul24((uint32_t)c0, HD) + v_poff));
-      vr[X][1] = load16(tb + (__umul24((uint32_t)c1, HD) + v_poff));
+      static_for<VPT>([&](auto ic) {
+        constexpr int i = decltype(ic)::value;
+        const int kc = k_key[i] <= last ? k_key[i] : last;
+        vr[X][i] = load16(tb + (__umul24((uint32_t)kc, HD) + k_off[i]));
+      });
     }
   };
   auto store_k = [&](auto xc, uint16_t* ks) {
@@ -283,18 +295,11 @@ __device__ __forceinline__ void tile_item(const TileParams& p, int item) {
         *reinterpret_cast<uint2*>(row + 4 * v_h[i]) = make_uint2(x.x, x.y);
         *reinterpret_cast<uint2*>(row + 8 + 4 * v_h[i]) = make_uint2(x.z, x.w);
       });
-    } else if (v_on) {
-      const int pos = vt_pos(2 * v_pr);
-      const uint32_t a[4] = {vr[X][0].x, vr[X][0].y, vr[X][0].z, vr[X][0].w};
-      const uint32_t b[4] = {vr[X][1].x, vr[X][1].y, vr[X][1].z, vr[X][1].w};
-#pragma unroll
-      for (int m = 0; m < 4; ++m) {
-        // d = dc*8 + 2m holds (key 2pr, key 2pr+1) low halves; d+1 the high
-        // halves (one byte permute each)
-        *reinterpret_cast<uint32_t*>(&vt[(v_dc * 8 + 2 * m) * VS + pos]) = __builtin_amdgcn_perm(b[m], a[m], 0x05040100u);
-        *reinterpret_cast<uint32_t*>(&vt[(v_dc * 8 + 2 * m + 1) * VS + pos]) =
-            __builtin_amdgcn_perm(b[m], a[m], 0x07060302u);
-      }
+    } else {
+      static_for<VPT>([&](auto ic) {
+        constexpr int i = decltype(ic)::value;
+        store16(&vt[k_key[i] * VSR + k_dc[i] * 8], vr[X][i]);
+      });
     }
   };
 
@@ -418,7 +423,13 @@ __device__ __forceinline__ void tile_item(const TileParams& p, int item) {
     auto frag = [&](int i) -> bf16x8_t {
       if (i < NPV) {
         const int g = i / NDB, db = i % NDB;
-        return *reinterpret_cast<const bf16x8_t*>(&vt[(db * 32 + l32) * VS + (g >> 1) * 32 + 16 * (g & 1) + hf * 8]);
+        if constexpr (PAGED) {
+          return *reinterpret_cast<const bf16x8_t*>(&vt[(db * 32 + l32) * VS + (g >> 1) * 32 + 16 * (g & 1) + hf * 8]);
+        } else {
+          // keys (g/2)*32 + 16(g%2) + 4*half + {0..3} and {8..11}
+          const uint16_t* b = vt + v_tr + ((g >> 1) * 32 + 16 * (g & 1)) * VSR + db * 32;
+          return tr_pair(b, b + 8 * VSR);
+        }
       }
       const int j = i - NPV, kk = j >> 1, mb = j & 1;
       return *reinterpret_cast<const bf16x8_t*>(&ks[(mb * 32 + l32) * KS + kk * 16 + hf * 8]);
@@ -484,7 +495,7 @@ __device__ __forceinline__ void tile_item(const TileParams& p, int item) {
   }
   load_bundle(Set0{});  // bundle 0: K(0) (its V part re-reads tile 0, unused)
   store_k(Set0{}, Ks[0]);
-  for (int i = tid; i < D * VS / 8; i += kThreads) reinterpret_cast<uint4*>(Vt[1])[i] = make_uint4(0, 0, 0, 0);
+  for (int i = tid; i < VEL / 8; i += kThreads) reinterpret_cast<uint4*>(Vt[1])[i] = make_uint4(0, 0, 0, 0);
   load_bundle(Set1{});  // bundle 1: K(1), V(0)
   load_bundle(Set0{});  // bundle 2: K(2), V(1)
   __syncthreads();
