@@ -449,8 +449,8 @@ def run_driver(args, torch, np, syn, pa, dev, wl):
                 c = sess.open(x, lay_len[x])
                 kind[c] = ("content", pg)
                 born.append(c)
-        if ended:
-            live = [x for x in live if x not in ended]
+        for x in ended:
+            live.remove(x)
         live += born
         t4 = time.perf_counter()
         if timed:
