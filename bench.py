@@ -65,6 +65,9 @@ def parse_args(argv=None):
                     help="bytes of each of the K and V pools in GiB (0: 45%% of HBM each, backing off on failure)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-backward", action="store_true", help="skip the backward of the forward workload")
+    ap.add_argument("--no-cold", action="store_true", help="skip the cold-cache decode timing")
+    ap.add_argument("--no-secondary", action="store_true",
+                    help="skip the single-page and dense-page decode configurations")
     ap.add_argument("--no-baselines", action="store_true",
                     help="skip the baselines (dense-mask SDPA, gather-varlen, per-stream decode)")
     ap.add_argument("--driver-steps", type=int, default=60,
@@ -186,11 +189,11 @@ def measured_traffic():
 PROFILE_COMMANDS = """\
     R=<repository root>; cd /tmp && export TMPDIR=/tmp
     rocprofv3 --kernel-trace --stats -d $R/gpurun_out/prof/trace -o bench -- \\
-        python3 $R/bench.py --steps 5 --warmup 1 --no-cpu-baseline --no-baselines --driver-steps 0 > $R/gpurun_out/prof/trace/bench.json
+        python3 $R/bench.py --steps 5 --warmup 1 --no-cpu-baseline --no-baselines --driver-steps 0 --no-secondary --no-cold > $R/gpurun_out/prof/trace/bench.json
     rocprofv3 --pmc FETCH_SIZE --kernel-include-regex padoc -f csv -d $R/gpurun_out/prof/fetch -o p -- \\
-        python3 $R/bench.py --steps 5 --warmup 1 --no-cpu-baseline --no-baselines --driver-steps 0
+        python3 $R/bench.py --steps 5 --warmup 1 --no-cpu-baseline --no-baselines --driver-steps 0 --no-secondary --no-cold
     rocprofv3 --pmc WRITE_SIZE --kernel-include-regex padoc -f csv -d $R/gpurun_out/prof/write -o p -- \\
-        python3 $R/bench.py --steps 5 --warmup 1 --no-cpu-baseline --no-baselines --driver-steps 0
+        python3 $R/bench.py --steps 5 --warmup 1 --no-cpu-baseline --no-baselines --driver-steps 0 --no-secondary --no-cold
     rocprofv3 --pmc FETCH_SIZE -f csv -d $R/gpurun_out/prof/copy_fetch -o c -- python3 $R/bench.py --calibrate-copy
     rocprofv3 --pmc WRITE_SIZE -f csv -d $R/gpurun_out/prof/copy_write -o c -- python3 $R/bench.py --calibrate-copy
     python3 $R/bench.py --summarize-profile $R/gpurun_out/prof
@@ -267,8 +270,13 @@ def summarize_profile(d: str) -> None:
 
 # ---------------------------------------------------------------- decode leg
 
-def run_decode(args, torch, np, syn, pa, dev):
-    wl = syn.make_workload(args.workload, args.seed)
+def run_decode(args, torch, np, syn, pa, dev, name=None, pool_gib=None, steps=None):
+    """One decode step of workload `name` (default: the headline workload),
+    timed warm (consecutive calls) and cold (a 1 GiB write between calls,
+    outside the timed span, so no K/V stays in L2 / the memory-side cache)."""
+    wl = syn.make_workload(name or args.workload, args.seed)
+    steps = args.steps if steps is None else steps
+    pool_gib = args.pool_gib if pool_gib is None else pool_gib
     assert wl.kind == "decode"
     Hq, Hkv, d = wl.num_heads_q, wl.num_heads_kv, wl.head_dim
     T = syn.count_tokens(wl.pages)
@@ -277,7 +285,7 @@ def run_decode(args, torch, np, syn, pa, dev):
     segs_paged = pa.segments_from_pages(wl.pages, 16)
     segs_packed = pa.segments_from_pages(wl.pages, 0)
 
-    kc, vc, n_pool = alloc_pools(torch, nb, Hkv, d, args.pool_gib, dev)
+    kc, vc, n_pool = alloc_pools(torch, nb, Hkv, d, pool_gib, dev)
     pool_gib = 2 * n_pool * Hkv * 16 * d * 2 / (1 << 30)
     log(f"decode workload {wl.name}: {len(wl.pages)} pages, {T} cached tokens, {nq} queries, "
         f"{nb} blocks in a {pool_gib:.1f} GiB K+V pool")
@@ -322,8 +330,26 @@ def run_decode(args, torch, np, syn, pa, dev):
     def step():
         pa.branch_decode(q, kc, vc, bt, plan, out=o, lse=lse, workspace=ws)
 
-    ms, kms = timed_steps(step, args.steps, args.warmup, torch, pa)
+    ms, kms = timed_steps(step, steps, args.warmup, torch, pa)
     k_ms = statistics.mean(kms)
+    # cold: flush between calls (not timed)
+    flush = torch.empty(1 << 30, dtype=torch.uint8, device=dev)
+    cold = []
+    n_cold = 0 if args.no_cold else max(10, steps // 2)
+    evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(n_cold)]
+    for b, a in evs:
+        b.record()  # creates the underlying events
+        a.record()
+    torch.cuda.synchronize()
+    for i, (b, a) in enumerate(evs):
+        flush.fill_(i & 255)
+        pa.set_kernel_events(b, a)
+        step()
+        pa.set_kernel_events()
+        cold.append((b, a))
+    torch.cuda.synchronize()
+    cold_ms = [b.elapsed_time(a) for b, a in cold] or [float("nan")]
+    del flush
 
     # algorithmic bytes: every cached K/V token read once, Q read, O/LSE written,
     # block-table ids of the referenced blocks read
@@ -345,6 +371,9 @@ def run_decode(args, torch, np, syn, pa, dev):
     res = {
         "workload": wl.name, "ms_per_step": ms, "kernel_ms": k_ms,
         "kernel_ms_p10": float(np.percentile(kms, 10)), "kernel_ms_p90": float(np.percentile(kms, 90)),
+        "kernel_ms_cold_p10": float(np.percentile(cold_ms, 10)), "kernel_ms_cold_p50": float(np.median(cold_ms)),
+        "kernel_ms_cold_p90": float(np.percentile(cold_ms, 90)),
+        "kernel_gbps_cold": kernel_bytes / (float(np.median(cold_ms)) * 1e-3) / 1e9,
         "tokens_per_s": nq / (ms * 1e-3), "step_gbps": step_bytes / (ms * 1e-3) / 1e9,
         "kernel_gbps": kernel_bytes / (k_ms * 1e-3) / 1e9, "kernel_bytes": kernel_bytes,
         "kv_bytes": kv_bytes, "naive_per_stream_kv_bytes": naive * Hkv * d * 2 * 2,
@@ -475,6 +504,38 @@ def run_driver(args, torch, np, syn, pa, dev, wl):
     del kc, vc, bt, q_buf, k_buf, v_buf, o_buf
     torch.cuda.empty_cache()
     return res
+
+
+# ---------------------------------------------------------------- attainable rates on this machine
+
+def attainable(torch, dev):
+    """Measured references next to the published peaks: a streaming read
+    (sum over a 4 GiB bf16 tensor) and a large bf16 matrix product (library
+    GEMM, 8192^3)."""
+    x = torch.ones(1 << 31, dtype=torch.bfloat16, device=dev)
+    ms_read = _event_ms(torch, lambda: x.sum(dtype=torch.float32), 5)
+    del x
+    a = torch.randn(8192, 8192, device=dev).to(torch.bfloat16)
+    b = torch.randn(8192, 8192, device=dev).to(torch.bfloat16)
+    ms_mm = _event_ms(torch, lambda: a @ b, 10)
+    del a, b
+    torch.cuda.empty_cache()
+    return {"read_gbps": (2 << 31) / (ms_read * 1e-3) / 1e9, "read_bytes": 2 << 31,
+            "gemm_bf16_tflops": 2 * 8192 ** 3 / (ms_mm * 1e-3) / 1e12, "gemm_shape": [8192, 8192, 8192]}
+
+
+def secondary_decode(args, torch, np, syn, pa, dev, name):
+    """A smaller decode configuration (its own pool size), summarised."""
+    wl = syn.make_workload(name, args.seed)
+    r, _ = run_decode(args, torch, np, syn, pa, dev, name=name, pool_gib=(wl.pool_bytes or (16 << 30)) / (1 << 30),
+                      steps=max(20, args.steps))
+    return {"workload": name, "queries": r["queries"], "cached_tokens": r["cached_tokens"],
+            "kernel_us": r["kernel_ms"] * 1e3, "kernel_us_cold_p50": r["kernel_ms_cold_p50"] * 1e3,
+            "kernel_us_cold_p10": r["kernel_ms_cold_p10"] * 1e3, "kernel_us_cold_p90": r["kernel_ms_cold_p90"] * 1e3,
+            "tokens_per_s": r["tokens_per_s"], "kernel_gbps": r["kernel_gbps"],
+            "hbm_frac": r["kernel_gbps"] / HBM_PEAK_GBS, "kernel_tflops": r["kernel_tflops"],
+            "mfma_frac": r["kernel_tflops"] / BF16_PEAK_TFLOPS, "sharing_factor": r["sharing_factor"],
+            "plan_ms": r["plan_ms"]}
 
 
 # ---------------------------------------------------------------- decoding-depth accounting
@@ -794,7 +855,13 @@ def run_cpu_baseline(args, wl, np, syn):
         cores = max([i.get("num_threads", 1) for i in info if i.get("user_api") == "blas"] or [1])
     except Exception:
         cores = len(os.sched_getaffinity(0))
-    return {"value": nq / dt, "unit": "tokens/s", "cores": int(cores), "kind": "oracle",
+    model = ""
+    try:
+        with open("/proc/cpuinfo") as fh:
+            model = next((l.split(":", 1)[1].strip() for l in fh if l.startswith("model name")), "")
+    except OSError:
+        pass
+    return {"value": nq / dt, "unit": "tokens/s", "cores": int(cores), "kind": "oracle", "cpu_model": model,
             "sample": f"{len(pages)} of {len(wl.pages)} pages ({nq} queries, {T} cached tokens), fp64 dense "
                       f"ancestor mask per page, {dt:.1f} s wall"}
 
@@ -832,6 +899,11 @@ def main(argv=None) -> int:
     pa.version()  # loads the library (fails loudly if it was not built)
 
     dec, wl = run_decode(args, torch, np, syn, pa, dev)
+    others = None
+    if not args.no_secondary:
+        others = [secondary_decode(args, torch, np, syn, pa, dev, n)
+                  for n in ("single_page_decode", "dense_page_mixed_step")]
+    refs = None if args.no_baselines else attainable(torch, dev)
     drv = run_driver(args, torch, np, syn, pa, dev, wl) if args.driver_steps > 0 else None
     if not args.no_baselines:
         log("decode baselines: per-stream sequences without tree sharing")
@@ -865,6 +937,8 @@ def main(argv=None) -> int:
                      "bytes_per_launch": dec["kernel_bytes"]},
         "cpu_baseline": cpu,
         "decode": dec,
+        "other_decode_configs": others,
+        "attainable": refs,
         "driver": drv,
         "accounting": [depth_accounting(pa, syn, np, n, args.seed)
                        for n in ("concurrent_decode_64pages", "packed_forward_8pages")],

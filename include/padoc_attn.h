@@ -136,10 +136,11 @@ typedef struct {
   int32_t max_chunk_keys;        /* decode: split keys into chunks of at most
                                     this many (multiple of 64); 0 = automatic */
   int32_t target_workgroups;     /* decode chunk sizes (0 = 1024): shared keys
-                                    are cut into about this / 4 tile items
-                                    (8 wavefronts each), private keys into
-                                    about 2x this many wavefront items; both
-                                    chunk sizes clamped to [512, 8192] keys   */
+                                    are cut into the fewest chunks that keep
+                                    the tile items (8 wavefronts each) within
+                                    this / 4, private keys into about 2x this
+                                    many wavefront items; both chunk sizes
+                                    clamped to [512, 8192] keys              */
 } padoc_tree_desc;
 
 typedef struct padoc_plan padoc_plan;

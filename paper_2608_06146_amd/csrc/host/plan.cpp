@@ -515,10 +515,9 @@ void build_decode(padoc_plan& P, Builder& B, const AncList& anc, const padoc_tre
       }
     }
   }
-  // Chunk sizes.  Shared keys: about one tile item (a whole compute unit's
-  // worth of wavefronts) per target_workgroups / 4, since every extra chunk
-  // costs a round of split partials.  Private keys: about
-  // target_workgroups x 2 wavefronts' worth of equal pieces.
+  // Chunk sizes.  Shared keys: at most target_workgroups / 4 tile items (one
+  // per compute unit, see below).  Private keys: about target_workgroups x 2
+  // wavefronts' worth of equal pieces.
   auto& svis = S.svis;
   auto& pvis = S.pvis;
   auto& svis_at = S.svis_at;
@@ -527,10 +526,9 @@ void build_decode(padoc_plan& P, Builder& B, const AncList& anc, const padoc_tre
   pvis.clear();
   svis_at.assign(1, 0);
   pvis_at.assign(1, 0);
-  int64_t total_s = 0, total_p = 0;
+  int64_t total_p = 0;
   for (const Task& t : stasks) {
     B.visible(t, shared, svis);
-    for (size_t r = svis_at.back(); r < svis.size(); ++r) total_s += round_up(svis[r].n_keys, 64) * P.Hkv;
     svis_at.push_back(svis.size());
   }
   for (const Task& t : ptasks) {
@@ -545,8 +543,45 @@ void build_decode(padoc_plan& P, Builder& B, const AncList& anc, const padoc_tre
     const int64_t ch = round_up(std::max<int64_t>(1, ceil_div(total, pieces)), 64);
     return std::min<int64_t>(std::max<int64_t>(ch, 512), 8192);
   };
-  const int64_t CHs = chunk_keys(total_s, std::max<int64_t>(1, tw / 4));
   const int64_t CHp = chunk_keys(total_p, 2 * tw);
+  // Shared keys: every tile item takes a whole compute unit, so the items
+  // should fit in one round of target_workgroups / 4 units -- a few items
+  // over that would double the step.  Smallest chunk (a multiple of 64 in
+  // [512, 8192]) whose items (over all tasks and KV heads) fit, else 8192.
+  auto shared_items = [&](int64_t CH) {
+    int64_t n = 0;
+    for (size_t i = 0; i + 1 < svis_at.size(); ++i) {
+      int64_t room = 0;
+      for (size_t r = svis_at[i]; r < svis_at[i + 1]; ++r)
+        for (int32_t kb = 0; kb < svis[r].n_keys;) {
+          if (room <= 0) {
+            ++n;
+            room = CH;
+          }
+          const int32_t take = (int32_t)std::min<int64_t>(svis[r].n_keys - kb, room);
+          kb += take;
+          room -= round_up(take, 64);
+        }
+    }
+    return n * P.Hkv;
+  };
+  int64_t CHs = d->max_chunk_keys;
+  if (CHs <= 0) {
+    const int64_t target = std::max<int64_t>(1, tw / 4);
+    int64_t lo = 8, hi = 128;  // chunk = 64 * k keys
+    if (shared_items(64 * hi) > target) {
+      lo = hi;
+    } else {
+      while (lo < hi) {
+        const int64_t mid = (lo + hi) / 2;
+        if (shared_items(64 * mid) <= target)
+          hi = mid;
+        else
+          lo = mid + 1;
+      }
+    }
+    CHs = 64 * lo;
+  }
 
   // (row * Hkv + kvh, slot) of every partial, in creation order.
   auto& parts = S.parts;
