@@ -83,26 +83,22 @@ padoc_status check_unprepared(const padoc_session* s) {
 }
 
 // The step's tree: every kept stream in id order with its length after the
-// step (lengths as they stand when n_new is null).  Region offsets of the
-// streams that move are taken from `moved_off` (stream id -> new offset, -1
-// = stays).
-void fill_tree(const padoc_session* s, const int32_t* n_new, const int32_t* n_query,
-               const std::vector<int64_t>* moved_off, std::vector<padoc_segment>& seg,
-               std::vector<int32_t>& seg_id, std::vector<int32_t>& plan_idx) {
+// step (lengths as they stand when n_new is null); a stream moving to a new
+// block-table region (moving_to >= 0) is placed there.
+void fill_tree(padoc_session* s, const int32_t* n_new, const int32_t* n_query, std::vector<padoc_segment>& seg,
+               std::vector<int32_t>& seg_id) {
   seg.clear();
   seg_id.clear();
-  plan_idx.assign(s->st.size(), -1);
   int64_t q = 0;
   size_t row = 0;
   for (int32_t id : s->kept_ids) {
-    const padoc_session::Stream& x = s->st[id];
+    padoc_session::Stream& x = s->st[id];
     padoc_segment g{};
-    g.parent = x.parent >= 0 ? plan_idx[x.parent] : -1;
+    g.parent = x.parent >= 0 ? s->st[x.parent].index : -1;  // kept parents come first
     g.fork = x.fork;
     g.len = x.len;
     g.q_len = 0;
-    g.kv_off = x.cls >= 0 ? x.bt_off : 0;
-    if (moved_off && (*moved_off)[id] >= 0) g.kv_off = (*moved_off)[id];
+    g.kv_off = x.moving_to >= 0 ? x.moving_to : (x.cls >= 0 ? x.bt_off : 0);
     g.q_off = q;
     if (row < s->open_ids.size() && s->open_ids[row] == id) {
       if (n_new) {
@@ -112,7 +108,7 @@ void fill_tree(const padoc_session* s, const int32_t* n_new, const int32_t* n_qu
       }
       ++row;
     }
-    plan_idx[id] = (int32_t)seg.size();
+    x.index = (int32_t)seg.size();
     seg.push_back(g);
     seg_id.push_back(id);
   }
@@ -239,9 +235,11 @@ extern "C" padoc_status padoc_session_prepare(padoc_session* s, const int32_t* n
       int64_t off;
     };
     std::vector<Move> moves;
-    std::vector<int64_t> moved_off(s->st.size(), -1);
     auto undo = [&] {
-      for (const Move& m : moves) s->free_regions[m.cls].push_back(m.off);
+      for (const Move& m : moves) {
+        s->free_regions[m.cls].push_back(m.off);
+        s->st[m.id].moving_to = -1;
+      }
     };
     for (size_t i = 0; i < R; ++i) {
       const int32_t id = s->open_ids[i];
@@ -255,10 +253,10 @@ extern "C" padoc_status padoc_session_prepare(padoc_session* s, const int32_t* n
                          (long long)s->desc.block_table_capacity);
       }
       moves.push_back(m);
-      moved_off[id] = m.off;
+      s->st[id].moving_to = m.off;
     }
     // The step's schedule.
-    fill_tree(s, n_new, n_query, &moved_off, s->seg, s->seg_id, s->plan_idx);
+    fill_tree(s, n_new, n_query, s->seg, s->seg_id);
     padoc_tree_desc d{};
     d.n_seg = (int32_t)s->seg.size();
     d.seg = s->seg.data();
@@ -292,6 +290,7 @@ extern "C" padoc_status padoc_session_prepare(padoc_session* s, const int32_t* n
     }
     for (const Move& m : moves) {
       padoc_session::Stream& x = s->st[m.id];
+      x.moving_to = -1;
       if (x.cls >= 0) free_region(s, x.cls, x.bt_off);
       x.cls = m.cls;
       x.bt_off = m.off;
@@ -353,7 +352,7 @@ extern "C" padoc_status padoc_session_view_get(const padoc_session* cs, padoc_se
   std::memset(v, 0, sizeof(*v));
   if (!s->prepared) {
     try {
-      fill_tree(s, nullptr, nullptr, nullptr, s->seg, s->seg_id, s->plan_idx);
+      fill_tree(s, nullptr, nullptr, s->seg, s->seg_id);
       s->row_id.assign(s->open_ids.begin(), s->open_ids.end());
     } catch (const std::bad_alloc&) {
       return set_error(PADOC_ERR_ARG, "out of host memory");

@@ -21,6 +21,10 @@ struct padoc_session {
     int64_t bt_off = 0;  // first entry of the block-table region
     int32_t cls = -1;    // region holds 1 << cls entries; -1 = no region yet
     std::vector<int32_t> blocks;
+    // per step: index in the step's tree, and a region the stream moves to
+    // (-1: none) while the step is being prepared
+    int32_t index = -1;
+    int64_t moving_to = -1;
   };
   std::vector<Stream> st;
   std::vector<int32_t> open_ids, kept_ids;  // ascending
@@ -33,7 +37,7 @@ struct padoc_session {
   bool prepared = false;
   padoc_plan plan;
   std::vector<padoc_segment> seg;
-  std::vector<int32_t> seg_id, row_id, new_off, q_off, new_slot, patch, plan_idx;
+  std::vector<int32_t> seg_id, row_id, new_off, q_off, new_slot, patch;
   std::vector<int32_t> row_n_new;
   size_t off_patch = 0, rec_bytes = 0;  // workspace: slots at 0, patches at off_patch
   size_t ws_records = 0, ws_bytes = 0;  // records area (aligned), total

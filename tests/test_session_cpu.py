@@ -230,3 +230,27 @@ def test_session_errors():
     with pytest.raises(pa.PadocError) as e:
         pa.DecodeSession(4, 3, 64, num_blocks=16)   # Hq not a multiple of Hkv
     assert e.value.status == _lib.ERR_SHAPE
+
+
+def test_steps_with_no_open_stream_and_closed_parents():
+    """A step with no open stream is empty; a closed stream with an open
+    child keeps its blocks and takes new children."""
+    sess = pa.DecodeSession(4, 2, 64, num_blocks=32)
+    n_kv, n_q, ws = sess.prepare()
+    assert (n_kv, n_q) == (0, 0) and len(sess.view()["seg"]) == 0
+    sess.commit()
+    r = sess.open(-1, 0)
+    sess.prepare(np.array([20], np.int32), np.array([0], np.int32))
+    sess.commit()
+    a = sess.open(r, 20)
+    sess.close(r)
+    b = sess.open(r, 7)                      # a closed but kept parent takes a child
+    sess.prepare()
+    v = sess.view()
+    assert list(v["seg"]["parent"]) == [-1, 0, 0] and list(v["seg"]["fork"]) == [0, 20, 7]
+    assert list(v["seg"]["q_len"]) == [0, 1, 1]
+    sess.commit()
+    sess.close(a)
+    sess.close(b)
+    v = sess.view()
+    assert len(v["seg"]) == 0 and v["free_blocks"] == 32
