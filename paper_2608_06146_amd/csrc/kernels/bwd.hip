@@ -20,15 +20,18 @@
 //              the same keys; results go to fp32 rows (stored by an item that
 //              holds the whole run, added by the pieces of a split run)
 //   bwd_finalize  fp32 accumulators -> bf16 dK, dV (round to nearest even)
-// All products are v_mfma_f32_32x32x16_bf16 with fp32 accumulation.  The
-// operand whose contraction index is not contiguous in memory (K^T for dQ,
-// dO^T and Q^T for dV and dK) is staged transposed in LDS with the column
-// permutation that makes a lane's 8 values one 16-byte read against the
-// matrix-core layout of the probabilities (the same permutation as the
-// forward's V^T).
+// All products are v_mfma_f32_32x32x16_bf16 with fp32 accumulation.  An
+// operand whose contraction index is not contiguous in memory is either
+// staged transposed in LDS with the column permutation that makes a lane's
+// 8 values one 16-byte read against the matrix-core layout of the
+// probabilities (K^T for dQ), or read from the row-major block with the
+// transposing LDS read of gfx950 (dO^T and Q^T for dV and dK: within each
+// group of 16 lanes, lane r supplies the address of 4 consecutive elements
+// and lane 4a+b receives element b of the pieces of lanes a, 4+a, 8+a, 12+a).
 #include <algorithm>
 
 #include "device_common.hpp"
+#include "tile_item.hpp"
 
 namespace padoc {
 
@@ -258,19 +261,24 @@ __global__ __launch_bounds__(kThreads) void bwd_dq_kernel(BwdParams p) {
 
 template <int D>
 __global__ __launch_bounds__(kThreads) void bwd_dkdv_kernel(BwdParams p) {
-  constexpr int QS = D + 8;   // row stride of the row-major Q / dO blocks
-  constexpr int TS = 32 + 8;  // row stride of the transposed blocks
   constexpr int NKK = D / 16;
   constexpr int NDB = D / 32;
   constexpr int CPR = D / 8;
+  // Q / dO blocks: 32 rows of D elements, 16-byte chunk c of row r stored at
+  // chunk c ^ sw(r), so that the row reads (16 rows, one chunk) and the
+  // transposing reads (4 rows, 4 aligned chunks) each touch distinct banks
+  // (d = 128: rows of 256 bytes, one bank row each; d = 64: two rows per
+  // bank row, so the swizzle keys on the row pair).
+  auto sw = [](int r) {
+    return CPR == 16 ? (((r & 3) << 2) | ((r >> 2) & 3)) : ((((r >> 1) & 1) << 2) | ((r >> 2) & 3));
+  };
+  auto at = [&](int r, int c) { return r * D + ((c ^ sw(r)) << 3); };
 
   // Two stages: block i is computed from stage i%2 while block i+1 is stored
   // into the other one (one barrier per block).
   struct Stage {
-    uint16_t q[32 * QS];  // Q rows (column-major block: row = column)
-    uint16_t g[32 * QS];  // dO rows
-    uint16_t qt[D * TS];  // Q transposed, columns permuted
-    uint16_t gt[D * TS];  // dO transposed, columns permuted
+    uint16_t q[32 * D];  // Q rows (row = column of the block), swizzled chunks
+    uint16_t g[32 * D];  // dO rows
     float ls[32];         // LSE * log2(e) per column
     float dd[32];         // dO . O per column
     int lm[32];           // keys of the item the column sees
@@ -298,12 +306,12 @@ __global__ __launch_bounds__(kThreads) void bwd_dkdv_kernel(BwdParams p) {
   }
 
   // Staging geometry: thread -> (column, 16-byte chunk) of a 32-column block,
-  // columns fastest: the transposed stores of a wave then spread over 32
-  // banks (chunk-fastest lanes would hit rows 8 * TS apart, two banks); with
-  // d = 64 the upper half of the threads repeats the lower half's loads and
-  // stores nothing.  Every thread also loads the per-column scalars of column
-  // tid % 32 (threads < 32 store them), so all threads issue the same loads
-  // and the compiler's load wait counts stay exact.
+  // columns fastest (16 lanes of a store write 16 rows of one chunk, which
+  // the swizzle spreads over all banks); with d = 64 the upper half of the
+  // threads repeats the lower half's loads and stores nothing.  Every thread
+  // also loads the per-column scalars of column tid % 32 (threads < 32 store
+  // them), so all threads issue the same loads and the compiler's load wait
+  // counts stay exact.
   const int s_col = tid % 32, s_dc = (tid / 32) % CPR;
   const bool s_on = tid < 32 * CPR;
   const int c_end = b.col0 + b.ncol;
@@ -344,30 +352,9 @@ __global__ __launch_bounds__(kThreads) void bwd_dkdv_kernel(BwdParams p) {
   };
   auto store = [&](auto xc, Stage& S) {
     constexpr int X = decltype(xc)::value;
-    // Transposed stores as 32-bit words of a column pair: lanes 2c and 2c+1
-    // (columns 2c, 2c+1, adjacent in the permuted order) swap halves; the
-    // even lane writes the even d rows, the odd lane the odd ones.
-    const uint32_t a[4] = {qr[X].x, qr[X].y, qr[X].z, qr[X].w};
-    const uint32_t g[4] = {gr[X].x, gr[X].y, gr[X].z, gr[X].w};
-    uint32_t an[4], gn[4];
-#pragma unroll
-    for (int m = 0; m < 4; ++m) {
-      an[m] = (uint32_t)__shfl_xor((int)a[m], 1);
-      gn[m] = (uint32_t)__shfl_xor((int)g[m], 1);
-    }
     if (s_on) {
-      store16(&S.q[s_col * QS + s_dc * 8], qr[X]);
-      store16(&S.g[s_col * QS + s_dc * 8], gr[X]);
-      const int odd = s_col & 1;
-      const int pos = perm_pos(s_col & ~1);
-#pragma unroll
-      for (int m = 0; m < 4; ++m) {
-        const int row = s_dc * 8 + 2 * m + odd;
-        const uint32_t wq = odd ? __builtin_amdgcn_perm(a[m], an[m], 0x07060302u) : __builtin_amdgcn_perm(an[m], a[m], 0x05040100u);
-        const uint32_t wg = odd ? __builtin_amdgcn_perm(g[m], gn[m], 0x07060302u) : __builtin_amdgcn_perm(gn[m], g[m], 0x05040100u);
-        *reinterpret_cast<uint32_t*>(&S.qt[row * TS + pos]) = wq;
-        *reinterpret_cast<uint32_t*>(&S.gt[row * TS + pos]) = wg;
-      }
+      store16(&S.q[at(s_col, s_dc)], qr[X]);
+      store16(&S.g[at(s_col, s_dc)], gr[X]);
     }
     if (tid < 32) {
       S.ls[tid] = lr[X];
@@ -383,14 +370,24 @@ __global__ __launch_bounds__(kThreads) void bwd_dkdv_kernel(BwdParams p) {
     for (int i = 0; i < 16; ++i) acc[db][i] = 0.f;
   const float sl2 = p.scale_log2;
 
+  // A operand d x columns (Q^T or dO^T) of d block db and column group j:
+  // lane (d, half) gets columns 16j + 4*half + {0..3} and + {8..11} of row
+  // d, with two transposing reads (lane r of a 16-lane group supplies row
+  // 16j + 4*half (+8) + r/4, elements d0 + 4*(r%4) .. +3).
+  const int tr_r = (lane & 15) >> 2, tr_c = 2 * ((lane >> 4) & 1) + ((lane & 3) >> 1), tr_o = 4 * (lane & 1);
+  auto trf = [&](const uint16_t* blk, int j, int db) __attribute__((always_inline)) -> bf16x8_t {
+    const int r0 = 16 * j + 4 * hf + tr_r, c = 4 * db + tr_c;
+    return tile::tr_pair(blk + at(r0, c) + tr_o, blk + at(r0 + 8, c) + tr_o);
+  };
+
   // Block computation from one stage.  Fragments of each product group are
   // requested together before its matrix products.
-  auto compute = [&](const Stage& S) {
+  auto compute = [&](const Stage& S) __attribute__((always_inline)) {
     // S = Q K^T: columns on M, this wave's 32 keys on N.  Element i of a lane
     // is column (i/4)*8 + hf*4 + i%4 of the block and key `key`.
     bf16x8_t fa[NKK];
 #pragma unroll
-    for (int kk = 0; kk < NKK; ++kk) fa[kk] = *reinterpret_cast<const bf16x8_t*>(&S.q[l32 * QS + kk * 16 + hf * 8]);
+    for (int kk = 0; kk < NKK; ++kk) fa[kk] = *reinterpret_cast<const bf16x8_t*>(&S.q[at(l32, 2 * kk + hf)]);
     f32x16_t sc;
 #pragma unroll
     for (int i = 0; i < 16; ++i) sc[i] = 0.f;
@@ -414,7 +411,7 @@ __global__ __launch_bounds__(kThreads) void bwd_dkdv_kernel(BwdParams p) {
       for (int j = 0; j < 2; ++j)
 #pragma unroll
         for (int db = 0; db < NDB; ++db)
-          fb[j * NDB + db] = *reinterpret_cast<const bf16x8_t*>(&S.gt[(db * 32 + l32) * TS + 16 * j + hf * 8]);
+          fb[j * NDB + db] = trf(S.g, j, db);
 #pragma unroll
       for (int j = 0; j < 2; ++j) {
         bf16x8_t pb;
@@ -427,12 +424,12 @@ __global__ __launch_bounds__(kThreads) void bwd_dkdv_kernel(BwdParams p) {
     } else {
       // dP = dO V^T; dS = P (dP - D); dK^T += Q^T dS
 #pragma unroll
-      for (int kk = 0; kk < NKK; ++kk) fa[kk] = *reinterpret_cast<const bf16x8_t*>(&S.g[l32 * QS + kk * 16 + hf * 8]);
+      for (int kk = 0; kk < NKK; ++kk) fa[kk] = *reinterpret_cast<const bf16x8_t*>(&S.g[at(l32, 2 * kk + hf)]);
 #pragma unroll
       for (int j = 0; j < 2; ++j)
 #pragma unroll
         for (int db = 0; db < NDB; ++db)
-          fb[j * NDB + db] = *reinterpret_cast<const bf16x8_t*>(&S.qt[(db * 32 + l32) * TS + 16 * j + hf * 8]);
+          fb[j * NDB + db] = trf(S.q, j, db);
       f32x16_t dP;
 #pragma unroll
       for (int i = 0; i < 16; ++i) dP[i] = 0.f;
