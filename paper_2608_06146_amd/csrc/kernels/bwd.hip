@@ -21,13 +21,12 @@
 //              holds the whole run, added by the pieces of a split run)
 //   bwd_finalize  fp32 accumulators -> bf16 dK, dV (round to nearest even)
 // All products are v_mfma_f32_32x32x16_bf16 with fp32 accumulation.  An
-// operand whose contraction index is not contiguous in memory is either
-// staged transposed in LDS with the column permutation that makes a lane's
-// 8 values one 16-byte read against the matrix-core layout of the
-// probabilities (K^T for dQ), or read from the row-major block with the
-// transposing LDS read of gfx950 (dO^T and Q^T for dV and dK: within each
-// group of 16 lanes, lane r supplies the address of 4 consecutive elements
-// and lane 4a+b receives element b of the pieces of lanes a, 4+a, 8+a, 12+a).
+// operand whose contraction index is not contiguous in memory (K^T for dQ,
+// dO^T and Q^T for dV and dK) is read from its row-major LDS block with the
+// transposing LDS read of gfx950 (within each group of 16 lanes, lane r
+// supplies the address of 4 consecutive elements and lane 4a+b receives
+// element b of the pieces of lanes a, 4+a, 8+a and 12+a), two reads per
+// operand, in the key / column order of the probabilities' registers.
 #include <algorithm>
 
 #include "device_common.hpp"
@@ -45,10 +44,16 @@ constexpr float kLog2e = 1.4426950408889634f;
 
 __device__ __forceinline__ bf16x8_t as_bf16x8(const uint4& u) { return *reinterpret_cast<const bf16x8_t*>(&u); }
 
-// Position of column / key r inside a transposed row (see the file comment).
-__device__ __forceinline__ int perm_pos(int r) {
-  const int q = r & 15;
-  return (r & ~15) + ((q >> 2) & 1) * 8 + (q >> 3) * 4 + (q & 3);
+// Row-major LDS blocks of CPR 16-byte chunks per row store chunk c of row r
+// at chunk c ^ sw(r): the row reads of the matrix products (16 rows, one
+// chunk) and the transposing reads (4 rows, 4 aligned chunks) then each
+// touch distinct banks.  CPR = 16 (d = 128): one row per 256-byte bank row;
+// CPR = 8 (d = 64): two rows per bank row, so the swizzle keys on the row
+// pair.
+template <int CPR>
+__device__ __forceinline__ int swizzled_chunk(int r, int c) {
+  const int sw = CPR == 16 ? (((r & 3) << 2) | ((r >> 2) & 3)) : ((((r >> 1) & 1) << 2) | ((r >> 2) & 3));
+  return c ^ sw;
 }
 
 // ------------------------------------------------------------------ prep
@@ -79,16 +84,16 @@ __global__ __launch_bounds__(256) void bwd_prep_kernel(BwdParams p, int64_t n_ro
 template <int D>
 __global__ __launch_bounds__(kThreads) void bwd_dq_kernel(BwdParams p) {
   constexpr int KT = kTileKeys;  // 64 keys per tile
-  constexpr int KS = D + 8;      // row stride of the row-major K and V tiles
-  constexpr int TS = KT + 8;     // row stride of the transposed K tile
   constexpr int NKK = D / 16;
   constexpr int NDB = D / 32;
   constexpr int CPR = D / 8;
   constexpr int KPT = KT * CPR / kThreads;  // row pieces per thread (2 or 1)
 
-  __shared__ __attribute__((aligned(16))) uint16_t Ks[KT * KS];
-  __shared__ __attribute__((aligned(16))) uint16_t Vs[KT * KS];
-  __shared__ __attribute__((aligned(16))) uint16_t Kt[D * TS];
+  // K and V tiles: KT rows of D elements with swizzled 16-byte chunks (see
+  // swizzled_chunk), read by rows for S and dP and transposed (K^T) for dQ.
+  __shared__ __attribute__((aligned(16))) uint16_t Ks[KT * D];
+  __shared__ __attribute__((aligned(16))) uint16_t Vs[KT * D];
+  auto at = [&](int r, int c) { return r * D + (swizzled_chunk<CPR>(r, c) << 3); };
 
   const WorkRec w = p.work[blockIdx.x];
   if (w.rng_count <= 0) return;
@@ -119,7 +124,7 @@ __global__ __launch_bounds__(kThreads) void bwd_dq_kernel(BwdParams p) {
 
   const uint16_t* Kg = static_cast<const uint16_t*>(p.k);
   const uint16_t* Vg = static_cast<const uint16_t*>(p.v);
-  // row pieces (key, 16-byte chunk) and key pairs for the transposed K tile
+  // row pieces (key, 16-byte chunk)
   int r_key[KPT], r_dc[KPT];
 #pragma unroll
   for (int i = 0; i < KPT; ++i) {
@@ -127,8 +132,6 @@ __global__ __launch_bounds__(kThreads) void bwd_dq_kernel(BwdParams p) {
     r_key[i] = u / CPR;
     r_dc[i] = u % CPR;
   }
-  const int t_pr = tid % (KT / 2), t_dc = (tid / (KT / 2)) % CPR;
-  const bool t_on = tid / (KT / 2) < CPR;
 
   struct Cursor {
     int ri, kt;
@@ -144,7 +147,7 @@ __global__ __launch_bounds__(kThreads) void bwd_dq_kernel(BwdParams p) {
         c.ok = 0;
     }
   };
-  uint4 kr[KPT], vr[KPT], tr[2];
+  uint4 kr[KPT], vr[KPT];
   // Tile loads: rows past the range end repeat its last row (finite values
   // whose scores the mask removes).
   auto load = [&](const Cursor& c) {
@@ -157,28 +160,21 @@ __global__ __launch_bounds__(kThreads) void bwd_dq_kernel(BwdParams p) {
       kr[i] = load16(Kg + off);
       vr[i] = load16(Vg + off);
     }
-    const int k0 = 2 * t_pr, k1 = k0 + 1;
-    const int c0 = k0 <= last ? k0 : last, c1 = k1 <= last ? k1 : last;
-    tr[0] = load16(Kg + ((row0 + c0) * Hkv + kvh) * D + t_dc * 8);
-    tr[1] = load16(Kg + ((row0 + c1) * Hkv + kvh) * D + t_dc * 8);
   };
   auto store = [&]() {
 #pragma unroll
     for (int i = 0; i < KPT; ++i) {
-      store16(&Ks[r_key[i] * KS + r_dc[i] * 8], kr[i]);
-      store16(&Vs[r_key[i] * KS + r_dc[i] * 8], vr[i]);
+      store16(&Ks[at(r_key[i], r_dc[i])], kr[i]);
+      store16(&Vs[at(r_key[i], r_dc[i])], vr[i]);
     }
-    if (t_on) {
-      const int pos = perm_pos(2 * t_pr);
-      const uint32_t a[4] = {tr[0].x, tr[0].y, tr[0].z, tr[0].w};
-      const uint32_t b[4] = {tr[1].x, tr[1].y, tr[1].z, tr[1].w};
-#pragma unroll
-      for (int m = 0; m < 4; ++m) {
-        *reinterpret_cast<uint32_t*>(&Kt[(t_dc * 8 + 2 * m) * TS + pos]) = __builtin_amdgcn_perm(b[m], a[m], 0x05040100u);
-        *reinterpret_cast<uint32_t*>(&Kt[(t_dc * 8 + 2 * m + 1) * TS + pos]) =
-            __builtin_amdgcn_perm(b[m], a[m], 0x07060302u);
-      }
-    }
+  };
+  // K^T operand of dQ^T += K^T dS^T for keys mb*32 + 16j + 4*half + {0..3},
+  // {8..11} and d block db: two transposing reads (lane r of a 16-lane group
+  // supplies key row .. + r/4, elements d0 + 4*(r%4) .. +3)
+  const int tr_r = (lane & 15) >> 2, tr_c = 2 * ((lane >> 4) & 1) + ((lane & 3) >> 1), tr_o = 4 * (lane & 1);
+  auto ktf = [&](int mb, int j, int db) __attribute__((always_inline)) -> bf16x8_t {
+    const int r0 = mb * 32 + 16 * j + 4 * hf + tr_r, c = 4 * db + tr_c;
+    return tile::tr_pair(Ks + at(r0, c) + tr_o, Ks + at(r0 + 8, c) + tr_o);
   };
   auto lim_of = [&](const RangeRec& R) -> int {
     return R.lim_off < 0 ? R.n_keys : (valid ? p.lims[R.lim_off + tok] : 0);
@@ -212,7 +208,7 @@ __global__ __launch_bounds__(kThreads) void bwd_dq_kernel(BwdParams p) {
       }
 #pragma unroll
       for (int kk = 0; kk < NKK; ++kk) {
-        const int off = (mb * 32 + l32) * KS + kk * 16 + hf * 8;
+        const int off = at(mb * 32 + l32, 2 * kk + hf);
         S = __builtin_amdgcn_mfma_f32_32x32x16_bf16(*reinterpret_cast<const bf16x8_t*>(&Ks[off]), bq[kk], S, 0, 0, 0);
         dP = __builtin_amdgcn_mfma_f32_32x32x16_bf16(*reinterpret_cast<const bf16x8_t*>(&Vs[off]), bdo[kk], dP, 0, 0, 0);
       }
@@ -228,9 +224,7 @@ __global__ __launch_bounds__(kThreads) void bwd_dq_kernel(BwdParams p) {
       for (int j = 0; j < 2; ++j)
 #pragma unroll
         for (int db = 0; db < NDB; ++db) {
-          const bf16x8_t a =
-              *reinterpret_cast<const bf16x8_t*>(&Kt[(db * 32 + l32) * TS + mb * 32 + 16 * j + hf * 8]);
-          acc[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, ds[j], acc[db], 0, 0, 0);
+          acc[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ktf(mb, j, db), ds[j], acc[db], 0, 0, 0);
         }
     }
     __syncthreads();
@@ -264,15 +258,8 @@ __global__ __launch_bounds__(kThreads) void bwd_dkdv_kernel(BwdParams p) {
   constexpr int NKK = D / 16;
   constexpr int NDB = D / 32;
   constexpr int CPR = D / 8;
-  // Q / dO blocks: 32 rows of D elements, 16-byte chunk c of row r stored at
-  // chunk c ^ sw(r), so that the row reads (16 rows, one chunk) and the
-  // transposing reads (4 rows, 4 aligned chunks) each touch distinct banks
-  // (d = 128: rows of 256 bytes, one bank row each; d = 64: two rows per
-  // bank row, so the swizzle keys on the row pair).
-  auto sw = [](int r) {
-    return CPR == 16 ? (((r & 3) << 2) | ((r >> 2) & 3)) : ((((r >> 1) & 1) << 2) | ((r >> 2) & 3));
-  };
-  auto at = [&](int r, int c) { return r * D + ((c ^ sw(r)) << 3); };
+  // Q / dO blocks: 32 rows of D elements with swizzled 16-byte chunks
+  auto at = [&](int r, int c) { return r * D + (swizzled_chunk<CPR>(r, c) << 3); };
 
   // Two stages: block i is computed from stage i%2 while block i+1 is stored
   // into the other one (one barrier per block).
