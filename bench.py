@@ -7,8 +7,8 @@ A step is one decode step of masked parallel decoding over the paged cache of
 the concurrent-decode workload (64 pages x [prefix 3072, layout stream 256,
 24 branches with lengths U[1,1024]]; 1600 live streams, Hq=16, Hkv=2, d=128,
 bf16, 16-token blocks shuffled across a pool that fills most of HBM): the
-decode plan is uploaded, the shared-key tile kernel and the private-key
-streaming kernel run, and the remaining split partials are combined.  Inputs (Q, the paged K/V cache, the block table) are resident in
+decode plan is uploaded, one kernel runs the shared-key tile items and the
+private-key streaming items side by side, and the split partials are combined.  Inputs (Q, the paged K/V cache, the block table) are resident in
 HBM before timing starts.  The headline value is branch tokens (queries) per
 second of one attention-layer call.  The same run also times the packed
 forward of the 8-page training/branch-creation workload (TFLOP/s), and the
@@ -40,8 +40,7 @@ BF16_PEAK_TFLOPS = 2516.6
 PROFILE_TAG = "concurrent_decode_64pages_packed_forward_8pages"
 TRACE_SUMMARY = os.path.join(ROOT, "profiles", f"kernel_trace_{PROFILE_TAG}.md")
 TRAFFIC_SUMMARY = os.path.join(ROOT, "profiles", f"hbm_traffic_{PROFILE_TAG}.txt")
-DECODE_KERNELS = ("tile_mfma_bf16_kernel<128, true, true>", "decode_private_kernel<128>",
-                  "lse_combine_kernel<128, true>")
+DECODE_KERNELS = ("decode_step_kernel<128>", "lse_combine_kernel<128, true>")
 FORWARD_KERNEL = "tile_mfma_bf16_kernel<128, false, false>"
 BACKWARD_KERNELS = ("bwd_prep_kernel<128>", "bwd_dq_kernel<128>", "bwd_dkdv_kernel<128>", "bwd_finalize_kernel")
 COPY_KERNEL = "__amd_rocclr_copyBuffer"
@@ -246,7 +245,7 @@ def summarize_profile(d: str) -> None:
         lines.append(f"| `{short_kernel_name(name)}` | {n} | {avg / 1e3:.1f} | {mn / 1e3:.1f} | {mx / 1e3:.1f} | "
                      f"{lds} | {gx // max(wx, 1)} | {wx} |")
     dec_avg = sum(r[2] for r in rows if short_kernel_name(r[0]) in DECODE_KERNELS) / 1e3
-    lines += ["", f"Decode call (sum of the three decode kernels' averages): {dec_avg:.1f} us."]
+    lines += ["", f"Decode call (sum of the decode kernels' averages: step + combine): {dec_avg:.1f} us."]
     if ev:
         lines.append(f"Same run, HIP events around each call (bench.py): decode call "
                      f"{ev['decode']['kernel_ms'] * 1e3:.1f} us, forward {ev['forward']['kernel_ms'] * 1e3:.1f} us.")

@@ -138,7 +138,7 @@ typedef struct {
   int32_t target_workgroups;     /* decode chunk sizes (0 = 1024): shared keys
                                     are cut into the fewest chunks that keep
                                     the tile items (8 wavefronts each) within
-                                    this / 4, private keys into about 2x this
+                                    3/16 of this, private keys into about 2x this
                                     many wavefront items; both chunk sizes
                                     clamped to [512, 8192] keys              */
 } padoc_tree_desc;
@@ -160,13 +160,11 @@ typedef struct padoc_plan padoc_plan;
    ceil(n_keys / tile_keys); tiles past n_keys are never visited.  Work items
    of different KV heads share token and range records.  Forward plans: one
    workgroup per item.  Decode plans: the first n_work_shared items (shared
-   prefix / stream keys, up to 256 columns) run one per workgroup on the
-   matrix-core tile kernel, the remaining items (a private branch's keys, 16
-   columns) one per wavefront on the streaming kernel; every item writes the
-   split partial of column c to slot out_base + c, except items with fin = 1,
-   which merge their rows' shared partials (their own slot is the last entry
-   of each row's list) and write O and LSE; the combine kernel merges the
-   rows listed in comb_rows.  Decode
+   prefix / stream keys, up to 256 columns) run one per 8-wavefront
+   workgroup on matrix cores, the remaining items (a private branch's keys,
+   16 columns) one per wavefront, all in one launch; every item writes the
+   split partial of column c to slot out_base + c and the combine kernel
+   merges the rows listed in comb_rows (every row with partials).  Decode
    plans write one partial result per (item, column) at slot out_base + column
    and combine, for Q row r and KV head g, the slots comb_slot[comb_ptr[r*Hkv+g]
    .. comb_ptr[r*Hkv+g+1]) (+ head within group) in that order. */
@@ -175,9 +173,7 @@ typedef struct {
   int32_t col0;  /* first column of the task this item computes              */
   int32_t ncol;  /* columns this item computes: col0 .. col0+ncol-1, clipped
                     to the task's ntok*G columns                             */
-  int32_t fin;   /* decode: 1 = this private item also merges its rows' other
-                    partials (all from shared items) and writes O and LSE    */
-  int32_t reserved[2];
+  int32_t reserved[3];
 } padoc_work_view;
 
 typedef struct {

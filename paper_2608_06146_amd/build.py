@@ -27,7 +27,7 @@ SOURCES = [
     "csrc/host/session.cpp",
     "csrc/abi.hip",
     "csrc/kernels/tile_mfma_bf16.hip",
-    "csrc/kernels/decode_private.hip",
+    "csrc/kernels/decode_step.hip",
     "csrc/kernels/tile_valu_f32.hip",
     "csrc/kernels/lse_combine.hip",
     "csrc/kernels/bwd.hip",

@@ -8,8 +8,8 @@
 #include "host/session.hpp"
 
 namespace padoc {
-hipError_t launch_tile_mfma_bf16(const TileParams& p, int n_work, int D, bool paged, hipStream_t s);
-hipError_t launch_decode_private_bf16(const TileParams& p, int n_items, int D, hipStream_t s);
+hipError_t launch_tile_mfma_bf16(const TileParams& p, int n_work, int D, hipStream_t s);
+hipError_t launch_decode_step_bf16(const TileParams& p, int n_shared, int n_private, int D, hipStream_t s);
 hipError_t launch_tile_valu_f32(const TileParams& p, int n_work, int D, bool paged, hipStream_t s);
 hipError_t launch_lse_combine(const CombineParams& p, int D, bool bf16, hipStream_t s);
 hipError_t launch_tree_attn_bwd(const BwdParams& p, int n_work, int n_bwd, int D, hipStream_t s);
@@ -120,8 +120,6 @@ padoc_status run(const padoc_plan* P, const void* q, const void* k, const void* 
   tp.toks = at<int32_t>(ws, P->off_toks);
   tp.part_o = reinterpret_cast<float*>(static_cast<char*>(ws) + P->off_part_o);
   tp.part_ml = reinterpret_cast<float*>(static_cast<char*>(ws) + P->off_part_ml);
-  tp.comb_ptr = at<int32_t>(ws, P->off_comb_ptr);
-  tp.comb_slot = at<int32_t>(ws, P->off_comb_slot);
   tp.Hq = P->Hq;
   tp.Hkv = P->Hkv;
   tp.G = P->G;
@@ -134,17 +132,10 @@ padoc_status run(const padoc_plan* P, const void* q, const void* k, const void* 
     if (e != hipSuccess) return hip_fail("hipEventRecord", e);
   }
   if (P->dtype == PADOC_BF16) {
-    if (!paged) {
-      e = launch_tile_mfma_bf16(tp, n_work, P->D, false, stream);
-    } else {
-      // Shared keys (all sibling columns per tile) on the tile kernel, then
-      // private keys on the streaming kernel, whose epilogue also merges the
-      // shared partials of its rows (they are complete: same stream, earlier).
-      TileParams tq = tp;
-      tq.work = tp.work + P->n_work_shared;
-      e = launch_tile_mfma_bf16(tp, P->n_work_shared, P->D, true, stream);
-      if (e == hipSuccess) e = launch_decode_private_bf16(tq, n_work - P->n_work_shared, P->D, stream);
-    }
+    if (!paged)
+      e = launch_tile_mfma_bf16(tp, n_work, P->D, stream);
+    else  // shared-key tile items and private-key items in one launch
+      e = launch_decode_step_bf16(tp, P->n_work_shared, n_work - P->n_work_shared, P->D, stream);
   } else {
     e = launch_tile_valu_f32(tp, n_work, P->D, paged, stream);
   }

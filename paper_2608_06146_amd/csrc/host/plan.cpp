@@ -104,7 +104,7 @@ void sort_by_cost(std::vector<padoc::WorkRec>& w, std::vector<padoc::WorkRec>& t
 // (a new schedule every decode step) reuses their memory.
 struct Scratch {
   std::vector<int32_t> tseg, tpos, vlim, slot, touched, l;
-  std::vector<char> sees, finished;
+  std::vector<char> sees;
   AncList anc;
   std::vector<int64_t> viewers;
   std::vector<int32_t> root, at, fill;
@@ -440,12 +440,13 @@ void build_backward(padoc_plan& P, const AncList& anc, int32_t target_workgroups
 
 // Decode.  A segment is shared when a query token of another segment sees
 // any of it (page prefix, layout stream), private otherwise (a branch seen
-// only by its own queries).  Shared keys are processed by the matrix-core
-// tile kernel: per page, the tokens that see shared segments are cut into
-// items of at most 256 columns, so siblings share every K/V tile (loaded from
-// HBM once per item and key chunk).  Private keys are streamed by wavefront
-// items of 16 columns.  Both kinds write split partials; the combine map lists
-// them per (query row, KV head) in creation order.
+// only by its own queries).  Shared keys are processed by matrix-core tile
+// items: per page, the tokens that see shared segments are cut into items of
+// at most 256 columns, so siblings share every K/V tile (loaded from HBM once
+// per item and key chunk).  Private keys are streamed by wavefront items of
+// 16 columns.  Both kinds run in one launch and write split partials; the
+// combine map lists them per (query row, KV head) in creation order, and
+// every row with partials is merged by the combine kernel.
 void build_decode(padoc_plan& P, Builder& B, const AncList& anc, const padoc_tree_desc* d) {
   const int32_t n = (int32_t)P.seg.size();
   const int32_t G = P.G;
@@ -515,9 +516,9 @@ void build_decode(padoc_plan& P, Builder& B, const AncList& anc, const padoc_tre
       }
     }
   }
-  // Chunk sizes.  Shared keys: at most target_workgroups / 4 tile items (one
-  // per compute unit, see below).  Private keys: about target_workgroups x 2
-  // wavefronts' worth of equal pieces.
+  // Chunk sizes.  Shared keys: at most 3/16 x target_workgroups tile items
+  // (see below).  Private keys: about target_workgroups x 2 wavefronts' worth
+  // of equal pieces.
   auto& svis = S.svis;
   auto& pvis = S.pvis;
   auto& svis_at = S.svis_at;
@@ -544,9 +545,13 @@ void build_decode(padoc_plan& P, Builder& B, const AncList& anc, const padoc_tre
     return std::min<int64_t>(std::max<int64_t>(ch, 512), 8192);
   };
   const int64_t CHp = chunk_keys(total_p, 2 * tw);
-  // Shared keys: every tile item takes a whole compute unit, so the items
-  // should fit in one round of target_workgroups / 4 units -- a few items
-  // over that would double the step.  Smallest chunk (a multiple of 64 in
+  // Shared keys: every tile item takes a whole compute unit (its registers)
+  // for its duration, and the private items stream keys on the units the
+  // tile items leave free.  The tile items are capped at three quarters of
+  // the target_workgroups / 4 units (one round), so that from the start at
+  // least a quarter of the units read private keys, while the shared keys
+  // still get most of the matrix cores; a step over the cap would need a
+  // second round of tile items.  Smallest chunk (a multiple of 64 in
   // [512, 8192]) whose items (over all tasks and KV heads) fit, else 8192.
   auto shared_items = [&](int64_t CH) {
     int64_t n = 0;
@@ -567,7 +572,7 @@ void build_decode(padoc_plan& P, Builder& B, const AncList& anc, const padoc_tre
   };
   int64_t CHs = d->max_chunk_keys;
   if (CHs <= 0) {
-    const int64_t target = std::max<int64_t>(1, tw / 4);
+    const int64_t target = std::max<int64_t>(1, tw * 3 / 16);
     int64_t lo = 8, hi = 128;  // chunk = 64 * k keys
     if (shared_items(64 * hi) > target) {
       lo = hi;
@@ -650,22 +655,9 @@ void build_decode(padoc_plan& P, Builder& B, const AncList& anc, const padoc_tre
     const int32_t tb = B.add_tokens(stasks[i]);
     cut_emit(stasks[i], tb, svis, svis_at[i], svis_at[i + 1], CHs, kTileCols, sitems);
   }
-  // A private task cut into a single chunk finishes its rows in the
-  // streaming kernel (bf16): every other partial of those rows comes from a
-  // shared item, which runs earlier on the same stream.
-  auto& finished = S.finished;
-  finished.assign((size_t)P.num_q_rows * P.Hkv, 0);
   for (size_t i = 0; i < ptasks.size(); ++i) {
     const int32_t tb = B.add_tokens(ptasks[i]);
-    const size_t first = pitems.size();
-    const int32_t n_chunks = cut_emit(ptasks[i], tb, pvis, pvis_at[i], pvis_at[i + 1], CHp, kPrivateCols, pitems);
-    if (P.dtype == PADOC_BF16 && n_chunks == 1) {
-      for (size_t j = first; j < pitems.size(); ++j) {
-        pitems[j].fin = 1;
-        for (int32_t t = 0; t < pitems[j].ntok; ++t)
-          finished[(size_t)P.toks[tb + t] * P.Hkv + pitems[j].kvh] = 1;
-      }
-    }
+    cut_emit(ptasks[i], tb, pvis, pvis_at[i], pvis_at[i + 1], CHp, kPrivateCols, pitems);
   }
   sort_by_cost(sitems, S.tmp);
   sort_by_cost(pitems, S.tmp);
@@ -687,7 +679,7 @@ void build_decode(padoc_plan& P, Builder& B, const AncList& anc, const padoc_tre
     for (const auto& pr : parts) P.comb_slot[fill[pr.first]++] = pr.second;
   }
   for (size_t r = 0; r < n_rows; ++r)
-    if (P.comb_ptr[r + 1] > P.comb_ptr[r] && !finished[r]) P.comb_rows.push_back((int32_t)r);
+    if (P.comb_ptr[r + 1] > P.comb_ptr[r]) P.comb_rows.push_back((int32_t)r);
 }
 
 template <class T>

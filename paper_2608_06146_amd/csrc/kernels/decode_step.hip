@@ -1,8 +1,21 @@
-// Decode kernel for private keys (a branch's own history, seen only by its
-// own queries): one wavefront per work item of up to 16 columns (query token
-// x head), streaming the item's paged keys from HBM straight into
-// matrix-core operand registers, 32 keys per step (App. E: one decode step
-// of the live streams; Attn equation with the ancestor mask).
+// One decode step of the live streams over the paged cache (App. E; Attn
+// equation with the ancestor mask), bf16: the shared-key tile items and the
+// private-key items in one launch.
+//
+// Workgroups 0 .. n_shared-1 each run one shared tile item on all 8
+// wavefronts (tile_item: every sibling column of a KV head against each K/V
+// tile).  The other workgroups run 8 private items each, one per wavefront.
+// A workgroup of either kind fills a compute unit's registers and workgroups
+// are dispatched in index order, so the tile items hold n_shared compute
+// units (the planner keeps them to part of the chip) while private items
+// stream keys on the rest, and take over the tile items' units as those
+// finish: the matrix-core-bound shared keys and the HBM-bound private keys
+// overlap.  Every item writes split partials; the combine kernel merges them.
+//
+// Private item (a branch's own history, seen only by its own queries): up to
+// 16 columns (query token x head) on one wavefront, streaming the item's
+// paged keys from HBM straight into matrix-core operand registers, 32 keys
+// per step.
 //
 // Per step, with v_mfma_f32_16x16x32_bf16 (lane l: row/column l%16, group
 // g = l/16 holding eight consecutive K-dimension elements; K blocks are
@@ -16,14 +29,13 @@
 //                   blocks ([d][16 tokens]) as one 16-byte load per lane.
 // Two register sets hold the K and V of two future steps: a set is refilled
 // right after its last use, so every load has two steps of compute to land.
-// Keys past a range's end are never used: K lanes are zeroed, V elements past
-// the end are zeroed before they reach a product.  Outputs are split
-// partials (unnormalised O, running max in log2 units, sum) for the combine,
-// or -- for an item that is its rows' only private piece -- O and LSE
-// directly, after merging the rows' shared-key partials in the plan's order.
+// Keys past a range's end are never used: their scores are masked and V
+// elements past the end are zeroed before they reach a product.  Outputs are
+// split partials (unnormalised O, running max in log2 units, sum).
 #include <type_traits>
 
 #include "device_common.hpp"
+#include "tile_item.hpp"
 
 namespace padoc {
 
@@ -37,12 +49,12 @@ __device__ __forceinline__ bf16x8_t as_bf16x8(const uint4& u) { return *reinterp
 // Key (within a 32-key step) held by row m of 16-key M block mb.
 __device__ __forceinline__ int step_key(int mb, int m) { return 8 * (m >> 2) + 4 * mb + (m & 3); }
 
+// Private work item `item` on the wavefront whose lane index is `lane`.
 template <int D>
-__global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(2, 2))) void decode_private_kernel(TileParams p) {
+__device__ __forceinline__ void private_item(const TileParams& p, int item, int lane) {
   constexpr int NDS = D / 32;  // K-slices (32 d each) of the score product
   constexpr int NDM = D / 16;  // 16-row blocks of O^T
-  const WorkRec w = p.work[blockIdx.x];
-  const int lane = threadIdx.x;
+  const WorkRec w = p.work[item];
   const int n = lane & 15, g = lane >> 4;
   const int G = p.G;
   const int kvh = w.kvh;
@@ -74,7 +86,7 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(2, 2))) void
     RangeRec R;
     int ok, unused;
   };
-  auto advance = [&](Cursor& c) {
+  auto advance = [&](Cursor& c) __attribute__((always_inline)) {
     if (++c.st * 32 >= c.R.n_keys) {
       c.st = 0;
       if (++c.ri < w.rng_count)
@@ -91,7 +103,7 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(2, 2))) void
   int vkeep[2];
   int64_t blk[2][2];    // [set][block of the step's first/second 16 keys]
 
-  auto load_k = [&](const Cursor& c, int X) {
+  auto load_k = [&](const Cursor& c, int X) __attribute__((always_inline)) {
     const int nk = c.R.n_keys, kb = c.st * 32;
     const int64_t base = c.R.kv_start + (kb >> 4);
     blk[X][0] = bt[base];
@@ -106,7 +118,7 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(2, 2))) void
       for (int ds = 0; ds < NDS; ++ds) kf[X][mb][ds] = load_stream16(kp + ds * 4 * (kBlock * 8));
     }
   };
-  auto load_v = [&](const Cursor& c, int X) {
+  auto load_v = [&](const Cursor& c, int X) __attribute__((always_inline)) {
     const int keep = c.R.n_keys - (c.st * 32 + 8 * g);  // keys 8g .. 8g+7 of the step
     const uint16_t* vp = Vc + ((blk[X][g >> 1] * Hkv + kvh) * D + n) * kBlock + 8 * (g & 1);
 #pragma unroll
@@ -120,7 +132,7 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(2, 2))) void
 #pragma unroll
   for (int dm = 0; dm < NDM; ++dm) acc[dm] = f32x4_t{0.f, 0.f, 0.f, 0.f};
   int lim = 0;
-  auto load_lim = [&]() { lim = C.R.lim_off < 0 ? C.R.n_keys : (valid ? p.lims[C.R.lim_off + t] : 0); };
+  auto load_lim = [&]() __attribute__((always_inline)) { lim = C.R.lim_off < 0 ? C.R.n_keys : (valid ? p.lims[C.R.lim_off + t] : 0); };
   load_lim();
   const float sl2 = p.scale_log2;
 
@@ -134,7 +146,7 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(2, 2))) void
     advance(L);
   }
 
-  auto step = [&](auto xc) -> bool {
+  auto step = [&](auto xc) __attribute__((always_inline)) -> bool {
     constexpr int X = decltype(xc)::value;
     const int kb = C.st * 32;
     f32x4_t S[2];
@@ -196,45 +208,6 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(2, 2))) void
   float lt = l_part + __shfl_xor(l_part, 16);
   lt += __shfl_xor(lt, 32);
   if (!valid) return;
-  if (w.fin) {
-    // Merge the row's other partials (shared items, complete: they ran
-    // earlier on this stream; this item's own slot is the list's last entry)
-    // with this one and write O and LSE (same arithmetic as the combine).
-    const int h = col - t * G;
-    const int64_t rk = (int64_t)qrow * Hkv + kvh;
-    const int32_t e0 = p.comb_ptr[rk], e1 = p.comb_ptr[rk + 1] - 1;
-    float M = m_run;
-    for (int32_t e = e0; e < e1; ++e) M = fmaxf(M, p.part_ml[2 * (int64_t)(p.comb_slot[e] + h)]);
-    const float so = fast_exp2(m_run - M);
-    float Ls = lt * so;
-#pragma unroll
-    for (int dm = 0; dm < NDM; ++dm) acc[dm] *= so;
-    for (int32_t e = e0; e < e1; ++e) {
-      const int64_t slot = p.comb_slot[e] + h;
-      const float sc = fast_exp2(p.part_ml[2 * slot] - M);
-      Ls = fmaf(p.part_ml[2 * slot + 1], sc, Ls);
-      const float* src = p.part_o + slot * D + 4 * g;
-#pragma unroll
-      for (int dm = 0; dm < NDM; ++dm) {
-        const float4 x = *reinterpret_cast<const float4*>(src + dm * 16);
-        acc[dm][0] = fmaf(x.x, sc, acc[dm][0]);
-        acc[dm][1] = fmaf(x.y, sc, acc[dm][1]);
-        acc[dm][2] = fmaf(x.z, sc, acc[dm][2]);
-        acc[dm][3] = fmaf(x.w, sc, acc[dm][3]);
-      }
-    }
-    const float inv = 1.f / Ls;
-    uint16_t* op = static_cast<uint16_t*>(p.o) + ((int64_t)qrow * p.Hq + hq) * D + 4 * g;
-#pragma unroll
-    for (int dm = 0; dm < NDM; ++dm) {
-      uint2 pk;
-      pk.x = (uint32_t)f32_to_bf16_bits(acc[dm][0] * inv) | ((uint32_t)f32_to_bf16_bits(acc[dm][1] * inv) << 16);
-      pk.y = (uint32_t)f32_to_bf16_bits(acc[dm][2] * inv) | ((uint32_t)f32_to_bf16_bits(acc[dm][3] * inv) << 16);
-      *reinterpret_cast<uint2*>(op + dm * 16) = pk;
-    }
-    if (g == 0) p.lse[(int64_t)qrow * p.Hq + hq] = (M + __log2f(Ls)) * kLn2;
-    return;
-  }
   const int64_t slot = (int64_t)w.out_base + col;
   float* op = p.part_o + slot * D + 4 * g;
 #pragma unroll
@@ -246,15 +219,27 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(2, 2))) void
   }
 }
 
+template <int D>
+__global__ __launch_bounds__(tile::kThreads) void decode_step_kernel(TileParams p, int n_shared, int n_private) {
+  const int b = blockIdx.x;
+  if (b < n_shared) {
+    tile::tile_item<D, true, true>(p, b);
+    return;
+  }
+  const int item = (b - n_shared) * tile::kWaves + (int)(threadIdx.x >> 6);
+  if (item < n_private) private_item<D>(p, n_shared + item, threadIdx.x & 63);
+}
+
 }  // namespace
 
-hipError_t launch_decode_private_bf16(const TileParams& p, int n_items, int D, hipStream_t stream) {
-  if (n_items <= 0) return hipSuccess;
-  const dim3 grid(n_items), block(64);
+hipError_t launch_decode_step_bf16(const TileParams& p, int n_shared, int n_private, int D, hipStream_t stream) {
+  const int n_blocks = n_shared + (n_private + tile::kWaves - 1) / tile::kWaves;
+  if (n_blocks <= 0) return hipSuccess;
+  const dim3 grid(n_blocks), block(tile::kThreads);
   if (D == 64)
-    hipLaunchKernelGGL((decode_private_kernel<64>), grid, block, 0, stream, p);
+    hipLaunchKernelGGL((decode_step_kernel<64>), grid, block, 0, stream, p, n_shared, n_private);
   else
-    hipLaunchKernelGGL((decode_private_kernel<128>), grid, block, 0, stream, p);
+    hipLaunchKernelGGL((decode_step_kernel<128>), grid, block, 0, stream, p, n_shared, n_private);
   return hipGetLastError();
 }
 

@@ -39,8 +39,6 @@ struct TileParams {
   const int32_t* toks;
   float* part_o;          // partial mode: [slots, D] unnormalised accumulators
   float* part_ml;         // partial mode: [slots, 2] (running max in log2 units, sum)
-  const int32_t* comb_ptr;   // decode: partial slots per (row, KV head) ...
-  const int32_t* comb_slot;  // ... merged by items with fin = 1
   int32_t Hq, Hkv, G;
   float scale_log2;       // softmax_scale * log2(e)
 };

@@ -156,9 +156,7 @@ def _check_decode(segs, G, Hkv, chunk=0, read_once=False):
     assert ex["kind"] == 1
     row_tok = _token_of_row(nodes, segs["q_off"])
     slot_cover = {}
-    slot_item = {}
     cols_of = {}
-    fin_rows = set()
     for idx, w in enumerate(ex["work"]):
         width = 256 if idx < ex["n_work_shared"] else 16
         assert 0 < w["ncol"] <= width and w["col0"] % width == 0
@@ -173,11 +171,7 @@ def _check_decode(segs, G, Hkv, chunk=0, read_once=False):
                 assert R["n_keys"] <= chunk
         for i in range(w["ntok"]):
             slot_cover[int(w["out_base"]) + i * G] = (int(toks[i]), int(w["kvh"]), cover[i])
-            slot_item.setdefault(int(w["out_base"]) + i * G, set()).add(idx)
-            if w["fin"]:
-                fin_rows.add(int(toks[i]) * Hkv + int(w["kvh"]))
-        if w["fin"]:
-            assert idx >= ex["n_work_shared"], "only private items finish rows"
+        assert not w["reserved"].any()
     for base, cols in cols_of.items():
         assert sorted(cols) == list(range(len(cols))), "task columns not covered exactly once"
     n_q = int(sum(n[3] for n in nodes))
@@ -192,16 +186,11 @@ def _check_decode(segs, G, Hkv, chunk=0, read_once=False):
                 keys += cov
             assert len(keys) == len(set(keys)), "a key is combined twice"
             assert set(keys) == _visible_keys(nodes, s, p)
-    # a row finished by a private item: that item's slot is the row's last
-    # entry and every other entry is a shared item's (computed before it);
-    # the combine kernel visits exactly the other rows that have entries
-    for rk in fin_rows:
-        ents = [int(e) for e in ex["comb_slot"][ex["comb_ptr"][rk]: ex["comb_ptr"][rk + 1]]]
-        assert ents and all(ex["work"]["fin"][i] for i in slot_item[ents[-1]])
-        for e in ents[:-1]:
-            assert all(i < ex["n_work_shared"] for i in slot_item[e])
+    # the combine kernel visits exactly the rows that have entries (every
+    # query row sees at least its own token)
     nonempty = {rk for rk in range(n_q * Hkv) if ex["comb_ptr"][rk + 1] > ex["comb_ptr"][rk]}
-    assert list(ex["comb_rows"]) == sorted(nonempty - fin_rows)
+    assert nonempty == set(range(n_q * Hkv))
+    assert list(ex["comb_rows"]) == sorted(nonempty)
     # slots the combine does not read belong to tokens that see no key there
     used = set(int(e) for e in ex["comb_slot"])
     for slot, (_, _, cov) in slot_cover.items():
