@@ -9,7 +9,8 @@
 
 namespace padoc {
 hipError_t launch_tile_mfma_bf16(const TileParams& p, int n_work, int D, hipStream_t s);
-hipError_t launch_decode_step_bf16(const TileParams& p, int n_shared, int n_private, int D, hipStream_t s);
+hipError_t launch_decode_step_bf16(const TileParams& p, int n_shared, int n_private, int n_groups, int* next, int D,
+                                   hipStream_t s);
 hipError_t launch_tile_valu_f32(const TileParams& p, int n_work, int D, bool paged, hipStream_t s);
 hipError_t launch_lse_combine(const CombineParams& p, int D, bool bf16, hipStream_t s);
 hipError_t launch_tree_attn_bwd(const BwdParams& p, int n_work, int n_bwd, int D, hipStream_t s);
@@ -135,7 +136,8 @@ padoc_status run(const padoc_plan* P, const void* q, const void* k, const void* 
     if (!paged)
       e = launch_tile_mfma_bf16(tp, n_work, P->D, stream);
     else  // shared-key tile items and private-key items in one launch
-      e = launch_decode_step_bf16(tp, P->n_work_shared, n_work - P->n_work_shared, P->D, stream);
+      e = launch_decode_step_bf16(tp, P->n_work_shared, n_work - P->n_work_shared, P->n_private_groups,
+                                  reinterpret_cast<int*>(static_cast<char*>(ws) + P->off_next), P->D, stream);
   } else {
     e = launch_tile_valu_f32(tp, n_work, P->D, paged, stream);
   }

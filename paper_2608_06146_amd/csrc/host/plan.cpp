@@ -665,6 +665,19 @@ void build_decode(padoc_plan& P, Builder& B, const AncList& anc, const padoc_tre
   P.work.assign(sitems.begin(), sitems.end());
   P.work.insert(P.work.end(), pitems.begin(), pitems.end());
   P.n_work_shared = (int32_t)sitems.size();
+  // Private items are taken from kPrivateQueues queues (queue of workgroup b:
+  // b % kPrivateQueues) by every wavefront of the launch: the tile
+  // workgroups' after their item, and workgroups of their own on the compute
+  // units the tile items leave free (target_workgroups / 4 units).  Every
+  // queue needs a workgroup: at least kPrivateQueues workgroups in all.
+  P.n_private_groups = 0;
+  if (!pitems.empty()) {
+    const int64_t groups = ceil_div((int64_t)pitems.size(), 8);
+    const int64_t free_units = std::max<int64_t>(0, tw / 4 - (int64_t)sitems.size());
+    int64_t g = std::min(groups, std::max<int64_t>(1, free_units));
+    g = std::max<int64_t>(g, padoc::kPrivateQueues - (int64_t)sitems.size());
+    P.n_private_groups = (int32_t)g;
+  }
 
   // Combine map: slots per (row, KV head) in creation order (stable counting
   // sort of the partials by row).
@@ -715,7 +728,8 @@ void serialise(padoc_plan& P) {
   P.off_comb_ptr = align256(P.off_toks + P.toks.size() * 4);
   P.off_comb_slot = align256(P.off_comb_ptr + P.comb_ptr.size() * 4);
   P.off_comb_rows = align256(P.off_comb_slot + P.comb_slot.size() * 4);
-  const size_t blob_bytes = P.off_comb_rows + P.comb_rows.size() * 4;
+  P.off_next = align256(P.off_comb_rows + P.comb_rows.size() * 4);
+  const size_t blob_bytes = P.off_next + padoc::kPrivateQueues * 256;  // queue counters, 256 bytes apart
   P.off_part_o = align256(blob_bytes);
   P.off_part_ml = align256(P.off_part_o + (size_t)P.n_slots * P.D * 4);
   P.ws_bytes = std::max<size_t>(256, align256(P.off_part_ml + (size_t)P.n_slots * 8));
@@ -753,6 +767,7 @@ padoc_status build_plan(const padoc_tree_desc* d, padoc_plan& P) {
     P.tile_tokens = std::max(1, P.tile_cols / P.G);
     P.work.clear();
     P.n_work_shared = 0;
+    P.n_private_groups = 0;
     P.ranges.clear();
     P.lims.clear();
     P.toks.clear();

@@ -25,7 +25,8 @@ struct padoc_plan {
   int32_t tile_tokens = 0;  // tokens per work item = tile_cols / G
 
   std::vector<padoc::WorkRec> work;
-  int32_t n_work_shared = 0;  // decode: work[0 .. n_work_shared) run on the tile kernel
+  int32_t n_work_shared = 0;  // decode: work[0 .. n_work_shared) are tile items
+  int32_t n_private_groups = 0;  // decode: workgroups that only take private items
   std::vector<padoc::RangeRec> ranges;
   std::vector<int32_t> lims;
   std::vector<int32_t> toks;
@@ -52,6 +53,7 @@ struct padoc_plan {
   std::vector<unsigned char> blob;
   size_t off_work = 0, off_ranges = 0, off_lims = 0, off_toks = 0;
   size_t off_comb_ptr = 0, off_comb_slot = 0, off_comb_rows = 0, off_part_o = 0, off_part_ml = 0;
+  size_t off_next = 0;  // decode: private item queue counters (zeros in the blob)
   size_t ws_bytes = 0;
 
   // Incremented by every build of the plan (plans rebuilt in place).

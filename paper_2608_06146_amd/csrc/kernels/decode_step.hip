@@ -4,13 +4,16 @@
 //
 // Workgroups 0 .. n_shared-1 each run one shared tile item on all 8
 // wavefronts (tile_item: every sibling column of a KV head against each K/V
-// tile).  The other workgroups run 8 private items each, one per wavefront.
-// A workgroup of either kind fills a compute unit's registers and workgroups
-// are dispatched in index order, so the tile items hold n_shared compute
-// units (the planner keeps them to part of the chip) while private items
-// stream keys on the rest, and take over the tile items' units as those
+// tile).  Then every wavefront of the launch -- of the tile workgroups and of
+// the workgroups after them -- takes private items, one at a time, from
+// queues (atomic counters that the schedule upload zeroes), in the plan's
+// order (largest first).  A workgroup fills a compute unit's registers and
+// workgroups are dispatched in index order, so the tile items hold n_shared
+// compute units (the planner keeps them to part of the chip) while private
+// items stream keys on the rest, and the tile items' units join in as they
 // finish: the matrix-core-bound shared keys and the HBM-bound private keys
-// overlap.  Every item writes split partials; the combine kernel merges them.
+// overlap, and no wavefront idles while private items are left.  Every item
+// writes split partials; the combine kernel merges them.
 //
 // Private item (a branch's own history, seen only by its own queries): up to
 // 16 columns (query token x head) on one wavefront, streaming the item's
@@ -219,27 +222,57 @@ __device__ __forceinline__ void private_item(const TileParams& p, int item, int 
   }
 }
 
+// Private items are dealt to kQueues queues (item j to queue j % kQueues),
+// one per XCD: workgroup b runs on XCD b % 8, and a wavefront takes from
+// the queue of its workgroup's index, so the atomics of a queue stay within
+// one XCD's compute units and the 8 counters (256 bytes apart) are served in
+// parallel.  The wavefronts of the workgroups after the tile items start with
+// a fixed item each (no atomic on the launch's critical start); every later
+// item comes from the queue's counter.
+constexpr int kQueues = kPrivateQueues;
+
+__device__ __forceinline__ int take_private(int* ctr, int lane) {
+  int v = 0;
+  if (lane == 0) v = atomicAdd(ctr, 1);
+  return __shfl(v, 0);
+}
+
 template <int D>
-__global__ __launch_bounds__(tile::kThreads) void decode_step_kernel(TileParams p, int n_shared, int n_private) {
+__global__ __launch_bounds__(tile::kThreads) void decode_step_kernel(TileParams p, int n_shared, int n_private,
+                                                                     int n_groups, int* next) {
   const int b = blockIdx.x;
-  if (b < n_shared) {
-    tile::tile_item<D, true, true>(p, b);
-    return;
+  if (b < n_shared) tile::tile_item<D, true, true>(p, b);
+  if (n_private <= 0) return;
+  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  const int q = b % kQueues;
+  const int n_q = (n_private - q + kQueues - 1) / kQueues;  // items q, q + 8, ... below n_private
+  // Private-only workgroups of queue q: b0, b0 + 8, ... below n_shared + n_groups.
+  const int end = n_shared + n_groups;
+  const int b0 = n_shared + (q - n_shared % kQueues + kQueues) % kQueues;
+  const int n_first = b0 < end ? ((end - 1 - b0) / kQueues + 1) * tile::kWaves : 0;
+  int* ctr = next + q * 64;
+  // An index is taken only when the wavefront is free: one reserved ahead
+  // would sit behind a long item while another wavefront idles.
+  int k = b >= n_shared ? ((b - b0) / kQueues) * tile::kWaves + wave : n_first + take_private(ctr, lane);
+  while (k < n_q) {
+    private_item<D>(p, n_shared + q + kQueues * k, lane);
+    k = n_first + take_private(ctr, lane);
   }
-  const int item = (b - n_shared) * tile::kWaves + (int)(threadIdx.x >> 6);
-  if (item < n_private) private_item<D>(p, n_shared + item, threadIdx.x & 63);
 }
 
 }  // namespace
 
-hipError_t launch_decode_step_bf16(const TileParams& p, int n_shared, int n_private, int D, hipStream_t stream) {
-  const int n_blocks = n_shared + (n_private + tile::kWaves - 1) / tile::kWaves;
+// n_groups: workgroups after the tile items (they take private items only).
+// `next`: kQueues counters 256 bytes apart, zero at launch.
+hipError_t launch_decode_step_bf16(const TileParams& p, int n_shared, int n_private, int n_groups, int* next, int D,
+                                   hipStream_t stream) {
+  const int n_blocks = n_shared + n_groups;
   if (n_blocks <= 0) return hipSuccess;
   const dim3 grid(n_blocks), block(tile::kThreads);
   if (D == 64)
-    hipLaunchKernelGGL((decode_step_kernel<64>), grid, block, 0, stream, p, n_shared, n_private);
+    hipLaunchKernelGGL((decode_step_kernel<64>), grid, block, 0, stream, p, n_shared, n_private, n_groups, next);
   else
-    hipLaunchKernelGGL((decode_step_kernel<128>), grid, block, 0, stream, p, n_shared, n_private);
+    hipLaunchKernelGGL((decode_step_kernel<128>), grid, block, 0, stream, p, n_shared, n_private, n_groups, next);
   return hipGetLastError();
 }
 

@@ -23,6 +23,7 @@ constexpr int kTileKeys = 64;
 constexpr int kTileCols = 256;
 constexpr int kBlock = 16;  // paged KV block (tokens)
 constexpr int kPrivateCols = 16;  // columns of a private decode item (one wavefront)
+constexpr int kPrivateQueues = 8;  // decode: private item queues (one per XCD)
 constexpr int kBwdKeys = 128;     // keys of a backward key-major item (4 x 32)
 
 // Everything a tile kernel needs.  Pointers are device pointers.
