@@ -669,14 +669,13 @@ void build_decode(padoc_plan& P, Builder& B, const AncList& anc, const padoc_tre
   // b % kPrivateQueues) by every wavefront of the launch: the tile
   // workgroups' after their item, and workgroups of their own on the compute
   // units the tile items leave free (target_workgroups / 4 units).  Every
-  // queue needs a workgroup: at least kPrivateQueues workgroups in all.
+  // queue gets at least one such workgroup, so that no queue waits for the
+  // tile items to end.
   P.n_private_groups = 0;
   if (!pitems.empty()) {
     const int64_t groups = ceil_div((int64_t)pitems.size(), 8);
     const int64_t free_units = std::max<int64_t>(0, tw / 4 - (int64_t)sitems.size());
-    int64_t g = std::min(groups, std::max<int64_t>(1, free_units));
-    g = std::max<int64_t>(g, padoc::kPrivateQueues - (int64_t)sitems.size());
-    P.n_private_groups = (int32_t)g;
+    P.n_private_groups = (int32_t)std::max<int64_t>(std::min(groups, free_units), padoc::kPrivateQueues);
   }
 
   // Combine map: slots per (row, KV head) in creation order (stable counting

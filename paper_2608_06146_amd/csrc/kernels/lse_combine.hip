@@ -7,8 +7,7 @@
 //   LSE = (M + log2 L) ln 2.
 // Partials are read in the planner's fixed order, so results are bitwise
 // reproducible.  32 threads per (query row, head), 8 per block, over the
-// (row, KV head) pairs the plan lists (rows a decode kernel already finished
-// are not listed).
+// (row, KV head) pairs the plan lists.
 #include "device_common.hpp"
 
 namespace padoc {
