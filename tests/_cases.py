@@ -101,7 +101,7 @@ def fill_pool(nodes, k_packed, v_packed, n_pool, seed, device="cuda", sentinel=f
 
 
 def decode_case(pages_or_nodes, Hq, Hkv, d, dtype, seed, pool_extra=7, check=True, rows=None,
-                max_chunk_keys=0, device="cuda"):
+                max_chunk_keys=0, device="cuda", target_workgroups=0):
     """Decode step over a paged cache: structure from pages (paper form) or
     generic nodes, canonical paged layout."""
     if len(pages_or_nodes) and isinstance(pages_or_nodes[0], syn.Page):
@@ -120,7 +120,7 @@ def decode_case(pages_or_nodes, Hq, Hkv, d, dtype, seed, pool_extra=7, check=Tru
     kc, vc, ids = fill_pool(nodes, k, v, n_pool, seed, device=device)
     bt = torch.as_tensor(ids, device=device)
     plan = pa.TreePlan(segs, Hq, Hkv, d, dtype, 16, num_kv_rows=n_pool, num_q_rows=nq, block_table_host=ids,
-                       max_chunk_keys=max_chunk_keys)
+                       max_chunk_keys=max_chunk_keys, target_workgroups=target_workgroups)
     print(f"[case] decode T={T} nq={nq} blocks={nb} Hq={Hq} Hkv={Hkv} d={d} {dtype} seed={seed} "
           f"work={len(plan.export()['work'])}", flush=True)
     o, lse = pa.branch_decode(q, kc, vc, bt, plan)

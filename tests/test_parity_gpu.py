@@ -215,6 +215,29 @@ def test_dense_page_mixed_step_full_size_sampled():
     decode_case(wl.pages, 28, 4, 128, "bf16", 0, pool_extra=3000, rows=rows)
 
 
+@pytest.mark.parametrize("target_wg", [0, 32])
+@pytest.mark.parametrize("chunk", [0, 64])
+def test_decode_step_queue_shapes(target_wg, chunk):
+    """Launch shapes of the one-launch decode step: shared tile items fewer
+    or (chunk 64 with 32 target workgroups, i.e. 8 compute units assumed)
+    many more than the units the plan assumes; private items fewer than the
+    8 queues, or many per queue."""
+    rng = np.random.default_rng(5)
+    few = [syn.Page(300, 0, 30, 1, (syn.Branch(4, 40, 1), syn.Branch(20, 70, 1)))]
+    many = [syn.Page(500, 0, 60, 1, tuple(syn.Branch(int(f), int(L), 1) for f, L in
+                                          zip(np.sort(rng.integers(1, 60, 40)), rng.integers(1, 400, 40))))]
+    for i, pages in enumerate((few, many)):
+        decode_case(pages, 16, 2, 128, "bf16", 20 + i, max_chunk_keys=chunk, target_workgroups=target_wg)
+
+
+def test_decode_without_shared_keys():
+    """Streams that share nothing (separate roots, queries at their ends):
+    no tile items, only private items from the queues."""
+    nodes = [(-1, 0, 37, 1), (-1, 0, 300, 1), (-1, 0, 1, 1), (-1, 0, 129, 2)]
+    decode_case(nodes, 16, 2, 128, "bf16", 31)
+    decode_case(nodes, 16, 2, 64, "bf16", 32)
+
+
 @pytest.mark.parametrize("heads", [(40, 2), (64, 1)])
 def test_decode_wide_gqa_groups(heads):
     """G = 20 and G = 64 heads per KV head: a private stream's columns are
