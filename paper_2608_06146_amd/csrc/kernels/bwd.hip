@@ -277,6 +277,7 @@ __global__ __launch_bounds__(kThreads) void bwd_dkdv_kernel(BwdParams p) {
   const int wave = tid >> 6, lane = tid & 63, l32 = lane & 31, hf = lane >> 5;
   const bool kwave = wave >= 4;          // waves 4-7: dK; 0-3: dV
   const int key = (wave & 3) * 32 + l32;  // this lane's key within the item
+  const int key_hi = (wave & 3) * 32 + 32;  // end of this wavefront's keys
   const int G = p.G, kvh = b.kvh;
   const int64_t Hkv = p.Hkv;
 
@@ -380,16 +381,30 @@ __global__ __launch_bounds__(kThreads) void bwd_dkdv_kernel(BwdParams p) {
     for (int i = 0; i < 16; ++i) sc[i] = 0.f;
 #pragma unroll
     for (int kk = 0; kk < NKK; ++kk) sc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[kk], bk[kk], sc, 0, 0, 0);
+    // P = exp(S - LSE), zero past each column's limit.  When every column
+    // of the block sees all 32 keys of this wavefront (limits are at most
+    // n_keys, so the keys are real), the mask is skipped.
     float pr[16];
+    float lv[16];
+    int mv[16];
 #pragma unroll
     for (int q4 = 0; q4 < 4; ++q4) {
       const int cb = q4 * 8 + hf * 4;  // columns cb .. cb+3 = elements 4*q4 .. 4*q4+3
       const float4 l4 = *reinterpret_cast<const float4*>(&S.ls[cb]);
       const int4 m4 = *reinterpret_cast<const int4*>(&S.lm[cb]);
-      const float lv[4] = {l4.x, l4.y, l4.z, l4.w};
-      const int mv[4] = {m4.x, m4.y, m4.z, m4.w};
+      lv[4 * q4] = l4.x, lv[4 * q4 + 1] = l4.y, lv[4 * q4 + 2] = l4.z, lv[4 * q4 + 3] = l4.w;
+      mv[4 * q4] = m4.x, mv[4 * q4 + 1] = m4.y, mv[4 * q4 + 2] = m4.z, mv[4 * q4 + 3] = m4.w;
+    }
+    int mn = mv[0];
 #pragma unroll
-      for (int e = 0; e < 4; ++e) pr[4 * q4 + e] = key < mv[e] ? fast_exp2(fmaf(sc[4 * q4 + e], sl2, -lv[e])) : 0.f;
+    for (int i = 1; i < 16; ++i) mn = min(mn, mv[i]);
+    mn = min(mn, __shfl_xor(mn, 32));  // lanes l and l^32 hold the other 16 columns
+    if (__builtin_amdgcn_readfirstlane((int)(mn >= key_hi))) {
+#pragma unroll
+      for (int i = 0; i < 16; ++i) pr[i] = fast_exp2(fmaf(sc[i], sl2, -lv[i]));
+    } else {
+#pragma unroll
+      for (int i = 0; i < 16; ++i) pr[i] = key < mv[i] ? fast_exp2(fmaf(sc[i], sl2, -lv[i])) : 0.f;
     }
     bf16x8_t fb[2 * NDB];
     if (!kwave) {
