@@ -303,40 +303,51 @@ __global__ __launch_bounds__(kThreads) void bwd_dkdv_kernel(BwdParams p) {
   const int s_col = tid % 32, s_dc = (tid / 32) % CPR;
   const bool s_on = tid < 32 * CPR;
   const int c_end = b.col0 + b.ncol;
-  const int c_last = b.col0 + ((b.ncol - 1) & ~31);  // first column of the last block
   // Register sets [i % 2]: Q / dO pieces and column scalars of a block
   // loaded two blocks ahead of its LDS store; the Q rows of its columns are
   // fetched one block before that.
   uint4 qr[2], gr[2];
   float lr[2], dr[2];
   int mr[2];
-  int rq[2], rc[2];  // Q rows of this thread's piece column and scalar column
-  auto fetch_rows = [&](auto xc, int c0) {
+  // Per set: Q row, token within the item and head of this thread's column
+  // (column tid % 32 of the block; past c_end: the last column, flagged).
+  int rq[2], tq[2], hq[2];
+  bool okq[2];
+  // fetch_rows visits the blocks in order, 32 columns apart: the column's
+  // (token, head) = (column / G, column % G) advances by (32 / G, 32 % G)
+  // with one carry, so no division runs per block.
+  int f_col = b.col0 + s_col, f_t = f_col / G, f_h = f_col % G;
+  const int t32 = 32 / G, h32 = 32 % G;
+  const int t_end = (c_end - 1) / G, h_end = (c_end - 1) % G;
+  auto fetch_rows = [&](auto xc) __attribute__((always_inline)) {
     constexpr int X = decltype(xc)::value;
-    c0 = c0 <= c_last ? c0 : c_last;  // past the end: re-read the last block
-    const int ca = c0 + s_col, cb = c0 + (tid & 31);
-    rq[X] = p.btoks[b.tok_begin + (ca < c_end ? ca : c_end - 1) / G];
-    rc[X] = p.btoks[b.tok_begin + (cb < c_end ? cb : c_end - 1) / G];
+    const bool ok = f_col < c_end;
+    tq[X] = ok ? f_t : t_end;
+    hq[X] = ok ? f_h : h_end;
+    okq[X] = ok;
+    rq[X] = p.btoks[b.tok_begin + tq[X]];
+    f_col += 32;
+    f_t += t32;
+    f_h += h32;
+    if (f_h >= G) {
+      f_h -= G;
+      ++f_t;
+    }
   };
-  auto load = [&](auto xc, int c0) {
+  auto load = [&](auto xc) __attribute__((always_inline)) {
     constexpr int X = decltype(xc)::value;
-    c0 = c0 <= c_last ? c0 : c_last;
-    const int ca = c0 + s_col;
-    const bool ok = ca < c_end;
-    const int ha = kvh * G + ca % G;
-    const int64_t off = ((int64_t)rq[X] * p.Hq + ha) * D + s_dc * 8;
+    const bool ok = okq[X];
+    const int64_t rh = (int64_t)rq[X] * p.Hq + kvh * G + hq[X];
+    const int64_t off = rh * D + s_dc * 8;
     const uint4 q = load16(static_cast<const uint16_t*>(p.q) + off);
     const uint4 g = load16(static_cast<const uint16_t*>(p.dout) + off);
     qr[X] = ok ? q : make_uint4(0, 0, 0, 0);
     gr[X] = ok ? g : make_uint4(0, 0, 0, 0);
-    const int cb = c0 + (tid & 31);
-    const bool okc = cb < c_end;
-    const int64_t li = (int64_t)rc[X] * p.Hq + kvh * G + cb % G;
-    const float l = p.lse[li], dd = p.dd[li];
-    const int m = p.blims[b.lim_begin + (okc ? cb : c_end - 1) / G];
-    lr[X] = okc ? l * kLog2e : 0.f;
-    dr[X] = okc ? dd : 0.f;
-    mr[X] = okc ? m : 0;
+    const float l = p.lse[rh], dd = p.dd[rh];
+    const int m = p.blims[b.lim_begin + tq[X]];
+    lr[X] = ok ? l * kLog2e : 0.f;
+    dr[X] = ok ? dd : 0.f;
+    mr[X] = ok ? m : 0;
   };
   auto store = [&](auto xc, Stage& S) {
     constexpr int X = decltype(xc)::value;
@@ -463,20 +474,20 @@ __global__ __launch_bounds__(kThreads) void bwd_dkdv_kernel(BwdParams p) {
   // (i+1) % 2.
   using Set0 = std::integral_constant<int, 0>;
   using Set1 = std::integral_constant<int, 1>;
-  fetch_rows(Set0{}, b.col0);
-  load(Set0{}, b.col0);
-  fetch_rows(Set1{}, b.col0 + 32);
-  load(Set1{}, b.col0 + 32);
+  fetch_rows(Set0{});  // block 0
+  load(Set0{});
+  fetch_rows(Set1{});  // block 1
+  load(Set1{});
   store(Set0{}, st[0]);
-  fetch_rows(Set0{}, b.col0 + 64);
+  fetch_rows(Set0{});  // block 2
   __syncthreads();
   auto step = [&](auto xc, int c0) {
     constexpr int X = decltype(xc)::value;
     using Y = std::integral_constant<int, X ^ 1>;
     compute(st[X]);
     if (c0 + 32 < c_end) store(Y{}, st[X ^ 1]);  // that stage was last read before the previous barrier
-    load(xc, c0 + 64);
-    fetch_rows(Y{}, c0 + 96);
+    load(xc);           // block i+2
+    fetch_rows(Y{});    // block i+3
     __syncthreads();
   };
   for (int c0 = b.col0;;) {
