@@ -334,20 +334,18 @@ __global__ __launch_bounds__(kThreads) void bwd_dkdv_kernel(BwdParams p) {
       ++f_t;
     }
   };
+  // A column past c_end carries the last column's (finite) Q, dO, LSE and
+  // D with a limit of 0: its P and dS are exactly 0, so it adds nothing.
   auto load = [&](auto xc) __attribute__((always_inline)) {
     constexpr int X = decltype(xc)::value;
-    const bool ok = okq[X];
     const int64_t rh = (int64_t)rq[X] * p.Hq + kvh * G + hq[X];
     const int64_t off = rh * D + s_dc * 8;
-    const uint4 q = load16(static_cast<const uint16_t*>(p.q) + off);
-    const uint4 g = load16(static_cast<const uint16_t*>(p.dout) + off);
-    qr[X] = ok ? q : make_uint4(0, 0, 0, 0);
-    gr[X] = ok ? g : make_uint4(0, 0, 0, 0);
-    const float l = p.lse[rh], dd = p.dd[rh];
+    qr[X] = load16(static_cast<const uint16_t*>(p.q) + off);
+    gr[X] = load16(static_cast<const uint16_t*>(p.dout) + off);
+    lr[X] = p.lse[rh] * kLog2e;
+    dr[X] = p.dd[rh];
     const int m = p.blims[b.lim_begin + tq[X]];
-    lr[X] = ok ? l * kLog2e : 0.f;
-    dr[X] = ok ? dd : 0.f;
-    mr[X] = ok ? m : 0;
+    mr[X] = okq[X] ? m : 0;
   };
   auto store = [&](auto xc, Stage& S) {
     constexpr int X = decltype(xc)::value;
