@@ -215,13 +215,13 @@ def test_dense_page_mixed_step_full_size_sampled():
     decode_case(wl.pages, 28, 4, 128, "bf16", 0, pool_extra=3000, rows=rows)
 
 
-@pytest.mark.parametrize("target_wg", [0, 32])
+@pytest.mark.parametrize("target_wg", [0, 32, 4])
 @pytest.mark.parametrize("chunk", [0, 64])
 def test_decode_step_queue_shapes(target_wg, chunk):
     """Launch shapes of the one-launch decode step: shared tile items fewer
     or (chunk 64 with 32 target workgroups, i.e. 8 compute units assumed)
-    many more than the units the plan assumes; private items fewer than the
-    8 queues, or many per queue."""
+    many more than the units the plan assumes (down to one unit at 4);
+    private items fewer than the 8 queues, or many per queue."""
     rng = np.random.default_rng(5)
     few = [syn.Page(300, 0, 30, 1, (syn.Branch(4, 40, 1), syn.Branch(20, 70, 1)))]
     many = [syn.Page(500, 0, 60, 1, tuple(syn.Branch(int(f), int(L), 1) for f, L in
