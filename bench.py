@@ -40,7 +40,7 @@ BF16_PEAK_TFLOPS = 2516.6
 PROFILE_TAG = "concurrent_decode_64pages_packed_forward_8pages"
 TRACE_SUMMARY = os.path.join(ROOT, "profiles", f"kernel_trace_{PROFILE_TAG}.md")
 TRAFFIC_SUMMARY = os.path.join(ROOT, "profiles", f"hbm_traffic_{PROFILE_TAG}.txt")
-DECODE_KERNELS = ("decode_step_kernel<128>", "lse_combine_kernel<128, true>")
+DECODE_KERNELS = ("decode_step_kernel<128>", "lse_combine_kernel<128, true, 8>")
 FORWARD_KERNEL = "tile_mfma_bf16_kernel<128, false, false>"
 BACKWARD_KERNELS = ("bwd_prep_kernel<128>", "bwd_dq_kernel<128>", "bwd_dkdv_kernel<128>", "bwd_finalize_kernel")
 COPY_KERNEL = "__amd_rocclr_copyBuffer"

@@ -6,17 +6,34 @@
 //   M = max m_i;  L = sum l_i 2^(m_i - M);  O = sum o_i 2^(m_i - M) / L;
 //   LSE = (M + log2 L) ln 2.
 // Partials are read in the planner's fixed order, so results are bitwise
-// reproducible.  32 threads per (query row, head), 8 per block, over the
-// (row, KV head) pairs the plan lists.
+// reproducible.  LANES threads per (query row, head), each with D/LANES
+// elements, 256 / LANES pairs per block, over the (row, KV head) pairs the
+// plan lists: 8 lanes (four independent 16-byte loads per partial at
+// D = 128) when there are enough pairs to fill the chip, else 32 (more
+// threads to cover the loads' latency in a small step).
 #include "device_common.hpp"
 
 namespace padoc {
 
-template <int D, bool BF16>
+template <int N>
+struct VecF;  // N consecutive floats as one load / store
+template <>
+struct VecF<2> {
+  typedef float2 T;
+};
+template <>
+struct VecF<4> {
+  typedef float4 T;
+};
+
+template <int D, bool BF16, int LANES>
 __global__ __launch_bounds__(256) void lse_combine_kernel(CombineParams p) {
-  constexpr int PER = D / 32;
-  const int64_t pair = (int64_t)blockIdx.x * 8 + (threadIdx.x >> 5);
-  const int sub = threadIdx.x & 31;
+  constexpr int PER = D / LANES;                // elements per thread
+  constexpr int VW = PER >= 4 ? 4 : PER;        // floats per vector load
+  constexpr int NV = PER / VW;                  // vector loads per partial
+  typedef typename VecF<VW>::T vec_t;
+  const int64_t pair = (int64_t)blockIdx.x * (256 / LANES) + (threadIdx.x / LANES);
+  const int sub = threadIdx.x % LANES;
   if (pair >= p.n_rows * p.G) return;
   const int64_t rk = p.comb_rows[pair / p.G];
   const int h = (int)(pair % p.G);
@@ -36,50 +53,60 @@ __global__ __launch_bounds__(256) void lse_combine_kernel(CombineParams p) {
     const int64_t slot = p.comb_slot[e] + h;
     const float sc = fast_exp2(p.part_ml[2 * slot] - M);
     L = fmaf(p.part_ml[2 * slot + 1], sc, L);
-    const float* src = p.part_o + slot * D + sub * PER;
-    if constexpr (PER == 4) {
-      const float4 x = *reinterpret_cast<const float4*>(src);
-      o[0] = fmaf(x.x, sc, o[0]);
-      o[1] = fmaf(x.y, sc, o[1]);
-      o[2] = fmaf(x.z, sc, o[2]);
-      o[3] = fmaf(x.w, sc, o[3]);
-    } else {
-      const float2 x = *reinterpret_cast<const float2*>(src);
-      o[0] = fmaf(x.x, sc, o[0]);
-      o[1] = fmaf(x.y, sc, o[1]);
-    }
+    const vec_t* src = reinterpret_cast<const vec_t*>(p.part_o + slot * D + sub * PER);
+    float x[PER];
+#pragma unroll
+    for (int k = 0; k < NV; ++k) *reinterpret_cast<vec_t*>(&x[VW * k]) = src[k];
+#pragma unroll
+    for (int k = 0; k < PER; ++k) o[k] = fmaf(x[k], sc, o[k]);
   }
   const float inv = 1.f / L;
   const int64_t base = (row * p.Hq + hq) * D + sub * PER;
   if constexpr (BF16) {
-    uint16_t* dst = static_cast<uint16_t*>(p.o) + base;
-    if constexpr (PER == 4) {
-      uint2 pk;
-      pk.x = (uint32_t)f32_to_bf16_bits(o[0] * inv) | ((uint32_t)f32_to_bf16_bits(o[1] * inv) << 16);
-      pk.y = (uint32_t)f32_to_bf16_bits(o[2] * inv) | ((uint32_t)f32_to_bf16_bits(o[3] * inv) << 16);
-      *reinterpret_cast<uint2*>(dst) = pk;
+    uint32_t w[PER / 2];
+#pragma unroll
+    for (int k = 0; k < PER / 2; ++k)
+      w[k] = (uint32_t)f32_to_bf16_bits(o[2 * k] * inv) | ((uint32_t)f32_to_bf16_bits(o[2 * k + 1] * inv) << 16);
+    uint32_t* dst = reinterpret_cast<uint32_t*>(static_cast<uint16_t*>(p.o) + base);
+    if constexpr (PER >= 8) {
+#pragma unroll
+      for (int k = 0; k < PER / 8; ++k) reinterpret_cast<uint4*>(dst)[k] = make_uint4(w[4 * k], w[4 * k + 1], w[4 * k + 2], w[4 * k + 3]);
+    } else if constexpr (PER == 4) {
+      *reinterpret_cast<uint2*>(dst) = make_uint2(w[0], w[1]);
     } else {
-      *reinterpret_cast<uint32_t*>(dst) =
-          (uint32_t)f32_to_bf16_bits(o[0] * inv) | ((uint32_t)f32_to_bf16_bits(o[1] * inv) << 16);
+      dst[0] = w[0];
     }
   } else {
     float* dst = static_cast<float*>(p.o) + base;
 #pragma unroll
-    for (int k = 0; k < PER; ++k) dst[k] = o[k] * inv;
+    for (int k = 0; k < PER; ++k) o[k] *= inv;
+#pragma unroll
+    for (int k = 0; k < NV; ++k) reinterpret_cast<vec_t*>(dst)[k] = *reinterpret_cast<const vec_t*>(&o[VW * k]);
   }
   if (sub == 0) p.lse[row * p.Hq + hq] = (M + __log2f(L)) * kLn2;
+}
+
+template <int D, bool BF16>
+void launch_d(const CombineParams& p, int64_t pairs, hipStream_t stream) {
+  // 8 lanes per pair once the pairs fill 256 compute units x 8 wavefronts
+  if (pairs >= 256 * 8 * 64 / 8) {
+    const dim3 grid((unsigned)((pairs + 31) / 32)), block(256);
+    hipLaunchKernelGGL((lse_combine_kernel<D, BF16, 8>), grid, block, 0, stream, p);
+  } else {
+    const dim3 grid((unsigned)((pairs + 7) / 8)), block(256);
+    hipLaunchKernelGGL((lse_combine_kernel<D, BF16, 32>), grid, block, 0, stream, p);
+  }
 }
 
 hipError_t launch_lse_combine(const CombineParams& p, int D, bool bf16, hipStream_t stream) {
   const int64_t pairs = p.n_rows * p.G;
   if (pairs == 0) return hipSuccess;
-  const dim3 grid((unsigned)((pairs + 7) / 8)), block(256);
   if (D == 64) {
-    if (bf16) hipLaunchKernelGGL((lse_combine_kernel<64, true>), grid, block, 0, stream, p);
-    else hipLaunchKernelGGL((lse_combine_kernel<64, false>), grid, block, 0, stream, p);
+    if (bf16) launch_d<64, true>(p, pairs, stream);
+    else launch_d<64, false>(p, pairs, stream);
   } else {
-    if (bf16) hipLaunchKernelGGL((lse_combine_kernel<128, true>), grid, block, 0, stream, p);
-    else hipLaunchKernelGGL((lse_combine_kernel<128, false>), grid, block, 0, stream, p);
+    if (bf16) launch_d<128, true>(p, pairs, stream);
+    else launch_d<128, false>(p, pairs, stream);
   }
   return hipGetLastError();
 }
