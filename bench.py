@@ -186,16 +186,16 @@ def measured_traffic():
 
 
 PROFILE_COMMANDS = """\
-    R=<repository root>; cd /tmp && export TMPDIR=/tmp
-    rocprofv3 --kernel-trace --stats -d $R/gpurun_out/prof/trace -o bench -- \\
-        python3 $R/bench.py --steps 5 --warmup 1 --no-cpu-baseline --no-baselines --driver-steps 0 --no-secondary --no-cold > $R/gpurun_out/prof/trace/bench.json
-    rocprofv3 --pmc FETCH_SIZE --kernel-include-regex padoc -f csv -d $R/gpurun_out/prof/fetch -o p -- \\
+    R=<repository root>; OUT=<output directory>; cd /tmp && export TMPDIR=/tmp
+    rocprofv3 --kernel-trace --stats -d $OUT/trace -o bench -- \\
+        python3 $R/bench.py --steps 5 --warmup 1 --no-cpu-baseline --no-baselines --driver-steps 0 --no-secondary --no-cold > $OUT/trace/bench.json
+    rocprofv3 --pmc FETCH_SIZE --kernel-include-regex padoc -f csv -d $OUT/fetch -o p -- \\
         python3 $R/bench.py --steps 5 --warmup 1 --no-cpu-baseline --no-baselines --driver-steps 0 --no-secondary --no-cold
-    rocprofv3 --pmc WRITE_SIZE --kernel-include-regex padoc -f csv -d $R/gpurun_out/prof/write -o p -- \\
+    rocprofv3 --pmc WRITE_SIZE --kernel-include-regex padoc -f csv -d $OUT/write -o p -- \\
         python3 $R/bench.py --steps 5 --warmup 1 --no-cpu-baseline --no-baselines --driver-steps 0 --no-secondary --no-cold
-    rocprofv3 --pmc FETCH_SIZE -f csv -d $R/gpurun_out/prof/copy_fetch -o c -- python3 $R/bench.py --calibrate-copy
-    rocprofv3 --pmc WRITE_SIZE -f csv -d $R/gpurun_out/prof/copy_write -o c -- python3 $R/bench.py --calibrate-copy
-    python3 $R/bench.py --summarize-profile $R/gpurun_out/prof
+    rocprofv3 --pmc FETCH_SIZE -f csv -d $OUT/copy_fetch -o c -- python3 $R/bench.py --calibrate-copy
+    rocprofv3 --pmc WRITE_SIZE -f csv -d $OUT/copy_write -o c -- python3 $R/bench.py --calibrate-copy
+    python3 $R/bench.py --summarize-profile $OUT
 """
 
 
