@@ -257,7 +257,10 @@ padoc_status padoc_tree_attn_fwd(const padoc_plan* plan, const void* q, const vo
 /* Decode step over a paged cache.  Needs a plan with block_size == 16.
    k_cache / v_cache follow the paged layouts above (chunk-major K, d-major
    V).  block_table is the device copy of the table the plan was built for
-   (block_table_len int32 entries, every id < num_kv_rows). */
+   (block_table_len int32 entries, every id < num_kv_rows).  The call copies
+   the schedule (with zeroed work-queue counters) into the workspace and
+   then runs the kernels, all on `stream`: calls that overlap on one
+   workspace race (give concurrent calls their own workspaces). */
 padoc_status padoc_branch_decode(const padoc_plan* plan, const void* q, const void* k_cache,
                                  const void* v_cache, const int32_t* block_table, void* o,
                                  float* lse, void* workspace, size_t workspace_bytes,
