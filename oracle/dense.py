@@ -394,64 +394,58 @@ def decoding_depths(nodes):
 
 
 # --------------------------------------------------------------------------
-# Algorithm "Masked parallel decoding" (App. E), logical fused form
+# Masked parallel decoding (App. E), on the logical fused mask
 # --------------------------------------------------------------------------
 
 def simulate_masked_parallel_decoding(prefix_len: int, decide, max_steps: int = 64):
-    """Replay the logical fused mask of masked parallel decoding.
+    """Replay masked parallel decoding (App. E, algorithm "Masked parallel
+    decoding") on its logical fused mask, held as one Boolean matrix whose
+    rows are the live streams and whose columns are the cache positions.
 
-    ``decide(step, stream_id, is_layout)`` returns the event after a stream's
-    decode at ``step``: ``"continue"``, ``"eos"`` (retire), or for the layout
-    stream also ``"fork"`` (its output closes a region).  Stream 0 is the
-    layout stream; content streams get ids 1, 2, ... in creation order.
+    ``decide(step, stream_id, is_layout)`` gives what happens after a stream
+    has been decoded at ``step``: ``"continue"``, ``"eos"`` (the stream
+    stops), or, for the layout stream only, ``"fork"`` (its output closes a
+    region, which opens a content stream).  Stream 0 is the layout stream;
+    content streams are numbered 1, 2, ... as they open.
 
-    Mask semantics (App. E): after prefilling X the layout row sees X; each
-    step appends one input per live stream with an identity block
-    (``M <- [M I_C]``), then decodes every live stream with its row; on a
-    region close the layout row as it stands (before the boundary output is
-    appended) is copied into a new content stream's row; retired rows are
-    removed.
+    The matrix changes in three ways.  A step puts one token of every live
+    stream into the cache: the matrix gains one column per live stream, set
+    only in that stream's own row (an identity block), and every stream's new
+    token is queried with its row as it then stands.  A region close gives
+    the new content stream a copy of the layout stream's row taken at that
+    moment, i.e. before the closing output itself reaches the cache (it
+    enters at the next step, seen by the layout stream alone).  A stopped
+    stream's row is dropped.
 
-    Returns ``(tags, queries, forks)``: ``tags[l] = (stream, index)`` for each
-    cache position (stream -1 = prefix), ``queries`` = list of ``(stream,
-    index, row)`` with the Boolean mask row used for the query that the stream
-    appended at that step, and ``forks[c]`` = number of layout-stream tokens
-    cached when content stream c was created."""
+    Returns ``(tags, queries, forks)``: ``tags[l] = (stream, index)`` names
+    the token at cache position l (stream -1 = page prefix); ``queries`` lists
+    ``(stream, index, row)`` with the Boolean row used for that token;
+    ``forks[c]`` = layout-stream tokens in the cache when stream c opened."""
+    streams = [0]                                  # stream of each matrix row
+    mask = np.ones((1, prefix_len), dtype=bool)    # the layout stream sees X
     tags: List[Tuple[int, int]] = [(-1, i) for i in range(prefix_len)]
-    rows: Dict[int, np.ndarray] = {0: np.ones(prefix_len, dtype=bool)}
-    count: Dict[int, int] = {0: 0}
+    made: Dict[int, int] = {0: 0}                  # tokens a stream has cached
     forks: Dict[int, int] = {}
     queries = []
-    next_id = 1
     for step in range(max_steps):
-        live = sorted(rows)
-        if not live:
+        if not streams:
             break
-        # append one input per live stream: M <- [M I_C]
-        L = len(tags)
-        for c in live:
-            tags.append((c, count[c]))
-        for c in live:
-            ext = np.zeros(len(live), dtype=bool)
-            ext[live.index(c)] = True
-            rows[c] = np.concatenate([rows[c], ext])
-        # decode: every live stream's new token is queried with its row
-        for c in live:
-            queries.append((c, count[c], rows[c].copy()))
-            count[c] += 1
-        # events
-        for c in live:
-            ev = decide(step, c, c == 0)
-            if c == 0 and ev == "fork":
-                cid = next_id
-                next_id += 1
-                rows[cid] = rows[0].copy()          # pre-boundary layout row
-                count[cid] = 0
-                forks[cid] = count[0]
-            elif ev == "eos":
-                del rows[c]
-        # rows of all streams cover the whole cache
-        for c in rows:
-            assert rows[c].size == len(tags)
-        del L
+        n = len(streams)
+        mask = np.concatenate([mask, np.eye(n, dtype=bool)], axis=1)
+        tags.extend((c, made[c]) for c in streams)
+        for r, c in enumerate(streams):
+            queries.append((c, made[c], mask[r].copy()))
+            made[c] += 1
+        events = [decide(step, c, c == 0) for c in streams]
+        opened = [mask[r].copy() for r, (c, ev) in enumerate(zip(streams, events)) if c == 0 and ev == "fork"]
+        alive = np.array([ev != "eos" for ev in events], dtype=bool)
+        mask = mask[alive]
+        streams = [c for c, a in zip(streams, alive) if a]
+        for row in opened:
+            cid = max(made) + 1
+            made[cid] = 0
+            forks[cid] = made[0]
+            streams.append(cid)
+            mask = np.concatenate([mask, row[None, :]], axis=0)
+        assert mask.shape == (len(streams), len(tags))
     return tags, queries, forks

@@ -11,8 +11,7 @@ import os
 
 import numpy as np
 
-# PADOC_LIB may name another build of the same library (experiments).
-LIB_PATH = os.environ.get("PADOC_LIB") or os.path.join(os.path.dirname(os.path.abspath(__file__)), "libpadoc_attn.so")
+LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libpadoc_attn.so")
 
 OK, ERR_ARG, ERR_TREE, ERR_SHAPE, ERR_DTYPE, ERR_BOUNDS, ERR_WORKSPACE, ERR_HIP, ERR_MODE = 0, -1, -2, -3, -4, -5, -6, -7, -8
 STATUS_NAMES = {0: "PADOC_OK", -1: "PADOC_ERR_ARG", -2: "PADOC_ERR_TREE", -3: "PADOC_ERR_SHAPE",

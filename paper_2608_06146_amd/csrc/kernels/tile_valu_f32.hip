@@ -3,7 +3,8 @@
 // ALUs.  This is the fp32 path of both entry points (the MFMA paths are
 // bf16); it reads the same schedules as the bf16 kernels, one workgroup per
 // work item (columns col0 .. col0+ncol-1 of the item's task), over packed
-// K/V or the paged cache (K blocks [16][d], V blocks d-major [d][16]).
+// K/V or the paged cache (K blocks chunk-major [d/8][16 slots][8], V blocks
+// d-major [d][16]).
 //
 // Per column and visible key j (App. E Attn equation, with the scale applied
 // in log2 units): s = scale*log2(e) * q.k_j; m' = max(m, s);

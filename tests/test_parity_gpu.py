@@ -204,6 +204,28 @@ def test_concurrent_decode_64pages_full_size():
     decode_case(wl.pages, 16, 2, 128, "bf16", 0, pool_extra=5000, rows=sorted(rows))
 
 
+@pytest.mark.parametrize("dtype,d", [("bf16", 128), ("f32", 64)])
+def test_decode_pool_offsets_beyond_4gib(dtype, d):
+    """Caches of 10 GiB each (1.31 M blocks of 8 KB): most used blocks lie
+    past byte offset 4 GiB (element offsets of 2^31 and more for bf16) and
+    some past 8 GiB, as in the pool spread over most of HBM that the
+    benchmark times.  The single-page decode workload (shared tile items and
+    private items) against the oracle, which gathers the blocks itself."""
+    wl = syn.make_workload("single_page_decode")
+    nodes = od.page_nodes(wl.pages)
+    nb = int(sum(-(-n[2] // 16) for n in nodes))
+    esz = 2 if dtype == "bf16" else 4
+    block_bytes = 2 * 16 * d * esz
+    n_pool = (10 << 30) // block_bytes
+    extra = n_pool - nb
+    ids = syn.draw_block_ids(nb, n_pool, 0)
+    assert (ids.astype(np.int64) * block_bytes >= (4 << 30)).sum() > nb // 2
+    assert (ids.astype(np.int64) * block_bytes >= (8 << 30)).any()
+    o, lse, plan, errs = decode_case(wl.pages, 16, 2, d, dtype, 0, pool_extra=extra)
+    del o, lse, plan
+    torch.cuda.empty_cache()
+
+
 @pytest.mark.slow
 def test_dense_page_mixed_step_full_size_sampled():
     """1 page, P=8192, S=1024, 128 branches (96 decoding + 32 new 8-token
