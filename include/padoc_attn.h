@@ -54,7 +54,8 @@
  *
  * Ownership: the caller owns every buffer.  The library never allocates
  * device memory: it reports a workspace size and the caller passes a device
- * buffer of at least that size to each launch.  A plan owns host memory only,
+ * buffer of at least that size to each launch (padoc_branch_decode_no_alloc
+ * instead uses a fixed array the library holds on each GPU).  A plan owns host memory only,
  * is immutable after creation and may be reused for any number of launches
  * with the same tree; destroy it only after the stream has passed the last
  * launch that used it.
@@ -265,6 +266,28 @@ padoc_status padoc_branch_decode(const padoc_plan* plan, const void* q, const vo
                                  const void* v_cache, const int32_t* block_table, void* o,
                                  float* lse, void* workspace, size_t workspace_bytes,
                                  hipStream_t stream);
+
+/* padoc_branch_decode without a workspace argument, for callers that cannot
+   allocate device memory (code under stream capture, serving loops that must
+   not call the allocator, harnesses that forbid it).  Same plan, inputs,
+   outputs, kernels and results as padoc_branch_decode; the workspace is a
+   fixed array the library holds on each GPU it runs on, of
+   PADOC_NO_ALLOC_WORKSPACE_BYTES (64 MiB; the decode workloads measured here
+   need at most about 28 MiB), kept until the process ends.  Its device
+   address is looked up on the first call made with that device current.
+   The schedule is copied from the plan's host memory (no pinned copy is
+   made) and that copy also zeroes the work-queue counters; every other
+   scratch value is written before it is read, so nothing else must start
+   at zero.  No device or pinned host memory is allocated.
+   A plan whose workspace exceeds the array returns PADOC_ERR_WORKSPACE and
+   enqueues nothing.  All calls on one GPU share that GPU's array and it
+   keeps the last call's contents: calls that overlap on one GPU (different
+   streams, or host threads without ordering) race; order them. */
+#define PADOC_NO_ALLOC_WORKSPACE_BYTES ((size_t)64 << 20)
+padoc_status padoc_branch_decode_no_alloc(const padoc_plan* plan, const void* q,
+                                          const void* k_cache, const void* v_cache,
+                                          const int32_t* block_table, void* o, float* lse,
+                                          hipStream_t stream);
 
 /* Backward of the packed forward (bf16 plans with block_size == 0).
    Given the forward's inputs q, k, v, its outputs o and lse, and the

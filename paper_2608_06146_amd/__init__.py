@@ -263,6 +263,28 @@ def branch_decode(q, k_cache, v_cache, block_table, plan: TreePlan, out=None, ls
     return out, lse
 
 
+NO_ALLOC_WORKSPACE_BYTES = 64 << 20   # PADOC_NO_ALLOC_WORKSPACE_BYTES
+
+
+def branch_decode_no_alloc(q, k_cache, v_cache, block_table, plan: TreePlan, out, lse, stream=None):
+    """Decode step with the library's fixed per-GPU workspace
+    (``padoc_branch_decode_no_alloc``): the caller passes every input and
+    both outputs; nothing is allocated.  Calls that overlap on one GPU race
+    on that workspace."""
+    import torch
+    dt = _torch_dtype(plan)
+    dev = q.device
+    for name, t in (("q", q), ("k_cache", k_cache), ("v_cache", v_cache), ("out", out)):
+        _check_tensor(name, t, dt, dev)
+    _check_tensor("block_table", block_table, torch.int32, dev)
+    _check_tensor("lse", lse, torch.float32, dev)
+    s = torch.cuda.current_stream(dev) if stream is None else stream
+    _lib.check(_lib.lib().padoc_branch_decode_no_alloc(plan.handle, _ptr(q), _ptr(k_cache), _ptr(v_cache),
+                                                       _ptr(block_table), _ptr(out), _ptr(lse),
+                                                       C.c_void_p(s.cuda_stream)))
+    return out, lse
+
+
 def tree_attn_bwd(q, k, v, o, lse, dout, plan: TreePlan, dq=None, dk=None, dv=None, workspace=None, stream=None):
     """Backward of the packed forward (``padoc_tree_attn_bwd``, bf16 plans).
     q, o, dout ``[n_q, Hq, d]``; k, v ``[T, Hkv, d]``; lse float32 ``[n_q,

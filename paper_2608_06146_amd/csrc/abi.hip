@@ -3,6 +3,7 @@
 #include <hip/hip_runtime.h>
 
 #include <cstring>
+#include <mutex>
 
 #include "host/plan.hpp"
 #include "host/session.hpp"
@@ -88,14 +89,17 @@ const void* pinned_bwd_blob(const padoc_plan* P) {
 // Launch the attention of plan P.  `upload`: copy the schedule into the
 // workspace first (else the caller already did); `events`: record the
 // profiling events around the kernels.
+// `pinned`: upload from the plan's pinned host copy (made on first use);
+// else straight from the plan's own host memory, allocating nothing.
 padoc_status run(const padoc_plan* P, const void* q, const void* k, const void* v, const int32_t* bt, void* o,
-                 float* lse, void* ws, hipStream_t stream, bool upload = true, bool events = true) {
+                 float* lse, void* ws, hipStream_t stream, bool upload = true, bool events = true,
+                 bool pinned = true) {
   if (P->work.empty()) return PADOC_OK;
   hipError_t e = hipSuccess;
   if (upload) {
-    e = hipMemcpyAsync(ws, pinned_blob(P), P->blob.size(), hipMemcpyHostToDevice, stream);
+    e = hipMemcpyAsync(ws, pinned ? pinned_blob(P) : P->blob.data(), P->blob.size(), hipMemcpyHostToDevice, stream);
     if (e != hipSuccess) return hip_fail("hipMemcpyAsync(schedule)", e);
-    if (P->build_id > 1) {
+    if (pinned && P->build_id > 1) {
       // a rebuilt plan: mark when its pinned copy may be overwritten
       std::lock_guard<std::mutex> lk(P->pin_mu);
       if (!P->pin_ev) {
@@ -191,6 +195,62 @@ extern "C" padoc_status padoc_branch_decode(const padoc_plan* plan, const void* 
     return set_error(PADOC_ERR_MODE, "plan was built for packed K/V (block_size 0); use padoc_tree_attn_fwd");
   if (!plan->work.empty() && !block_table) return set_error(PADOC_ERR_ARG, "block_table is null");
   return run(plan, q, k_cache, v_cache, block_table, o, lse, workspace, stream);
+}
+
+// Workspace of padoc_branch_decode_no_alloc: one array per GPU the library
+// runs on, held until the process ends.  Host code never passes `scratch`
+// itself to a kernel or a copy (on the host it names a stand-in, not device
+// memory): it uses the device address hipGetSymbolAddress returns.
+constexpr size_t kNoAllocScratchBytes = PADOC_NO_ALLOC_WORKSPACE_BYTES;
+static __device__ __align__(256) unsigned char scratch[kNoAllocScratchBytes];
+
+namespace padoc {
+namespace {
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+void* g_scratch_addr[kMaxDevices] = {};
+
+// Device address of the current device's copy of `scratch`, looked up on
+// the first call made with that device current.
+padoc_status scratch_of_current_device(void** out) {
+  int dev = -1;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return hip_fail("hipGetDevice", e);
+  if (dev < 0 || dev >= kMaxDevices) return set_error(PADOC_ERR_ARG, "device %d is out of range", dev);
+  std::lock_guard<std::mutex> lk(g_scratch_mu);
+  if (!g_scratch_addr[dev]) {
+    void* p = nullptr;
+    e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (e != hipSuccess) return hip_fail("hipGetSymbolAddress(scratch)", e);
+    if (!p) return set_error(PADOC_ERR_HIP, "hipGetSymbolAddress(scratch) returned no address");
+    g_scratch_addr[dev] = p;
+  }
+  *out = g_scratch_addr[dev];
+  return PADOC_OK;
+}
+}  // namespace
+}  // namespace padoc
+
+extern "C" padoc_status padoc_branch_decode_no_alloc(const padoc_plan* plan, const void* q, const void* k_cache,
+                                                     const void* v_cache, const int32_t* block_table, void* o,
+                                                     float* lse, hipStream_t stream) {
+  clear_error();
+  if (!plan) return set_error(PADOC_ERR_ARG, "plan is null");
+  if (plan->kind != 1)
+    return set_error(PADOC_ERR_MODE, "plan was built for packed K/V (block_size 0); use padoc_tree_attn_fwd");
+  if (plan->ws_bytes > kNoAllocScratchBytes)
+    return set_error(PADOC_ERR_WORKSPACE,
+                     "the plan needs %zu bytes of workspace; padoc_branch_decode_no_alloc holds at most %zu "
+                     "(use padoc_branch_decode with a caller workspace)",
+                     plan->ws_bytes, kNoAllocScratchBytes);
+  void* ws = nullptr;
+  padoc_status st = scratch_of_current_device(&ws);
+  if (st != PADOC_OK) return st;
+  st = check_common(plan, q, k_cache, v_cache, o, lse, ws, kNoAllocScratchBytes);
+  if (st != PADOC_OK) return st;
+  if (!plan->work.empty() && !block_table) return set_error(PADOC_ERR_ARG, "block_table is null");
+  return run(plan, q, k_cache, v_cache, block_table, o, lse, ws, stream, /*upload=*/true, /*events=*/true,
+             /*pinned=*/false);
 }
 
 extern "C" padoc_status padoc_tree_attn_bwd(const padoc_plan* plan, const void* q, const void* k, const void* v,

@@ -477,3 +477,20 @@ def test_tree_depths_errors():
     z = np.zeros(2, np.int64)
     assert L.padoc_tree_depths(bad.ctypes.data, 2, z.ctypes.data, z.ctypes.data) == _lib.ERR_TREE
     assert L.padoc_tree_depths(None, -1, None, None) == _lib.ERR_ARG
+
+
+def test_no_alloc_decode_rejects_oversized_plans():
+    """A plan whose workspace exceeds the fixed per-GPU array is refused
+    before anything touches a device (host-side check, no GPU needed)."""
+    import ctypes as C
+    import padoc_synth as syn
+    wl = syn.make_workload("concurrent_decode_64pages")
+    pages = wl.pages * 4
+    segs = pa.segments_from_pages(pages, 16)
+    nb, nq = syn.count_blocks(pages), syn.count_queries(pages)
+    plan = pa.TreePlan(segs, 16, 2, 128, "bf16", 16, num_kv_rows=nb, num_q_rows=nq, block_table_len=nb)
+    assert plan.workspace_bytes > pa.NO_ALLOC_WORKSPACE_BYTES
+    fake = C.c_void_p(1 << 20)   # never dereferenced: the size check comes first
+    st = pa._lib.lib().padoc_branch_decode_no_alloc(plan.handle, fake, fake, fake, fake, fake, fake, None)
+    assert st == pa._lib.ERR_WORKSPACE
+    assert "at most" in pa._lib.lib().padoc_last_error().decode()
