@@ -135,13 +135,15 @@ typedef struct {
                                     used only to check ids are in the pool     */
   int64_t block_table_len;       /* paged: entries in the block table           */
   int32_t max_chunk_keys;        /* decode: split keys into chunks of at most
-                                    this many (multiple of 64); 0 = automatic */
+                                    this many (multiple of 64, at most 8192);
+                                    0 = automatic                           */
   int32_t target_workgroups;     /* decode chunk sizes (0 = 1024): shared keys
-                                    are cut into the fewest chunks that keep
-                                    the tile items (8 wavefronts each) within
-                                    3/16 of this, private keys into about 2x this
-                                    many wavefront items; both chunk sizes
-                                    clamped to [512, 8192] keys              */
+                                    are cut into the fewest chunks (64 to 8192
+                                    keys) that keep the tile items (8
+                                    wavefronts each) within 3/16 of this,
+                                    private keys into about 2x this many
+                                    wavefront items (chunks of 512 to 8192
+                                    keys)                                    */
 } padoc_tree_desc;
 
 typedef struct padoc_plan padoc_plan;

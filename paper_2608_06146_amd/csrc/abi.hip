@@ -148,9 +148,8 @@ padoc_status run(const padoc_plan* P, const void* q, const void* k, const void* 
   if (e != hipSuccess) return hip_fail("tile kernel launch", e);
   if (partial) {
     CombineParams cp{};
-    cp.comb_ptr = at<int32_t>(ws, P->off_comb_ptr);
     cp.comb_slot = at<int32_t>(ws, P->off_comb_slot);
-    cp.comb_rows = at<int32_t>(ws, P->off_comb_rows);
+    cp.comb_rows = at<int4>(ws, P->off_comb_rows);
     cp.n_rows = (int64_t)P->comb_rows.size();
     cp.part_o = tp.part_o;
     cp.part_ml = tp.part_ml;

@@ -255,9 +255,9 @@ padoc_status validate(const padoc_tree_desc* d) {
   if (d->num_kv_rows < 0 || d->num_q_rows < 0 || d->block_table_len < 0)
     return set_error(PADOC_ERR_ARG, "negative buffer size");
   if (d->num_q_rows > kI32Max) return set_error(PADOC_ERR_BOUNDS, "num_q_rows exceeds 2^31-1");
-  if (d->max_chunk_keys < 0 || d->max_chunk_keys % kTileKeys != 0)
-    return set_error(PADOC_ERR_ARG, "max_chunk_keys=%d must be a non-negative multiple of %d",
-                     d->max_chunk_keys, kTileKeys);
+  if (d->max_chunk_keys < 0 || d->max_chunk_keys % kTileKeys != 0 || d->max_chunk_keys > padoc::kMaxItemKeys)
+    return set_error(PADOC_ERR_ARG, "max_chunk_keys=%d must be a multiple of %d in [0, %d]", d->max_chunk_keys,
+                     kTileKeys, padoc::kMaxItemKeys);
   if (d->target_workgroups < 0) return set_error(PADOC_ERR_ARG, "target_workgroups is negative");
   const int32_t n = d->n_seg;
   for (int32_t i = 0; i < n; ++i) {
@@ -542,7 +542,7 @@ void build_decode(padoc_plan& P, Builder& B, const AncList& anc, const padoc_tre
   auto chunk_keys = [&](int64_t total, int64_t pieces) {
     if (d->max_chunk_keys > 0) return (int64_t)d->max_chunk_keys;
     const int64_t ch = round_up(std::max<int64_t>(1, ceil_div(total, pieces)), 64);
-    return std::min<int64_t>(std::max<int64_t>(ch, 512), 8192);
+    return std::min<int64_t>(std::max<int64_t>(ch, 512), padoc::kMaxItemKeys);
   };
   const int64_t CHp = chunk_keys(total_p, 2 * tw);
   // Shared keys: every tile item takes a whole compute unit (its registers)
@@ -551,8 +551,10 @@ void build_decode(padoc_plan& P, Builder& B, const AncList& anc, const padoc_tre
   // the target_workgroups / 4 units (one round), so that from the start at
   // least a quarter of the units read private keys, while the shared keys
   // still get most of the matrix cores; a step over the cap would need a
-  // second round of tile items.  Smallest chunk (a multiple of 64 in
-  // [512, 8192]) whose items (over all tasks and KV heads) fit, else 8192.
+  // second round of tile items.  Smallest chunk (a multiple of 64 up to
+  // 8192) whose items (over all tasks and KV heads) fit, else 8192: a small
+  // step (one page) gets short chunks, so its few shared keys still spread
+  // over many compute units instead of forming a few long serial chains.
   auto shared_items = [&](int64_t CH) {
     int64_t n = 0;
     for (size_t i = 0; i + 1 < svis_at.size(); ++i) {
@@ -573,7 +575,7 @@ void build_decode(padoc_plan& P, Builder& B, const AncList& anc, const padoc_tre
   int64_t CHs = d->max_chunk_keys;
   if (CHs <= 0) {
     const int64_t target = std::max<int64_t>(1, tw * 3 / 16);
-    int64_t lo = 8, hi = 128;  // chunk = 64 * k keys
+    int64_t lo = 1, hi = 128;  // chunk = 64 * k keys
     if (shared_items(64 * hi) > target) {
       lo = hi;
     } else {
@@ -724,10 +726,9 @@ void serialise(padoc_plan& P) {
   P.off_ranges = align256(P.off_work + P.work.size() * sizeof(padoc::WorkRec));
   P.off_lims = align256(P.off_ranges + P.ranges.size() * sizeof(padoc::RangeRec));
   P.off_toks = align256(P.off_lims + P.lims.size() * 4);
-  P.off_comb_ptr = align256(P.off_toks + P.toks.size() * 4);
-  P.off_comb_slot = align256(P.off_comb_ptr + P.comb_ptr.size() * 4);
+  P.off_comb_slot = align256(P.off_toks + P.toks.size() * 4);
   P.off_comb_rows = align256(P.off_comb_slot + P.comb_slot.size() * 4);
-  P.off_next = align256(P.off_comb_rows + P.comb_rows.size() * 4);
+  P.off_next = align256(P.off_comb_rows + P.comb_rows.size() * 16);
   const size_t blob_bytes = P.off_next + padoc::kPrivateQueues * 256;  // queue counters, 256 bytes apart
   P.off_part_o = align256(blob_bytes);
   P.off_part_ml = align256(P.off_part_o + (size_t)P.n_slots * P.D * 4);
@@ -737,9 +738,17 @@ void serialise(padoc_plan& P) {
   put(P.blob, P.off_ranges, P.ranges);
   put(P.blob, P.off_lims, P.lims);
   put(P.blob, P.off_toks, P.toks);
-  put(P.blob, P.off_comb_ptr, P.comb_ptr);
   put(P.blob, P.off_comb_slot, P.comb_slot);
-  put(P.blob, P.off_comb_rows, P.comb_rows);
+  // merged pairs as device records {row*Hkv + kvh, first, end, 0}: the
+  // combine kernel finds a pair and its slot list with one load
+  std::vector<int32_t> rec(P.comb_rows.size() * 4, 0);
+  for (size_t i = 0; i < P.comb_rows.size(); ++i) {
+    const int32_t rk = P.comb_rows[i];
+    rec[4 * i] = rk;
+    rec[4 * i + 1] = P.comb_ptr[rk];
+    rec[4 * i + 2] = P.comb_ptr[rk + 1];
+  }
+  put(P.blob, P.off_comb_rows, rec);
 }
 
 }  // namespace
@@ -807,6 +816,15 @@ padoc_status build_plan(const padoc_tree_desc* d, padoc_plan& P) {
     if (P.n_slots > kI32Max) return set_error(PADOC_ERR_ARG, "schedule too large (%lld partial slots)", (long long)P.n_slots);
     if ((int64_t)P.lims.size() > kI32Max || (int64_t)P.ranges.size() > kI32Max)
       return set_error(PADOC_ERR_ARG, "schedule too large");
+    // a paged tile item stages the block ids of all its tiles (one per thread)
+    for (int32_t i = 0; P.kind == 1 && i < P.n_work_shared; ++i) {
+      const padoc::WorkRec& w = P.work[i];
+      int64_t nt = 0;
+      for (int32_t r = 0; r < w.rng_count; ++r) nt += ceil_div(P.ranges[w.rng_begin + r].n_keys, kTileKeys);
+      if (nt > padoc::kMaxItemTiles)
+        return set_error(PADOC_ERR_ARG, "internal: shared item %d has %lld tiles (at most %d)", i, (long long)nt,
+                         padoc::kMaxItemTiles);
+    }
     // Costliest items first: the hardware dispatcher then assigns work
     // greedily to the first free compute unit (longest-processing-time
     // order).  Decode items are already ordered by workgroup.

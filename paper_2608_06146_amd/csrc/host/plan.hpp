@@ -52,7 +52,7 @@ struct padoc_plan {
   // Serialised schedule (uploaded into the workspace before every launch).
   std::vector<unsigned char> blob;
   size_t off_work = 0, off_ranges = 0, off_lims = 0, off_toks = 0;
-  size_t off_comb_ptr = 0, off_comb_slot = 0, off_comb_rows = 0, off_part_o = 0, off_part_ml = 0;
+  size_t off_comb_slot = 0, off_comb_rows = 0, off_part_o = 0, off_part_ml = 0;
   size_t off_next = 0;  // decode: private item queue counters (zeros in the blob)
   size_t ws_bytes = 0;
 

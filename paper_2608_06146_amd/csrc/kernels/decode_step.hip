@@ -32,6 +32,10 @@
 //                   blocks ([d][16 tokens]) as one 16-byte load per lane.
 // Two register sets hold the K and V of two future steps: a set is refilled
 // right after its last use, so every load has two steps of compute to land.
+// The item's records and the block ids are scalar loads (their own wait
+// counter), and a step's block ids are requested one step before its K/V
+// loads, so no wait for metadata also waits for K/V data in flight; the
+// column maxima use lane-swap instructions rather than LDS shuffles.
 // Keys past a range's end are never used: their scores are masked and V
 // elements past the end are zeroed before they reach a product.  Outputs are
 // split partials (unnormalised O, running max in log2 units, sum).
@@ -57,7 +61,7 @@ template <int D>
 __device__ __forceinline__ void private_item(const TileParams& p, int item, int lane) {
   constexpr int NDS = D / 32;  // K-slices (32 d each) of the score product
   constexpr int NDM = D / 16;  // 16-row blocks of O^T
-  const WorkRec w = p.work[item];
+  const WorkRec w = load_scalar(p.work + item);
   const int n = lane & 15, g = lane >> 4;
   const int G = p.G;
   const int kvh = w.kvh;
@@ -73,12 +77,10 @@ __device__ __forceinline__ void private_item(const TileParams& p, int item, int 
 
   // Q fragments (B operand): column n, d = ds*32 + 8g .. +7.
   bf16x8_t bq[NDS];
-  {
-    const uint16_t* qp = static_cast<const uint16_t*>(p.q) + ((int64_t)qrow * p.Hq + hq) * D + 8 * g;
+  const uint16_t* qp = static_cast<const uint16_t*>(p.q) + ((int64_t)qrow * p.Hq + hq) * D + 8 * g;
 #pragma unroll
-    for (int ds = 0; ds < NDS; ++ds)
-      bq[ds] = as_bf16x8(valid ? *reinterpret_cast<const uint4*>(qp + ds * 32) : make_uint4(0, 0, 0, 0));
-  }
+  for (int ds = 0; ds < NDS; ++ds)
+    bq[ds] = as_bf16x8(valid ? *reinterpret_cast<const uint4*>(qp + ds * 32) : make_uint4(0, 0, 0, 0));
 
   // Step cursors over the item's ranges: C = step being computed, L = next
   // step to load (two ahead of C once the pipeline is full).
@@ -93,24 +95,34 @@ __device__ __forceinline__ void private_item(const TileParams& p, int item, int 
     if (++c.st * 32 >= c.R.n_keys) {
       c.st = 0;
       if (++c.ri < w.rng_count)
-        c.R = p.ranges[w.rng_begin + c.ri];
+        c.R = load_scalar(p.ranges + w.rng_begin + c.ri);
       else
         c.ok = 0;
     }
   };
-  Cursor C{0, 0, p.ranges[w.rng_begin], 1, 0};
-  Cursor L = C;
+  Cursor C{0, 0, load_scalar(p.ranges + w.rng_begin), 1, 0};
+  Cursor L = C;  // once exhausted (ok = 0) it still names a valid step of the last range
 
   uint4 kf[2][2][NDS];  // [set][M block][K-slice]
   uint4 vf[2][NDM];     // [set][16-row d block]
   int vkeep[2];
   int64_t blk[2][2];    // [set][block of the step's first/second 16 keys]
+  int32_t nid[2];       // block ids of the load cursor's step, requested ahead
 
-  auto load_k = [&](const Cursor& c, int X) __attribute__((always_inline)) {
-    const int nk = c.R.n_keys, kb = c.st * 32;
-    const int64_t base = c.R.kv_start + (kb >> 4);
-    blk[X][0] = bt[base];
-    blk[X][1] = bt[base + ((kb + 16 < nk) ? 1 : 0)];
+  auto fetch_ids = [&](const Cursor& c) __attribute__((always_inline)) {
+    const int kb = c.st * 32;
+    const int32_t* b = bt + c.R.kv_start + (kb >> 4);
+    nid[0] = load_scalar(b);
+    nid[1] = load_scalar(b + ((kb + 16 < c.R.n_keys) ? 1 : 0));
+  };
+  // Loads of set X for the load cursor's step.  Past the item's last step
+  // (real = false) the same loads read this lane's Q row instead (cached,
+  // in bounds, never used): every step issues the same loads, so the
+  // compiler's waits for a set stay exact (a load under a branch would make
+  // it wait for every load in flight).
+  auto load_k = [&](int X, bool real) __attribute__((always_inline)) {
+    blk[X][0] = nid[0];
+    blk[X][1] = nid[1];
 #pragma unroll
     for (int mb = 0; mb < 2; ++mb) {
       // dims ds*32 + 8g .. +7 = chunk 4ds + g; with the chunk-major block
@@ -118,15 +130,16 @@ __device__ __forceinline__ void private_item(const TileParams& p, int item, int 
       const int key = step_key(mb, n);
       const uint16_t* kp = Kc + paged_k_offset<D>(blk[X][key >> 4], kvh, (int32_t)Hkv, key & 15, g);
 #pragma unroll
-      for (int ds = 0; ds < NDS; ++ds) kf[X][mb][ds] = load_stream16(kp + ds * 4 * (kBlock * 8));
+      for (int ds = 0; ds < NDS; ++ds)
+        kf[X][mb][ds] = load_stream16(real ? kp + ds * 4 * (kBlock * 8) : qp + ds * 32);
     }
   };
-  auto load_v = [&](const Cursor& c, int X) __attribute__((always_inline)) {
+  auto load_v = [&](const Cursor& c, int X, bool real) __attribute__((always_inline)) {
     const int keep = c.R.n_keys - (c.st * 32 + 8 * g);  // keys 8g .. 8g+7 of the step
     const uint16_t* vp = Vc + ((blk[X][g >> 1] * Hkv + kvh) * D + n) * kBlock + 8 * (g & 1);
 #pragma unroll
     for (int dm = 0; dm < NDM; ++dm)
-      vf[X][dm] = load_stream16(vp + dm * 16 * kBlock);
+      vf[X][dm] = load_stream16(real ? vp + dm * 16 * kBlock : qp + dm * 16);
     vkeep[X] = keep;
   };
 
@@ -134,21 +147,42 @@ __device__ __forceinline__ void private_item(const TileParams& p, int item, int 
   f32x4_t acc[NDM];
 #pragma unroll
   for (int dm = 0; dm < NDM; ++dm) acc[dm] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+  // This column's limit in the compute cursor's range: the range's length
+  // when it has no limits, else the entry of the column's token (scalar
+  // loads of the item's tokens' entries, picked per lane).
   int lim = 0;
-  auto load_lim = [&]() __attribute__((always_inline)) { lim = C.R.lim_off < 0 ? C.R.n_keys : (valid ? p.lims[C.R.lim_off + t] : 0); };
+  const int t_lo = w.col0 / G, t_hi = min(w.ntok - 1, (w.col0 + kPrivateCols - 1) / G);
+  auto load_lim = [&]() __attribute__((always_inline)) {
+    if (C.R.lim_off < 0) {
+      lim = C.R.n_keys;
+      return;
+    }
+    int v = 0;
+    for (int i = t_lo; i <= t_hi; ++i) {
+      const int32_t li = load_scalar(p.lims + C.R.lim_off + i);
+      v = t == i ? li : v;
+    }
+    lim = valid ? v : 0;
+  };
   load_lim();
   const float sl2 = p.scale_log2;
 
-  // Prologue: steps 0 and 1 into sets 0 and 1.
-  load_k(L, 0);
-  load_v(L, 0);
+  // Prologue: steps 0 and 1 into sets 0 and 1, the block ids of step 2.
+  // Branch-free: an exhausted load cursor still names a valid step.
+  fetch_ids(L);
+  load_k(0, true);
+  load_v(L, 0, true);
   advance(L);
-  if (L.ok) {
-    load_k(L, 1);
-    load_v(L, 1);
-    advance(L);
-  }
+  const bool two = L.ok;
+  fetch_ids(L);
+  load_k(1, two);
+  load_v(L, 1, two);
+  advance(L);
+  fetch_ids(L);
 
+  // Step of the compute cursor on register set X, then refill set X with the
+  // load cursor's step (two ahead) and request the block ids of the step
+  // after it; false once the item's last step is done.
   auto step = [&](auto xc) __attribute__((always_inline)) -> bool {
     constexpr int X = decltype(xc)::value;
     const int kb = C.st * 32;
@@ -161,7 +195,7 @@ __device__ __forceinline__ void private_item(const TileParams& p, int item, int 
         S[mb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf16x8(kf[X][mb][ds]), bq[ds], S[mb], 0, 0, 0);
     }
     const bool more = L.ok;
-    if (more) load_k(L, X);  // set X's K is consumed
+    load_k(X, more);  // set X's K is consumed
     if (kb + 32 > C.R.min_lim) {
 #pragma unroll
       for (int mb = 0; mb < 2; ++mb)
@@ -171,8 +205,7 @@ __device__ __forceinline__ void private_item(const TileParams& p, int item, int 
     }
     float mx = fmaxf(fmaxf(fmaxf(S[0][0], S[0][1]), fmaxf(S[0][2], S[0][3])),
                      fmaxf(fmaxf(S[1][0], S[1][1]), fmaxf(S[1][2], S[1][3])));
-    mx = fmaxf(mx, __shfl_xor(mx, 16));
-    mx = fmaxf(mx, __shfl_xor(mx, 32));
+    mx = max_lane_halves(max_lane_rows(mx));
     const float m_new = fmaxf(m_run, mx * sl2);
     const float m_sub = m_new == -INFINITY ? 0.f : m_new;
     const float alpha = fast_exp2(m_run - m_sub);
@@ -195,10 +228,9 @@ __device__ __forceinline__ void private_item(const TileParams& p, int item, int 
       acc[dm] *= alpha;
       acc[dm] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf16x8(keep_first(vf[X][dm], vkeep[X])), pb, acc[dm], 0, 0, 0);
     }
-    if (more) {
-      load_v(L, X);  // set X's V is consumed
-      advance(L);
-    }
+    load_v(L, X, more);  // set X's V is consumed
+    advance(L);
+    fetch_ids(L);  // used by the next step's K loads
     const int ri_before = C.ri;
     advance(C);
     if (!C.ok) return false;
@@ -234,7 +266,7 @@ constexpr int kQueues = kPrivateQueues;
 __device__ __forceinline__ int take_private(int* ctr, int lane) {
   int v = 0;
   if (lane == 0) v = atomicAdd(ctr, 1);
-  return __shfl(v, 0);
+  return __builtin_amdgcn_readfirstlane(v);
 }
 
 template <int D>

@@ -45,6 +45,26 @@ __device__ __forceinline__ void store16(void* p, const uint4& v) {
 
 __device__ __forceinline__ float fast_exp2(float x) { return __builtin_amdgcn_exp2f(x); }
 
+// Load of a wave-uniform value through the scalar data cache (s_load).  The
+// address must be the same in every lane (it is made so) and the memory
+// read-only while the kernel runs.  Scalar loads are counted by lgkmcnt, not
+// vmcnt: waiting for one does not wait for the vector loads in flight.
+template <class T>
+__device__ __forceinline__ T load_scalar(const T* p) {
+  static_assert(sizeof(T) % 4 == 0, "scalar loads move whole dwords");
+  typedef const __attribute__((address_space(4))) uint32_t* cptr;
+  const uint64_t a = (uint64_t)p;
+  const uint64_t u = ((uint64_t)(uint32_t)__builtin_amdgcn_readfirstlane((int)(a >> 32)) << 32) |
+                     (uint32_t)__builtin_amdgcn_readfirstlane((int)a);
+  const cptr q = (cptr)u;
+  uint32_t w[sizeof(T) / 4];
+#pragma unroll
+  for (int i = 0; i < (int)(sizeof(T) / 4); ++i) w[i] = q[i];
+  T r;
+  __builtin_memcpy(&r, w, sizeof(T));
+  return r;
+}
+
 // max(a, b, c) as one v_max3_f32.  Written as an instruction so the compiler
 // does not first canonicalise each operand (it cannot prove that values
 // merged from masked and unmasked paths are canonical); inputs here are

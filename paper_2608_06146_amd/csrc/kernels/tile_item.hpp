@@ -209,17 +209,19 @@ __device__ __forceinline__ void tile_item(const TileParams& p, int item) {
   struct Cursor {
     int ri, kt;
     RangeRec R;
-    int ok, unused;
+    int ok, tb;  // tb: the item's tiles before this range
   };
   // Past the item's last tile a cursor keeps pointing at a valid tile of the
   // last range (kt * KT < n_keys always holds), so loads stay in bounds.
   auto advance = [&](Cursor& c) {
     if (++c.kt * KT >= c.R.n_keys) {
       c.kt = 0;
-      if (++c.ri < w.rng_count)
+      if (++c.ri < w.rng_count) {
+        c.tb += (c.R.n_keys + KT - 1) / KT;
         c.R = uniform_range(p.ranges[__builtin_amdgcn_readfirstlane(w.rng_begin + c.ri)]);  // scalar loads
-      else
+      } else {
         c.ok = 0;
+      }
     }
   };
 
@@ -228,13 +230,34 @@ __device__ __forceinline__ void tile_item(const TileParams& p, int item) {
   int vkeep[2][PAGED ? VPT : 1];  // paged V: keys of each chunk inside the range
   bool vfull[2] = {true, true};     // paged V: the whole tile lies inside the range
 
-  // Block ids of a tile: lane l (mod NB) loads the id of block l with a
-  // vector load.  Scalar loads would share the LDS wait counter (and return
-  // out of order), so every LDS wait would also wait for the block table.
-  auto fetch_idv = [&](const Cursor& c) -> int {
-    const int kbase = c.kt * KT, bi = lane & (NB - 1);
-    return p.block_table[c.R.kv_start + (kbase >> 4) + ((kbase + bi * kBlock < c.R.n_keys) ? bi : 0)];
-  };
+  // Paged: the block ids of every tile of the item are read once, at the
+  // start (thread u: tile u / NB, block u % NB; an item has at most
+  // kMaxItemTiles tiles, so one id per thread), into LDS; a step's loads then
+  // wait for no block-table read.  Blocks wholly past a range's end take the
+  // id of the tile's first block.  Lane l (mod NB) of a wavefront reads the
+  // id of block l of a tile.
+  __shared__ int32_t tile_ids[PAGED ? kMaxItemTiles * NB : 1];
+  static_assert(!PAGED || kMaxItemTiles * NB == kThreads, "one block id per thread");
+  if constexpr (PAGED) {
+    const int tile = tid / NB, bi = tid % NB;
+    if (tile < n_tiles) {
+      int64_t start = 0;
+      int kbase = 0, nk = 0;
+      for (int r = 0, tb = 0; r < w.rng_count; ++r) {
+        const RangeRec R = uniform_range(p.ranges[__builtin_amdgcn_readfirstlane(w.rng_begin + r)]);
+        const int nt = (R.n_keys + KT - 1) / KT;
+        if (tile >= tb && tile < tb + nt) {
+          start = R.kv_start;
+          kbase = (tile - tb) * KT;
+          nk = R.n_keys;
+        }
+        tb += nt;
+      }
+      tile_ids[tid] = p.block_table[start + (kbase >> 4) + ((kbase + bi * kBlock < nk) ? bi : 0)];
+    }
+    __syncthreads();
+  }
+  auto fetch_idv = [&](const Cursor& c) -> int { return tile_ids[(c.tb + c.kt) * NB + (lane & (NB - 1))]; };
   // Global -> registers, branch-free.  Packed rows past the range end are
   // read from the range's last row (the buffer may end there).  Paged slots
   // past the end are read as they are (their block exists: the block ids of
@@ -487,6 +510,8 @@ __device__ __forceinline__ void tile_item(const TileParams& p, int item) {
   };
 
   // Prologue: bundle 0 (K(0)) into LDS, bundles 1 and 2 into register sets.
+  // Bundle 1 is requested before K(0) is stored, so K(0), K(1) and V(0) are
+  // in flight together (a short item is a chain of load latencies).
   using Set0 = std::integral_constant<int, 0>;
   using Set1 = std::integral_constant<int, 1>;
   if constexpr (PAGED) {
@@ -494,22 +519,26 @@ __device__ __forceinline__ void tile_item(const TileParams& p, int item) {
     idv[1] = idk[1];
   }
   load_bundle(Set0{});  // bundle 0: K(0) (its V part re-reads tile 0, unused)
+  load_bundle(Set1{});  // bundle 1: K(1), V(0)
   store_k(Set0{}, Ks[0]);
   for (int i = tid; i < VEL / 8; i += kThreads) reinterpret_cast<uint4*>(Vt[1])[i] = make_uint4(0, 0, 0, 0);
-  load_bundle(Set1{});  // bundle 1: K(1), V(0)
   load_bundle(Set0{});  // bundle 2: K(2), V(1)
   __syncthreads();
 
   // Step t: leading half (waves 0-3): matrix phase, barrier, vector phase,
   // barrier.  Lagging half (waves 4-7): vector phase of step t-1's scores,
   // barrier, matrix phase, barrier.  Both halves pass the same barriers.
+  // The last step (t = n_tiles) stages nothing: bundle n_tiles + 1 holds no
+  // tile the item uses, and waiting for its loads would only add latency.
   if (wave < 4) {
     auto step = [&](auto xc, int t) {
       constexpr int X = decltype(xc)::value;
       mfma_phase(Ks[X], Vt[X ^ 1]);
       __syncthreads();
-      if (t < n_tiles) valu_phase(xc);  // tile t
-      staging(xc);
+      if (t < n_tiles) {
+        valu_phase(xc);  // tile t
+        staging(xc);
+      }
       __syncthreads();
     };
     for (int t = 0;;) {
@@ -522,7 +551,7 @@ __device__ __forceinline__ void tile_item(const TileParams& p, int item) {
     auto step = [&](auto xc, int t) {
       constexpr int X = decltype(xc)::value;
       if (t >= 1) valu_phase(std::integral_constant<int, X ^ 1>{});  // tile t-1
-      staging(xc);
+      if (t < n_tiles) staging(xc);
       __syncthreads();
       mfma_phase(Ks[X], Vt[X ^ 1]);
       __syncthreads();

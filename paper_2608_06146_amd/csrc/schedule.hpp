@@ -25,6 +25,8 @@ constexpr int kBlock = 16;  // paged KV block (tokens)
 constexpr int kPrivateCols = 16;  // columns of a private decode item (one wavefront)
 constexpr int kPrivateQueues = 8;  // decode: private item queues (one per XCD)
 constexpr int kBwdKeys = 128;     // keys of a backward key-major item (4 x 32)
+constexpr int kMaxItemKeys = 8192;  // decode: keys of a chunk (item) at most
+constexpr int kMaxItemTiles = kMaxItemKeys / kTileKeys;  // tiles of a paged tile item at most
 
 // Everything a tile kernel needs.  Pointers are device pointers.
 struct TileParams {
@@ -71,9 +73,8 @@ struct BwdParams {
 };
 
 struct CombineParams {
-  const int32_t* comb_ptr;   // [n_q * Hkv + 1]
-  const int32_t* comb_slot;
-  const int32_t* comb_rows;  // (row*Hkv + kvh) pairs to merge
+  const int32_t* comb_slot;  // partial slots, grouped by (row, KV head)
+  const int4* comb_rows;     // per merged pair: {row*Hkv + kvh, first, end, 0} into comb_slot
   int64_t n_rows;
   const float* part_o;
   const float* part_ml;

@@ -163,6 +163,9 @@ def _check_decode(segs, G, Hkv, chunk=0, read_once=False):
         assert w["col0"] + w["ncol"] <= w["ntok"] * G
         cols_of.setdefault(int(w["out_base"]), []).extend(range(w["col0"], w["col0"] + w["ncol"]))
         toks, cover = _item_coverage(ex, w, G)
+        if idx < ex["n_work_shared"]:  # a tile item stages the ids of at most 128 64-key tiles
+            rr = ex["ranges"][w["rng_begin"]: w["rng_begin"] + w["rng_count"]]
+            assert sum(-(-int(n) // 64) for n in rr["n_keys"]) <= 128
         for r in range(w["rng_begin"], w["rng_begin"] + w["rng_count"]):
             R = ex["ranges"][r]
             assert R["key_begin"] % 16 == 0
@@ -293,6 +296,8 @@ def test_plan_errors():
     assert _err(good, softmax_scale=float("inf")) == _lib.ERR_ARG
     assert _err(good, block_size=8) == _lib.ERR_ARG
     assert _err(good, max_chunk_keys=100) == _lib.ERR_ARG
+    assert _err(good, max_chunk_keys=8192 + 64) == _lib.ERR_ARG                            # chunk > 8192 keys
+    pa.TreePlan(good, **_desc(good, max_chunk_keys=8192))
     # paged: block table too short, block id outside the pool
     pg = _segs([(-1, 0, 20, 0, 0, 0), (0, 20, 5, 1, 2, 0)])
     pa.TreePlan(pg, **_desc(pg, block_size=16, num_kv_rows=8, block_table_host=np.arange(3)))
