@@ -51,6 +51,17 @@ TRACE_SUMMARY = os.path.join(ROOT, "profiles", f"kernel_trace_{PROFILE_TAG}.md")
 TRAFFIC_SUMMARY = os.path.join(ROOT, "profiles", f"hbm_traffic_{PROFILE_TAG}.txt")
 DECODE_KERNELS = ("decode_step_kernel<128>", "lse_combine_kernel<128, true, 8>")
 FORWARD_KERNEL = "tile_mfma_bf16_kernel<128, false, false>"
+COUNTER_SUMMARY = os.path.join(ROOT, "profiles", f"sq_counters_{PROFILE_TAG}.md")
+# SQ counter passes (at most 8 SQ counters each, plus GRBM_GUI_ACTIVE)
+SQ_PASSES = {
+    "sqA": "SQ_BUSY_CYCLES SQ_VALU_MFMA_BUSY_CYCLES SQ_WAVE_CYCLES SQ_WAIT_INST_LDS SQ_WAIT_ANY "
+           "SQ_ACTIVE_INST_LDS SQ_ACTIVE_INST_VALU SQ_ACTIVE_INST_ANY GRBM_GUI_ACTIVE",
+    "sqB": "SQ_LDS_BANK_CONFLICT SQ_LDS_IDX_ACTIVE SQ_INSTS_LDS SQ_LDS_ADDR_CONFLICT SQ_WAIT_INST_ANY "
+           "SQ_VALU_MFMA_COEXEC_CYCLES SQ_BUSY_CU_CYCLES SQ_WAVES GRBM_GUI_ACTIVE",
+    "sqC": "SQ_INSTS_MFMA SQ_INSTS_VALU SQ_INSTS_SALU SQ_INSTS_VMEM_RD SQ_INSTS_SMEM SQ_ACTIVE_INST_VMEM "
+           "SQ_ACTIVE_INST_SCA SQ_INSTS_BRANCH GRBM_GUI_ACTIVE",
+}
+SQ_KERNELS = (FORWARD_KERNEL, DECODE_KERNELS[0])
 BACKWARD_KERNELS = ("bwd_prep_kernel<128>", "bwd_dq_kernel<128>", "bwd_dkdv_kernel<128>", "bwd_finalize_kernel")
 COPY_KERNEL = "__amd_rocclr_copyBuffer"
 COPY_BYTES = 1 << 30
@@ -196,6 +207,78 @@ def measured_traffic():
     return float(kv["decode_call_bytes"]), float(kv["forward_launch_bytes"])
 
 
+def measured_counters():
+    """Per-kernel derived SQ counter figures from the committed summary, or
+    {} when it was taken on other sources."""
+    try:
+        with open(COUNTER_SUMMARY) as fh:
+            lines = [ln.strip() for ln in fh if ln.startswith("value ")]
+            fh.seek(0)
+            tag = next((ln.split(":", 1)[1].strip() for ln in fh if ln.startswith("sources_sha256:")), None)
+    except OSError:
+        return {}
+    if tag != source_digest():
+        return {}
+    out = {}
+    for ln in lines:  # value <kernel> | <name>: <number>
+        kern, rest = ln[len("value "):].split(" | ", 1)
+        name, val = rest.split(":", 1)
+        out.setdefault(kern.strip(), {})[name.strip()] = float(val)
+    return out
+
+
+def summarize_counters(d: str) -> None:
+    """Derived SQ figures per kernel from the three counter passes.  Busy
+    fractions divide by the kernel's cycles: GRBM_GUI_ACTIVE sums the 8 XCDs'
+    graphics-busy cycles, so a dispatch lasts GRBM_GUI_ACTIVE / 8 cycles, on
+    256 CUs x 4 SIMDs; SQ_*_CYCLES-type counters of the SQ block count per
+    SIMD (MFMA busy) or per CU (LDS active) over the whole chip."""
+    import csv
+    import glob
+    import statistics
+    vals = {}
+    dur = {}
+    for p in SQ_PASSES:
+        for f in glob.glob(os.path.join(d, p, "**", "*counter_collection.csv"), recursive=True):
+            with open(f) as fh:
+                for r in csv.DictReader(fh):
+                    k = short_kernel_name(r["Kernel_Name"])
+                    vals.setdefault(k, {}).setdefault(r["Counter_Name"], []).append(float(r["Counter_Value"]))
+                    dur.setdefault(k, []).append((int(r["End_Timestamp"]) - int(r["Start_Timestamp"])) * 1e-3)
+    lines = ["# SQ counters: bench.py default workloads (packed forward, 8 pages; concurrent decode, 64 pages)", "",
+             "Commands (GPU host, repository root as $R): as in kernel_trace_" + PROFILE_TAG + ".md; counters of",
+             "each pass (one rocprofv3 run per pass, at most 8 SQ counters):", ""]
+    for p, c in SQ_PASSES.items():
+        lines.append(f"- {p}: `{c}`")
+    lines += ["", f"sources_sha256: {source_digest()}", ""]
+    for k in SQ_KERNELS:
+        if k not in vals:
+            continue
+        v = {c: statistics.mean(x) for c, x in vals[k].items()}
+        cyc = v["GRBM_GUI_ACTIVE"] / 8.0  # cycles of one dispatch
+        us = statistics.mean(dur[k])
+        mf = max(v.get("SQ_INSTS_MFMA", 0.0), 1.0)
+        derived = {
+            "clock_ghz": cyc / (us * 1e3),
+            "mfma_busy": v["SQ_VALU_MFMA_BUSY_CYCLES"] / (1024 * cyc),
+            "valu_insts_per_mfma": v["SQ_INSTS_VALU"] / mf,
+            "salu_insts_per_mfma": v["SQ_INSTS_SALU"] / mf,
+            "lds_insts_per_mfma": v["SQ_INSTS_LDS"] / mf,
+            "lds_active": v["SQ_LDS_IDX_ACTIVE"] / (256 * cyc),
+            "lds_bank_conflict_per_active": v["SQ_LDS_BANK_CONFLICT"] / max(v["SQ_LDS_IDX_ACTIVE"], 1.0),
+            "wait_any_per_wave_cycle": v["SQ_WAIT_ANY"] / max(v["SQ_WAVE_CYCLES"], 1.0),
+            "valu_active_per_wave_cycle": v["SQ_ACTIVE_INST_VALU"] / max(v["SQ_WAVE_CYCLES"], 1.0),
+        }
+        lines += [f"## `{k}`", "", f"dispatches: {len(vals[k]['GRBM_GUI_ACTIVE'])}, mean duration under counters "
+                  f"{us:.1f} us", "", "| counter | mean per dispatch |", "|---|---|"]
+        lines += [f"| {c} | {x:.4g} |" for c, x in sorted(v.items())]
+        lines += ["", "| derived | value |", "|---|---|"] + [f"| {n} | {x:.3f} |" for n, x in derived.items()]
+        lines += [""] + [f"value {k} | {n}: {x:.5g}" for n, x in derived.items()] + [""]
+    with open(COUNTER_SUMMARY, "w") as fh:
+        fh.write("\n".join(lines))
+    print(f"wrote {COUNTER_SUMMARY}")
+
+
 PROFILE_COMMANDS = """\
     R=<repository root>; OUT=<output directory>; cd /tmp && export TMPDIR=/tmp
     rocprofv3 --kernel-trace --stats -d $OUT/trace -o bench -- \\
@@ -206,6 +289,10 @@ PROFILE_COMMANDS = """\
         python3 $R/bench.py --steps 5 --warmup 1 --no-cpu-baseline --no-baselines --driver-steps 0 --no-secondary --no-cold
     rocprofv3 --pmc FETCH_SIZE -f csv -d $OUT/copy_fetch -o c -- python3 $R/bench.py --calibrate-copy
     rocprofv3 --pmc WRITE_SIZE -f csv -d $OUT/copy_write -o c -- python3 $R/bench.py --calibrate-copy
+    for P in sqA sqB sqC; do   # counters of each pass: SQ_PASSES in bench.py
+      rocprofv3 --pmc <SQ_PASSES[$P]> --kernel-include-regex "tile_mfma|decode_step" -f csv -d $OUT/$P -o p -- \\
+          python3 $R/bench.py --steps 3 --warmup 1 --no-cpu-baseline --no-baselines --no-backward --driver-steps 0 --no-secondary --no-cold
+    done
     python3 $R/bench.py --summarize-profile $OUT
 """
 
@@ -218,6 +305,9 @@ def summarize_profile(d: str) -> None:
     import sqlite3
     import statistics
 
+    if not os.path.isdir(os.path.join(d, "trace")):  # counter passes only
+        summarize_counters(d)
+        return
     db = sorted(glob.glob(os.path.join(d, "trace", "**", "*.db"), recursive=True))[0]
     con = sqlite3.connect(db)
     rows = con.execute("select name, count(*), avg(duration), min(duration), max(duration), max(lds_size), "
@@ -276,6 +366,8 @@ def summarize_profile(d: str) -> None:
     with open(TRAFFIC_SUMMARY, "w") as fh:
         fh.write("\n".join(tl))
     print(f"wrote {TRACE_SUMMARY} and {TRAFFIC_SUMMARY}")
+    if any(os.path.isdir(os.path.join(d, p)) for p in SQ_PASSES):
+        summarize_counters(d)
 
 
 # ---------------------------------------------------------------- decode leg
@@ -641,7 +733,8 @@ def run_forward(args, torch, np, syn, pa, dev):
         "kernel_tflops": flops / (k_ms * 1e-3) / 1e12, "plan_ms": plan_ms,
         "roofline": {"bound": "mfma", "achieved": flops / (k_ms * 1e-3) / 1e12, "peak": BF16_PEAK_TFLOPS,
                      "unit": "TFLOP/s", "frac": flops / (k_ms * 1e-3) / 1e12 / BF16_PEAK_TFLOPS,
-                     "traffic": measured_traffic()[1], "kernel": FORWARD_KERNEL},
+                     "traffic": measured_traffic()[1], "kernel": FORWARD_KERNEL,
+                     "mfma_busy": measured_counters().get(FORWARD_KERNEL, {}).get("mfma_busy")},
         "backward": bwd,
         "baselines": base,
     }
