@@ -497,62 +497,130 @@ def run_decode(args, torch, np, syn, pa, dev, name=None, pool_gib=None, steps=No
 
 # ---------------------------------------------------------------- session (step driver) leg
 
+class _DriverSet:
+    """A DecodeSession holding some pages of the decode workload, built as
+    the decoding loop builds them: prefix prefill, layout stream, then the
+    content streams at their forks (App. E loop), plus its step buffers."""
+
+    def __init__(self, args, torch, np, syn, pa, dev, wl, pages, steps, seed, stream=None):
+        Hq, Hkv, d = wl.num_heads_q, wl.num_heads_kv, wl.head_dim
+        nb = syn.count_blocks(pages)
+        rows0 = syn.count_queries(pages)
+        n_pool = int(nb * 1.25) + (steps + args.warmup + 2) * (rows0 // 16 + 64) + 4096
+        self.torch, self.np = torch, np
+        self.kc = torch.empty((n_pool, Hkv, d // 8, 16, 8), dtype=torch.bfloat16, device=dev)
+        self.vc = torch.empty((n_pool, Hkv, d, 16), dtype=torch.bfloat16, device=dev)
+        self.bt = torch.full((4 * n_pool,), -1, dtype=torch.int32, device=dev)
+        sess = pa.DecodeSession(Hq, Hkv, d, n_pool, "bf16", k_cache=self.kc, v_cache=self.vc, block_table=self.bt,
+                                max_chunk_keys=args.decode_chunk, target_workgroups=args.decode_target_wg)
+        self.sess, self.n_pool = sess, n_pool
+        gen = torch.Generator(device=dev)
+        gen.manual_seed(seed * 1000003 + 17)
+
+        def rows(n, h):
+            return torch.randn((n, h, d), generator=gen, device=dev, dtype=torch.float32).to(torch.bfloat16)
+
+        def build_step(n_new, n_q):
+            nk, nq, _ = sess.prepare(np.asarray(n_new, np.int32), np.asarray(n_q, np.int32))
+            sess.launch(rows(nq, Hq) if nq else None, rows(nk, Hkv), rows(nk, Hkv))
+            torch.cuda.synchronize()
+
+        roots = [sess.open(-1, 0) for _ in pages]
+        build_step([p.prefix_len for p in pages], [0] * len(pages))
+        lay = [sess.open(r, p.prefix_len) for r, p in zip(roots, pages)]
+        for r in roots:
+            sess.close(r)
+        build_step([p.stream_len - 1 for p in pages], [0] * len(pages))
+        self.kind = {x: ("layout", i) for i, x in enumerate(lay)}
+        for i, p in enumerate(pages):
+            for b in p.branches:
+                self.kind[sess.open(lay[i], b.fork)] = ("content", i)
+        ids = [int(x) for x in sess.view(block_table=False)["row_id"]]
+        branch_len = {i: iter([b.length - 1 for b in p.branches]) for i, p in enumerate(pages)}
+        build_step([0 if self.kind[x][0] == "layout" else next(branch_len[self.kind[x][1]]) for x in ids],
+                   [0] * len(ids))
+        self.lay_len = {x: p.stream_len - 1 for x, p in zip(lay, pages)}
+        self.live = ids  # open streams, ascending id (the session's row order)
+        self.q_buf = rows(rows0 + 4096, Hq)
+        self.k_buf = rows(rows0 + 4096, Hkv)
+        self.v_buf = rows(rows0 + 4096, Hkv)
+        self.o_buf = torch.empty_like(self.q_buf)
+        self.l_buf = torch.empty(self.q_buf.shape[:2], dtype=torch.float32, device=dev)
+        self.rng = np.random.default_rng(seed + 5)
+        self.done = torch.cuda.Event()
+        self.stream = stream  # None: the current stream
+
+    def prepare_launch(self):
+        """Host plan of the step, then its launch; returns (rows, prepare s, launch s)."""
+        t0 = time.perf_counter()
+        nk, nq, _ = self.sess.prepare()
+        t1 = time.perf_counter()
+        if nq > self.q_buf.shape[0]:
+            raise RuntimeError("driver: more live streams than the step buffers hold")
+        if self.stream is None:
+            self.sess.launch(self.q_buf[:nq], self.k_buf[:nk], self.v_buf[:nk], out=self.o_buf[:nq],
+                             lse=self.l_buf[:nq])
+            self.done.record()
+        else:
+            with self.torch.cuda.stream(self.stream):
+                self.sess.launch(self.q_buf[:nq], self.k_buf[:nk], self.v_buf[:nk], out=self.o_buf[:nq],
+                                 lse=self.l_buf[:nq])
+                self.done.record()
+        return nq, t1 - t0, time.perf_counter() - t1
+
+    def events(self):
+        """The step's events: a content stream ends with probability 1/512, a
+        layout stream opens a content stream with probability 24/512."""
+        sess, np = self.sess, self.np
+        for x in self.lay_len:
+            self.lay_len[x] += 1
+        u = self.rng.random(len(self.live))
+        ended, born = set(), []
+        for j in np.nonzero(u < 24.0 / 512)[0]:     # only these streams can have an event
+            x = self.live[j]
+            k_, pg = self.kind[x]
+            if k_ == "content" and u[j] < 1.0 / 512:
+                sess.close(x)
+                ended.add(x)
+            elif k_ == "layout":
+                c = sess.open(x, self.lay_len[x])
+                self.kind[c] = ("content", pg)
+                born.append(c)
+        for x in ended:
+            self.live.remove(x)
+        self.live += born
+
+    def free_blocks(self):
+        return int(self.sess.view(block_table=False)["free_blocks"])
+
+    def destroy(self):
+        self.sess.destroy()
+        del self.kc, self.vc, self.bt, self.q_buf, self.k_buf, self.v_buf, self.o_buf
+
+
 def run_driver(args, torch, np, syn, pa, dev, wl):
-    """Masked parallel decoding steps through a DecodeSession (App. E loop):
-    the decode workload's streams are built in the session (prefix prefill,
-    layout stream, 24 content streams per page at their forks), then each
-    timed step prepares (host plan), launches (append of one new token per
+    """Masked parallel decoding steps through DecodeSessions (App. E loop).
+    Each step prepares (host plan), launches (append of one new token per
     live stream + attention) and waits for the outputs, as a decoding loop
-    must before it samples; then the step's events are applied: a content
-    stream ends with probability 1/512 (mean length 512, as U[1,1024]), a
-    layout stream opens a content stream with probability 24/512, keeping
-    about 24 per page.  Reported: per-step wall time split into prepare /
-    launch / wait / events, and tokens/s with and without the host work."""
-    Hq, Hkv, d = wl.num_heads_q, wl.num_heads_kv, wl.head_dim
+    must before it samples; then the step's events are applied (content
+    streams end with probability 1/512, i.e. mean length 512 as U[1,1024];
+    layout streams open content streams with probability 24/512, keeping
+    about 24 per page).
+    serial: one session holds every page; per step prepare -> launch -> wait
+      -> events, so the host work and the GPU work add up.
+    pipelined: two sessions hold half the pages each and alternate, a
+      serving loop's two micro-batches, each on a stream of its own (default
+      priority): while the GPU runs one session's step the host waits for,
+      samples and prepares the other's, so the host work hides behind the
+      GPU, and the two sessions' kernels may overlap on the GPU (each
+      session still waits for its own outputs before its next step).
+    Reported: per-step wall time split into prepare / launch / wait /
+    events, and tokens/s with and without the host work."""
     steps = args.driver_steps
-    nb = syn.count_blocks(wl.pages)
-    rows0 = syn.count_queries(wl.pages)
-    n_pool = int(nb * 1.25) + (steps + args.warmup + 2) * (rows0 // 16 + 64) + 4096
-    kc = torch.empty((n_pool, Hkv, d // 8, 16, 8), dtype=torch.bfloat16, device=dev)
-    vc = torch.empty((n_pool, Hkv, d, 16), dtype=torch.bfloat16, device=dev)
-    bt = torch.full((4 * n_pool,), -1, dtype=torch.int32, device=dev)
-    sess = pa.DecodeSession(Hq, Hkv, d, n_pool, "bf16", k_cache=kc, v_cache=vc, block_table=bt,
-                            max_chunk_keys=args.decode_chunk, target_workgroups=args.decode_target_wg)
-    gen = torch.Generator(device=dev)
-    gen.manual_seed(args.seed * 1000003 + 17)
-
-    def rows(n, h):
-        return torch.randn((n, h, d), generator=gen, device=dev, dtype=torch.float32).to(torch.bfloat16)
-
-    def build_step(n_new, n_q):
-        nk, nq, _ = sess.prepare(np.asarray(n_new, np.int32), np.asarray(n_q, np.int32))
-        sess.launch(rows(nq, Hq) if nq else None, rows(nk, Hkv), rows(nk, Hkv))
-        torch.cuda.synchronize()
-
-    roots = [sess.open(-1, 0) for _ in wl.pages]
-    build_step([p.prefix_len for p in wl.pages], [0] * len(wl.pages))
-    lay = [sess.open(r, p.prefix_len) for r, p in zip(roots, wl.pages)]
-    for r in roots:
-        sess.close(r)
-    build_step([p.stream_len - 1 for p in wl.pages], [0] * len(wl.pages))
-    kind = {x: ("layout", i) for i, x in enumerate(lay)}
-    for i, p in enumerate(wl.pages):
-        for b in p.branches:
-            kind[sess.open(lay[i], b.fork)] = ("content", i)
-    ids = [int(x) for x in sess.view(block_table=False)["row_id"]]
-    branch_len = {i: iter([b.length - 1 for b in p.branches]) for i, p in enumerate(wl.pages)}
-    build_step([0 if kind[x][0] == "layout" else next(branch_len[kind[x][1]]) for x in ids], [0] * len(ids))
-    lay_len = {x: p.stream_len - 1 for x, p in zip(lay, wl.pages)}
-    live = ids  # open streams, ascending id (the session's row order)
-    log(f"driver: session holds {len(live)} streams, {sess.view(block_table=False)['free_blocks']} of {n_pool} "
-        "blocks free")
-
-    q_buf = rows(rows0 + 4096, Hq)
-    k_buf = rows(rows0 + 4096, Hkv)
-    v_buf = rows(rows0 + 4096, Hkv)
-    o_buf = torch.empty_like(q_buf)
-    l_buf = torch.empty(q_buf.shape[:2], dtype=torch.float32, device=dev)
-    rng = np.random.default_rng(args.seed + 5)
+    res = {}
+    # ---- serial: one session, all pages
+    D = _DriverSet(args, torch, np, syn, pa, dev, wl, wl.pages, steps, args.seed)
+    log(f"driver: session holds {len(D.live)} streams, {D.free_blocks()} of {D.n_pool} blocks free")
     rec = []
     ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(steps)]
     for b, a in ev:
@@ -563,40 +631,19 @@ def run_driver(args, torch, np, syn, pa, dev, wl):
         timed = s >= args.warmup
         if timed:
             pa.set_kernel_events(*ev[s - args.warmup])
-        t0 = time.perf_counter()
-        nk, nq, _ = sess.prepare()
-        t1 = time.perf_counter()
-        if nq > q_buf.shape[0]:
-            raise RuntimeError("driver: more live streams than the step buffers hold")
-        sess.launch(q_buf[:nq], k_buf[:nk], v_buf[:nk], out=o_buf[:nq], lse=l_buf[:nq])
+        nq, t_prep, t_launch = D.prepare_launch()
         t2 = time.perf_counter()
-        torch.cuda.synchronize()
+        D.done.synchronize()
         t3 = time.perf_counter()
-        for x in lay_len:
-            lay_len[x] += 1
-        u = rng.random(len(live))
-        ended, born = set(), []
-        for j in np.nonzero(u < 24.0 / 512)[0]:     # only these streams can have an event
-            x = live[j]
-            k_, pg = kind[x]
-            if k_ == "content" and u[j] < 1.0 / 512:
-                sess.close(x)
-                ended.add(x)
-            elif k_ == "layout":
-                c = sess.open(x, lay_len[x])
-                kind[c] = ("content", pg)
-                born.append(c)
-        for x in ended:
-            live.remove(x)
-        live += born
+        D.events()
         t4 = time.perf_counter()
         if timed:
             pa.set_kernel_events()
-            rec.append((nq, t1 - t0, t2 - t1, t3 - t2, t4 - t3))
+            rec.append((nq, t_prep, t_launch, t3 - t2, t4 - t3))
     gpu = [b.elapsed_time(a) for b, a in ev]
     n_rows = sum(r[0] for r in rec)
     wall = sum(r[1] + r[2] + r[3] + r[4] for r in rec)
-    res = {
+    res.update({
         "steps": steps, "rows_per_step": n_rows / steps,
         "step_ms": wall * 1e3 / steps,
         "prepare_ms": 1e3 * statistics.mean(r[1] for r in rec),
@@ -606,11 +653,53 @@ def run_driver(args, torch, np, syn, pa, dev, wl):
         "gpu_ms": statistics.mean(gpu),
         "tokens_per_s": n_rows / wall,
         "tokens_per_s_gpu": n_rows / (sum(gpu) * 1e-3),
-        "pool_blocks": n_pool, "free_blocks_end": int(sess.view(block_table=False)["free_blocks"]),
-    }
-    sess.destroy()
-    del kc, vc, bt, q_buf, k_buf, v_buf, o_buf
+        "pool_blocks": D.n_pool, "free_blocks_end": D.free_blocks(),
+    })
+    D.destroy()
     torch.cuda.empty_cache()
+
+    # ---- pipelined: two sessions of half the pages each, alternating
+    half = len(wl.pages) // 2
+    sets = [_DriverSet(args, torch, np, syn, pa, dev, wl, wl.pages[:half], steps, args.seed, torch.cuda.Stream()),
+            _DriverSet(args, torch, np, syn, pa, dev, wl, wl.pages[half:], steps, args.seed + 1, torch.cuda.Stream())]
+    torch.cuda.synchronize()
+    rows_done = 0
+    host = {"prepare": 0.0, "launch": 0.0, "events": 0.0, "wait": 0.0}
+    t_start = None
+    for X in sets:  # first step of each session in flight
+        X.prepare_launch()
+    for s in range(args.warmup + steps):
+        if s == args.warmup:
+            t_start = time.perf_counter()
+            rows_done = 0
+            host = dict.fromkeys(host, 0.0)
+        for X in sets:
+            t0 = time.perf_counter()
+            X.done.synchronize()   # this session's step is done: sample, apply its events
+            t1 = time.perf_counter()
+            X.events()
+            t2 = time.perf_counter()
+            nq, t_prep, t_launch = X.prepare_launch()
+            rows_done += nq
+            host["wait"] += t1 - t0
+            host["events"] += t2 - t1
+            host["prepare"] += t_prep
+            host["launch"] += t_launch
+    for X in sets:
+        X.done.synchronize()
+    wall = time.perf_counter() - t_start
+    # rows launched in the timed loop; the last launches finish inside `wall`
+    res["pipelined"] = {
+        "sessions": 2, "pages_per_session": [half, len(wl.pages) - half], "steps": steps,
+        "rows_per_step": rows_done / steps, "step_ms": wall * 1e3 / steps,
+        "prepare_ms": 1e3 * host["prepare"] / steps, "launch_ms": 1e3 * host["launch"] / steps,
+        "events_ms": 1e3 * host["events"] / steps, "wait_ms": 1e3 * host["wait"] / steps,
+        "tokens_per_s": rows_done / wall, "streams": "one per session (default priority)",
+    }
+    for X in sets:
+        X.destroy()
+    torch.cuda.empty_cache()
+
     return res
 
 

@@ -114,8 +114,71 @@ struct Scratch {
   std::vector<Piece> pieces;
   std::vector<std::pair<size_t, int32_t>> parts;
   std::vector<padoc::WorkRec> sitems, pitems, tmp;
+  std::vector<std::tuple<int32_t, int64_t, int32_t, uint32_t>> xkeys;
+  std::vector<uint32_t> xgroup, xorder;
+  std::vector<int64_t> xcost;
 };
 thread_local Scratch t_scratch;
+
+// Tile items that read the same keys -- the column groups of one key chunk
+// of one KV head -- are placed on one XCD: workgroup b runs on XCD b % 8,
+// each XCD has an L2 cache of its own, and the tile items run at the same
+// time, so the K/V tiles one of them reads are L2 hits for the others.
+// Groups go to the XCDs largest first, each to the least loaded; within an
+// XCD items keep their (cost) order; a position whose XCD has no item left
+// takes one from the XCD with the most items left.
+void xcd_group(std::vector<padoc::WorkRec>& w, const std::vector<padoc::RangeRec>& ranges, Scratch& S) {
+  constexpr int kXcd = 8;
+  const uint32_t n = (uint32_t)w.size();
+  if (n <= 1) return;
+  auto& keys = S.xkeys;
+  keys.resize(n);
+  for (uint32_t i = 0; i < n; ++i) {
+    const padoc::RangeRec& r = ranges[w[i].rng_begin];
+    keys[i] = {w[i].kvh, r.kv_start, r.key_begin, i};
+  }
+  std::sort(keys.begin(), keys.end());
+  auto& grp = S.xgroup;  // group of item i
+  auto& cost = S.xcost;  // cost of group g
+  grp.assign(n, 0);
+  cost.clear();
+  for (uint32_t k = 0; k < n; ++k) {
+    const bool same = k > 0 && std::get<0>(keys[k]) == std::get<0>(keys[k - 1]) &&
+                      std::get<1>(keys[k]) == std::get<1>(keys[k - 1]) && std::get<2>(keys[k]) == std::get<2>(keys[k - 1]);
+    if (!same) cost.push_back(0);
+    const uint32_t i = std::get<3>(keys[k]);
+    grp[i] = (uint32_t)cost.size() - 1;
+    cost.back() += w[i].cost;
+  }
+  const uint32_t ng = (uint32_t)cost.size();
+  auto& order = S.xorder;  // groups, costliest first
+  order.resize(ng);
+  for (uint32_t g = 0; g < ng; ++g) order[g] = g;
+  std::stable_sort(order.begin(), order.end(), [&](uint32_t a, uint32_t b) { return cost[a] > cost[b]; });
+  int64_t load[kXcd] = {};
+  std::vector<int32_t> xcd_of(ng);
+  for (uint32_t g : order) {
+    const int x = (int)(std::min_element(load, load + kXcd) - load);
+    xcd_of[g] = x;
+    load[x] += cost[g];
+  }
+  std::vector<std::vector<uint32_t>> lists(kXcd);
+  for (uint32_t i = 0; i < n; ++i) lists[xcd_of[grp[i]]].push_back(i);  // items keep their order
+  size_t next[kXcd] = {};
+  S.tmp.assign(w.begin(), w.end());
+  for (uint32_t p = 0; p < n; ++p) {
+    int x = (int)(p % kXcd);
+    if (next[x] == lists[x].size()) {
+      size_t most = 0;
+      for (int y = 0; y < kXcd; ++y)
+        if (lists[y].size() - next[y] > most) {
+          most = lists[y].size() - next[y];
+          x = y;
+        }
+    }
+    w[p] = S.tmp[lists[x][next[x]++]];
+  }
+}
 
 class Builder {
  public:
@@ -136,6 +199,19 @@ class Builder {
   std::vector<int32_t>& vlim;
   // Tokens of the last emit_ranges call that see at least one key.
   std::vector<char>& sees;
+
+  // visible() for a task of one private segment's query tokens: the only
+  // private segment they see is their own (an ancestor whose keys they see
+  // is seen by another segment's queries, so it is shared), with the limit
+  // position + 1 of each token.
+  void visible_own(const Task& task, std::vector<VisRange>& out) {
+    VisRange v{tseg[task.begin], 0, (int64_t)vlim.size()};
+    for (int32_t i = task.begin; i < task.begin + task.count; ++i) {
+      vlim.push_back(tpos[i] + 1);
+      v.n_keys = std::max(v.n_keys, tpos[i] + 1);
+    }
+    out.push_back(v);
+  }
 
   // Appends to `out` the segments visible to any token of `task` for which
   // include(t) holds, in ascending segment order.
@@ -533,7 +609,7 @@ void build_decode(padoc_plan& P, Builder& B, const AncList& anc, const padoc_tre
     svis_at.push_back(svis.size());
   }
   for (const Task& t : ptasks) {
-    B.visible(t, priv, pvis);
+    B.visible_own(t, pvis);
     const int64_t splits = ceil_div((int64_t)t.count * G, kPrivateCols);
     for (size_t r = pvis_at.back(); r < pvis.size(); ++r) total_p += round_up(pvis[r].n_keys, 32) * P.Hkv * splits;
     pvis_at.push_back(pvis.size());
@@ -659,9 +735,49 @@ void build_decode(padoc_plan& P, Builder& B, const AncList& anc, const padoc_tre
   }
   for (size_t i = 0; i < ptasks.size(); ++i) {
     const int32_t tb = B.add_tokens(ptasks[i]);
-    cut_emit(ptasks[i], tb, pvis, pvis_at[i], pvis_at[i + 1], CHp, kPrivateCols, pitems);
+    if (ptasks[i].count != 1) {
+      cut_emit(ptasks[i], tb, pvis, pvis_at[i], pvis_at[i + 1], CHp, kPrivateCols, pitems);
+      continue;
+    }
+    // One query token (the usual decode step): what cut_emit makes of its
+    // one range [0, n) -- chunks of CHp keys, each fully visible (no
+    // limits), one partial per KV head -- written out directly.
+    const VisRange& v = pvis[pvis_at[i]];
+    const padoc_segment& sg = P.seg[v.t];
+    for (int32_t kb = 0; kb < v.n_keys; kb += (int32_t)CHp) {
+      const int32_t take = (int32_t)std::min<int64_t>(v.n_keys - kb, CHp);
+      padoc::RangeRec rr{};
+      rr.kv_start = sg.kv_off + kb / P.block_size;
+      rr.n_keys = take;
+      rr.min_lim = take;
+      rr.lim_off = -1;
+      rr.seg = v.t;
+      rr.key_begin = kb;
+      const int32_t rb = (int32_t)P.ranges.size();
+      P.ranges.push_back(rr);
+      const int32_t cost = 1 + (int32_t)ceil_div(take, P.tile_keys);
+      for (int32_t kvh = 0; kvh < P.Hkv; ++kvh) {
+        const int32_t base = (int32_t)P.n_slots;
+        parts.push_back({(size_t)P.toks[tb] * P.Hkv + kvh, base});
+        P.n_slots += G;
+        for (int32_t c0 = 0; c0 < G; c0 += kPrivateCols) {
+          padoc::WorkRec w{};
+          w.tok_begin = tb;
+          w.ntok = 1;
+          w.rng_begin = rb;
+          w.rng_count = 1;
+          w.kvh = kvh;
+          w.out_base = base;
+          w.cost = cost;
+          w.col0 = c0;
+          w.ncol = std::min(kPrivateCols, G - c0);
+          pitems.push_back(w);
+        }
+      }
+    }
   }
   sort_by_cost(sitems, S.tmp);
+  xcd_group(sitems, P.ranges, S);
   sort_by_cost(pitems, S.tmp);
   P.work.reserve(sitems.size() + pitems.size());
   P.work.assign(sitems.begin(), sitems.end());
@@ -733,22 +849,29 @@ void serialise(padoc_plan& P) {
   P.off_part_o = align256(blob_bytes);
   P.off_part_ml = align256(P.off_part_o + (size_t)P.n_slots * P.D * 4);
   P.ws_bytes = std::max<size_t>(256, align256(P.off_part_ml + (size_t)P.n_slots * 8));
-  P.blob.assign(blob_bytes, 0);
-  put(P.blob, P.off_work, P.work);
-  put(P.blob, P.off_ranges, P.ranges);
-  put(P.blob, P.off_lims, P.lims);
-  put(P.blob, P.off_toks, P.toks);
-  put(P.blob, P.off_comb_slot, P.comb_slot);
+  // Every byte is written once: the sections, the zero padding after each
+  // (up to the next 256-byte offset) and the zeroed queue counters (a plan
+  // rebuilt every decode step does not clear the whole blob first).
+  P.blob.resize(blob_bytes);
+  unsigned char* b = P.blob.data();
+  auto section = [&](size_t off, const void* src, size_t bytes, size_t end) {
+    if (bytes) std::memcpy(b + off, src, bytes);
+    std::memset(b + off + bytes, 0, end - off - bytes);
+  };
+  section(P.off_work, P.work.data(), P.work.size() * sizeof(padoc::WorkRec), P.off_ranges);
+  section(P.off_ranges, P.ranges.data(), P.ranges.size() * sizeof(padoc::RangeRec), P.off_lims);
+  section(P.off_lims, P.lims.data(), P.lims.size() * 4, P.off_toks);
+  section(P.off_toks, P.toks.data(), P.toks.size() * 4, P.off_comb_slot);
+  section(P.off_comb_slot, P.comb_slot.data(), P.comb_slot.size() * 4, P.off_comb_rows);
   // merged pairs as device records {row*Hkv + kvh, first, end, 0}: the
   // combine kernel finds a pair and its slot list with one load
-  std::vector<int32_t> rec(P.comb_rows.size() * 4, 0);
+  int32_t* rec = reinterpret_cast<int32_t*>(b + P.off_comb_rows);
   for (size_t i = 0; i < P.comb_rows.size(); ++i) {
     const int32_t rk = P.comb_rows[i];
-    rec[4 * i] = rk;
-    rec[4 * i + 1] = P.comb_ptr[rk];
-    rec[4 * i + 2] = P.comb_ptr[rk + 1];
+    const int32_t r4[4] = {rk, P.comb_ptr[rk], P.comb_ptr[rk + 1], 0};
+    std::memcpy(rec + 4 * i, r4, sizeof r4);
   }
-  put(P.blob, P.off_comb_rows, rec);
+  std::memset(b + P.off_comb_rows + P.comb_rows.size() * 16, 0, blob_bytes - P.off_comb_rows - P.comb_rows.size() * 16);
 }
 
 }  // namespace
