@@ -335,18 +335,27 @@ __device__ __forceinline__ void tile_item(const TileParams& p, int item) {
   Cursor Lk{0, 0, R0, 1, 0};
   Cursor Lv = Lk;
   int idk[2] = {0, 0}, idv[2] = {0, 0};  // [slot]: block ids of a K / V tile
-  auto load_bundle = [&](auto xc) {
+  // In two parts (K, then V), so a step can spread them over its MFMAs.
+  Cursor nk = Lk;
+  auto load_bundle_k = [&](auto xc) {
     constexpr int X = decltype(xc)::value;
-    Cursor nk = Lk;
+    nk = Lk;
     advance(nk);
     if constexpr (PAGED) {
       idk[X] = fetch_idv(nk);
       idv[X] = fetch_idv(Lk);
     }
     load_k(xc, Lk, idk[X ^ 1]);
+  };
+  auto load_bundle_v = [&](auto xc) {
+    constexpr int X = decltype(xc)::value;
     load_v(xc, Lv, idv[X ^ 1]);
     Lv = Lk;
     Lk = nk;
+  };
+  auto load_bundle = [&](auto xc) {
+    load_bundle_k(xc);
+    load_bundle_v(xc);
   };
 
   // Compute cursor (tile of the next S product) and this column's limit
@@ -440,7 +449,7 @@ __device__ __forceinline__ void tile_item(const TileParams& p, int item) {
   // nothing; after the last tile the S product reads a stale stage and its
   // result is never used.
   constexpr int NPV = 4 * NDB, NMF = NPV + 2 * NKK, kPrefetch = PAGED ? 6 : 8;
-  auto mfma_phase = [&](const uint16_t* ks, const uint16_t* vt) {
+  auto mfma_phase = [&](const uint16_t* ks, const uint16_t* vt, auto&& hook) {
     // fragment of MFMA i: PV key group g = i / NDB (keys (g/2)*32 + 16(g%2)
     // + [0,16)) and d block i % NDB; then S K-slice kk = j / 2 of half j % 2
     auto frag = [&](int i) -> bf16x8_t {
@@ -466,19 +475,20 @@ __device__ __forceinline__ void tile_item(const TileParams& p, int item) {
       for (int e = 0; e < 16; ++e) S[mb][e] = 0.f;
     // the scheduler may not sink the reads back towards their uses
     __builtin_amdgcn_sched_barrier(0);
-#pragma unroll
-    for (int i = 0; i < NMF; ++i) {
+    static_for<NMF>([&](auto ic) {
+      constexpr int i = decltype(ic)::value;
       const bf16x8_t a = f[i % kPrefetch];
-      if (i < NPV) {
-        const int g = i / NDB, db = i % NDB;
+      if constexpr (i < NPV) {
+        constexpr int g = i / NDB, db = i % NDB;
         acc[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, P[g >> 1][g & 1], acc[db], 0, 0, 0);
       } else {
-        const int j = i - NPV, kk = j >> 1, mb = j & 1;
+        constexpr int j = i - NPV, kk = j >> 1, mb = j & 1;
         S[mb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, bq[kk], S[mb], 0, 0, 0);
       }
-      if (i + kPrefetch < NMF) f[i % kPrefetch] = frag(i + kPrefetch);
+      if constexpr (i + kPrefetch < NMF) f[i % kPrefetch] = frag(i + kPrefetch);
+      hook(ic);  // work placed between this MFMA and the next
       __builtin_amdgcn_sched_barrier(0);
-    }
+    });
   };
 
   // Vector phase of tile c (parity Y): mask data from the compute cursor and
@@ -501,12 +511,26 @@ __device__ __forceinline__ void tile_item(const TileParams& p, int item) {
   // into V stage t%2; both stages were last read at step t-1) from register
   // set (t+1)%2, then load bundle t+3 into the same set.  Past the item's end
   // the stores write re-read tiles into stages nobody reads again.
-  auto staging = [&](auto xc) {
-    constexpr int X = decltype(xc)::value;  // t % 2
-    using Next = std::integral_constant<int, X ^ 1>;
-    store_k(Next{}, Ks[X ^ 1]);
-    store_v(Next{}, Vt[X]);
-    load_bundle(Next{});
+  // It runs inside the step's matrix-core phase, a part after MFMAs 2, 5, 8
+  // and 11 (the phase reads K stage t%2 and V stage (t-1)%2, the stores
+  // write the other two), so its vector work fills the gaps between MFMAs
+  // of this wavefront while the other half of the workgroup runs its
+  // softmax on the vector ALU.
+  auto staging = [&](auto xc, bool store) {
+    return [&, store](auto ic) {
+      constexpr int X = decltype(xc)::value;  // t % 2
+      constexpr int i = decltype(ic)::value;
+      using Next = std::integral_constant<int, X ^ 1>;
+      if constexpr (i == 2) {
+        if (store) store_k(Next{}, Ks[X ^ 1]);
+      } else if constexpr (i == 5) {
+        if (store) store_v(Next{}, Vt[X]);
+      } else if constexpr (i == 8) {
+        load_bundle_k(Next{});
+      } else if constexpr (i == 11) {
+        load_bundle_v(Next{});
+      }
+    };
   };
 
   // Prologue: bundle 0 (K(0)) into LDS, bundles 1 and 2 into register sets.
@@ -525,20 +549,21 @@ __device__ __forceinline__ void tile_item(const TileParams& p, int item) {
   load_bundle(Set0{});  // bundle 2: K(2), V(1)
   __syncthreads();
 
-  // Step t: leading half (waves 0-3): matrix phase, barrier, vector phase,
-  // barrier.  Lagging half (waves 4-7): vector phase of step t-1's scores,
-  // barrier, matrix phase, barrier.  Both halves pass the same barriers.
-  // The last step (t = n_tiles) stages nothing: bundle n_tiles + 1 holds no
+  // Step t: leading half (waves 0-3): matrix phase (with the staging),
+  // barrier, vector phase, barrier.  Lagging half (waves 4-7): vector phase
+  // of step t-1's scores, barrier, matrix phase (with the staging), barrier.
+  // Both halves pass the same barriers.
+  // The last step (t = n_tiles) stores nothing: bundle n_tiles + 1 holds no
   // tile the item uses, and waiting for its loads would only add latency.
+  // Its loads are still issued (of a valid tile, never read): every step
+  // issues the same loads, so the compiler's waits for a register set stay
+  // exact (a load under a branch makes it wait for every load in flight).
   if (wave < 4) {
     auto step = [&](auto xc, int t) {
       constexpr int X = decltype(xc)::value;
-      mfma_phase(Ks[X], Vt[X ^ 1]);
+      mfma_phase(Ks[X], Vt[X ^ 1], staging(xc, t < n_tiles));
       __syncthreads();
-      if (t < n_tiles) {
-        valu_phase(xc);  // tile t
-        staging(xc);
-      }
+      if (t < n_tiles) valu_phase(xc);  // tile t
       __syncthreads();
     };
     for (int t = 0;;) {
@@ -551,9 +576,8 @@ __device__ __forceinline__ void tile_item(const TileParams& p, int item) {
     auto step = [&](auto xc, int t) {
       constexpr int X = decltype(xc)::value;
       if (t >= 1) valu_phase(std::integral_constant<int, X ^ 1>{});  // tile t-1
-      if (t < n_tiles) staging(xc);
       __syncthreads();
-      mfma_phase(Ks[X], Vt[X ^ 1]);
+      mfma_phase(Ks[X], Vt[X ^ 1], staging(xc, t < n_tiles));
       __syncthreads();
     };
     for (int t = 0;;) {
