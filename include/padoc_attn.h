@@ -138,7 +138,7 @@ typedef struct {
                                     this many (multiple of 64, at most 8192);
                                     0 = automatic                           */
   int32_t target_workgroups;     /* decode chunk sizes (0 = 1024): shared keys
-                                    are cut into the fewest chunks (64 to 8192
+                                    are cut into the fewest chunks (128 to 8192
                                     keys) that keep the tile items (8
                                     wavefronts each) within 3/16 of this,
                                     private keys into about 2x this many

@@ -627,10 +627,12 @@ void build_decode(padoc_plan& P, Builder& B, const AncList& anc, const padoc_tre
   // the target_workgroups / 4 units (one round), so that from the start at
   // least a quarter of the units read private keys, while the shared keys
   // still get most of the matrix cores; a step over the cap would need a
-  // second round of tile items.  Smallest chunk (a multiple of 64 up to
-  // 8192) whose items (over all tasks and KV heads) fit, else 8192: a small
-  // step (one page) gets short chunks, so its few shared keys still spread
-  // over many compute units instead of forming a few long serial chains.
+  // second round of tile items.  Smallest chunk (a multiple of 64 from 128
+  // up to 8192) whose items (over all tasks and KV heads) fit, else 8192: a
+  // small step (one page) gets short chunks, so its few shared keys still
+  // spread over many compute units instead of forming a few long serial
+  // chains (below 128 keys an item's fixed latency stays while the combine
+  // gets more partials per row).
   auto shared_items = [&](int64_t CH) {
     int64_t n = 0;
     for (size_t i = 0; i + 1 < svis_at.size(); ++i) {
@@ -651,7 +653,7 @@ void build_decode(padoc_plan& P, Builder& B, const AncList& anc, const padoc_tre
   int64_t CHs = d->max_chunk_keys;
   if (CHs <= 0) {
     const int64_t target = std::max<int64_t>(1, tw * 3 / 16);
-    int64_t lo = 1, hi = 128;  // chunk = 64 * k keys
+    int64_t lo = 2, hi = 128;  // chunk = 64 * k keys
     if (shared_items(64 * hi) > target) {
       lo = hi;
     } else {
