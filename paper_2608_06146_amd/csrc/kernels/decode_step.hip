@@ -42,7 +42,7 @@
 #include <type_traits>
 
 #include "device_common.hpp"
-#include "tile_item.hpp"
+#include "fwd_item.hpp"
 
 namespace padoc {
 
@@ -273,7 +273,7 @@ template <int D>
 __global__ __launch_bounds__(tile::kThreads) void decode_step_kernel(TileParams p, int n_shared, int n_private,
                                                                      int n_groups, int* next) {
   const int b = blockIdx.x;
-  if (b < n_shared) tile::tile_item<D, true, true>(p, b);
+  if (b < n_shared) tile::fwd_item<D, true>(p, b);
   if (n_private <= 0) return;
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
   const int q = b % kQueues;

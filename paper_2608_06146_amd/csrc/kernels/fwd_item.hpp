@@ -111,12 +111,17 @@ __device__ __forceinline__ uint32_t lds_addr(const void* p) { return (uint32_t)(
 __device__ __forceinline__ void dma16(const void* base, uint32_t voff, uint32_t lds) {
   asm volatile("s_mov_b32 m0, %0\n\tglobal_load_lds_dwordx4 %1, %2" ::"s"(lds), "v"(voff), "s"(base) : "memory", "m0");
 }
+// The same with the non-temporal hint (paged K/V, read once per call: the
+// caches need not keep the lines).
+__device__ __forceinline__ void dma16_nt(const void* base, uint32_t voff, uint32_t lds) {
+  asm volatile("s_mov_b32 m0, %0\n\tglobal_load_lds_dwordx4 %1, %2 nt" ::"s"(lds), "v"(voff), "s"(base) : "memory", "m0");
+}
 __device__ __forceinline__ void dma4(const void* base, uint32_t voff, uint32_t lds) {
   asm volatile("s_mov_b32 m0, %0\n\tglobal_load_lds_dword %1, %2" ::"s"(lds), "v"(voff), "s"(base) : "memory", "m0");
 }
 #pragma clang diagnostic pop
 
-template <int D>
+template <int D, bool PAGED>
 __device__ __forceinline__ void fwd_item(const TileParams& p, int item) {
   using Gm = FwdGeom<D>;
   constexpr int KT = Gm::KT, CPR = Gm::CPR, RPI = Gm::RPI, IPW = Gm::IPW, SEL = Gm::SEL;
@@ -127,6 +132,9 @@ __device__ __forceinline__ void fwd_item(const TileParams& p, int item) {
   // per-lane base plus an immediate offset below 64 KB); limit stages.
   __shared__ __attribute__((aligned(1024))) uint16_t smem[8 * SEL];
   __shared__ int32_t Lb[4][kThreads];
+  constexpr int NBT = KT / kBlock;  // paged blocks per tile
+  __shared__ int32_t tile_ids[PAGED ? kMaxItemTiles * NBT : 1];
+  static_assert(!PAGED || kMaxItemTiles * NBT == kThreads, "one block id per thread");
 
   const WorkRec w = load_scalar(&p.work[item]);
   if (w.rng_count <= 0) return;
@@ -161,20 +169,46 @@ __device__ __forceinline__ void fwd_item(const TileParams& p, int item) {
   const uint16_t* Vg = static_cast<const uint16_t*>(p.v);
   const uint32_t HD = (uint32_t)p.Hkv * D;
 
+  // Load geometry.  Piece i = wave*IPW + j of a K tile holds tile rows
+  // RPI*i .. +RPI-1; lane l fills row RPI*i + l/CPR at chunk position l%CPR,
+  // i.e. global chunk (l%CPR) ^ kswz(row).  Packed: row r is K/V row
+  // kv_start + kbase + r.  Paged: row r is slot r%16 of the tile's block
+  // r/16 (K blocks are chunk-major with token t in slot kslot(t), so the
+  // rows are in slot order); a V tile is stored block by block as the cache
+  // holds it ([block][d][16 tokens], the two 8-token halves of d row swapped
+  // when bit 3 of d is set), piece i holding d rows 32*(i%(D/32)) .. +31 of
+  // block i/(D/32).
   int ld_row[IPW];
   uint32_t ld_k[IPW], ld_v[IPW];
 #pragma unroll
   for (int j = 0; j < IPW; ++j) {
-    const int r = RPI * (wave * IPW + j) + lane / CPR, pp = lane % CPR;
+    const int i = wave * IPW + j;
+    const int r = RPI * i + lane / CPR, pp = lane % CPR;
     ld_row[j] = r;
-    ld_k[j] = (uint32_t)kvh * D + 8 * (pp ^ Gm::kswz(r));
-    ld_v[j] = (uint32_t)kvh * D + 8 * (pp ^ Gm::vswz(r));
+    if constexpr (PAGED) {
+      const int c = pp ^ Gm::kswz(r);
+      ld_k[j] = (((uint32_t)kvh * (D / 8) + c) * kBlock + (r % kBlock)) * 8;
+      const int d = 32 * (i % (D / 32)) + (lane >> 1), h = (lane & 1) ^ ((d >> 3) & 1);
+      ld_v[j] = ((uint32_t)kvh * D + d) * kBlock + 8 * h;
+    } else {
+      ld_k[j] = (uint32_t)kvh * D + 8 * (pp ^ Gm::kswz(r));
+      ld_v[j] = (uint32_t)kvh * D + 8 * (pp ^ Gm::vswz(r));
+    }
   }
   const uint16_t* rkb[NKK];
 #pragma unroll
   for (int kk = 0; kk < NKK; ++kk) rkb[kk] = smem + l32 * D + 8 * ((2 * kk + hf) ^ Gm::kswz(l32));
+  // V^T fragment bases.  Packed (transposing reads): lane r of a 16-lane
+  // group reads key row 4*hf + (r%16)/4 (+ the key group's offset, a
+  // multiple of 4) and the 4 d values 32*db + 16*((l/16)%2) + 4*(r%4) .. +3.
+  // Paged (16-byte reads): lane (l32, hf) reads tokens 8*hf .. +7 of d row
+  // 32*db + l32 of the key group's block.
   const uint16_t* rvb[NDB];
-  {
+  if constexpr (PAGED) {
+#pragma unroll
+    for (int db = 0; db < NDB; ++db)
+      rvb[db] = smem + 4 * SEL + (32 * db + l32) * kBlock + 8 * (hf ^ ((l32 >> 3) & 1));
+  } else {
     const int vr = 4 * hf + ((lane & 15) >> 2);
     const int sw = Gm::vswz(vr);
 #pragma unroll
@@ -204,15 +238,35 @@ __device__ __forceinline__ void fwd_item(const TileParams& p, int item) {
   auto kst = [&](auto sc) -> uint16_t* { return smem + (decltype(sc)::value % 4) * SEL; };
   auto vst = [&](auto sc) -> uint16_t* { return smem + (4 + decltype(sc)::value % 4) * SEL; };
   auto lst = [&](auto sc) -> int32_t* { return Lb[decltype(sc)::value % 4]; };
-  auto load_tile = [&](const uint16_t* g, const Cursor& c, uint16_t* st, const uint32_t* ldc) {
-    const int kbase = c.kt * KT;
-    const int last = c.R.n_keys - 1 - kbase;
-    const uint16_t* tb = g + uniform64(c.R.kv_start + kbase) * (int64_t)HD;
+  // Block ids (paged): lane l (mod NBT) of a wavefront holds the id of block
+  // l of the tile at cursor c (read from the item's staged ids).
+  auto tile_blocks = [&](const Cursor& c) -> int {
+    if constexpr (PAGED) return tile_ids[(c.tb + c.kt) * NBT + (lane & (NBT - 1))];
+    else return 0;
+  };
+  // This wavefront's pieces of the K (or V: is_v) tile at cursor c into stage
+  // st; ids: the tile's block ids (paged).
+  auto load_tile = [&](const uint16_t* g, const Cursor& c, uint16_t* st, const uint32_t* ldc, bool is_v, int ids) {
     const uint32_t sb = lds_addr(st) + wave * IPW * 1024;
+    if constexpr (PAGED) {
+      // slots past a range's end are read as they are (their blocks exist:
+      // ids of blocks wholly past the end are the tile's first block)
 #pragma unroll
-    for (int j = 0; j < IPW; ++j) {
-      const int r = ld_row[j] <= last ? ld_row[j] : last;
-      dma16(tb, 2 * (__umul24((uint32_t)r, HD) + ldc[j]), sb + j * 1024);
+      for (int j = 0; j < IPW; ++j) {
+        const int i = wave * IPW + j;
+        const int b = is_v ? i / (D / 32) : (RPI * i) / kBlock;
+        const int64_t blk = __builtin_amdgcn_readlane(ids, b);
+        dma16_nt(g + blk * (int64_t)(HD * kBlock), 2 * ldc[j], sb + j * 1024);
+      }
+    } else {
+      const int kbase = c.kt * KT;
+      const int last = c.R.n_keys - 1 - kbase;
+      const uint16_t* tb = g + uniform64(c.R.kv_start + kbase) * (int64_t)HD;
+#pragma unroll
+      for (int j = 0; j < IPW; ++j) {
+        const int r = ld_row[j] <= last ? ld_row[j] : last;
+        dma16(tb, 2 * (__umul24((uint32_t)r, HD) + ldc[j]), sb + j * 1024);
+      }
     }
   };
   auto load_lim = [&](const Cursor& c, int32_t* dst) {
@@ -222,8 +276,7 @@ __device__ __forceinline__ void fwd_item(const TileParams& p, int item) {
   };
 
   const RangeRec R0 = load_scalar(&p.ranges[w.rng_begin]);
-  Cursor Lk{0, 0, R0, 1, 0};  // next K (and limit) tile to load
-  Cursor Lv = Lk;             // next V tile to load
+  Cursor Lk{0, 0, R0, 1, 0};  // next tile to load (K, V, limits)
   Cursor C = Lk;              // tile whose scores were computed last
 
   float m_run = -INFINITY, l_run = 0.f, m_sub = 0.f, alpha = 1.f;
@@ -245,12 +298,18 @@ __device__ __forceinline__ void fwd_item(const TileParams& p, int item) {
     constexpr int Y = decltype(yc)::value;
     const int kb = C.kt * KT;
     if (kb + KT > C.R.min_lim) {
-      const int rel = (C.R.lim_off < 0 ? C.R.n_keys : (valid ? lim[tid] : 0)) - kb - hf * 4;
+      // element i of half mb of lane (col, hf) is tile row mb*32 + 8*(i/4) +
+      // 4*hf + i%4; paged rows are in slot order (bits 2 and 3 of the key
+      // swapped within each block)
+      const int rel = (C.R.lim_off < 0 ? C.R.n_keys : (valid ? lim[tid] : 0)) - kb - hf * (PAGED ? 8 : 4);
 #pragma unroll
       for (int mb = 0; mb < 2; ++mb)
 #pragma unroll
-        for (int i = 0; i < 16; ++i)
-          if (mb * 32 + (i >> 2) * 8 + (i & 3) >= rel) Sb[Y][mb][i] = -INFINITY;
+        for (int i = 0; i < 16; ++i) {
+          const int key = PAGED ? mb * 32 + 16 * ((i >> 3) & 1) + 4 * ((i >> 2) & 1) + (i & 3)
+                                : mb * 32 + (i >> 2) * 8 + (i & 3);
+          if (key >= rel) Sb[Y][mb][i] = -INFINITY;
+        }
     }
   };
   // Row maximum of score buffer Y as a v_max3 tree, in pieces 0..6; piece 6
@@ -358,13 +417,18 @@ __device__ __forceinline__ void fwd_item(const TileParams& p, int item) {
     });
   };
   // O^T += V^T P^T from stage vt, with hook(i) after MFMA i.
-  // vs: V stage index (0-3); rvb = smem + V region + per-lane offset.
+  // O^T += V^T P^T from V stage vsc%4 (rvb: per-lane bases), with hook(i)
+  // after MFMA i.
   auto pv_product = [&](auto vsc, auto&& hook) {
     constexpr int VS = decltype(vsc)::value % 4;
     auto frag = [&](int i) -> bf16x8_t {
       const int g = i / NDB, db = i % NDB;
-      const uint16_t* b = rvb[db] + VS * SEL + ((g >> 1) * 32 + 16 * (g & 1)) * D;
-      return tr_pair(b, b + 8 * D);
+      if constexpr (PAGED) {
+        return *reinterpret_cast<const bf16x8_t*>(rvb[db] + VS * SEL + g * kBlock * D);
+      } else {
+        const uint16_t* b = rvb[db] + VS * SEL + ((g >> 1) * 32 + 16 * (g & 1)) * D;
+        return tr_pair(b, b + 8 * D);
+      }
     };
     bf16x8_t f[kPre];
 #pragma unroll
@@ -380,28 +444,85 @@ __device__ __forceinline__ void fwd_item(const TileParams& p, int item) {
     });
   };
 
-  // Prologue: K(0..2) and the limit entries of tiles 0..2, V(0..1); then
-  // S(0), its mask, its exact row maximum and its scaling.
+  // Paged V slots of the tile at cursor C at or past its range's end are
+  // zeroed in V stage vst (its scores are masked, so P is 0 there, but the
+  // cache slots may hold anything, and 0 * NaN is NaN).  Thread u takes d row
+  // u % D of block u / D; the caller has waited for the stage's loads and a
+  // barrier separates this from the stage's reads.
+  auto zero_v_tail = [&](uint16_t* vs) {
+    if constexpr (PAGED) {
+      const int keep = C.R.n_keys - C.kt * KT;  // valid keys of the tile
+      if (keep < KT && tid < NBT * D) {
+        const int b = tid / D, d = tid % D;
+#pragma unroll
+        for (int hp = 0; hp < 2; ++hp) {
+          const int kh = keep - (16 * b + 8 * (hp ^ ((d >> 3) & 1)));  // valid keys of this 8-key half
+          if (kh < 8) {
+            uint4* q = reinterpret_cast<uint4*>(vs + b * D * kBlock + d * kBlock + 8 * hp);
+            *q = kh <= 0 ? make_uint4(0, 0, 0, 0) : keep_first(*q, kh);
+          }
+        }
+      }
+      if (keep < KT) __builtin_amdgcn_s_waitcnt(0xC07F);  // LDS stores done before the next barrier
+    }
+  };
+
+  // Prologue: K, V and the limit entries of tiles 0..2; then S(0), its
+  // mask, its exact row maximum and its scaling, and the zeroed tail of V(0).
   using I0 = std::integral_constant<int, 0>;
   using I1 = std::integral_constant<int, 1>;
   using I2 = std::integral_constant<int, 2>;
-  load_tile(Kg, Lk, kst(I0{}), ld_k); load_lim(Lk, lst(I0{})); advance(Lk);
-  load_tile(Kg, Lk, kst(I1{}), ld_k); load_lim(Lk, lst(I1{})); advance(Lk);
-  load_tile(Kg, Lk, kst(I2{}), ld_k); load_lim(Lk, lst(I2{})); advance(Lk);
-  load_tile(Vg, Lv, vst(I0{}), ld_v); advance(Lv);
-  load_tile(Vg, Lv, vst(I1{}), ld_v); advance(Lv);
+  if constexpr (PAGED) {
+    // The block ids of every tile of the item (thread u: tile u / NBT, block
+    // u % NBT; an item has at most kMaxItemTiles tiles), read once into LDS
+    // so no step waits for a block-table read.  Blocks wholly past a range's
+    // end take the id of the tile's first block.
+    const int tile = tid / NBT, bi = tid % NBT;
+    if (tile < n_tiles) {
+      int64_t start = 0;
+      int kbase = 0, nk = 0;
+      for (int r = 0, tb = 0; r < w.rng_count; ++r) {
+        const RangeRec R = load_scalar(&p.ranges[w.rng_begin + r]);
+        const int nt = (R.n_keys + KT - 1) / KT;
+        if (tile >= tb && tile < tb + nt) {
+          start = R.kv_start;
+          kbase = (tile - tb) * KT;
+          nk = R.n_keys;
+        }
+        tb += nt;
+      }
+      tile_ids[tid] = p.block_table[start + (kbase >> 4) + ((kbase + bi * kBlock < nk) ? bi : 0)];
+    }
+    __builtin_amdgcn_s_waitcnt(0);
+    bar();
+  }
+  static_for<3>([&](auto sc) {
+    const int ids = tile_blocks(Lk);
+    load_tile(Kg, Lk, kst(sc), ld_k, false, ids);
+    load_tile(Vg, Lk, vst(sc), ld_v, true, ids);
+    load_lim(Lk, lst(sc));
+    advance(Lk);
+  });
   __builtin_amdgcn_s_waitcnt(0);
   bar();
+  if constexpr (PAGED) {
+    zero_v_tail(vst(I0{}));
+    __builtin_amdgcn_s_waitcnt(0);
+    bar();
+  }
   s_product(I0{}, I0{}, [&](auto) {});
   mask_tile(I0{}, Lb[0]);
   static_for<7>([&](auto kc) { stats_piece(I0{}, kc); });
   static_for<kPieces>([&](auto kc) { fma_piece(I0{}, kc); });
 
-  // Step t (SC = t mod 4): tile t's scaled scores are in buffer SC%2; K(t+1),
-  // V(t) and the limits of tile t+1 are in their stages, and K(t) and the
-  // limits of tile t still are (the slow path below reads them).  The
-  // step's loads go to the stages of tiles t-1 (K, limits) and t-2 (V),
-  // which every wavefront finished reading before this step's barrier.
+  // Step t (SC = t mod 4): tile t's scaled scores are in buffer SC%2; K, V
+  // and the limits of tiles t+1 and t+2 are in their stages (loaded at steps
+  // t-2 and t-1; this step's barrier is preceded by the wait for those of
+  // step t-2), and K(t), V(t) and the limits of tile t still are (the slow
+  // path reads K(t)).  The step's loads (tile t+3) go to the stages of tile
+  // t-1, which every wavefront finished reading before this barrier.  The
+  // paged V slots of tile t+1 past its range's end are zeroed here, read
+  // after the next barrier.
   using Scaled = std::integral_constant<bool, true>;
   using Raw = std::integral_constant<bool, false>;
   auto step = [&](auto sc, int t) {
@@ -441,20 +562,21 @@ __device__ __forceinline__ void fwd_item(const TileParams& p, int item) {
     }
     l_run += ls0 + ls1;
     advance(C);
-    if (t + 1 < n_tiles) mask_tile(YN{}, lst(std::integral_constant<int, SC + 1>{}));
+    if (t + 1 < n_tiles) {
+      mask_tile(YN{}, lst(std::integral_constant<int, SC + 1>{}));
+      zero_v_tail(vst(std::integral_constant<int, SC + 1>{}));
+    }
+    const int ids = tile_blocks(Lk);
     pv_product(std::integral_constant<int, SC>{}, [&](auto ic) {
       constexpr int i = decltype(ic)::value;
       static_for<kPieces / NB>([&](auto uc) {
         fma_piece(YN{}, std::integral_constant<int, i * (kPieces / NB) + decltype(uc)::value>{});
       });
-      if constexpr (i == NB / 2) {
-        load_tile(Kg, Lk, kst(std::integral_constant<int, SC + 3>{}), ld_k);
-        load_lim(Lk, lst(std::integral_constant<int, SC + 3>{}));
-      }
-      if constexpr (i == NB / 2 + 1) load_tile(Vg, Lv, vst(std::integral_constant<int, SC + 2>{}), ld_v);
+      if constexpr (i == NB / 2) load_tile(Kg, Lk, kst(std::integral_constant<int, SC + 3>{}), ld_k, false, ids);
+      if constexpr (i == NB / 2 + 1) load_tile(Vg, Lk, vst(std::integral_constant<int, SC + 3>{}), ld_v, true, ids);
       if constexpr (i == NB / 2 + 2) {
+        load_lim(Lk, lst(std::integral_constant<int, SC + 3>{}));
         advance(Lk);
-        advance(Lv);
       }
     });
   };
@@ -472,6 +594,25 @@ __device__ __forceinline__ void fwd_item(const TileParams& p, int item) {
 
   const float lt = l_run + __shfl_xor(l_run, 32);
   if (!valid) return;
+  if constexpr (PAGED) {
+    // split partial of column col: unnormalised O, reference maximum (log2
+    // units), sum
+    const int64_t slot = (int64_t)w.out_base + col;
+    float* op = p.part_o + slot * D;
+#pragma unroll
+    for (int db = 0; db < NDB; ++db)
+#pragma unroll
+      for (int i4 = 0; i4 < 4; ++i4) {
+        const int d0 = db * 32 + i4 * 8 + hf * 4;
+        *reinterpret_cast<float4*>(op + d0) =
+            make_float4(acc[db][4 * i4], acc[db][4 * i4 + 1], acc[db][4 * i4 + 2], acc[db][4 * i4 + 3]);
+      }
+    if (hf == 0) {
+      p.part_ml[2 * slot] = m_run;
+      p.part_ml[2 * slot + 1] = lt;
+    }
+    return;
+  }
   const float inv = 1.f / lt;
   uint16_t* op = static_cast<uint16_t*>(p.o) + ((int64_t)qrow * p.Hq + hq) * D;
 #pragma unroll

@@ -10,7 +10,7 @@ namespace {
 
 template <int D>
 __global__ __launch_bounds__(tile::kThreads) void tile_mfma_bf16_kernel(TileParams p) {
-  tile::fwd_item<D>(p, blockIdx.x);
+  tile::fwd_item<D, false>(p, blockIdx.x);
 }
 
 }  // namespace
