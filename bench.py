@@ -50,7 +50,7 @@ PROFILE_TAG = "concurrent_decode_64pages_packed_forward_8pages"
 TRACE_SUMMARY = os.path.join(ROOT, "profiles", f"kernel_trace_{PROFILE_TAG}.md")
 TRAFFIC_SUMMARY = os.path.join(ROOT, "profiles", f"hbm_traffic_{PROFILE_TAG}.txt")
 DECODE_KERNELS = ("decode_step_kernel<128>", "lse_combine_kernel<128, true, 8>")
-FORWARD_KERNEL = "tile_mfma_bf16_kernel<128, false, false>"
+FORWARD_KERNEL = "tile_mfma_bf16_kernel<128>"
 COUNTER_SUMMARY = os.path.join(ROOT, "profiles", f"sq_counters_{PROFILE_TAG}.md")
 # SQ counter passes (at most 8 SQ counters each, plus GRBM_GUI_ACTIVE)
 SQ_PASSES = {

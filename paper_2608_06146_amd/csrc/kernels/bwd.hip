@@ -30,7 +30,7 @@
 #include <algorithm>
 
 #include "device_common.hpp"
-#include "tile_item.hpp"
+#include "tile_common.hpp"
 
 namespace padoc {
 

@@ -3,7 +3,7 @@
 // private-key items in one launch.
 //
 // Workgroups 0 .. n_shared-1 each run one shared tile item on all 8
-// wavefronts (tile_item: every sibling column of a KV head against each K/V
+// wavefronts (fwd_item: every sibling column of a KV head against each K/V
 // tile).  Then every wavefront of the launch -- of the tile workgroups and of
 // the workgroups after them -- takes private items, one at a time, from
 // queues (atomic counters that the schedule upload zeroes), in the plan's

@@ -60,7 +60,7 @@
 // range's last row (the buffer may end there); their scores are masked.
 #pragma once
 
-#include "tile_item.hpp"
+#include "tile_common.hpp"
 
 namespace padoc {
 namespace tile {

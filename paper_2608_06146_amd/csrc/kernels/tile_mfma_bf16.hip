@@ -1,6 +1,6 @@
 // bf16 packed forward: one 8-wavefront workgroup per work item (packed K/V,
 // final O and LSE); the computation is fwd_item.  The paged form of the tile
-// computation (shared keys of a decode step) is tile_item, inside
+// computation (shared keys of a decode step) runs inside
 // decode_step_kernel.
 #include "fwd_item.hpp"
 
