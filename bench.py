@@ -141,10 +141,12 @@ def timed_steps(fn, steps, warmup, torch, pa):
     for b, a in evs:
         pa.set_kernel_events(b, a)
         fn()
+    te = time.perf_counter()
     torch.cuda.synchronize()
     t1 = time.perf_counter()
     pa.set_kernel_events()
     kms = [b.elapsed_time(a) for b, a in evs]
+    timed_steps.enqueue_ms = (te - t0) * 1e3 / steps  # host time to submit one step
     return (t1 - t0) * 1e3 / steps, kms
 
 
@@ -474,7 +476,7 @@ def run_decode(args, torch, np, syn, pa, dev, name=None, pool_gib=None, steps=No
     flops = 4 * d * Hq * visible_pairs_of(segs_paged)
     ex = plan.export()
     res = {
-        "workload": wl.name, "ms_per_step": ms, "kernel_ms": k_ms,
+        "workload": wl.name, "ms_per_step": ms, "enqueue_ms": timed_steps.enqueue_ms, "kernel_ms": k_ms,
         "kernel_ms_p10": float(np.percentile(kms, 10)), "kernel_ms_p90": float(np.percentile(kms, 90)),
         "kernel_ms_cold_p10": float(np.percentile(cold_ms, 10)), "kernel_ms_cold_p50": float(np.median(cold_ms)),
         "kernel_ms_cold_p90": float(np.percentile(cold_ms, 90)),
