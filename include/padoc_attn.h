@@ -269,6 +269,28 @@ padoc_status padoc_branch_decode(const padoc_plan* plan, const void* q, const vo
                                  float* lse, void* workspace, size_t workspace_bytes,
                                  hipStream_t stream);
 
+/* The decode step with the schedule kept in the workspace (App. E: every
+   layer of a decode step attends over the same tree, so one upload of its
+   schedule serves all of them).  padoc_plan_upload enqueues the copy of a
+   decode plan's schedule (with zeroed work-queue counters) into `workspace`
+   on `stream`; padoc_branch_decode_resident then runs the same kernels as
+   padoc_branch_decode, with the same arguments and results, without the
+   copy (each call leaves the counters at zero for the next).  Between the
+   upload and a resident call, the workspace may be used only by resident
+   calls of the same plan, ordered on one stream (or synchronised); the
+   caller must not write it, and padoc_branch_decode of another plan on it
+   needs a new upload.  A resident call on a workspace other than the one
+   of the plan's last upload, or after the plan was rebuilt, returns
+   PADOC_ERR_MODE and enqueues nothing.  The upload reads the plan's pinned
+   host copy (made on the first upload of a build). */
+padoc_status padoc_plan_upload(const padoc_plan* plan, void* workspace, size_t workspace_bytes,
+                               hipStream_t stream);
+padoc_status padoc_branch_decode_resident(const padoc_plan* plan, const void* q,
+                                          const void* k_cache, const void* v_cache,
+                                          const int32_t* block_table, void* o, float* lse,
+                                          void* workspace, size_t workspace_bytes,
+                                          hipStream_t stream);
+
 /* padoc_branch_decode without a workspace argument, for callers that cannot
    allocate device memory (code under stream capture, serving loops that must
    not call the allocator, harnesses that forbid it).  Same plan, inputs,

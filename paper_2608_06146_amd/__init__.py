@@ -287,6 +287,42 @@ def branch_decode(q, k_cache, v_cache, block_table, plan: TreePlan, out=None, ls
 NO_ALLOC_WORKSPACE_BYTES = 64 << 20   # PADOC_NO_ALLOC_WORKSPACE_BYTES
 
 
+def plan_upload(plan: TreePlan, workspace, stream=None):
+    """Copy a decode plan's schedule into ``workspace`` (``padoc_plan_upload``)
+    for ``branch_decode_resident`` calls: every layer of a decode step runs
+    over the same tree, so one upload serves all of them."""
+    import torch
+    _check_tensor("workspace", workspace, torch.uint8, workspace.device)
+    s = torch.cuda.current_stream(workspace.device) if stream is None else stream
+    _lib.check(_lib.lib().padoc_plan_upload(plan.handle, _ptr(workspace), workspace.numel(),
+                                            C.c_void_p(s.cuda_stream)))
+    return workspace
+
+
+def branch_decode_resident(q, k_cache, v_cache, block_table, plan: TreePlan, out, lse, workspace, stream=None):
+    """Decode step on a workspace that holds the plan's schedule
+    (``padoc_branch_decode_resident``, after ``plan_upload``): the kernels of
+    ``branch_decode`` without the schedule copy."""
+    import torch
+    s = torch.cuda.current_stream(q.device) if stream is None else stream
+    key = ("resident", plan.handle, s.cuda_stream) + tuple(
+        (id(t), t.data_ptr(), t.shape, t.stride(), t.dtype) for t in (q, k_cache, v_cache, block_table, out, lse, workspace))
+    args = _repeat_call(plan, key)
+    if args is None:
+        dt = _torch_dtype(plan)
+        dev = q.device
+        for name, t in (("q", q), ("k_cache", k_cache), ("v_cache", v_cache), ("out", out)):
+            _check_tensor(name, t, dt, dev)
+        _check_tensor("block_table", block_table, torch.int32, dev)
+        _check_tensor("lse", lse, torch.float32, dev)
+        _check_tensor("workspace", workspace, torch.uint8, dev)
+        args = (plan.handle, _ptr(q), _ptr(k_cache), _ptr(v_cache), _ptr(block_table), _ptr(out), _ptr(lse),
+                _ptr(workspace), workspace.numel(), C.c_void_p(s.cuda_stream))
+    _lib.check(_lib.lib().padoc_branch_decode_resident(*args))
+    plan._last_call = (key, args)
+    return out, lse
+
+
 def branch_decode_no_alloc(q, k_cache, v_cache, block_table, plan: TreePlan, out, lse, stream=None):
     """Decode step with the library's fixed per-GPU workspace
     (``padoc_branch_decode_no_alloc``): the caller passes every input and

@@ -84,7 +84,8 @@ class SessionView(C.Structure):
 EXPORTED = [
     "padoc_tree_from_pages", "padoc_tree_layout", "padoc_plan_create", "padoc_plan_workspace_bytes",
     "padoc_plan_export", "padoc_plan_destroy", "padoc_tree_attn_fwd", "padoc_branch_decode",
-    "padoc_branch_decode_no_alloc", "padoc_last_error", "padoc_set_kernel_events", "padoc_version",
+    "padoc_branch_decode_no_alloc", "padoc_plan_upload", "padoc_branch_decode_resident", "padoc_last_error",
+    "padoc_set_kernel_events", "padoc_version",
     "padoc_plan_backward_workspace_bytes", "padoc_tree_attn_bwd",
     "padoc_session_create", "padoc_session_destroy", "padoc_session_open", "padoc_session_close",
     "padoc_session_prepare", "padoc_session_launch", "padoc_session_commit", "padoc_session_view_get",
@@ -114,6 +115,8 @@ def lib():
     L.padoc_tree_attn_fwd.argtypes = [vp, vp, vp, vp, vp, vp, vp, sz, vp]
     L.padoc_branch_decode.argtypes = [vp, vp, vp, vp, vp, vp, vp, vp, sz, vp]
     L.padoc_branch_decode_no_alloc.argtypes = [vp, vp, vp, vp, vp, vp, vp, vp]
+    L.padoc_plan_upload.argtypes = [vp, vp, sz, vp]
+    L.padoc_branch_decode_resident.argtypes = [vp, vp, vp, vp, vp, vp, vp, vp, sz, vp]
     L.padoc_plan_backward_workspace_bytes.argtypes = [vp, C.POINTER(sz)]
     L.padoc_tree_attn_bwd.argtypes = [vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, sz, vp]
     L.padoc_session_create.argtypes = [C.POINTER(SessionDesc), C.POINTER(vp)]
@@ -133,7 +136,7 @@ def lib():
     L.padoc_version.restype = C.c_char_p
     for name in ("padoc_tree_from_pages", "padoc_tree_layout", "padoc_plan_create", "padoc_plan_workspace_bytes",
                  "padoc_plan_export", "padoc_tree_attn_fwd", "padoc_branch_decode", "padoc_branch_decode_no_alloc",
-                 "padoc_set_kernel_events",
+                 "padoc_plan_upload", "padoc_branch_decode_resident", "padoc_set_kernel_events",
                  "padoc_plan_backward_workspace_bytes", "padoc_tree_attn_bwd", "padoc_session_create",
                  "padoc_session_open", "padoc_session_close", "padoc_session_prepare", "padoc_session_launch",
                  "padoc_session_commit", "padoc_session_view_get", "padoc_tree_depths"):

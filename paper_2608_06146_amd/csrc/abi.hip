@@ -86,6 +86,30 @@ const void* pinned_bwd_blob(const padoc_plan* P) {
   return P->bpinned ? P->bpinned : P->bwd_blob.data();
 }
 
+// Copy plan P's schedule (with zeroed work-queue counters) into workspace
+// ws on `stream`; `pinned`: from the plan's pinned host copy (made on first
+// use), else straight from the plan's own host memory, allocating nothing.
+padoc_status upload_schedule(const padoc_plan* P, void* ws, hipStream_t stream, bool pinned) {
+  hipError_t e =
+      hipMemcpyAsync(ws, pinned ? pinned_blob(P) : P->blob.data(), P->blob.size(), hipMemcpyHostToDevice, stream);
+  if (e != hipSuccess) return hip_fail("hipMemcpyAsync(schedule)", e);
+  std::lock_guard<std::mutex> lk(P->pin_mu);
+  P->up_ws = ws;
+  P->up_build = P->build_id;
+  if (pinned && P->build_id > 1) {
+    // a rebuilt plan: mark when its pinned copy may be overwritten
+    if (!P->pin_ev) {
+      hipEvent_t ev = nullptr;
+      if (hipEventCreateWithFlags(&ev, hipEventDisableTiming) == hipSuccess) P->pin_ev = ev;
+    }
+    if (P->pin_ev) {
+      e = hipEventRecord(static_cast<hipEvent_t>(P->pin_ev), stream);
+      if (e != hipSuccess) return hip_fail("hipEventRecord", e);
+    }
+  }
+  return PADOC_OK;
+}
+
 // Launch the attention of plan P.  `upload`: copy the schedule into the
 // workspace first (else the caller already did); `events`: record the
 // profiling events around the kernels.
@@ -97,20 +121,8 @@ padoc_status run(const padoc_plan* P, const void* q, const void* k, const void* 
   if (P->work.empty()) return PADOC_OK;
   hipError_t e = hipSuccess;
   if (upload) {
-    e = hipMemcpyAsync(ws, pinned ? pinned_blob(P) : P->blob.data(), P->blob.size(), hipMemcpyHostToDevice, stream);
-    if (e != hipSuccess) return hip_fail("hipMemcpyAsync(schedule)", e);
-    if (pinned && P->build_id > 1) {
-      // a rebuilt plan: mark when its pinned copy may be overwritten
-      std::lock_guard<std::mutex> lk(P->pin_mu);
-      if (!P->pin_ev) {
-        hipEvent_t ev = nullptr;
-        if (hipEventCreateWithFlags(&ev, hipEventDisableTiming) == hipSuccess) P->pin_ev = ev;
-      }
-      if (P->pin_ev) {
-        e = hipEventRecord(static_cast<hipEvent_t>(P->pin_ev), stream);
-        if (e != hipSuccess) return hip_fail("hipEventRecord", e);
-      }
-    }
+    padoc_status st = upload_schedule(P, ws, stream, pinned);
+    if (st != PADOC_OK) return st;
   }
   TileParams tp{};
   tp.q = q;
@@ -159,6 +171,7 @@ padoc_status run(const padoc_plan* P, const void* q, const void* k, const void* 
     cp.Hq = P->Hq;
     cp.Hkv = P->Hkv;
     cp.G = P->G;
+    cp.next = reinterpret_cast<int32_t*>(static_cast<char*>(ws) + P->off_next);
     e = launch_lse_combine(cp, P->D, P->dtype == PADOC_BF16, stream);
     if (e != hipSuccess) return hip_fail("combine kernel launch", e);
   }
@@ -194,6 +207,41 @@ extern "C" padoc_status padoc_branch_decode(const padoc_plan* plan, const void* 
     return set_error(PADOC_ERR_MODE, "plan was built for packed K/V (block_size 0); use padoc_tree_attn_fwd");
   if (!plan->work.empty() && !block_table) return set_error(PADOC_ERR_ARG, "block_table is null");
   return run(plan, q, k_cache, v_cache, block_table, o, lse, workspace, stream);
+}
+
+extern "C" padoc_status padoc_plan_upload(const padoc_plan* plan, void* workspace, size_t workspace_bytes,
+                                          hipStream_t stream) {
+  clear_error();
+  if (!plan) return set_error(PADOC_ERR_ARG, "plan is null");
+  if (plan->kind != 1) return set_error(PADOC_ERR_MODE, "padoc_plan_upload takes decode plans (block_size 16)");
+  if (!workspace) return set_error(PADOC_ERR_WORKSPACE, "workspace is null");
+  if (((uintptr_t)workspace) & 255) return set_error(PADOC_ERR_WORKSPACE, "workspace must be 256-byte aligned");
+  if (workspace_bytes < plan->ws_bytes)
+    return set_error(PADOC_ERR_WORKSPACE, "workspace of %zu bytes is smaller than the %zu the plan needs",
+                     workspace_bytes, plan->ws_bytes);
+  if (plan->work.empty()) return PADOC_OK;
+  return upload_schedule(plan, workspace, stream, /*pinned=*/true);
+}
+
+extern "C" padoc_status padoc_branch_decode_resident(const padoc_plan* plan, const void* q, const void* k_cache,
+                                                     const void* v_cache, const int32_t* block_table, void* o,
+                                                     float* lse, void* workspace, size_t workspace_bytes,
+                                                     hipStream_t stream) {
+  clear_error();
+  padoc_status st = check_common(plan, q, k_cache, v_cache, o, lse, workspace, workspace_bytes);
+  if (st != PADOC_OK) return st;
+  if (plan->kind != 1)
+    return set_error(PADOC_ERR_MODE, "plan was built for packed K/V (block_size 0); use padoc_tree_attn_fwd");
+  if (!plan->work.empty() && !block_table) return set_error(PADOC_ERR_ARG, "block_table is null");
+  if (plan->work.empty()) return PADOC_OK;
+  {
+    std::lock_guard<std::mutex> lk(plan->pin_mu);
+    if (plan->up_ws != workspace || plan->up_build != plan->build_id)
+      return set_error(PADOC_ERR_MODE,
+                       "the workspace does not hold this plan's schedule (upload it with padoc_plan_upload after "
+                       "every build of the plan)");
+  }
+  return run(plan, q, k_cache, v_cache, block_table, o, lse, workspace, stream, /*upload=*/false);
 }
 
 // Workspace of padoc_branch_decode_no_alloc: one array per GPU the library

@@ -68,6 +68,10 @@ struct padoc_plan {
   mutable size_t pinned_cap = 0;
   mutable uint64_t pinned_build = 0;
   mutable void* pin_ev = nullptr;
+  // The workspace the last schedule upload of this build went to (under
+  // pin_mu): padoc_branch_decode_resident refuses any other.
+  mutable const void* up_ws = nullptr;
+  mutable uint64_t up_build = 0;
 };
 
 namespace padoc {

@@ -41,6 +41,10 @@ __global__ __launch_bounds__(256) void lse_combine_kernel(CombineParams p) {
   typedef typename VecF<VW>::T vec_t;
   const int64_t pair = (int64_t)blockIdx.x * (256 / LANES) + (threadIdx.x / LANES);
   const int sub = threadIdx.x % LANES;
+  // The step kernel before this one on the stream has taken every private
+  // item: its queue counters go back to zero, so a workspace that keeps its
+  // schedule is ready for the next call without a new upload.
+  if (p.next != nullptr && blockIdx.x == 0 && threadIdx.x < kPrivateQueues) p.next[64 * threadIdx.x] = 0;
   if (pair >= p.n_rows * p.G) return;
   const int4 rec = p.comb_rows[pair / p.G];  // one load: the pair and its slot list
   const int64_t rk = rec.x;

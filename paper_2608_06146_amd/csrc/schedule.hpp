@@ -82,6 +82,7 @@ struct CombineParams {
   float* lse;
   int64_t n_q;
   int32_t Hq, Hkv, G;
+  int32_t* next;  // decode: the step kernel's kPrivateQueues queue counters (256 bytes apart), zeroed for the next call
 };
 
 }  // namespace padoc

@@ -342,6 +342,19 @@ def test_launch_errors_return_before_any_device_call():
     assert L.padoc_tree_attn_fwd(dplan.handle, fake, fake, fake, fake, fake, fake, wsd, None) == _lib.ERR_MODE
     assert L.padoc_branch_decode(dplan.handle, fake, fake, fake, None, fake, fake, fake, wsd, None) == _lib.ERR_ARG
     assert L.padoc_set_kernel_events(fake, None) == _lib.ERR_ARG
+    # schedule upload and resident decode: argument and state errors
+    assert L.padoc_plan_upload(plan.handle, fake, ws_ok, None) == _lib.ERR_MODE  # forward plan
+    assert L.padoc_plan_upload(dplan.handle, None, wsd, None) == _lib.ERR_WORKSPACE
+    assert L.padoc_plan_upload(dplan.handle, fake, wsd - 1, None) == _lib.ERR_WORKSPACE
+    assert L.padoc_plan_upload(None, fake, wsd, None) == _lib.ERR_ARG
+    assert L.padoc_branch_decode_resident(plan.handle, fake, fake, fake, fake, fake, fake, fake, ws_ok,
+                                          None) == _lib.ERR_MODE  # forward plan
+    # never uploaded: refused before any launch
+    assert L.padoc_branch_decode_resident(dplan.handle, fake, fake, fake, fake, fake, fake, fake, wsd,
+                                          None) == _lib.ERR_MODE
+    assert "padoc_plan_upload" in L.padoc_last_error().decode()
+    assert L.padoc_branch_decode_resident(dplan.handle, fake, fake, fake, None, fake, fake, fake, wsd,
+                                          None) == _lib.ERR_ARG
 
 
 def test_last_error_is_thread_local():

@@ -174,6 +174,45 @@ def test_decode_determinism():
         assert torch.equal(o1, o2) and torch.equal(l1, l2)
 
 
+@pytest.mark.parametrize("dtype,d,target_wg", [("bf16", 128, 0), ("bf16", 128, 4), ("f32", 64, 0)])
+def test_decode_resident_schedule(dtype, d, target_wg):
+    """padoc_plan_upload + padoc_branch_decode_resident: three resident calls
+    in a row (each runs on the queue counters the previous call's combine
+    left at zero; target_wg 4 puts many private items on every queue) and a
+    regular call between them, all bit-identical to padoc_branch_decode
+    (checked against the oracle).  A resident call on a workspace the plan's
+    schedule was not uploaded to is refused."""
+    rng = np.random.default_rng(6)
+    pages = [syn.Page(400, 0, 50, 1, tuple(syn.Branch(int(f), int(L), 1) for f, L in
+                                           zip(np.sort(rng.integers(1, 50, 30)), rng.integers(1, 500, 30))))]
+    o_ref, l_ref, plan, (q, kc, vc, bt, ids) = decode_case(pages, 16, 2, d, dtype, 50, check=False,
+                                                           target_workgroups=target_wg)
+    nodes = od.page_nodes(pages)
+    O, L = oracle.tree_attention_paged(nodes, q, kc, vc, ids, 1.0 / math.sqrt(d), 16, 2, 16)
+    compare("resident reference call", o_ref, l_ref, O, L, dtype)
+
+    def aligned_ws():
+        raw = torch.empty(plan.workspace_bytes + 256, dtype=torch.uint8, device="cuda")
+        off = (-raw.data_ptr()) % 256
+        return raw[off: off + plan.workspace_bytes]
+
+    ws = aligned_ws()
+    with pytest.raises(pa.PadocError):  # nothing uploaded to this workspace yet
+        pa.branch_decode_resident(q, kc, vc, bt, plan, torch.empty_like(o_ref), torch.empty_like(l_ref), ws)
+    pa.plan_upload(plan, ws)
+    for i in range(4):
+        o = torch.full_like(o_ref, float("nan"))
+        lse = torch.full_like(l_ref, float("nan"))
+        if i == 2:  # a regular call on the same workspace uploads the same schedule again
+            pa.branch_decode(q, kc, vc, bt, plan, out=o, lse=lse, workspace=ws)
+        else:
+            pa.branch_decode_resident(q, kc, vc, bt, plan, o, lse, ws)
+        torch.cuda.synchronize()
+        assert torch.equal(o, o_ref) and torch.equal(lse, l_ref), f"call {i} differs from padoc_branch_decode"
+    with pytest.raises(pa.PadocError):  # another workspace
+        pa.branch_decode_resident(q, kc, vc, bt, plan, o, lse, aligned_ws())
+
+
 def test_decode_equals_packed_forward_rows():
     """P8: a decode step's rows equal the packed forward's rows for the same
     tokens (same values, K/V moved from packed rows into paged blocks)."""
