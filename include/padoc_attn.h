@@ -176,7 +176,11 @@ typedef struct {
   int32_t col0;  /* first column of the task this item computes              */
   int32_t ncol;  /* columns this item computes: col0 .. col0+ncol-1, clipped
                     to the task's ntok*G columns                             */
-  int32_t reserved[3];
+  int32_t direct[3]; /* decode private items with one range, one query token
+                        and no per-token limits: the range's kv_start, its
+                        n_keys and the token's Q row (the kernel then reads
+                        neither the range nor the token record); -1, 0, 0 in
+                        every other item                                      */
 } padoc_work_view;
 
 typedef struct {

@@ -23,7 +23,7 @@ SEGMENT_DTYPE = np.dtype([("parent", "<i4"), ("fork", "<i4"), ("len", "<i4"), ("
                           ("kv_off", "<i8"), ("q_off", "<i8")])
 WORK_DTYPE = np.dtype([("tok_begin", "<i4"), ("ntok", "<i4"), ("rng_begin", "<i4"), ("rng_count", "<i4"),
                        ("kvh", "<i4"), ("out_base", "<i4"), ("cost", "<i4"), ("col0", "<i4"),
-                       ("ncol", "<i4"), ("reserved", "<i4", (3,))])
+                       ("ncol", "<i4"), ("direct", "<i4", (3,))])
 BWD_DTYPE = np.dtype([("key_row0", "<i8"), ("n_keys", "<i4"), ("tok_begin", "<i4"), ("ntok", "<i4"),
                       ("lim_begin", "<i4"), ("col0", "<i4"), ("ncol", "<i4"), ("kvh", "<i4"), ("cost", "<i4")])
 RANGE_DTYPE = np.dtype([("kv_start", "<i8"), ("n_keys", "<i4"), ("min_lim", "<i4"), ("lim_off", "<i4"),

@@ -425,6 +425,7 @@ void build_forward(padoc_plan& P, Builder& B) {
     B.emit_ranges(vis, pieces.data(), pieces.size(), task.count, rb, rc, cost);
     for (int32_t g = 0; g < P.Hkv; ++g) {
       padoc::WorkRec w{};
+      w.direct[0] = -1;
       w.tok_begin = tok_begin;
       w.ntok = task.count;
       w.rng_begin = rb;
@@ -688,6 +689,7 @@ void build_decode(padoc_plan& P, Builder& B, const AncList& anc, const padoc_tre
       P.n_slots += (int64_t)ntok * G;
       for (int32_t c0 = 0; c0 < ntok * G; c0 += width) {
         padoc::WorkRec w{};
+        w.direct[0] = -1;
         w.tok_begin = tok_begin;
         w.ntok = ntok;
         w.rng_begin = rb;
@@ -764,6 +766,11 @@ void build_decode(padoc_plan& P, Builder& B, const AncList& anc, const padoc_tre
         P.n_slots += G;
         for (int32_t c0 = 0; c0 < G; c0 += kPrivateCols) {
           padoc::WorkRec w{};
+          // the range and the Q row, copied so the kernel's first K/V loads
+          // wait for one record instead of three
+          w.direct[0] = rr.kv_start <= INT32_MAX ? (int32_t)rr.kv_start : -1;
+          w.direct[1] = take;
+          w.direct[2] = P.toks[tb];
           w.tok_begin = tb;
           w.ntok = 1;
           w.rng_begin = rb;

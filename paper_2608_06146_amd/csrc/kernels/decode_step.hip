@@ -56,12 +56,18 @@ __device__ __forceinline__ bf16x8_t as_bf16x8(const uint4& u) { return *reinterp
 // Key (within a 32-key step) held by row m of 16-key M block mb.
 __device__ __forceinline__ int step_key(int mb, int m) { return 8 * (m >> 2) + 4 * mb + (m & 3); }
 
+// Register sets of a private item's K/V pipeline: steps in flight.
+constexpr int kSets = 2;
+
 // Private work item `item` on the wavefront whose lane index is `lane`.
 template <int D>
 __device__ __forceinline__ void private_item(const TileParams& p, int item, int lane) {
   constexpr int NDS = D / 32;  // K-slices (32 d each) of the score product
   constexpr int NDM = D / 16;  // 16-row blocks of O^T
   const WorkRec w = load_scalar(p.work + item);
+  // A one-range, one-token item without limits carries its range and its Q
+  // row in the work record: its first loads wait for one record, not three.
+  const bool direct = w.direct[0] >= 0;
   const int n = lane & 15, g = lane >> 4;
   const int G = p.G;
   const int kvh = w.kvh;
@@ -69,7 +75,7 @@ __device__ __forceinline__ void private_item(const TileParams& p, int item, int 
   const int col = w.col0 + n;
   const int t = col / G;
   const bool valid = n < w.ncol && t < w.ntok;
-  const int32_t qrow = valid ? p.toks[w.tok_begin + t] : 0;
+  const int32_t qrow = !valid ? 0 : direct ? w.direct[2] : p.toks[w.tok_begin + t];
   const int32_t hq = kvh * G + (col - t * G);
   const uint16_t* Kc = static_cast<const uint16_t*>(p.k);
   const uint16_t* Vc = static_cast<const uint16_t*>(p.v);
@@ -100,13 +106,25 @@ __device__ __forceinline__ void private_item(const TileParams& p, int item, int 
         c.ok = 0;
     }
   };
-  Cursor C{0, 0, load_scalar(p.ranges + w.rng_begin), 1, 0};
+  RangeRec R0;
+  if (direct) {
+    R0.kv_start = w.direct[0];
+    R0.n_keys = w.direct[1];
+    R0.min_lim = w.direct[1];
+    R0.lim_off = -1;
+    R0.seg = 0;
+    R0.key_begin = 0;
+    R0.reserved = 0;
+  } else {
+    R0 = load_scalar(p.ranges + w.rng_begin);
+  }
+  Cursor C{0, 0, R0, 1, 0};
   Cursor L = C;  // once exhausted (ok = 0) it still names a valid step of the last range
 
-  uint4 kf[2][2][NDS];  // [set][M block][K-slice]
-  uint4 vf[2][NDM];     // [set][16-row d block]
-  int vkeep[2];
-  int64_t blk[2][2];    // [set][block of the step's first/second 16 keys]
+  uint4 kf[kSets][2][NDS];  // [set][M block][K-slice]
+  uint4 vf[kSets][NDM];     // [set][16-row d block]
+  int vkeep[kSets];
+  int64_t blk[kSets][2];    // [set][block of the step's first/second 16 keys]
   int32_t nid[2];       // block ids of the load cursor's step, requested ahead
 
   auto fetch_ids = [&](const Cursor& c) __attribute__((always_inline)) {
@@ -167,21 +185,25 @@ __device__ __forceinline__ void private_item(const TileParams& p, int item, int 
   load_lim();
   const float sl2 = p.scale_log2;
 
-  // Prologue: steps 0 and 1 into sets 0 and 1, the block ids of step 2.
-  // Branch-free: an exhausted load cursor still names a valid step.
+  // Prologue: steps 0 .. kSets-1 into sets 0 .. kSets-1, the block ids of
+  // step kSets.  Branch-free: an exhausted load cursor still names a valid
+  // step.
   fetch_ids(L);
   load_k(0, true);
   load_v(L, 0, true);
   advance(L);
-  const bool two = L.ok;
-  fetch_ids(L);
-  load_k(1, two);
-  load_v(L, 1, two);
-  advance(L);
+#pragma unroll
+  for (int X = 1; X < kSets; ++X) {
+    const bool real = L.ok;
+    fetch_ids(L);
+    load_k(X, real);
+    load_v(L, X, real);
+    advance(L);
+  }
   fetch_ids(L);
 
   // Step of the compute cursor on register set X, then refill set X with the
-  // load cursor's step (two ahead) and request the block ids of the step
+  // load cursor's step (kSets ahead) and request the block ids of the step
   // after it; false once the item's last step is done.
   auto step = [&](auto xc) __attribute__((always_inline)) -> bool {
     constexpr int X = decltype(xc)::value;
@@ -237,8 +259,10 @@ __device__ __forceinline__ void private_item(const TileParams& p, int item, int 
     if (C.ri != ri_before) load_lim();
     return true;
   };
-  while (step(std::integral_constant<int, 0>{}) && step(std::integral_constant<int, 1>{})) {
-  }
+  for (bool go = true; go;)
+    tile::static_for<kSets>([&](auto xc) __attribute__((always_inline)) {
+      if (go) go = step(xc);
+    });
 
   float lt = l_part + __shfl_xor(l_part, 16);
   lt += __shfl_xor(lt, 32);

@@ -174,7 +174,14 @@ def _check_decode(segs, G, Hkv, chunk=0, read_once=False):
                 assert R["n_keys"] <= chunk
         for i in range(w["ntok"]):
             slot_cover[int(w["out_base"]) + i * G] = (int(toks[i]), int(w["kvh"]), cover[i])
-        assert not w["reserved"].any()
+        dr = w["direct"]
+        if dr[0] >= 0:  # a private item carrying its one range and its Q row
+            R = ex["ranges"][w["rng_begin"]]
+            assert idx >= ex["n_work_shared"] and w["rng_count"] == 1 and w["ntok"] == 1
+            assert (dr[0], dr[1]) == (R["kv_start"], R["n_keys"]) and R["lim_off"] < 0
+            assert dr[2] == ex["toks"][w["tok_begin"]]
+        else:
+            assert (dr[0], dr[1], dr[2]) == (-1, 0, 0)
     for base, cols in cols_of.items():
         assert sorted(cols) == list(range(len(cols))), "task columns not covered exactly once"
     n_q = int(sum(n[3] for n in nodes))
