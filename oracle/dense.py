@@ -23,9 +23,10 @@ What it computes, and where the paper defines it
   ancestor mask and runs masked softmax attention on it (App. C, Dense SDPA);
   this oracle does exactly that, per page, in fp64.
 * Masked parallel decoding (App. E, Algorithm "Masked parallel decoding"):
-  :func:`simulate_masked_parallel_decoding` replays the logical fused mask
-  updates (identity append, row copy on fork, row removal on retire) so the
-  tests can pin the visibility rule and the fork-offset reading to it.
+  :func:`simulate_masked_parallel_decoding` runs a synthetic event trace and
+  writes down the fused mask rows it implies (a row is what its stream was
+  given when it opened plus its own cached tokens), so the tests can pin the
+  visibility rule and the fork-offset reading to the decoding semantics.
 
 Readings of points the paper leaves open are listed in the repository's design
 notes; the ones this file depends on: fork offsets are half-open counts
@@ -397,10 +398,37 @@ def decoding_depths(nodes):
 # Masked parallel decoding (App. E), on the logical fused mask
 # --------------------------------------------------------------------------
 
+def _run_event_trace(decide, max_steps: int):
+    """The event trace alone: at each step every live stream emits one token
+    (live streams in opening order, the layout stream 0 first), then
+    ``decide`` says what follows for each.  Returns ``(emitted, born)``:
+    ``emitted[t]`` lists ``(stream, index)`` of the tokens cached at step t,
+    ``born[c]`` is the step after which content stream c opened (the step at
+    which the layout stream's output closed a region)."""
+    live = [0]
+    count = {0: 0}
+    born: Dict[int, int] = {}
+    emitted: List[List[Tuple[int, int]]] = []
+    for t in range(max_steps):
+        if not live:
+            break
+        emitted.append([(c, count[c]) for c in live])
+        for c in live:
+            count[c] += 1
+        outcome = {c: decide(t, c, c == 0) for c in live}
+        nxt = [c for c in live if outcome[c] != "eos"]
+        if outcome.get(0) == "fork":
+            c_new = max(count) + 1
+            count[c_new] = 0
+            born[c_new] = t
+            nxt.append(c_new)
+        live = nxt
+    return emitted, born
+
+
 def simulate_masked_parallel_decoding(prefix_len: int, decide, max_steps: int = 64):
-    """Replay masked parallel decoding (App. E, algorithm "Masked parallel
-    decoding") on its logical fused mask, held as one Boolean matrix whose
-    rows are the live streams and whose columns are the cache positions.
+    """Masked parallel decoding (App. E, algorithm "Masked parallel
+    decoding") reduced to the fused mask it builds over the shared cache.
 
     ``decide(step, stream_id, is_layout)`` gives what happens after a stream
     has been decoded at ``step``: ``"continue"``, ``"eos"`` (the stream
@@ -408,44 +436,49 @@ def simulate_masked_parallel_decoding(prefix_len: int, decide, max_steps: int = 
     region, which opens a content stream).  Stream 0 is the layout stream;
     content streams are numbered 1, 2, ... as they open.
 
-    The matrix changes in three ways.  A step puts one token of every live
-    stream into the cache: the matrix gains one column per live stream, set
-    only in that stream's own row (an identity block), and every stream's new
-    token is queried with its row as it then stands.  A region close gives
-    the new content stream a copy of the layout stream's row taken at that
-    moment, i.e. before the closing output itself reaches the cache (it
-    enters at the next step, seen by the layout stream alone).  A stopped
-    stream's row is dropped.
+    The trace is run first (:func:`_run_event_trace`); the fused mask is then
+    written down as a function of it.  The method gives each stream one mask
+    row over the cache columns.  A row holds what the stream was given when
+    it opened -- the page prefix for the layout stream, the layout stream's
+    row of that moment for a content stream -- and, from then on, exactly
+    the columns of the tokens the stream itself puts into the cache (each
+    step appends one column per live stream, set only in its own row).  The
+    token a stream caches at step t is queried with its row as it stands
+    after that step's columns are added.  A region close happens after the
+    step's outputs are sampled, so the closing output is not yet cached when
+    the content stream's row is taken (it enters at the next step, in the
+    layout row only).
 
     Returns ``(tags, queries, forks)``: ``tags[l] = (stream, index)`` names
     the token at cache position l (stream -1 = page prefix); ``queries`` lists
-    ``(stream, index, row)`` with the Boolean row used for that token;
-    ``forks[c]`` = layout-stream tokens in the cache when stream c opened."""
-    streams = [0]                                  # stream of each matrix row
-    mask = np.ones((1, prefix_len), dtype=bool)    # the layout stream sees X
+    ``(stream, index, row)`` with the Boolean row used for that token, over
+    the cache positions present at that step; ``forks[c]`` = layout-stream
+    tokens in the cache when stream c opened."""
+    emitted, born = _run_event_trace(decide, max_steps)
     tags: List[Tuple[int, int]] = [(-1, i) for i in range(prefix_len)]
-    made: Dict[int, int] = {0: 0}                  # tokens a stream has cached
-    forks: Dict[int, int] = {}
+    step_of: List[int] = [-1] * prefix_len       # step that cached each column
+    width: List[int] = []                        # cache columns after each step
+    for t, toks in enumerate(emitted):
+        tags.extend(toks)
+        step_of.extend([t] * len(toks))
+        width.append(len(tags))
+    tag_stream = np.array([c for c, _ in tags], dtype=np.int64)
+    col_step = np.array(step_of, dtype=np.int64)
+
+    def row_after(c: int, t: int) -> np.ndarray:
+        """Stream c's row once step t's columns are in the cache (over every
+        column of the trace; columns cached later are never set)."""
+        own = (tag_stream == c) & (col_step <= t)
+        if c == 0:
+            given = tag_stream == -1
+        else:
+            given = row_after(0, born[c])
+        return given | own
+
     queries = []
-    for step in range(max_steps):
-        if not streams:
-            break
-        n = len(streams)
-        mask = np.concatenate([mask, np.eye(n, dtype=bool)], axis=1)
-        tags.extend((c, made[c]) for c in streams)
-        for r, c in enumerate(streams):
-            queries.append((c, made[c], mask[r].copy()))
-            made[c] += 1
-        events = [decide(step, c, c == 0) for c in streams]
-        opened = [mask[r].copy() for r, (c, ev) in enumerate(zip(streams, events)) if c == 0 and ev == "fork"]
-        alive = np.array([ev != "eos" for ev in events], dtype=bool)
-        mask = mask[alive]
-        streams = [c for c, a in zip(streams, alive) if a]
-        for row in opened:
-            cid = max(made) + 1
-            made[cid] = 0
-            forks[cid] = made[0]
-            streams.append(cid)
-            mask = np.concatenate([mask, row[None, :]], axis=0)
-        assert mask.shape == (len(streams), len(tags))
+    for t, toks in enumerate(emitted):
+        for c, i in toks:
+            queries.append((c, i, row_after(c, t)[: width[t]]))
+    forks = {c: sum(1 for t2 in range(tb + 1) for s, _ in emitted[t2] if s == 0)
+             for c, tb in born.items()}
     return tags, queries, forks
