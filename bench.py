@@ -94,6 +94,9 @@ def parse_args(argv=None):
                     help="skip the baselines (dense-mask SDPA, gather-varlen, per-stream decode)")
     ap.add_argument("--driver-steps", type=int, default=60,
                     help="decode-session steps timed on the decode workload's streams (0 to skip)")
+    ap.add_argument("--budget-pages", type=int, default=16,
+                    help="pages of complete traces decoded under a row budget (0 skips that leg)")
+    ap.add_argument("--budget-rows", type=int, default=256, help="rows per step in the budgeted leg")
     ap.add_argument("--decode-chunk", type=int, default=0,
                     help="decode plan: max keys per work item (0 = planner's choice)")
     ap.add_argument("--decode-target-wg", type=int, default=0,
@@ -716,6 +719,169 @@ def run_driver(args, torch, np, syn, pa, dev, wl):
     return res
 
 
+# ---------------------------------------------------------------- budgeted steps (critical-path order)
+
+class BudgetedReplay:
+    """A known decoding tree (the segments of complete traces: page roots
+    prefilled, every other segment decoded one token per step) run through a
+    DecodeSession with at most ``max_rows`` rows per step.  Each step the
+    session's open streams are ranked by ``padoc_session_select``: oldest
+    first, or (``by_priority``) by their remaining critical path from
+    ``padoc_tree_remaining`` at the step's progress (Sec. 3.1).  A segment is
+    opened once it has started (a child of a root with its page, a deeper one
+    once its parent has produced ``fork`` tokens; newly started segments in
+    index order) and closed once it has produced all its tokens.  ``launch``
+    runs a prepared step on the GPU (``launch(replay, n_kv_rows, n_q_rows)``);
+    without it the session is host-only and steps are committed."""
+
+    def __init__(self, pa, np, sess, nodes, max_rows, by_priority, launch=None):
+        self.pa, self.np, self.sess = pa, np, sess
+        self.nodes = [tuple(int(x) for x in nd) for nd in nodes]
+        n = len(self.nodes)
+        seg = np.zeros(n, dtype=pa.SEGMENT_DTYPE)
+        seg["parent"] = [nd[0] for nd in self.nodes]
+        seg["fork"] = [nd[1] for nd in self.nodes]
+        seg["len"] = [nd[2] for nd in self.nodes]
+        self.seg = seg
+        self.max_rows, self.by_priority, self.launch = int(max_rows), bool(by_priority), launch
+        self.produced = np.zeros(n, np.int32)
+        self.id_of = {}
+        self.seg_of = {}
+        self.open_ids = []
+        roots = [s for s in range(n) if self.nodes[s][0] < 0]
+        for s in roots:
+            self._open(s, -1, 0)
+        self._run([self.nodes[s][2] for s in roots], [0] * len(roots))
+        self._open_started()
+        for s in roots:
+            self._close(s)
+        self.steps = []   # advanced segments per step
+
+    def _open(self, s, parent_id, fork):
+        i = self.sess.open(parent_id, fork)
+        self.id_of[s], self.seg_of[i] = i, s
+        self.open_ids.append(i)
+
+    def _close(self, s):
+        i = self.id_of[s]
+        self.sess.close(i)
+        self.open_ids.remove(i)
+
+    def _run(self, n_new, n_query):
+        nk, nq, _ = self.sess.prepare(self.np.asarray(n_new, self.np.int32), self.np.asarray(n_query, self.np.int32))
+        if self.launch is None:
+            self.sess.commit()
+        else:
+            self.launch(self, nk, nq)
+        return nq
+
+    def _open_started(self):
+        # parents precede children, so one pass settles which have started
+        # and opening in index order opens every parent before its children
+        started = [False] * len(self.nodes)
+        for s, (parent, fork, _, _) in enumerate(self.nodes):
+            if parent >= 0:
+                started[s] = self.nodes[parent][0] < 0 or (started[parent] and self.produced[parent] >= fork)
+            if started[s] and s not in self.id_of:
+                p = self.id_of[parent]
+                self._open(s, p, fork if self.nodes[parent][0] >= 0 else self.nodes[parent][2])
+
+    def done(self):
+        return not self.open_ids
+
+    def step(self):
+        """One step; returns its query rows."""
+        np = self.np
+        pr = None
+        if self.by_priority:
+            rem = self.pa.tree_remaining(self.seg, self.produced)
+            pr = np.array([rem[self.seg_of[i]] for i in self.open_ids], np.int64)
+        n_new, n_query = self.sess.select(self.max_rows, pr)
+        nq = self._run(n_new, n_query)
+        adv = [self.seg_of[i] for i, x in zip(self.open_ids, n_new) if x]
+        for s in adv:
+            self.produced[s] += 1
+        self.steps.append(sorted(adv))
+        self._open_started()
+        for s in adv:
+            if self.produced[s] == self.nodes[s][2]:
+                self._close(s)
+        return nq
+
+
+def schedule_trace_pages(np, n_pages, seed):
+    """Complete decoding traces shaped as the decode workload's pages: per
+    page a 3,072-token prefix (prefilled), a 256-token layout stream and 24
+    content streams with forks f ~ U{1..255} (sorted) and lengths
+    L ~ U{1..1024}; the layout stream starts at its first token."""
+    rng = np.random.default_rng(seed)
+    nodes = []
+    for _ in range(n_pages):
+        L = rng.integers(1, 1025, size=24)
+        f = np.sort(rng.integers(1, 256, size=24))
+        r = len(nodes)
+        nodes.append((-1, 0, 3072, 0))
+        nodes.append((r, 3072, 256, 256))
+        nodes += [(r + 1, int(a), int(b), int(b)) for a, b in zip(f, L)]
+    return nodes
+
+
+def run_budgeted(args, torch, np, pa, dev):
+    """Steps to decode complete traces with a row budget per step, oldest
+    streams first against critical-path first (the remaining paths of
+    padoc_tree_remaining as the session's priorities), on the GPU (append +
+    attention each step, the loop waiting for each step's outputs)."""
+    nodes = schedule_trace_pages(np, args.budget_pages, args.seed + 11)
+    segs = np.zeros(len(nodes), dtype=pa.SEGMENT_DTYPE)
+    segs["parent"] = [x[0] for x in nodes]
+    segs["fork"] = [x[1] for x in nodes]
+    segs["len"] = [x[2] for x in nodes]
+    _, d_seq, d_crit = pa.tree_depths(segs)
+    decoded = int(d_seq.sum())
+    budget = args.budget_rows
+    Hq, Hkv, d = 16, 2, 128
+    tokens = sum(x[2] for x in nodes)
+    n_pool = tokens // 16 + len(nodes) + 1024
+    kc = torch.empty((n_pool, Hkv, d // 8, 16, 8), dtype=torch.bfloat16, device=dev)
+    vc = torch.empty((n_pool, Hkv, d, 16), dtype=torch.bfloat16, device=dev)
+    bt = torch.full((4 * n_pool,), -1, dtype=torch.int32, device=dev)
+    gen = torch.Generator(device=dev)
+    gen.manual_seed(args.seed + 29)
+    big = max(x[2] for x in nodes if x[0] < 0) * args.budget_pages
+    kv_buf = torch.randn((big, Hkv, d), generator=gen, device=dev).to(torch.bfloat16)
+    q_buf = torch.randn((max(budget, 1) + 64 * args.budget_pages, Hq, d), generator=gen, device=dev).to(torch.bfloat16)
+    o_buf = torch.empty_like(q_buf)
+    l_buf = torch.empty(q_buf.shape[:2], dtype=torch.float32, device=dev)
+
+    def launch(R, nk, nq):
+        R.sess.launch(q_buf[:nq] if nq else None, kv_buf[:nk], kv_buf[:nk], out=o_buf[:nq], lse=l_buf[:nq])
+
+    out = {"pages": args.budget_pages, "max_rows": budget, "decoded_tokens": decoded,
+           "d_crit_max": int(d_crit.max()), "lower_bound_steps": int(max(d_crit.max(), -(-decoded // budget)))}
+    for name, by_pr in (("oldest_first", False), ("critical_path_first", True)):
+        bt.fill_(-1)
+        sess = pa.DecodeSession(Hq, Hkv, d, n_pool, "bf16", k_cache=kc, v_cache=vc, block_table=bt)
+        R = BudgetedReplay(pa, np, sess, nodes, budget, by_pr, launch)
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        host = 0.0
+        rows = 0
+        while not R.done():
+            h0 = time.perf_counter()
+            rows += R.step()
+            host += time.perf_counter() - h0
+            torch.cuda.synchronize()   # a decoding loop waits for its outputs before it samples
+        wall = time.perf_counter() - t0
+        out[name] = {"steps": len(R.steps), "wall_s": wall, "host_s": host, "rows": rows,
+                     "tokens_per_s": rows / wall, "mean_rows_per_step": rows / max(1, len(R.steps))}
+        sess.destroy()
+        log(f"budgeted steps ({name}): {len(R.steps)} steps, {wall:.2f} s")
+    del kc, vc, bt, kv_buf, q_buf, o_buf, l_buf
+    torch.cuda.empty_cache()
+    out["steps_saved"] = out["oldest_first"]["steps"] - out["critical_path_first"]["steps"]
+    return out
+
+
 # ---------------------------------------------------------------- attainable rates on this box
 
 def attainable(torch, dev):
@@ -1269,6 +1435,8 @@ def main(argv=None) -> int:
                   for n in ("single_page_decode", "dense_page_mixed_step")]
     refs = None if args.no_baselines else attainable(torch, dev)
     drv = run_driver(args, torch, np, syn, pa, dev, wl) if args.driver_steps > 0 else None
+    if drv is not None and args.budget_pages > 0:
+        drv["budgeted"] = run_budgeted(args, torch, np, pa, dev)
     if not args.no_baselines:
         log("decode baselines: per-stream sequences without tree sharing")
         dec["baselines"] = decode_baselines(args, torch, np, syn, pa, dev, wl, dec["kernel_ms"])

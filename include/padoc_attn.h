@@ -247,6 +247,28 @@ padoc_status padoc_tree_layout(padoc_segment* seg, int32_t n, int32_t block_size
    0 <= fork <= len(parent); PADOC_ERR_TREE otherwise. */
 padoc_status padoc_tree_depths(const padoc_segment* seg, int32_t n, int64_t* d_seq, int64_t* d_crit);
 
+/* Remaining critical path of every segment from a point in decoding
+   (Sec. 3.1: the decoding depth of a page under ideal parallel scheduling is
+   its longest layout-content dependency path), host only.  progress[s] =
+   tokens segment s has produced so far (NULL: all 0; roots are page inputs,
+   prefilled, and their entry is not read).  A child of a root starts with
+   the page; a deeper segment starts once its parent has started and
+   produced the `fork` tokens it conditions on.  Every started segment
+   produces one token per step.  For a decoded segment s, remaining[s] =
+   steps until s and the segments below it that have not started yet have
+   produced all their tokens (counted from the step s starts in, if it has
+   not started): the larger of len(s) - progress[s] and, over
+   children c not started, fork(c) - progress[s] + remaining[c] (started
+   children are counted on their own).  For a root, steps until the whole
+   page has: the largest remaining[] of its started segments; with all
+   progress 0 this is d_crit of padoc_tree_depths.  Use: the priority of an
+   open stream when a step can take fewer rows than there are streams
+   (padoc_session_select).  Tree checks as padoc_tree_depths
+   (PADOC_ERR_TREE); PADOC_ERR_ARG when a progress lies outside [0, len] or
+   a segment that has not started has progress. */
+padoc_status padoc_tree_remaining(const padoc_segment* seg, int32_t n, const int32_t* progress,
+                                  int64_t* remaining);
+
 /* Validate the tree and build the schedule (host only; no HIP call). */
 padoc_status padoc_plan_create(const padoc_tree_desc* desc, padoc_plan** out);
 padoc_status padoc_plan_workspace_bytes(const padoc_plan* plan, size_t* bytes);
@@ -438,6 +460,20 @@ padoc_status padoc_session_open(padoc_session* session, int32_t parent, int32_t 
    and block-table region; a closed stream's tokens stay visible to the
    streams below it until they are released. */
 padoc_status padoc_session_close(padoc_session* session, int32_t id);
+
+/* Choose the open streams that advance in the next step when at most
+   max_rows rows fit in it (a serving loop's batch budget; 0 = no limit):
+   fills n_new[i] = n_query[i] = 1 for the chosen rows and 0 for the others
+   (one entry per open stream in ascending id, the arrays of
+   padoc_session_prepare).  priority (one entry per open stream, or NULL):
+   the rows with the largest priority are chosen, equal priorities in
+   ascending id; NULL chooses the oldest streams (ascending id).  With the
+   remaining critical paths of padoc_tree_remaining as priorities, the
+   streams that gate the longest dependency chains (a layout stream whose
+   later regions still have to open, long branches) go first.  Host only;
+   reads the session, changes nothing. */
+padoc_status padoc_session_select(const padoc_session* session, int32_t max_rows, const int64_t* priority,
+                                  int32_t* n_new, int32_t* n_query);
 
 /* Prepare the next step (host only).  n_new / n_query: one entry per open
    stream in ascending id (NULL = 1 each), 0 <= n_query[i] <= n_new[i].  On

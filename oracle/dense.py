@@ -48,7 +48,7 @@ __all__ = [
     "page_nodes", "canonical_layout", "ancestors", "visible_counts", "page_of",
     "dense_mask", "masked_attention", "tree_attention", "tree_attention_paged",
     "gather_paged", "paged_slots", "chunk_slot", "simulate_masked_parallel_decoding",
-    "visible_pair_count", "decoding_depths",
+    "visible_pair_count", "decoding_depths", "remaining_paths", "budgeted_decoding",
 ]
 
 Node = Tuple[int, int, int, int]   # (parent, fork, length, q_len)
@@ -392,6 +392,105 @@ def decoding_depths(nodes):
         start[s] = (start[parent] if nodes[parent][0] >= 0 else 0) + (fork if nodes[parent][0] >= 0 else 0)
         out[r] = (seq + n, max(crit, start[s] + n))
     return out
+
+
+def _started(nodes, produced):
+    """Which decoded segments have started: a child of a root with its page,
+    a deeper one once its parent has started and produced ``fork`` tokens
+    (Sec. 3.1 dependency: a content stream conditions on the layout tokens
+    before its region)."""
+    started = [False] * len(nodes)
+    for s, (parent, fork, _, _) in enumerate(nodes):
+        if parent < 0:
+            continue
+        if nodes[parent][0] < 0:
+            started[s] = True
+        else:
+            started[s] = started[parent] and produced[parent] >= fork
+    return started
+
+
+def remaining_paths(nodes, progress=None):
+    """Remaining critical path of every segment, by running the decoding:
+    from the state where segment s has produced ``progress[s]`` tokens,
+    every started segment produces one token per step (ideal parallel
+    scheduling, Sec. 3.1).  For a decoded segment s: the steps until s and
+    the segments below it that have not started yet are done, counted from
+    the step s starts in if it has not started.  For a root: the steps until
+    its whole page is done.  Returns an int64 array."""
+    nodes = _as_nodes(nodes)
+    n = len(nodes)
+    prog = [0] * n if progress is None else [int(x) for x in progress]
+    for s, nd in enumerate(nodes):
+        if nd[0] < 0:
+            prog[s] = 0
+    start_state = _started(nodes, prog)
+    root = page_of(nodes)
+    children: Dict[int, List[int]] = {}
+    for s, nd in enumerate(nodes):
+        if nd[0] >= 0:
+            children.setdefault(nd[0], []).append(s)
+
+    def group(s):
+        """Segments whose completion s waits for, as defined above."""
+        if nodes[s][0] < 0:
+            return [t for t in range(n) if root[t] == s and nodes[t][0] >= 0]
+        out, todo = [s], [c for c in children.get(s, []) if not start_state[c]]
+        while todo:
+            c = todo.pop()
+            out.append(c)
+            todo.extend(children.get(c, []))
+        return out
+
+    out = np.zeros(n, dtype=np.int64)
+    for s in range(n):
+        members = group(s)
+        produced = list(prog)
+        steps = 0
+        while any(produced[t] < nodes[t][2] for t in members):
+            started = _started(nodes, produced)
+            if nodes[s][0] < 0 or started[s]:
+                steps += 1
+            for t in range(n):
+                if nodes[t][0] >= 0 and started[t] and produced[t] < nodes[t][2]:
+                    produced[t] += 1
+        out[s] = steps
+    return out
+
+
+def budgeted_decoding(nodes, max_rows: int, by_priority: bool):
+    """Decode every page of the tree with at most ``max_rows`` rows per step.
+    Each step the started, unfinished segments are the candidates, ranked by
+    the order they started in (ties by segment index: the opening order);
+    if more than ``max_rows``, the first ``max_rows`` of them in that order
+    advance (``by_priority`` False), or those with the largest remaining
+    critical path (:func:`remaining_paths` at the step's progress), equal
+    paths in that order.  Returns the list of advanced segment sets, one per
+    step."""
+    nodes = _as_nodes(nodes)
+    n = len(nodes)
+    produced = [0] * n
+    opened_at: Dict[int, int] = {}
+    steps = []
+    step = 0
+    while True:
+        started = _started(nodes, produced)
+        for s in range(n):
+            if started[s] and s not in opened_at:
+                opened_at[s] = step
+        cand = [s for s in range(n) if nodes[s][0] >= 0 and started[s] and produced[s] < nodes[s][2]]
+        if not cand:
+            return steps
+        cand.sort(key=lambda s: (opened_at[s], s))
+        if 0 < max_rows < len(cand):
+            if by_priority:
+                rem = remaining_paths(nodes, produced)
+                cand = sorted(cand, key=lambda s: -int(rem[s]))   # stable: keeps the opening order
+            cand = cand[:max_rows]
+        for s in cand:
+            produced[s] += 1
+        steps.append(sorted(cand))
+        step += 1
 
 
 # --------------------------------------------------------------------------

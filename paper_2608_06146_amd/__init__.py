@@ -21,7 +21,7 @@ from . import _lib
 from ._lib import PadocError, SEGMENT_DTYPE, WORK_DTYPE, RANGE_DTYPE, BWD_DTYPE
 
 __all__ = ["TreePlan", "segments_from_pages", "segments_layout", "tree_attn_fwd", "tree_attn_bwd", "branch_decode",
-           "DecodeSession", "tree_depths", "PadocError", "SEGMENT_DTYPE", "version", "set_kernel_events", "make_workspace"]
+           "DecodeSession", "tree_depths", "tree_remaining", "PadocError", "SEGMENT_DTYPE", "version", "set_kernel_events", "make_workspace"]
 
 _DTYPES = {"f32": _lib.F32, "fp32": _lib.F32, "float32": _lib.F32, "bf16": _lib.BF16, "bfloat16": _lib.BF16}
 
@@ -82,6 +82,24 @@ def tree_depths(segments: np.ndarray):
                                             d_crit.ctypes.data))
     roots = np.nonzero(segs["parent"] < 0)[0]
     return roots, d_seq[roots], d_crit[roots]
+
+
+def tree_remaining(segments: np.ndarray, progress=None) -> np.ndarray:
+    """Remaining critical path of every segment (``padoc_tree_remaining``,
+    Sec. 3.1) when segment s has produced ``progress[s]`` tokens (None: 0);
+    int64, one entry per segment."""
+    segs = np.ascontiguousarray(segments, dtype=SEGMENT_DTYPE)
+    n = len(segs)
+    prog = None
+    if progress is not None:
+        prog = np.ascontiguousarray(progress, dtype=np.int32)
+        if prog.shape != (n,):
+            raise ValueError(f"progress needs one entry per segment ({n}), got shape {prog.shape}")
+    out = np.zeros(n, np.int64)
+    _lib.check(_lib.lib().padoc_tree_remaining(segs.ctypes.data if n else None, n,
+                                               prog.ctypes.data if prog is not None and n else None,
+                                               out.ctypes.data if n else None))
+    return out
 
 
 class TreePlan:
@@ -452,6 +470,23 @@ class DecodeSession:
     def close(self, stream_id: int) -> None:
         _lib.check(_lib.lib().padoc_session_close(self.handle, int(stream_id)))
         self.n_open -= 1
+
+    def select(self, max_rows: int, priority=None):
+        """``(n_new, n_query)`` for a step that takes at most ``max_rows``
+        rows (``padoc_session_select``): the open streams with the largest
+        ``priority`` (one entry per open stream, ascending id), or the oldest
+        when ``priority`` is None."""
+        n_new = np.zeros(self.n_open, np.int32)
+        n_query = np.zeros(self.n_open, np.int32)
+        pr = None
+        if priority is not None:
+            pr = np.ascontiguousarray(priority, dtype=np.int64)
+            if pr.shape != (self.n_open,):
+                raise ValueError(f"need one priority per open stream ({self.n_open}), got shape {pr.shape}")
+        _lib.check(_lib.lib().padoc_session_select(self.handle, int(max_rows),
+                                                   pr.ctypes.data if pr is not None and self.n_open else None,
+                                                   n_new.ctypes.data, n_query.ctypes.data))
+        return n_new, n_query
 
     def prepare(self, n_new=None, n_query=None):
         """Returns ``(n_kv_rows, n_q_rows, workspace_bytes)`` of the step."""

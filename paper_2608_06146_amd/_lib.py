@@ -89,7 +89,7 @@ EXPORTED = [
     "padoc_plan_backward_workspace_bytes", "padoc_tree_attn_bwd",
     "padoc_session_create", "padoc_session_destroy", "padoc_session_open", "padoc_session_close",
     "padoc_session_prepare", "padoc_session_launch", "padoc_session_commit", "padoc_session_view_get",
-    "padoc_tree_depths",
+    "padoc_tree_depths", "padoc_tree_remaining", "padoc_session_select",
 ]
 
 _lib = None
@@ -129,6 +129,8 @@ def lib():
     L.padoc_session_commit.argtypes = [vp]
     L.padoc_session_view_get.argtypes = [vp, C.POINTER(SessionView)]
     L.padoc_tree_depths.argtypes = [vp, i32, vp, vp]
+    L.padoc_tree_remaining.argtypes = [vp, i32, vp, vp]
+    L.padoc_session_select.argtypes = [vp, i32, vp, vp, vp]
     L.padoc_last_error.argtypes = []
     L.padoc_last_error.restype = C.c_char_p
     L.padoc_set_kernel_events.argtypes = [vp, vp]
@@ -139,7 +141,8 @@ def lib():
                  "padoc_plan_upload", "padoc_branch_decode_resident", "padoc_set_kernel_events",
                  "padoc_plan_backward_workspace_bytes", "padoc_tree_attn_bwd", "padoc_session_create",
                  "padoc_session_open", "padoc_session_close", "padoc_session_prepare", "padoc_session_launch",
-                 "padoc_session_commit", "padoc_session_view_get", "padoc_tree_depths"):
+                 "padoc_session_commit", "padoc_session_view_get", "padoc_tree_depths",
+                 "padoc_tree_remaining", "padoc_session_select"):
         getattr(L, name).restype = C.c_int
     _lib = L
     return L

@@ -1056,6 +1056,58 @@ extern "C" padoc_status padoc_tree_depths(const padoc_segment* seg, int32_t n, i
   return PADOC_OK;
 }
 
+extern "C" padoc_status padoc_tree_remaining(const padoc_segment* seg, int32_t n, const int32_t* progress,
+                                             int64_t* remaining) {
+  clear_error();
+  if (n < 0) return set_error(PADOC_ERR_ARG, "n = %d is negative", n);
+  if (n > 0 && (!seg || !remaining)) return set_error(PADOC_ERR_ARG, "null pointer");
+  auto done = [&](int32_t s) -> int32_t { return progress ? progress[s] : 0; };
+  try {
+    // started: a child of a root starts with the page; deeper, once its
+    // parent has started and produced the `fork` tokens it conditions on
+    std::vector<int32_t> root(n);
+    std::vector<char> started(n, 0);
+    for (int32_t s = 0; s < n; ++s) {
+      const padoc_segment& g = seg[s];
+      if (g.len < 0) return set_error(PADOC_ERR_TREE, "segment %d: negative length", s);
+      if (g.parent < -1 || g.parent >= s)
+        return set_error(PADOC_ERR_TREE, "segment %d: parent %d is not an earlier segment", s, g.parent);
+      if (g.parent < 0) {
+        root[s] = s;
+        continue;  // roots are prefilled: their progress is not read
+      }
+      const int32_t p = g.parent;
+      if (g.fork < 0 || g.fork > seg[p].len)
+        return set_error(PADOC_ERR_TREE, "segment %d: fork %d outside [0, %d]", s, g.fork, seg[p].len);
+      root[s] = root[p];
+      started[s] = seg[p].parent < 0 || (started[p] && done(p) >= g.fork);
+      if (done(s) < 0 || done(s) > g.len)
+        return set_error(PADOC_ERR_ARG, "segment %d: progress %d outside [0, %d]", s, done(s), g.len);
+      if (done(s) > 0 && !started[s])
+        return set_error(PADOC_ERR_ARG, "segment %d has progress %d before its parent reached its fork", s, done(s));
+    }
+    // Children have larger indices than their parents, so one pass from the
+    // last segment down sees every child's remaining path before its parent.
+    // A decoded segment's path: its own tokens still to come, or, through a
+    // child not started yet, the steps until that child's fork point plus
+    // the child's whole path.  Started segments run on their own: the page
+    // ends with the longest of their paths.
+    for (int32_t s = 0; s < n; ++s) remaining[s] = 0;
+    for (int32_t s = n - 1; s >= 0; --s) {
+      const padoc_segment& g = seg[s];
+      if (g.parent < 0) continue;
+      remaining[s] = std::max<int64_t>(remaining[s], (int64_t)g.len - done(s));
+      if (started[s])
+        remaining[root[s]] = std::max(remaining[root[s]], remaining[s]);
+      else
+        remaining[g.parent] = std::max(remaining[g.parent], (int64_t)(g.fork - done(g.parent)) + remaining[s]);
+    }
+  } catch (const std::bad_alloc&) {
+    return set_error(PADOC_ERR_ARG, "out of host memory");
+  }
+  return PADOC_OK;
+}
+
 extern "C" padoc_status padoc_plan_create(const padoc_tree_desc* d, padoc_plan** out) {
   clear_error();
   if (!out) return set_error(PADOC_ERR_ARG, "out is null");

@@ -203,6 +203,31 @@ extern "C" padoc_status padoc_session_close(padoc_session* s, int32_t id) {
   return PADOC_OK;
 }
 
+extern "C" padoc_status padoc_session_select(const padoc_session* s, int32_t max_rows, const int64_t* priority,
+                                             int32_t* n_new, int32_t* n_query) {
+  clear_error();
+  padoc_status st = check_session(s);
+  if (st != PADOC_OK) return st;
+  const size_t R = s->open_ids.size();
+  if (R > 0 && (!n_new || !n_query)) return set_error(PADOC_ERR_ARG, "null pointer");
+  if (max_rows < 0) return set_error(PADOC_ERR_ARG, "max_rows = %d is negative", max_rows);
+  try {
+    std::vector<int32_t> order(R);
+    for (size_t i = 0; i < R; ++i) order[i] = (int32_t)i;
+    const size_t take = max_rows == 0 ? R : std::min(R, (size_t)max_rows);
+    // rows are in ascending stream id, so without priorities the first
+    // `take` rows are the oldest streams; with them, the largest priority
+    // first, equal priorities by ascending id
+    if (priority && take < R)
+      std::stable_sort(order.begin(), order.end(), [&](int32_t a, int32_t b) { return priority[a] > priority[b]; });
+    for (size_t i = 0; i < R; ++i) n_new[i] = n_query[i] = 0;
+    for (size_t i = 0; i < take; ++i) n_new[order[i]] = n_query[order[i]] = 1;
+  } catch (const std::bad_alloc&) {
+    return set_error(PADOC_ERR_ARG, "out of host memory");
+  }
+  return PADOC_OK;
+}
+
 extern "C" padoc_status padoc_session_prepare(padoc_session* s, const int32_t* n_new_in, const int32_t* n_query_in,
                                               int32_t* n_kv_rows, int32_t* n_q_rows, size_t* workspace_bytes) {
   clear_error();

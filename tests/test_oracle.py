@@ -466,3 +466,106 @@ def test_P9_depths_equal_alg1_step_counts(seed):
     d_seq, d_crit = ot.decoding_depths(nodes)[0]
     assert d_seq == len(queries)
     assert d_crit == steps
+
+
+# ---------------------------------------------------------------- P10 remaining paths, budgeted steps
+
+def _worked_page():
+    return [(-1, 0, 50, 0), (0, 50, 12, 12), (1, 3, 20, 20), (1, 7, 2, 2), (1, 12, 5, 5),
+            (2, 4, 9, 9), (5, 9, 3, 3), (2, 20, 8, 8)]
+
+
+def test_P10_remaining_paths_of_the_worked_page():
+    """The worked page of P9 by hand.  From the start every segment's path
+    is counted from its own start: layout max(12, 3+20+8, 3+4+9+3, 7+2,
+    12+5) = 31 (= D_crit); branch 2: max(20, 4+9+3, 20+8) = 28; branch 5:
+    9+3 = 12.  After the layout has produced 5 tokens and branch 2 one
+    (branch 3 not yet: it starts at 7): layout max(12-5, 7-5+2, 12-5+5) =
+    12; branch 2: max(19, 4-1+12, 20-1+8) = 27; the page: max(12, 27) = 27
+    (the started segments 1 and 2)."""
+    nodes = _worked_page()
+    assert ot.remaining_paths(nodes).tolist() == [31, 31, 28, 2, 5, 12, 3, 8]
+    prog = [0, 5, 1, 0, 0, 0, 0, 0]
+    assert ot.remaining_paths(nodes, prog).tolist() == [27, 12, 27, 2, 5, 12, 3, 8]
+
+
+@pytest.mark.parametrize("seed", range(8))
+def test_P10_root_path_is_the_critical_path(seed):
+    """From the start, each root's remaining path is its page's D_crit."""
+    nodes = [(a.parent, a.fork, a.length, a.q_len)
+             for a in syn.random_tree(seed, n_pages=2, max_len=6, max_depth=4)]
+    dep = ot.decoding_depths(nodes)
+    rem = ot.remaining_paths(nodes)
+    for r, (_, crit) in dep.items():
+        assert rem[r] == crit
+
+
+def _brute_force_min_steps(nodes, max_rows):
+    """Fewest steps to decode the tree with at most max_rows segments
+    advancing per step, by breadth-first search over progress states
+    (tiny trees only)."""
+    import itertools
+    n = len(nodes)
+    dec = [s for s in range(n) if nodes[s][0] >= 0]
+    start = tuple(0 for _ in range(n))
+    frontier, seen, steps = {start}, {start}, 0
+    while True:
+        if any(all(st[s] == nodes[s][2] for s in dec) for st in frontier):
+            return steps
+        nxt = set()
+        for st in frontier:
+            started = ot._started(nodes, list(st))
+            cand = [s for s in dec if started[s] and st[s] < nodes[s][2]]
+            for k in range(1, min(max_rows, len(cand)) + 1):
+                for pick in itertools.combinations(cand, k):
+                    t = list(st)
+                    for s in pick:
+                        t[s] += 1
+                    t = tuple(t)
+                    if t not in seen:
+                        seen.add(t)
+                        nxt.add(t)
+        frontier, steps = nxt, steps + 1
+
+
+@pytest.mark.parametrize("seed", range(6))
+def test_P10_budgeted_steps_bounds(seed):
+    """Every schedule advances at most max_rows segments a step, decodes
+    every token exactly once, and takes at least max(D_crit, D_seq /
+    max_rows) steps; with room for every started segment both orders take
+    exactly D_crit steps."""
+    nodes = [(a.parent, a.fork, a.length, a.q_len)
+             for a in syn.random_tree(seed + 3, n_pages=2, max_len=7, max_depth=4, max_children=3)]
+    dep = ot.decoding_depths(nodes)
+    d_seq = sum(v[0] for v in dep.values())
+    d_crit = max(v[1] for v in dep.values())
+    for B in (1, 2, 3, 1000):
+        for by_pr in (False, True):
+            steps = ot.budgeted_decoding(nodes, B, by_pr)
+            assert all(len(x) <= B for x in steps)
+            count = {}
+            for x in steps:
+                for s in x:
+                    count[s] = count.get(s, 0) + 1
+            assert all(count.get(s, 0) == nodes[s][2] for s in range(len(nodes)) if nodes[s][0] >= 0)
+            assert len(steps) >= max(d_crit, -(-d_seq // B))
+            if B == 1000:
+                assert len(steps) == d_crit
+
+
+@pytest.mark.parametrize("seed", range(6))
+def test_P10_critical_path_first_is_optimal_on_independent_streams(seed):
+    """Streams that fork nothing (chains below a root): taking the longest
+    remaining path first is optimal -- checked against an exhaustive search
+    of every schedule on small cases -- and oldest first is not always."""
+    rng = np.random.default_rng(seed)
+    n = int(rng.integers(3, 5))
+    nodes = [(-1, 0, 4, 0)] + [(0, 4, int(x), int(x)) for x in rng.integers(1, 5, size=n)]
+    for B in (1, 2):
+        best = _brute_force_min_steps(nodes, B)
+        assert len(ot.budgeted_decoding(nodes, B, True)) == best
+        assert len(ot.budgeted_decoding(nodes, B, False)) >= best
+    # a case where the order matters: short streams opened first
+    nodes = [(-1, 0, 4, 0), (0, 4, 1, 1), (0, 4, 1, 1), (0, 4, 4, 4)]
+    assert len(ot.budgeted_decoding(nodes, 2, True)) == _brute_force_min_steps(nodes, 2) == 4
+    assert len(ot.budgeted_decoding(nodes, 2, False)) == 5

@@ -254,3 +254,104 @@ def test_steps_with_no_open_stream_and_closed_parents():
     sess.close(b)
     v = sess.view()
     assert len(v["seg"]) == 0 and v["free_blocks"] == 32
+
+
+# ---------------------------------------------------------------- remaining paths and budgeted steps
+
+def _segs_of(nodes):
+    seg = np.zeros(len(nodes), dtype=pa.SEGMENT_DTYPE)
+    seg["parent"] = [x[0] for x in nodes]
+    seg["fork"] = [x[1] for x in nodes]
+    seg["len"] = [x[2] for x in nodes]
+    return seg
+
+
+def _random_states(nodes, rng, count):
+    """Reachable progress states: random started segments advance."""
+    from oracle import dense as od
+    prog = [0] * len(nodes)
+    out = [list(prog)]
+    for _ in range(count):
+        st = od._started(nodes, prog)
+        cand = [s for s in range(len(nodes)) if nodes[s][0] >= 0 and st[s] and prog[s] < nodes[s][2]]
+        if not cand:
+            break
+        for s in cand:
+            if rng.random() < 0.6:
+                prog[s] += 1
+        out.append(list(prog))
+    return out
+
+
+@pytest.mark.parametrize("seed", range(10))
+def test_tree_remaining_matches_oracle(seed):
+    import padoc_synth as syn
+    from oracle import dense as od
+    nodes = [(a.parent, a.fork, a.length, a.q_len)
+             for a in syn.random_tree(seed, n_pages=3, max_len=6, max_depth=5, max_children=3)]
+    segs = _segs_of(nodes)
+    rng = np.random.default_rng(seed)
+    for prog in _random_states(nodes, rng, 12):
+        got = pa.tree_remaining(segs, prog)
+        want = od.remaining_paths(nodes, prog)
+        assert got.tolist() == want.tolist(), prog
+    _, _, crit = pa.tree_depths(segs)
+    roots = [s for s in range(len(nodes)) if nodes[s][0] < 0]
+    assert pa.tree_remaining(segs)[roots].tolist() == crit.tolist()
+
+
+def test_tree_remaining_errors():
+    nodes = [(-1, 0, 5, 0), (0, 5, 4, 0), (1, 2, 3, 0)]
+    segs = _segs_of(nodes)
+    with pytest.raises(pa.PadocError):
+        pa.tree_remaining(segs, [0, 5, 0])      # progress past the length
+    with pytest.raises(pa.PadocError):
+        pa.tree_remaining(segs, [0, 1, 1])      # child progressed before its fork
+    with pytest.raises(pa.PadocError):
+        pa.tree_remaining(segs, [0, -1, 0])
+    bad = segs.copy()
+    bad["fork"][2] = 9                          # fork past the parent's length
+    with pytest.raises(pa.PadocError):
+        pa.tree_remaining(bad)
+    assert pa.tree_remaining(segs, [0, 2, 1]).tolist() == [2, 2, 2]
+
+
+def test_session_select_orders():
+    s = pa.DecodeSession(4, 2, 64, 64, "bf16")
+    r = s.open(-1, 0)
+    s.prepare(np.array([4], np.int32), np.array([0], np.int32))
+    s.commit()
+    ids = [s.open(r, 4) for _ in range(5)]
+    s.close(r)
+    n_new, n_q = s.select(0)
+    assert n_new.tolist() == [1] * 5 and n_q.tolist() == [1] * 5
+    n_new, _ = s.select(2)
+    assert n_new.tolist() == [1, 1, 0, 0, 0]            # the oldest
+    n_new, n_q = s.select(3, [5, 9, 5, 9, 1])
+    assert n_new.tolist() == [1, 1, 0, 1, 0]            # 9, 9, then the older 5
+    assert n_q.tolist() == n_new.tolist()
+    assert len(ids) == 5
+    s.destroy()
+
+
+@pytest.mark.parametrize("seed", range(8))
+def test_budgeted_replay_matches_oracle(seed):
+    """The session driven by padoc_session_select (oldest first, or with
+    padoc_tree_remaining as priorities) advances, step by step, exactly the
+    segments of the oracle's budgeted decoding."""
+    import bench
+    import padoc_synth as syn
+    from oracle import dense as od
+    nodes = [(a.parent, a.fork, a.length, a.q_len)
+             for a in syn.random_tree(seed + 40, n_pages=2, max_len=7, max_depth=4, max_children=3)]
+    if not any(x[0] >= 0 for x in nodes):
+        pytest.skip("no decoded segment")
+    for B in (1, 2, 3, 0):
+        for by_pr in (False, True):
+            s = pa.DecodeSession(4, 2, 64, 4096, "bf16")
+            R = bench.BudgetedReplay(pa, np, s, nodes, B, by_pr)
+            while not R.done():
+                R.step()
+            want = od.budgeted_decoding(nodes, B, by_pr)
+            assert R.steps == want, (B, by_pr)
+            s.destroy()

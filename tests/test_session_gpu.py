@@ -216,3 +216,65 @@ def test_decoupled_mode_with_branch_decode():
         O_ref, L_ref = oracle.tree_attention(nodes, q64, K, V, 1.0 / math.sqrt(d), Hq, Hkv)
         _check(f"decoupled step {step}", o, lse, O_ref, L_ref, "bf16")
         sess.commit()
+
+
+@pytest.mark.parametrize("by_priority", [False, True])
+def test_budgeted_steps_attention(by_priority):
+    """Complete traces decoded with at most 3 rows per step, the rows chosen
+    by padoc_session_select (oldest first, or by padoc_tree_remaining's
+    critical paths): every step's outputs against the oracle's packed tree
+    attention over the test's own record of every segment's K/V rows."""
+    import bench
+    dtype = "bf16"
+    Hq, Hkv, d = 8, 2, 64
+    scale = 1.0 / math.sqrt(d)
+    rng = np.random.default_rng(31)
+    nodes = []
+    for _ in range(2):
+        r = len(nodes)
+        nodes.append((-1, 0, 40, 0))
+        nodes.append((r, 40, 12, 12))
+        for f, L in zip(sorted(rng.integers(1, 12, size=4)), rng.integers(1, 9, size=4)):
+            nodes.append((r + 1, int(f), int(L), int(L)))
+    sess = _session(Hq, Hkv, d, dtype, n_blocks=128, cap=1024)
+    rec_k = {s: np.zeros((0, Hkv, d)) for s in range(len(nodes))}
+    rec_v = {s: np.zeros((0, Hkv, d)) for s in range(len(nodes))}
+
+    def launch(R, nk, nq):
+        s = R.sess
+        view = s.view(block_table=False)
+        row_seg = [R.seg_of[int(i)] for i in view["row_id"]]
+        new_off = view["new_off"]
+        kt, k64 = _draw(rng, (nk, Hkv, d), dtype)
+        vt, v64 = _draw(rng, (nk, Hkv, d), dtype)
+        qt, q64 = _draw(rng, (nq, Hq, d), dtype)
+        qlen = {}
+        for i, sg in enumerate(row_seg):
+            a, b = int(new_off[i]), int(new_off[i + 1])
+            rec_k[sg] = np.concatenate([rec_k[sg], k64[a:b]])
+            rec_v[sg] = np.concatenate([rec_v[sg], v64[a:b]])
+            qlen[sg] = (b - a) if nq else 0
+        print(f"[case] budgeted steps priority={by_priority}: rows {len(row_seg)} new {nk} queries {nq}", flush=True)
+        o, lse = s.launch(qt.cuda() if nq else None, kt.cuda(), vt.cuda())
+        torch.cuda.synchronize()
+        if not nq:
+            return
+        # the record's tree: every segment opened so far, in opening (id) order
+        order = sorted(R.seg_of.items())
+        segs = [sg for _, sg in order]
+        pos = {sg: j for j, sg in enumerate(segs)}
+        tree = []
+        for sg in segs:
+            p, f = nodes[sg][0], nodes[sg][1]
+            tree.append((pos[p] if p >= 0 else -1, f if p >= 0 and nodes[p][0] >= 0 else (len(rec_k[p]) if p >= 0 else 0),
+                         len(rec_k[sg]), qlen.get(sg, 0)))
+        K = np.concatenate([rec_k[sg] for sg in segs])
+        V = np.concatenate([rec_v[sg] for sg in segs])
+        O_ref, L_ref = oracle.tree_attention(tree, q64, K, V, scale, Hq, Hkv)
+        _check(f"budgeted step priority={by_priority}", o, lse, O_ref, L_ref, dtype)
+
+    R = bench.BudgetedReplay(pa, np, sess, nodes, 3, by_priority, launch=launch)
+    while not R.done():
+        R.step()
+    want = __import__("oracle.dense", fromlist=["budgeted_decoding"]).budgeted_decoding(nodes, 3, by_priority)
+    assert R.steps == want
