@@ -15,10 +15,11 @@
 //              item's key ranges); per 64-key tile S^T, dP^T, dS^T and
 //              dQ^T += K^T dS^T; dQ is complete per item and written directly
 //   bwd_dkdv   key-major: up to 128 keys of one segment against the query
-//              columns that see them, 32 columns per step; waves 0-3 compute
-//              dV^T += dO^T P for 32 keys each, waves 4-7 dK^T += Q^T dS for
-//              the same keys; results go to fp32 rows (stored by an item that
-//              holds the whole run, added by the pieces of a split run)
+//              columns that see them, 32 columns per step; waves 4-7 compute
+//              S and P for 32 keys each and dK^T += Q^T dS, waves 0-3
+//              dV^T += dO^T P for the same keys with P handed over through
+//              LDS; results go to fp32 rows (stored by an item that holds the
+//              whole run, added by the pieces of a split run)
 //   bwd_finalize  fp32 accumulators -> bf16 dK, dV (round to nearest even)
 // All products are v_mfma_f32_32x32x16_bf16 with fp32 accumulation.  An
 // operand whose contraction index is not contiguous in memory (K^T for dQ,
@@ -271,6 +272,9 @@ __global__ __launch_bounds__(kThreads) void bwd_dkdv_kernel(BwdParams p) {
     int lm[32];           // keys of the item the column sees
   };
   __shared__ __attribute__((aligned(16))) Stage st[2];
+  // P of the block in bf16 per key group (wave & 3), as the dK wavefront's
+  // lanes hold it: [group][j][lane][8]
+  __shared__ __attribute__((aligned(16))) __bf16 Psh[4][2][64 * 8];
 
   const BwdRec b = p.bwd[blockIdx.x];
   const int tid = threadIdx.x;
@@ -377,57 +381,70 @@ __global__ __launch_bounds__(kThreads) void bwd_dkdv_kernel(BwdParams p) {
     return tile::tr_pair(blk + at(r0, c) + tr_o, blk + at(r0 + 8, c) + tr_o);
   };
 
-  // Block computation from one stage.  Fragments of each product group are
-  // requested together before its matrix products.
+  // Block computation from one stage.  The dK wavefront of each key group
+  // (wave w + 4) computes S and P and hands P (bf16, in its score registers'
+  // layout) to the dV wavefront of the same keys (wave w) through LDS; the
+  // dV wavefront reads it after the block's first barrier, so S and the
+  // exponentials run once per key group.  Fragments of each product group
+  // are requested together before its matrix products.
   auto compute = [&](const Stage& S) __attribute__((always_inline)) {
-    // S = Q K^T: columns on M, this wave's 32 keys on N.  Element i of a lane
-    // is column (i/4)*8 + hf*4 + i%4 of the block and key `key`.
     bf16x8_t fa[NKK];
-#pragma unroll
-    for (int kk = 0; kk < NKK; ++kk) fa[kk] = *reinterpret_cast<const bf16x8_t*>(&S.q[at(l32, 2 * kk + hf)]);
-    f32x16_t sc;
-#pragma unroll
-    for (int i = 0; i < 16; ++i) sc[i] = 0.f;
-#pragma unroll
-    for (int kk = 0; kk < NKK; ++kk) sc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[kk], bk[kk], sc, 0, 0, 0);
-    // P = exp(S - LSE), zero past each column's limit.  When every column
-    // of the block sees all 32 keys of this wavefront (limits are at most
-    // n_keys, so the keys are real), the mask is skipped.
-    float pr[16];
-    float lv[16];
-    int mv[16];
-#pragma unroll
-    for (int q4 = 0; q4 < 4; ++q4) {
-      const int cb = q4 * 8 + hf * 4;  // columns cb .. cb+3 = elements 4*q4 .. 4*q4+3
-      const float4 l4 = *reinterpret_cast<const float4*>(&S.ls[cb]);
-      const int4 m4 = *reinterpret_cast<const int4*>(&S.lm[cb]);
-      lv[4 * q4] = l4.x, lv[4 * q4 + 1] = l4.y, lv[4 * q4 + 2] = l4.z, lv[4 * q4 + 3] = l4.w;
-      mv[4 * q4] = m4.x, mv[4 * q4 + 1] = m4.y, mv[4 * q4 + 2] = m4.z, mv[4 * q4 + 3] = m4.w;
-    }
-    int mn = mv[0];
-#pragma unroll
-    for (int i = 1; i < 16; ++i) mn = min(mn, mv[i]);
-    mn = min(mn, __shfl_xor(mn, 32));  // lanes l and l^32 hold the other 16 columns
-    if (__builtin_amdgcn_readfirstlane((int)(mn >= key_hi))) {
-#pragma unroll
-      for (int i = 0; i < 16; ++i) pr[i] = fast_exp2(fmaf(sc[i], sl2, -lv[i]));
-    } else {
-#pragma unroll
-      for (int i = 0; i < 16; ++i) pr[i] = key < mv[i] ? fast_exp2(fmaf(sc[i], sl2, -lv[i])) : 0.f;
-    }
     bf16x8_t fb[2 * NDB];
-    if (!kwave) {
-      // dV^T += dO^T P: d on M (block db), keys on N, columns on K
+    float pr[16];
+    if (kwave) {
+      // S = Q K^T: columns on M, this wave's 32 keys on N.  Element i of a
+      // lane is column (i/4)*8 + hf*4 + i%4 of the block and key `key`.
 #pragma unroll
-      for (int j = 0; j < 2; ++j)
+      for (int kk = 0; kk < NKK; ++kk) fa[kk] = *reinterpret_cast<const bf16x8_t*>(&S.q[at(l32, 2 * kk + hf)]);
+      f32x16_t sc;
 #pragma unroll
-        for (int db = 0; db < NDB; ++db)
-          fb[j * NDB + db] = trf(S.g, j, db);
+      for (int i = 0; i < 16; ++i) sc[i] = 0.f;
+#pragma unroll
+      for (int kk = 0; kk < NKK; ++kk) sc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[kk], bk[kk], sc, 0, 0, 0);
+      // P = exp(S - LSE), zero past each column's limit.  When every column
+      // of the block sees all 32 keys of this wavefront (limits are at most
+      // n_keys, so the keys are real), the mask is skipped.
+      float lv[16];
+      int mv[16];
+#pragma unroll
+      for (int q4 = 0; q4 < 4; ++q4) {
+        const int cb = q4 * 8 + hf * 4;  // columns cb .. cb+3 = elements 4*q4 .. 4*q4+3
+        const float4 l4 = *reinterpret_cast<const float4*>(&S.ls[cb]);
+        const int4 m4 = *reinterpret_cast<const int4*>(&S.lm[cb]);
+        lv[4 * q4] = l4.x, lv[4 * q4 + 1] = l4.y, lv[4 * q4 + 2] = l4.z, lv[4 * q4 + 3] = l4.w;
+        mv[4 * q4] = m4.x, mv[4 * q4 + 1] = m4.y, mv[4 * q4 + 2] = m4.z, mv[4 * q4 + 3] = m4.w;
+      }
+      int mn = mv[0];
+#pragma unroll
+      for (int i = 1; i < 16; ++i) mn = min(mn, mv[i]);
+      mn = min(mn, __shfl_xor(mn, 32));  // lanes l and l^32 hold the other 16 columns
+      if (__builtin_amdgcn_readfirstlane((int)(mn >= key_hi))) {
+#pragma unroll
+        for (int i = 0; i < 16; ++i) pr[i] = fast_exp2(fmaf(sc[i], sl2, -lv[i]));
+      } else {
+#pragma unroll
+        for (int i = 0; i < 16; ++i) pr[i] = key < mv[i] ? fast_exp2(fmaf(sc[i], sl2, -lv[i])) : 0.f;
+      }
 #pragma unroll
       for (int j = 0; j < 2; ++j) {
         bf16x8_t pb;
 #pragma unroll
         for (int e = 0; e < 8; ++e) pb[e] = (__bf16)pr[8 * j + e];
+        *reinterpret_cast<bf16x8_t*>(&Psh[wave & 3][j][lane * 8]) = pb;
+      }
+    } else {
+#pragma unroll
+      for (int j = 0; j < 2; ++j)
+#pragma unroll
+        for (int db = 0; db < NDB; ++db)
+          fb[j * NDB + db] = trf(S.g, j, db);
+    }
+    __syncthreads();  // P of this block is in Psh
+    if (!kwave) {
+      // dV^T += dO^T P: d on M (block db), keys on N, columns on K
+#pragma unroll
+      for (int j = 0; j < 2; ++j) {
+        const bf16x8_t pb = *reinterpret_cast<const bf16x8_t*>(&Psh[wave][j][lane * 8]);
 #pragma unroll
         for (int db = 0; db < NDB; ++db)
           acc[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fb[j * NDB + db], pb, acc[db], 0, 0, 0);
