@@ -61,7 +61,7 @@ SQ_PASSES = {
     "sqC": "SQ_INSTS_MFMA SQ_INSTS_VALU SQ_INSTS_SALU SQ_INSTS_VMEM_RD SQ_INSTS_SMEM SQ_ACTIVE_INST_VMEM "
            "SQ_ACTIVE_INST_SCA SQ_INSTS_BRANCH GRBM_GUI_ACTIVE",
 }
-SQ_KERNELS = (FORWARD_KERNEL, DECODE_KERNELS[0])
+SQ_KERNELS = (FORWARD_KERNEL, DECODE_KERNELS[0], "bwd_dkdv_kernel<128>", "bwd_dq_kernel<128>")
 BACKWARD_KERNELS = ("bwd_prep_kernel<128>", "bwd_dq_kernel<128>", "bwd_dkdv_kernel<128>", "bwd_finalize_kernel")
 COPY_KERNEL = "__amd_rocclr_copyBuffer"
 COPY_BYTES = 1 << 30
@@ -250,7 +250,8 @@ def summarize_counters(d: str) -> None:
                     k = short_kernel_name(r["Kernel_Name"])
                     vals.setdefault(k, {}).setdefault(r["Counter_Name"], []).append(float(r["Counter_Value"]))
                     dur.setdefault(k, []).append((int(r["End_Timestamp"]) - int(r["Start_Timestamp"])) * 1e-3)
-    lines = ["# SQ counters: bench.py default workloads (packed forward, 8 pages; concurrent decode, 64 pages)", "",
+    lines = ["# SQ counters: bench.py default workloads (packed forward, 8 pages, and its backward; concurrent "
+             "decode, 64 pages)", "",
              "Commands (GPU host, repository root as $R): as in kernel_trace_" + PROFILE_TAG + ".md; counters of",
              "each pass (one rocprofv3 run per pass, at most 8 SQ counters):", ""]
     for p, c in SQ_PASSES.items():
@@ -295,8 +296,8 @@ PROFILE_COMMANDS = """\
     rocprofv3 --pmc FETCH_SIZE -f csv -d $OUT/copy_fetch -o c -- python3 $R/bench.py --calibrate-copy
     rocprofv3 --pmc WRITE_SIZE -f csv -d $OUT/copy_write -o c -- python3 $R/bench.py --calibrate-copy
     for P in sqA sqB sqC; do   # counters of each pass: SQ_PASSES in bench.py
-      rocprofv3 --pmc <SQ_PASSES[$P]> --kernel-include-regex "tile_mfma|decode_step" -f csv -d $OUT/$P -o p -- \\
-          python3 $R/bench.py --steps 3 --warmup 1 --no-cpu-baseline --no-baselines --no-backward --driver-steps 0 --no-secondary --no-cold
+      rocprofv3 --pmc <SQ_PASSES[$P]> --kernel-include-regex "tile_mfma|decode_step|bwd_dkdv|bwd_dq" -f csv -d $OUT/$P -o p -- \\
+          python3 $R/bench.py --steps 3 --warmup 1 --no-cpu-baseline --no-baselines --driver-steps 0 --budget-pages 0 --no-secondary --no-cold
     done
     python3 $R/bench.py --summarize-profile $OUT
 """
@@ -364,9 +365,10 @@ def summarize_profile(d: str) -> None:
           "# roofline.traffic only while sources_sha256 matches the library sources.",
           f"sources_sha256: {source_digest()}",
           f"fetch_factor: {fetch_factor:.4f}", f"write_factor: {write_factor:.4f}"]
-    for k in DECODE_KERNELS + (FORWARD_KERNEL,):
-        tl.append(f"kernel {k} fetch_kib: {fetch[k]:.1f}")
-        tl.append(f"kernel {k} write_kib: {write[k]:.1f}")
+    for k in DECODE_KERNELS + (FORWARD_KERNEL,) + BACKWARD_KERNELS:
+        if k in fetch and k in write:
+            tl.append(f"kernel {k} fetch_kib: {fetch[k]:.1f}")
+            tl.append(f"kernel {k} write_kib: {write[k]:.1f}")
     tl += [f"decode_call_bytes: {dec_bytes:.0f}", f"forward_launch_bytes: {fwd_bytes:.0f}", ""]
     with open(TRAFFIC_SUMMARY, "w") as fh:
         fh.write("\n".join(tl))
