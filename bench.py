@@ -1010,6 +1010,54 @@ def run_forward(args, torch, np, syn, pa, dev):
     }
 
 
+def small_forward(args, torch, np, syn, pa, dev, name="tiny_fp32_forward"):
+    """A latency-bound forward configuration (the fp32 path): per-call time
+    (HIP events, median of the calls and after a cache flush) and, with the
+    CPU leg, every output row against the oracle."""
+    wl = syn.make_workload(name, args.seed)
+    Hq, Hkv, d = wl.num_heads_q, wl.num_heads_kv, wl.head_dim
+    T = syn.count_tokens(wl.pages)
+    nq = syn.count_queries(wl.pages)
+    segs = pa.segments_from_pages(wl.pages, 0)
+    plan = pa.TreePlan(segs, Hq, Hkv, d, wl.dtype, 0, num_kv_rows=T, num_q_rows=nq)
+    q = syn.draw_normal((nq, Hq, d), args.seed, 1, wl.dtype, device=dev)
+    k = syn.draw_normal((T, Hkv, d), args.seed, 2, wl.dtype, device=dev)
+    v = syn.draw_normal((T, Hkv, d), args.seed, 3, wl.dtype, device=dev)
+    o = torch.empty_like(q)
+    lse = torch.empty(nq, Hq, dtype=torch.float32, device=dev)
+    ws = plan.workspace(dev)
+    ms, kms = timed_steps(lambda: pa.tree_attn_fwd(q, k, v, plan, out=o, lse=lse, workspace=ws),
+                          max(20, args.steps), args.warmup, torch, pa)
+    flush = torch.empty(1 << 28, dtype=torch.float32, device=dev)
+    cold = []
+    for _ in range(max(10, args.cold_steps // 5)):
+        flush.fill_(1.0)
+        b, a = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        b.record()  # creates the underlying events
+        a.record()
+        pa.set_kernel_events(b, a)
+        pa.tree_attn_fwd(q, k, v, plan, out=o, lse=lse, workspace=ws)
+        pa.set_kernel_events()
+        torch.cuda.synchronize()
+        cold.append(b.elapsed_time(a))
+    del flush
+    pairs = visible_pairs_of(segs)
+    res = {"workload": name, "dtype": wl.dtype, "tokens": T, "flops": 4 * d * Hq * pairs,
+           "kernel_us": statistics.median(kms) * 1e3, "kernel_us_cold_p50": statistics.median(cold) * 1e3,
+           "ms_per_step": ms, "bound": "latency"}
+    if not args.no_cpu_baseline:
+        import oracle
+        from oracle import dense as od
+        t0 = time.perf_counter()
+        O, L = oracle.tree_attention(od.page_nodes(wl.pages), q, k, v, 1.0 / math.sqrt(d), Hq, Hkv)
+        rows = np.arange(nq)
+        res["oracle"] = _compare(np, torch, o, lse, O, L, rows, wl.dtype)
+        res["oracle"]["oracle_s"] = time.perf_counter() - t0
+        log(f"oracle: {name} {nq} rows, O max-abs {res['oracle']['o_max_abs']:.3g}, "
+            f"{'ok' if res['oracle']['ok'] else 'FAILED'}")
+    return res
+
+
 # ---------------------------------------------------------------- baselines (measurement only)
 
 def _page_row_ranges(segs):
@@ -1247,7 +1295,13 @@ def cpu_info():
     model = ""
     try:
         out = subprocess.run(["lscpu"], capture_output=True, text=True, timeout=20).stdout
-        model = next((l.split(":", 1)[1].strip() for l in out.splitlines() if l.startswith("Model name")), "")
+        kv = {l.split(":", 1)[0].strip(): l.split(":", 1)[1].strip() for l in out.splitlines() if ":" in l}
+        model = kv.get("Model name", "")
+        # a virtual machine may name only the vendor line; family / model /
+        # stepping and the core count still identify the part
+        extra = [f"{k.lower()} {kv[k]}" for k in ("CPU family", "Model", "Stepping") if kv.get(k)]
+        if model and extra:
+            model += " (" + ", ".join(extra) + f"; {kv.get('CPU(s)', '?')} CPUs)"
     except (OSError, subprocess.SubprocessError):
         pass
     if not model:
@@ -1443,6 +1497,9 @@ def main(argv=None) -> int:
         log("decode baselines: per-stream sequences without tree sharing")
         dec["baselines"] = decode_baselines(args, torch, np, syn, pa, dev, wl, dec["kernel_ms"])
     fwd, fwd_check = None, None
+    small = None
+    if args.forward_workload != "none" and not args.no_secondary:
+        small = [small_forward(args, torch, np, syn, pa, dev)]
     if args.forward_workload != "none":
         fwd_t, fwd = run_forward(args, torch, np, syn, pa, dev)
         if not args.no_cpu_baseline:
@@ -1455,7 +1512,7 @@ def main(argv=None) -> int:
         parity = {"tolerance": {"bf16_max_abs": TOL["bf16"][0], "bf16_mean_abs": TOL["bf16"][1],
                                 "f32_max_abs": TOL["f32"][0]},
                   "decode": dec_or}
-        for x in others or []:
+        for x in (others or []) + (small or []):
             parity[x["workload"]] = x.pop("oracle")
         if fwd_check:
             parity.update(fwd_check)
@@ -1491,6 +1548,7 @@ def main(argv=None) -> int:
         "parity": parity,
         "decode": dec,
         "other_decode_configs": others,
+        "other_forward_configs": small,
         "attainable": refs,
         "driver": drv,
         "accounting": [depth_accounting(pa, syn, np, n, args.seed)
