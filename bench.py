@@ -97,6 +97,8 @@ def parse_args(argv=None):
     ap.add_argument("--budget-pages", type=int, default=16,
                     help="pages of complete traces decoded under a row budget (0 skips that leg)")
     ap.add_argument("--budget-rows", type=int, default=256, help="rows per step in the budgeted leg")
+    ap.add_argument("--budget-layers", type=int, default=28,
+                    help="attention calls per step in the budgeted leg (a model's layers over one tree)")
     ap.add_argument("--decode-chunk", type=int, default=0,
                     help="decode plan: max keys per work item (0 = planner's choice)")
     ap.add_argument("--decode-target-wg", type=int, default=0,
@@ -749,7 +751,12 @@ class BudgetedReplay:
         self.produced = np.zeros(n, np.int32)
         self.id_of = {}
         self.seg_of = {}
+        self.seg_by_id = np.full(n, -1, np.int64)   # session ids are 0, 1, ... in opening order
         self.open_ids = []
+        self.children = [[] for _ in range(n)]
+        for s, nd in enumerate(self.nodes):
+            if nd[0] >= 0:
+                self.children[nd[0]].append(s)
         roots = [s for s in range(n) if self.nodes[s][0] < 0]
         for s in roots:
             self._open(s, -1, 0)
@@ -762,6 +769,7 @@ class BudgetedReplay:
     def _open(self, s, parent_id, fork):
         i = self.sess.open(parent_id, fork)
         self.id_of[s], self.seg_of[i] = i, s
+        self.seg_by_id[i] = s
         self.open_ids.append(i)
 
     def _close(self, s):
@@ -777,16 +785,32 @@ class BudgetedReplay:
             self.launch(self, nk, nq)
         return nq
 
-    def _open_started(self):
-        # parents precede children, so one pass settles which have started
-        # and opening in index order opens every parent before its children
-        started = [False] * len(self.nodes)
-        for s, (parent, fork, _, _) in enumerate(self.nodes):
-            if parent >= 0:
-                started[s] = self.nodes[parent][0] < 0 or (started[parent] and self.produced[parent] >= fork)
-            if started[s] and s not in self.id_of:
-                p = self.id_of[parent]
-                self._open(s, p, fork if self.nodes[parent][0] >= 0 else self.nodes[parent][2])
+    def _open_started(self, advanced=None):
+        """Open the segments that have started and are not open yet, in index
+        order (every parent before its children).  Only children of
+        `advanced` (the segments that just produced a token) and, through
+        fork offsets of 0, their descendants can start after the first call."""
+        if advanced is None:
+            cand = [s for s in range(len(self.nodes)) if self.nodes[s][0] >= 0]
+        else:
+            cand = [c for s in advanced for c in self.children[s]]
+        new = []
+        seen = set()
+        while cand:
+            nxt = []
+            for s in cand:
+                if s in self.id_of or s in seen:
+                    continue
+                parent, fork = self.nodes[s][0], self.nodes[s][1]
+                root_child = self.nodes[parent][0] < 0
+                if root_child or ((parent in self.id_of or parent in seen) and self.produced[parent] >= fork):
+                    seen.add(s)
+                    new.append(s)
+                    nxt.extend(self.children[s])  # a fork of 0 starts with its parent
+            cand = nxt
+        for s in sorted(new):
+            parent, fork = self.nodes[s][0], self.nodes[s][1]
+            self._open(s, self.id_of[parent], fork if self.nodes[parent][0] >= 0 else self.nodes[parent][2])
 
     def done(self):
         return not self.open_ids
@@ -795,16 +819,15 @@ class BudgetedReplay:
         """One step; returns its query rows."""
         np = self.np
         pr = None
+        open_seg = self.seg_by_id[np.asarray(self.open_ids, np.int64)]
         if self.by_priority:
-            rem = self.pa.tree_remaining(self.seg, self.produced)
-            pr = np.array([rem[self.seg_of[i]] for i in self.open_ids], np.int64)
+            pr = self.pa.tree_remaining(self.seg, self.produced)[open_seg]
         n_new, n_query = self.sess.select(self.max_rows, pr)
         nq = self._run(n_new, n_query)
-        adv = [self.seg_of[i] for i, x in zip(self.open_ids, n_new) if x]
-        for s in adv:
-            self.produced[s] += 1
+        adv = open_seg[n_new > 0].tolist()
+        self.produced[adv] += 1
         self.steps.append(sorted(adv))
-        self._open_started()
+        self._open_started(adv)
         for s in adv:
             if self.produced[s] == self.nodes[s][2]:
                 self._close(s)
@@ -831,8 +854,10 @@ def schedule_trace_pages(np, n_pages, seed):
 def run_budgeted(args, torch, np, pa, dev):
     """Steps to decode complete traces with a row budget per step, oldest
     streams first against critical-path first (the remaining paths of
-    padoc_tree_remaining as the session's priorities), on the GPU (append +
-    attention each step, the loop waiting for each step's outputs)."""
+    padoc_tree_remaining as the session's priorities), on the GPU: each step
+    appends the new rows and runs the attention of `--budget-layers` layers
+    over the step's tree (the same caches stand in for every layer's), and
+    the loop waits for each step's outputs."""
     nodes = schedule_trace_pages(np, args.budget_pages, args.seed + 11)
     segs = np.zeros(len(nodes), dtype=pa.SEGMENT_DTYPE)
     segs["parent"] = [x[0] for x in nodes]
@@ -855,10 +880,28 @@ def run_budgeted(args, torch, np, pa, dev):
     o_buf = torch.empty_like(q_buf)
     l_buf = torch.empty(q_buf.shape[:2], dtype=torch.float32, device=dev)
 
-    def launch(R, nk, nq):
-        R.sess.launch(q_buf[:nq] if nq else None, kv_buf[:nk], kv_buf[:nk], out=o_buf[:nq], lse=l_buf[:nq])
+    import ctypes as C
+    from paper_2608_06146_amd import _lib
+    layers = max(1, args.budget_layers)
+    lws = torch.empty(64 << 20, dtype=torch.uint8, device=dev)
 
-    out = {"pages": args.budget_pages, "max_rows": budget, "decoded_tokens": decoded,
+    def launch(R, nk, nq):
+        # the step's append and its first layer's attention, then the
+        # attention of the other layers on the same tree (a model's decode
+        # step attends over one tree in every layer)
+        v = R.sess.view(block_table=False) if layers > 1 and nq else None  # the prepared step's plan
+        R.sess.launch(q_buf[:nq] if nq else None, kv_buf[:nk], kv_buf[:nk], out=o_buf[:nq], lse=l_buf[:nq])
+        if v is not None:
+            if v["workspace_bytes"] > lws.numel():
+                raise RuntimeError("budgeted leg: layer workspace too small")
+            st = torch.cuda.current_stream(dev).cuda_stream
+            for _ in range(layers - 1):
+                _lib.check(_lib.lib().padoc_branch_decode(
+                    C.c_void_p(v["plan"]), C.c_void_p(q_buf.data_ptr()), C.c_void_p(kc.data_ptr()),
+                    C.c_void_p(vc.data_ptr()), C.c_void_p(bt.data_ptr()), C.c_void_p(o_buf.data_ptr()),
+                    C.c_void_p(l_buf.data_ptr()), C.c_void_p(lws.data_ptr()), lws.numel(), C.c_void_p(st)))
+
+    out = {"pages": args.budget_pages, "max_rows": budget, "layers_per_step": layers, "decoded_tokens": decoded,
            "d_crit_max": int(d_crit.max()), "lower_bound_steps": int(max(d_crit.max(), -(-decoded // budget)))}
     for name, by_pr in (("oldest_first", False), ("critical_path_first", True)):
         bt.fill_(-1)
@@ -878,7 +921,7 @@ def run_budgeted(args, torch, np, pa, dev):
                      "tokens_per_s": rows / wall, "mean_rows_per_step": rows / max(1, len(R.steps))}
         sess.destroy()
         log(f"budgeted steps ({name}): {len(R.steps)} steps, {wall:.2f} s")
-    del kc, vc, bt, kv_buf, q_buf, o_buf, l_buf
+    del kc, vc, bt, kv_buf, q_buf, o_buf, l_buf, lws
     torch.cuda.empty_cache()
     out["steps_saved"] = out["oldest_first"]["steps"] - out["critical_path_first"]["steps"]
     return out
