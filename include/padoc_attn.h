@@ -269,19 +269,47 @@ padoc_status padoc_tree_depths(const padoc_segment* seg, int32_t n, int64_t* d_s
 padoc_status padoc_tree_remaining(const padoc_segment* seg, int32_t n, const int32_t* progress,
                                   int64_t* remaining);
 
-/* Validate the tree and build the schedule (host only; no HIP call). */
+/* Validate the tree and build the schedule (host only; no HIP call).  The
+   schedule lists, for every group of query columns, the key ranges their
+   ancestor sets make visible (Sec. 3.2: a node's tokens see its ancestors
+   and its own earlier tokens; App. C: a branch sees the layout stream up to
+   its fork offset), so keys outside them are never visited.  Packed plans
+   (block_size 0) serve padoc_tree_attn_fwd / _bwd, paged plans (16) the
+   decode calls.  *out receives a plan the caller destroys; on error *out is
+   NULL and padoc_last_error() names the offending segment or field. */
 padoc_status padoc_plan_create(const padoc_tree_desc* desc, padoc_plan** out);
 padoc_status padoc_plan_workspace_bytes(const padoc_plan* plan, size_t* bytes);
 padoc_status padoc_plan_export(const padoc_plan* plan, padoc_schedule_view* out);
 void padoc_plan_destroy(padoc_plan* plan);
 
-/* Packed forward.  Needs a plan with block_size == 0.  q/k/v/o are device
-   pointers in the plan's dtype, lse a device float pointer; workspace a
-   device buffer of at least padoc_plan_workspace_bytes; stream may be NULL
-   (the null stream). */
+/* Packed forward (App. C tree-varlen relation: the layout stream's queries
+   against its own causal keys after the prefix, each branch's queries
+   against the stream's first fork-offset tokens and its own causal keys;
+   App. E Attn equation).  Needs a plan with block_size == 0.  q/k/v/o are
+   device pointers in the plan's dtype, lse a device float pointer; workspace
+   a device buffer of at least padoc_plan_workspace_bytes; stream may be NULL
+   (the null stream).  Argument errors are returned before anything is
+   enqueued. */
 padoc_status padoc_tree_attn_fwd(const padoc_plan* plan, const void* q, const void* k,
                                  const void* v, void* o, float* lse, void* workspace,
                                  size_t workspace_bytes, hipStream_t stream);
+
+/* Rewrite paged K/V blocks from row layout into the paged layouts above,
+   for callers whose cache keeps each token's row contiguous: k_rows and
+   v_rows are [num_blocks, Hkv, 16, head_dim] (block, KV head, slot,
+   dimension; the layout a row-per-token paged cache uses), k_cache and
+   v_cache receive the same blocks in the chunk-major K and d-major V
+   layouts, block for block (so block ids and block tables are unchanged).
+   The decode step (App. E) reads the cached rows wherever they are stored;
+   this only changes where.  Device pointers, caller-owned, four distinct
+   buffers (no conversion in place); dtype bf16 or fp32 for all four;
+   head_dim 64 or 128.  Enqueued on `stream` (NULL: the null stream), no
+   allocation; call it once for a whole cache, or for the blocks a step
+   wrote by passing pointers to their first block and their count.
+   PADOC_ERR_ARG / _SHAPE / _DTYPE / _BOUNDS before anything is enqueued. */
+padoc_status padoc_cache_from_rows(const void* k_rows, const void* v_rows, void* k_cache, void* v_cache,
+                                   int64_t num_blocks, int32_t num_heads_kv, int32_t head_dim,
+                                   padoc_dtype dtype, hipStream_t stream);
 
 /* Decode step over a paged cache.  Needs a plan with block_size == 16.
    k_cache / v_cache follow the paged layouts above (chunk-major K, d-major

@@ -21,7 +21,7 @@ from . import _lib
 from ._lib import PadocError, SEGMENT_DTYPE, WORK_DTYPE, RANGE_DTYPE, BWD_DTYPE
 
 __all__ = ["TreePlan", "segments_from_pages", "segments_layout", "tree_attn_fwd", "tree_attn_bwd", "branch_decode",
-           "DecodeSession", "tree_depths", "tree_remaining", "PadocError", "SEGMENT_DTYPE", "version", "set_kernel_events", "make_workspace"]
+           "DecodeSession", "tree_depths", "tree_remaining", "cache_from_rows", "PadocError", "SEGMENT_DTYPE", "version", "set_kernel_events", "make_workspace"]
 
 _DTYPES = {"f32": _lib.F32, "fp32": _lib.F32, "float32": _lib.F32, "bf16": _lib.BF16, "bfloat16": _lib.BF16}
 
@@ -100,6 +100,36 @@ def tree_remaining(segments: np.ndarray, progress=None) -> np.ndarray:
                                                prog.ctypes.data if prog is not None and n else None,
                                                out.ctypes.data if n else None))
     return out
+
+
+def cache_from_rows(k_rows, v_rows, k_cache=None, v_cache=None, stream=None):
+    """Paged K/V blocks in row layout ``[num_blocks, Hkv, 16, d]`` rewritten
+    into the library's paged layouts (``padoc_cache_from_rows``): K
+    ``[num_blocks, Hkv, d/8, 16, 8]``, V ``[num_blocks, Hkv, d, 16]``, block
+    for block.  Returns ``(k_cache, v_cache)`` (allocated when not given)."""
+    import torch
+    if k_rows.dim() != 4 or k_rows.shape[2] != 16 or tuple(v_rows.shape) != tuple(k_rows.shape):
+        raise ValueError("k_rows / v_rows must both be [num_blocks, Hkv, 16, d]")
+    nb, hkv, _, d = k_rows.shape
+    dt = k_rows.dtype
+    if dt not in (torch.bfloat16, torch.float32) or v_rows.dtype != dt:
+        raise ValueError("k_rows / v_rows must share dtype bfloat16 or float32")
+    dev = k_rows.device
+    for name, t in (("k_rows", k_rows), ("v_rows", v_rows)):
+        _check_tensor(name, t, dt, dev)
+    if k_cache is None:
+        k_cache = torch.empty((nb, hkv, d // 8, 16, 8), dtype=dt, device=dev)
+    if v_cache is None:
+        v_cache = torch.empty((nb, hkv, d, 16), dtype=dt, device=dev)
+    for name, t, shape in (("k_cache", k_cache, (nb, hkv, d // 8, 16, 8)), ("v_cache", v_cache, (nb, hkv, d, 16))):
+        _check_tensor(name, t, dt, dev)
+        if tuple(t.shape) != shape:
+            raise ValueError(f"{name} must be {shape}")
+    s = torch.cuda.current_stream(dev) if stream is None else stream
+    _lib.check(_lib.lib().padoc_cache_from_rows(_ptr(k_rows), _ptr(v_rows), _ptr(k_cache), _ptr(v_cache), int(nb),
+                                                int(hkv), int(d), _lib.BF16 if dt == torch.bfloat16 else _lib.F32,
+                                                C.c_void_p(s.cuda_stream)))
+    return k_cache, v_cache
 
 
 class TreePlan:

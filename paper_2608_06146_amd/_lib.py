@@ -89,7 +89,7 @@ EXPORTED = [
     "padoc_plan_backward_workspace_bytes", "padoc_tree_attn_bwd",
     "padoc_session_create", "padoc_session_destroy", "padoc_session_open", "padoc_session_close",
     "padoc_session_prepare", "padoc_session_launch", "padoc_session_commit", "padoc_session_view_get",
-    "padoc_tree_depths", "padoc_tree_remaining", "padoc_session_select",
+    "padoc_tree_depths", "padoc_tree_remaining", "padoc_session_select", "padoc_cache_from_rows",
 ]
 
 _lib = None
@@ -131,6 +131,7 @@ def lib():
     L.padoc_tree_depths.argtypes = [vp, i32, vp, vp]
     L.padoc_tree_remaining.argtypes = [vp, i32, vp, vp]
     L.padoc_session_select.argtypes = [vp, i32, vp, vp, vp]
+    L.padoc_cache_from_rows.argtypes = [vp, vp, vp, vp, C.c_int64, i32, i32, C.c_int, vp]
     L.padoc_last_error.argtypes = []
     L.padoc_last_error.restype = C.c_char_p
     L.padoc_set_kernel_events.argtypes = [vp, vp]
@@ -142,7 +143,7 @@ def lib():
                  "padoc_plan_backward_workspace_bytes", "padoc_tree_attn_bwd", "padoc_session_create",
                  "padoc_session_open", "padoc_session_close", "padoc_session_prepare", "padoc_session_launch",
                  "padoc_session_commit", "padoc_session_view_get", "padoc_tree_depths",
-                 "padoc_tree_remaining", "padoc_session_select"):
+                 "padoc_tree_remaining", "padoc_session_select", "padoc_cache_from_rows"):
         getattr(L, name).restype = C.c_int
     _lib = L
     return L

@@ -32,6 +32,7 @@ SOURCES = [
     "csrc/kernels/lse_combine.hip",
     "csrc/kernels/bwd.hip",
     "csrc/kernels/append.hip",
+    "csrc/kernels/relayout.hip",
 ]
 # Every header under csrc/ (and the public header) enters each object's
 # digest, so an edit to any of them rebuilds every object.

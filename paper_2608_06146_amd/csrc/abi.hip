@@ -15,6 +15,8 @@ hipError_t launch_decode_step_bf16(const TileParams& p, int n_shared, int n_priv
 hipError_t launch_tile_valu_f32(const TileParams& p, int n_work, int D, bool paged, hipStream_t s);
 hipError_t launch_lse_combine(const CombineParams& p, int D, bool bf16, hipStream_t s);
 hipError_t launch_tree_attn_bwd(const BwdParams& p, int n_work, int n_bwd, int D, hipStream_t s);
+hipError_t launch_relayout_kv(const void* k_rows, const void* v_rows, void* k_cache, void* v_cache, int64_t n_blocks,
+                              int Hkv, int D, int elem_bytes, hipStream_t stream);
 hipError_t launch_append_kv(const void* k_new, const void* v_new, void* k_cache, void* v_cache, const int32_t* slots,
                             int64_t n_rows, int Hkv, int D, bool bf16, const int32_t* patch, int64_t n_patch,
                             int32_t* block_table, hipStream_t s);
@@ -298,6 +300,27 @@ extern "C" padoc_status padoc_branch_decode_no_alloc(const padoc_plan* plan, con
   if (!plan->work.empty() && !block_table) return set_error(PADOC_ERR_ARG, "block_table is null");
   return run(plan, q, k_cache, v_cache, block_table, o, lse, ws, stream, /*upload=*/true, /*events=*/true,
              /*pinned=*/false);
+}
+
+extern "C" padoc_status padoc_cache_from_rows(const void* k_rows, const void* v_rows, void* k_cache, void* v_cache,
+                                              int64_t num_blocks, int32_t num_heads_kv, int32_t head_dim,
+                                              padoc_dtype dtype, hipStream_t stream) {
+  clear_error();
+  if (num_blocks < 0) return set_error(PADOC_ERR_ARG, "num_blocks = %lld is negative", (long long)num_blocks);
+  if (num_heads_kv < 1) return set_error(PADOC_ERR_SHAPE, "num_heads_kv = %d must be >= 1", num_heads_kv);
+  if (head_dim != 64 && head_dim != 128) return set_error(PADOC_ERR_SHAPE, "head_dim = %d is not 64 or 128", head_dim);
+  if (dtype != PADOC_BF16 && dtype != PADOC_F32)
+    return set_error(PADOC_ERR_DTYPE, "dtype %d is not PADOC_F32 or PADOC_BF16", (int)dtype);
+  if (num_blocks == 0) return PADOC_OK;
+  if (!k_rows || !v_rows || !k_cache || !v_cache) return set_error(PADOC_ERR_ARG, "null buffer pointer");
+  if (k_rows == k_cache || v_rows == v_cache || k_rows == v_cache || v_rows == k_cache)
+    return set_error(PADOC_ERR_ARG, "source and destination buffers must be distinct");
+  if (num_blocks > INT64_MAX / ((int64_t)num_heads_kv * 16 * head_dim * 4))
+    return set_error(PADOC_ERR_BOUNDS, "num_blocks = %lld overflows the cache size", (long long)num_blocks);
+  const hipError_t e = launch_relayout_kv(k_rows, v_rows, k_cache, v_cache, num_blocks, num_heads_kv, head_dim,
+                                          dtype == PADOC_BF16 ? 2 : 4, stream);
+  if (e != hipSuccess) return hip_fail("relayout kernel launch", e);
+  return PADOC_OK;
 }
 
 extern "C" padoc_status padoc_tree_attn_bwd(const padoc_plan* plan, const void* q, const void* k, const void* v,
