@@ -290,11 +290,11 @@ def summarize_counters(d: str) -> None:
 PROFILE_COMMANDS = """\
     R=<repository root>; OUT=<output directory>; cd /tmp && export TMPDIR=/tmp
     rocprofv3 --kernel-trace --stats -d $OUT/trace -o bench -- \\
-        python3 $R/bench.py --steps 5 --warmup 1 --no-cpu-baseline --no-baselines --driver-steps 0 --no-secondary --no-cold > $OUT/trace/bench.json
+        python3 $R/bench.py --steps 30 --warmup 5 --no-cpu-baseline --no-baselines --driver-steps 0 --no-secondary --no-cold > $OUT/trace/bench.json
     rocprofv3 --pmc FETCH_SIZE --kernel-include-regex padoc -f csv -d $OUT/fetch -o p -- \\
-        python3 $R/bench.py --steps 5 --warmup 1 --no-cpu-baseline --no-baselines --driver-steps 0 --no-secondary --no-cold
+        python3 $R/bench.py --steps 30 --warmup 5 --no-cpu-baseline --no-baselines --driver-steps 0 --no-secondary --no-cold
     rocprofv3 --pmc WRITE_SIZE --kernel-include-regex padoc -f csv -d $OUT/write -o p -- \\
-        python3 $R/bench.py --steps 5 --warmup 1 --no-cpu-baseline --no-baselines --driver-steps 0 --no-secondary --no-cold
+        python3 $R/bench.py --steps 30 --warmup 5 --no-cpu-baseline --no-baselines --driver-steps 0 --no-secondary --no-cold
     rocprofv3 --pmc FETCH_SIZE -f csv -d $OUT/copy_fetch -o c -- python3 $R/bench.py --calibrate-copy
     rocprofv3 --pmc WRITE_SIZE -f csv -d $OUT/copy_write -o c -- python3 $R/bench.py --calibrate-copy
     for P in sqA sqB sqC; do   # counters of each pass: SQ_PASSES in bench.py
